@@ -1,0 +1,222 @@
+#!/usr/bin/env python3
+"""Benchmark of SMAT's fused per-step transform on one MI355X.
+
+One step = one pass of the whole hot path over the tensor list with inputs resident in HBM:
+    set per-tensor params -> simulate (theta~ into the buffers) -> switch to simulated storage
+    -> backward-accumulate (grad_theta += lambda t m g~) -> restore the expert storage.
+Default workload: the 7B-shaped decoder list (290 tensors, 7,504,924,672 parameters, fp32 master
+weights, bf16 base / simulated weights / upstream gradient).  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--config c4] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fused simulate+backward params/s and achieved HBM GB/s (% of peak), 7B-shaped"
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
+KERNEL_SOURCES = ("paper_2609_33437_amd/csrc/smat_kernels.hip", "paper_2609_33437_amd/csrc/smat_device.h")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on the current kernels."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_sha") != kernel_hash():
+        return None
+    return rec
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--cpu-sample", type=int, default=1 << 27, help="most elements the CPU oracle baseline visits")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU work budget of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(cfg, inp, params, step, max_elems, budget_s, torch, np):
+    """The CPU oracle on a bounded sample of the same workload: a window of every tensor with size
+    proportional to the tensor, simulate (with its rounding) then backward, on one core, visited
+    in random order until `budget_s` seconds of work are done."""
+    import oracle
+
+    frac = min(1.0, max_elems / cfg.numel)
+    rng = np.random.default_rng(1234)
+    order = rng.permutation(cfg.count)
+    t0_dt, g_dt, out_dt = cfg.theta0_dtype, cfg.grad_dtype, cfg.out_dtype
+
+    def bits(x):
+        return x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
+
+    done = tensors = 0
+    secs = 0.0
+    for i in order:
+        t = inp.theta[i]
+        n = t.numel()
+        m = max(1, int(round(n * frac)))
+        a = int(rng.integers(0, n - m + 1))
+        win = lambda x: x.view(-1)[a:a + m].cpu()
+        th, t0, gs, gt = win(t).numpy(), bits(win(inp.theta0[i])), bits(win(inp.grad_sim[i])), win(inp.grad_theta[i]).numpy()
+        start = time.perf_counter()
+        oracle.simulate(th, t0, t0_dt, out_dt, params[i], cfg.smat_seed, step, int(i), a)
+        oracle.backward_accum(gs, g_dt, gt, params[i], cfg.lam, cfg.smat_seed, step, int(i), a)
+        secs += time.perf_counter() - start
+        done += m
+        tensors += 1
+        if secs >= budget_s:
+            break
+    log(f"cpu oracle: {done} elements of {tensors} tensors in {secs:.1f} s")
+    return {"value": done / secs, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} elements: windows of {100 * frac:.3f}% of {tensors} of the {cfg.count} tensors in "
+                      f"random order (simulate + backward, fp64 NumPy, one process), {secs:.1f} s of work"}
+
+
+def main() -> int:
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the transform is elementwise "
+              "and shards by elem_offset without communication, so no multi-GPU figure is produced.",
+              file=sys.stderr)
+        return 2
+    import numpy as np
+    import torch
+
+    import paper_2609_33437_amd as smat
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    smat.lib()  # fail loudly if the HIP library is missing
+    cfg = workloads.config(args.config)
+    dt = {"bf16": torch.bfloat16, "f32": torch.float32}
+    nbytes = {"bf16": 2, "f32": 4}
+    log(f"generating {cfg.name}: {cfg.count} tensors, {cfg.numel} params")
+    t_gen = time.perf_counter()
+    inp = workloads.make_inputs(cfg, device="cuda")
+    outs = [torch.empty(t.numel(), dtype=dt[cfg.out_dtype], device="cuda") for t in inp.theta]
+    torch.cuda.synchronize()
+    log(f"generated in {time.perf_counter() - t_gen:.1f} s")
+
+    plan = smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta)
+    K, W = args.steps, args.warmup
+    # the hot path runs on simulated steps only: every step, or steps = 3 mod 4 for the periodic list
+    step_ids = [k * cfg.period + cfg.period - 1 for k in range(W + K)]
+    params = [workloads.step_params(cfg, inp.settings, s) for s in step_ids]
+    seed = cfg.smat_seed
+
+    def one(k, ev=None):
+        plan.set_params(params[k])
+        if ev:
+            ev[0].record()
+        plan.simulate(seed, step_ids[k])
+        if ev:
+            ev[1].record()
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        if ev:
+            ev[2].record()
+        plan.backward_accum(seed, step_ids[k], cfg.lam)
+        if ev:
+            ev[3].record()
+        plan.switch_storage(smat.SMAT_EXPERT)
+
+    log(f"warmup {W} steps")
+    for k in range(W):
+        one(k)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"timing {K} steps")
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(K):
+        one(W + k, evs[k])
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_step = total_ms / K
+    sim_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    bwd_ms = [e[2].elapsed_time(e[3]) for e in evs]
+    sim_avg, bwd_avg = sum(sim_ms) / K, sum(bwd_ms) / K
+    log(f"step {ms_step:.3f} ms  simulate {sim_avg:.3f} ms  backward {bwd_avg:.3f} ms")
+
+    P = cfg.numel
+    sim_bytes = P * (4 + nbytes[cfg.theta0_dtype] + nbytes[cfg.out_dtype])
+    bwd_bytes = P * (nbytes[cfg.grad_dtype] + 4 + 4)
+    step_gbps = (sim_bytes + bwd_bytes) / (ms_step * 1e6)
+    sim_gbps = sim_bytes / (sim_avg * 1e6)
+    bwd_gbps = bwd_bytes / (bwd_avg * 1e6)
+
+    dominant = "simulate" if sim_avg >= bwd_avg else "backward"
+    dom_gbps, dom_bytes = (sim_gbps, sim_bytes) if dominant == "simulate" else (bwd_gbps, bwd_bytes)
+    traffic = load_traffic(dominant, cfg.name)
+    roofline = {"bound": "hbm", "achieved": round(dom_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(dom_gbps / PEAK_HBM_GBPS, 4),
+                "traffic": traffic["bytes_per_launch"] if traffic else None,
+                "kernel": dominant, "algorithmic_bytes_per_launch": dom_bytes,
+                "avg_launch_ms": round(sim_avg if dominant == "simulate" else bwd_avg, 4)}
+
+    result = {
+        "metric": METRIC,
+        "value": P / (ms_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.description}", "params": P, "tensors": cfg.count,
+                   "theta": "f32", "theta0": cfg.theta0_dtype, "theta_tilde": cfg.out_dtype,
+                   "grad_sim": cfg.grad_dtype, "grad_theta": "f32",
+                   "bytes_per_param_per_step": (sim_bytes + bwd_bytes) / P, "period": cfg.period},
+        "hbm_gbps": round(step_gbps, 1),
+        "hbm_frac_of_peak": round(step_gbps / PEAK_HBM_GBPS, 4),
+        "kernels": {"simulate": {"avg_ms": round(sim_avg, 4), "gbps": round(sim_gbps, 1)},
+                    "backward": {"avg_ms": round(bwd_avg, 4), "gbps": round(bwd_gbps, 1)}},
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        last = W + K - 1
+        result["cpu_baseline"] = cpu_baseline(cfg, inp, params[last], step_ids[last], args.cpu_sample,
+                                              args.cpu_seconds, torch, np)
+    plan.close()
+    print(json.dumps(result))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,225 @@
+/*
+ * smat.h -- C ABI of the SMAT per-step parameter transform on MI355X (gfx950).
+ *
+ * SMAT ("SMAT: Simple and Efficient Merge-Aware Training") trains an expert
+ * while also evaluating its loss at a simulated merged state
+ *
+ *     theta~ = theta0 + s * m (.) (theta - theta0) + eps           (Sec. 4.1, Eq. smat-state)
+ *
+ * with a sampled scale s, a DARE-style keep mask m (drop probability
+ * p = 1 - keep, kept coordinates rescaled by 1/keep; Eq. smat-mask) and
+ * additive noise eps of RMS sigma (Sec. 4.1, "Perturb").  The gradient reaches
+ * the expert weights through the participation coefficient s*m
+ * (Sec. 4.2, Eq. smat-gradient); this library accumulates it weighted by the
+ * simulated-loss weight lambda (Eq. smat-objective).  Simulated weights live
+ * in one reusable buffer that the model reads for its forward and backward
+ * pass; the expert storage is restored before the optimizer
+ * (Sec. 4.3, "Parameter storage switching"; App. "Implementation details").
+ *
+ * Conventions for every entry point:
+ *   - Every function returns an smat_status; SMAT_OK is 0.  On failure nothing
+ *     is enqueued and smat_last_error() describes the cause.  No C++
+ *     exception crosses this boundary.
+ *   - Tensor arguments are device pointers to contiguous memory owned by the
+ *     caller (for example PyTorch tensors); the library never frees them.
+ *     Element counts are int64_t; 0 elements is a valid no-op.
+ *   - Work is enqueued on the caller's HIP stream (NULL = the default
+ *     stream) without synchronising the host.
+ *   - Random draws are never stored.  They are regenerated from Philox4x32-10
+ *     (Salmon et al., SC'11) with key = seed and counter
+ *     (g_lo, g_hi, tensor_id, 4*step + stream), where g = e >> 2 for the
+ *     global element index e = elem_offset + i and element e takes word e & 3.
+ *     Stream 0 draws the mask (kept iff word < floor(keep * 2^32)), stream 1
+ *     the noise.  Gaussian noise pairs words (w0, w1) for lanes 0/1 and
+ *     (w2, w3) for lanes 2/3 by Box-Muller on 24-bit uniforms
+ *     u1 = ((a >> 8) + 1) 2^-24, u2 = (b >> 8) 2^-24 (cosine on the even lane).
+ *     step must be below 2^30.
+ *   - A tensor split into shards (elem_offset = index of its first element
+ *     in the whole tensor) produces exactly the bytes of the whole tensor.
+ */
+#ifndef SMAT_H
+#define SMAT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum smat_status {
+  SMAT_OK = 0,
+  SMAT_ERR_INVALID = 1, /* null pointer with n > 0, n < 0, keep outside [0,1], sigma < 0 or not
+                           finite, s or lambda not finite, step >= 2^30, forbidden aliasing,
+                           duplicate tensor_id, too small workspace */
+  SMAT_ERR_DTYPE = 2,   /* unsupported dtype code */
+  SMAT_ERR_STATE = 3,   /* call not allowed in the plan's current state */
+  SMAT_ERR_HIP = 4      /* a HIP runtime call failed; smat_last_error() holds its message */
+} smat_status;
+
+typedef enum smat_dtype {
+  SMAT_F32 = 0,  /* IEEE binary32 */
+  SMAT_BF16 = 1  /* bfloat16, rounded to nearest even when written */
+} smat_dtype;
+
+typedef enum smat_noise_kind {
+  SMAT_NOISE_GAUSSIAN = 0, /* eps = sigma * z, z standard normal by Box-Muller */
+  SMAT_NOISE_UNIFORM = 1   /* eps = sigma * sqrt(3) * (2u - 1), u = ((w >> 8) + 1/2) 2^-24:
+                              the paper's default U[-sqrt(3) sigma, sqrt(3) sigma] (Sec. 4.1) */
+} smat_noise_kind;
+
+typedef enum smat_storage {
+  SMAT_EXPERT = 0,   /* the model sees the expert (fp32 master) storage */
+  SMAT_SIMULATED = 1 /* the model sees the reusable buffer holding theta~ */
+} smat_storage;
+
+/* Per-tensor operation parameters (Sec. 4.1).
+ *   s          scale (the paper's alpha), finite
+ *   keep       keep probability 1 - p in [0, 1]; keep >= 1 leaves the tensor outside the mask
+ *              set (no draw), keep == 0 drops every coordinate (no draw, theta~ = theta0 + eps)
+ *   sigma      noise RMS, finite and >= 0; 0 disables the noise (no draw)
+ *   rescale    nonzero: kept coordinates are multiplied by 1/keep (Eq. smat-mask)
+ *   noise_kind an smat_noise_kind value */
+typedef struct smat_op_params {
+  float s;
+  float keep;
+  float sigma;
+  int32_t rescale;
+  int32_t noise_kind;
+} smat_op_params;
+
+/* Random-draw key of one tensor (or shard) for one step. */
+typedef struct smat_rng_key {
+  uint64_t seed;        /* Philox key */
+  uint32_t step;        /* global training step, < 2^30 (fresh draws every step, Sec. 4.2) */
+  uint32_t tensor_id;   /* identifies the tensor; shards of one tensor share it */
+  uint64_t elem_offset; /* global index of element 0 of this range within its tensor */
+} smat_rng_key;
+
+/* smat_simulate -- theta~ for one flat tensor (Sec. 4.1, Eq. smat-state, Eq. smat-mask).
+ *   theta   [n] fp32 expert weights (device)
+ *   theta0  [n] frozen base weights in theta0_dtype (device); may be the same pointer as out
+ *           (in-place over a buffer that holds theta0), must not overlap it otherwise
+ *   out     [n] simulated weights in out_dtype (device); must not overlap theta
+ * For kept coordinates out = theta0 + t (theta - theta0) + eps with t = s/keep (rescale) or s,
+ * evaluated in fp32 as fma(t, theta, fma(-t, theta0, theta0)) + sigma z and rounded once to
+ * out_dtype; dropped coordinates get theta0 + eps.
+ * Errors: SMAT_ERR_INVALID, SMAT_ERR_DTYPE, SMAT_ERR_HIP. */
+smat_status smat_simulate(const float* theta, const void* theta0, smat_dtype theta0_dtype, void* out,
+                          smat_dtype out_dtype, int64_t n, smat_op_params p, smat_rng_key key,
+                          hipStream_t stream);
+
+/* smat_backward_accum -- grad_theta += lambda * t * m (.) grad_sim (Sec. 4.2, Eq. smat-gradient).
+ *   grad_sim    [n] gradient of the loss at theta~ in grad_dtype (device)
+ *   grad_theta  [n] fp32 accumulator (device), updated in place; must not overlap grad_sim
+ * The mask is regenerated from (key, p.keep) exactly as smat_simulate drew it, so the same key
+ * and keep must be passed (App. "Implementation details").  Kept coordinates become
+ * fma(lambda * t, grad_sim, grad_theta) in fp32; dropped coordinates keep their bits.
+ * Errors: SMAT_ERR_INVALID, SMAT_ERR_DTYPE, SMAT_ERR_HIP. */
+smat_status smat_backward_accum(const void* grad_sim, smat_dtype grad_dtype, float* grad_theta, int64_t n,
+                                smat_op_params p, float lambda, smat_rng_key key, hipStream_t stream);
+
+/* smat_debug_draws -- the raw draws of n elements, for bit-exact checks of the RNG layout.
+ *   mask_words  [n] uint32: stream-0 word of each element, or NULL
+ *   noise_words [n] uint32: stream-1 word of each element, or NULL
+ *   kept        [n] uint8: 1 where the mask keeps the element under p.keep, or NULL
+ *   z           [n] fp32: the standard-normal Box-Muller value of each element, or NULL
+ * All outputs are device pointers.  Test and diagnosis use only.
+ * Errors: SMAT_ERR_INVALID, SMAT_ERR_HIP. */
+smat_status smat_debug_draws(smat_rng_key key, int64_t n, smat_op_params p, uint32_t* mask_words,
+                             uint32_t* noise_words, uint8_t* kept, float* z, hipStream_t stream);
+
+/* ---------------------------------------------------------------- ragged tensor lists
+ * A plan covers a fixed list of parameter tensors ("compatible tensors" handled by one
+ * launch, Sec. 4.3 "Kernel fusion").  It holds host-side tables only; its device tables live
+ * in a caller-allocated workspace.  One launch per operation covers the whole list, split
+ * into equal-sized chunks so that thousands of small vectors and a few huge matrices share
+ * the GPU evenly. */
+typedef struct smat_plan smat_plan;
+
+/* One tensor of a plan.  Pointers are device pointers unless stated. */
+typedef struct smat_tensor_desc {
+  const float* theta;       /* [n] fp32 expert storage */
+  const void* theta0;       /* [n] frozen base in the plan's theta0 dtype; resident mode only
+                               (NULL in offload mode, where the buffer `out` holds theta0) */
+  void* out;                /* [n] reusable buffer for theta~ in the plan's out dtype */
+  const void* grad_sim;     /* [n] gradient at theta~ (grad dtype), or NULL if no backward */
+  float* grad_theta;        /* [n] fp32 gradient accumulator, or NULL if no backward */
+  const void* theta0_host;  /* offload mode: [n] pinned host copy of theta0 (out dtype); else NULL */
+  int64_t n;                /* element count, >= 0 */
+  uint32_t tensor_id;       /* unique within the plan */
+  uint32_t reserved;        /* must be 0 */
+  uint64_t elem_offset;     /* global index of element 0 within the tensor (shards) */
+} smat_tensor_desc;
+
+/* smat_plan_create -- validate a tensor list and build its tables.
+ *   offload  0: theta0 resident in device memory (the plan reads desc.theta0).
+ *            1: the paper's pinned-host layout (Sec. 4.3; App. "Hardware, Software, and
+ *               Implementation"): theta0 lives in desc.theta0_host and is copied into the
+ *               buffer `out` on a copy stream whenever the expert storage is restored, so each
+ *               simulate runs in place over the buffer.  Requires theta0_dtype == out_dtype.
+ * The caller owns *out_plan and must release it with smat_plan_destroy.
+ * Errors: SMAT_ERR_INVALID (bad descriptor, duplicate tensor_id, aliasing), SMAT_ERR_DTYPE. */
+smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t count, smat_dtype theta0_dtype,
+                             smat_dtype out_dtype, smat_dtype grad_dtype, int32_t offload,
+                             smat_plan** out_plan);
+
+/* smat_plan_workspace_bytes -- device bytes the plan's tables need (256-byte aligned start). */
+smat_status smat_plan_workspace_bytes(const smat_plan* plan, size_t* bytes);
+
+/* smat_plan_bind_workspace -- hand the plan its device workspace and upload its static tables on
+ * `stream` (in offload mode also the first theta0 prefetch).  The workspace stays owned by the
+ * caller and must outlive the plan.  Errors: SMAT_ERR_INVALID (null, misaligned or too small),
+ * SMAT_ERR_STATE (already bound), SMAT_ERR_HIP. */
+smat_status smat_plan_bind_workspace(smat_plan* plan, void* workspace, size_t bytes, hipStream_t stream);
+
+/* smat_plan_set_params -- per-tensor s, keep, sigma for the next operations (count entries, in
+ * descriptor order), uploaded asynchronously on `stream`.  The backward of a step must see the
+ * same keep values as its simulate.  Errors: SMAT_ERR_INVALID, SMAT_ERR_STATE (no workspace),
+ * SMAT_ERR_HIP. */
+smat_status smat_plan_set_params(smat_plan* plan, const smat_op_params* per_tensor, hipStream_t stream);
+
+/* smat_simulate_multi -- smat_simulate over every tensor of the plan in one launch, keys
+ * (seed, step, desc.tensor_id, desc.elem_offset).  Allowed only while the expert storage is
+ * active.  Errors: SMAT_ERR_INVALID (step), SMAT_ERR_STATE (no workspace, no params, simulated
+ * storage active), SMAT_ERR_HIP. */
+smat_status smat_simulate_multi(smat_plan* plan, uint64_t seed, uint32_t step, hipStream_t stream);
+
+/* smat_backward_accum_multi -- smat_backward_accum over every tensor of the plan in one launch.
+ * Errors: SMAT_ERR_INVALID (lambda, step, plan without gradient pointers), SMAT_ERR_STATE,
+ * SMAT_ERR_HIP. */
+smat_status smat_backward_accum_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda,
+                                      hipStream_t stream);
+
+/* smat_switch_storage -- point the model at the simulated buffer (SMAT_SIMULATED) or back at the
+ * expert storage (SMAT_EXPERT) (Sec. 4.3, "Parameter storage switching").  The plan keeps a
+ * device table of the active pointer of every tensor (see smat_plan_active_ptrs) and rewrites it
+ * on `stream`.  SMAT_SIMULATED requires a simulate since the last restore and is an error when
+ * already active; SMAT_EXPERT is idempotent.  In offload mode, restoring the expert storage also
+ * starts the theta0 prefetch into the buffers on the plan's copy stream once `stream` has
+ * reached this point; the next simulate waits for it.  Expert storage is never written.
+ * Errors: SMAT_ERR_INVALID (bad `to`), SMAT_ERR_STATE, SMAT_ERR_HIP. */
+smat_status smat_switch_storage(smat_plan* plan, int32_t to, hipStream_t stream);
+
+/* smat_plan_state -- the active storage (an smat_storage value) in *state. */
+smat_status smat_plan_state(const smat_plan* plan, int32_t* state);
+
+/* smat_plan_active_ptrs -- the active pointer of every tensor.  host_out, if not NULL, receives
+ * count pointers; *dev_table, if dev_table is not NULL, receives the device address of the
+ * count-entry pointer table that smat_switch_storage maintains (inside the workspace). */
+smat_status smat_plan_active_ptrs(const smat_plan* plan, void** host_out, void** dev_table);
+
+/* smat_plan_destroy -- wait for the plan's own pending uploads and prefetches, then free its host
+ * tables.  NULL is a no-op.  The workspace is not touched. */
+smat_status smat_plan_destroy(smat_plan* plan);
+
+/* smat_last_error -- message of the last failure on the calling thread ("" if none). */
+const char* smat_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SMAT_H */

@@ -1,0 +1,12 @@
+"""SMAT's per-step Scale/Mask/Perturb parameter transform on MI355X (gfx950).
+
+`libsmat.so` (C ABI in include/smat.h) holds the HIP kernels; this package binds it with
+ctypes.  Build it with `python -m paper_2609_33437_amd.build`.
+"""
+from ._lib import (EXPORTS, SMAT_BF16, SMAT_EXPERT, SMAT_F32, SMAT_NOISE_GAUSSIAN, SMAT_NOISE_UNIFORM,
+                   SMAT_SIMULATED, Plan, SmatError, lib, load_library, op_params, rng_key, smat_backward_accum,
+                   smat_debug_draws, smat_simulate)
+
+__all__ = ["EXPORTS", "SMAT_BF16", "SMAT_EXPERT", "SMAT_F32", "SMAT_NOISE_GAUSSIAN", "SMAT_NOISE_UNIFORM",
+           "SMAT_SIMULATED", "Plan", "SmatError", "lib", "load_library", "op_params", "rng_key",
+           "smat_backward_accum", "smat_debug_draws", "smat_simulate"]

@@ -1,0 +1,264 @@
+"""ctypes binding of libsmat (argument marshalling only; every step runs in the HIP kernels).
+
+The functions keep the C names.  Tensors are PyTorch tensors on the GPU (torch supplies device
+memory and the HIP stream); scalars and parameter records are marshalled into the C structs of
+include/smat.h.  There is no fallback: without the built library importing this module fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_char_p, c_float, c_int32, c_int64, c_size_t, c_uint8, c_uint32, c_uint64, c_void_p
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsmat.so")
+
+SMAT_OK, SMAT_ERR_INVALID, SMAT_ERR_DTYPE, SMAT_ERR_STATE, SMAT_ERR_HIP = 0, 1, 2, 3, 4
+SMAT_F32, SMAT_BF16 = 0, 1
+SMAT_NOISE_GAUSSIAN, SMAT_NOISE_UNIFORM = 0, 1
+SMAT_EXPERT, SMAT_SIMULATED = 0, 1
+
+STATUS_NAMES = {0: "SMAT_OK", 1: "SMAT_ERR_INVALID", 2: "SMAT_ERR_DTYPE", 3: "SMAT_ERR_STATE", 4: "SMAT_ERR_HIP"}
+
+EXPORTS = (
+    "smat_simulate", "smat_backward_accum", "smat_debug_draws", "smat_plan_create", "smat_plan_workspace_bytes",
+    "smat_plan_bind_workspace", "smat_plan_set_params", "smat_simulate_multi", "smat_backward_accum_multi",
+    "smat_switch_storage", "smat_plan_state", "smat_plan_active_ptrs", "smat_plan_destroy", "smat_last_error",
+)
+
+
+class smat_op_params(ctypes.Structure):
+    _fields_ = [("s", c_float), ("keep", c_float), ("sigma", c_float), ("rescale", c_int32), ("noise_kind", c_int32)]
+
+
+class smat_rng_key(ctypes.Structure):
+    _fields_ = [("seed", c_uint64), ("step", c_uint32), ("tensor_id", c_uint32), ("elem_offset", c_uint64)]
+
+
+class smat_tensor_desc(ctypes.Structure):
+    _fields_ = [("theta", c_void_p), ("theta0", c_void_p), ("out", c_void_p), ("grad_sim", c_void_p),
+                ("grad_theta", c_void_p), ("theta0_host", c_void_p), ("n", c_int64), ("tensor_id", c_uint32),
+                ("reserved", c_uint32), ("elem_offset", c_uint64)]
+
+
+class SmatError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build the HIP library first "
+                          "(python -m paper_2609_33437_amd.build)")
+    lib = ctypes.CDLL(path)
+    P = c_void_p
+    sig = {
+        "smat_simulate": [P, P, c_int32, P, c_int32, c_int64, smat_op_params, smat_rng_key, P],
+        "smat_backward_accum": [P, c_int32, P, c_int64, smat_op_params, c_float, smat_rng_key, P],
+        "smat_debug_draws": [smat_rng_key, c_int64, smat_op_params, P, P, P, P, P],
+        "smat_plan_create": [POINTER(smat_tensor_desc), c_int32, c_int32, c_int32, c_int32, c_int32, POINTER(P)],
+        "smat_plan_workspace_bytes": [P, POINTER(c_size_t)],
+        "smat_plan_bind_workspace": [P, P, c_size_t, P],
+        "smat_plan_set_params": [P, POINTER(smat_op_params), P],
+        "smat_simulate_multi": [P, c_uint64, c_uint32, P],
+        "smat_backward_accum_multi": [P, c_uint64, c_uint32, c_float, P],
+        "smat_switch_storage": [P, c_int32, P],
+        "smat_plan_state": [P, POINTER(c_int32)],
+        "smat_plan_active_ptrs": [P, POINTER(P), POINTER(P)],
+        "smat_plan_destroy": [P],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = c_int32
+    lib.smat_last_error.argtypes = []
+    lib.smat_last_error.restype = c_char_p
+    return lib
+
+
+_LIB: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    global _LIB
+    if _LIB is None:
+        _LIB = load_library()
+    return _LIB
+
+
+def _check(status: int) -> None:
+    if status != SMAT_OK:
+        raise SmatError(status, lib().smat_last_error().decode())
+
+
+# ------------------------------------------------------------------ marshalling helpers
+def _torch():
+    import torch
+    return torch
+
+
+def dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return SMAT_F32
+    if t.dtype == torch.bfloat16:
+        return SMAT_BF16
+    raise SmatError(SMAT_ERR_DTYPE, f"unsupported tensor dtype {t.dtype}")
+
+
+def _stream_handle(stream) -> c_void_p:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return c_void_p(s.cuda_stream)
+
+
+def _dev_ptr(t, what: str):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise SmatError(SMAT_ERR_INVALID, f"{what} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise SmatError(SMAT_ERR_INVALID, f"{what} must be contiguous")
+    return c_void_p(t.data_ptr()) if t.numel() else None
+
+
+def op_params(p) -> smat_op_params:
+    """dict(s, keep, sigma, rescale=1, noise_kind=0) or an smat_op_params -> smat_op_params."""
+    if isinstance(p, smat_op_params):
+        return p
+    return smat_op_params(float(p["s"]), float(p["keep"]), float(p["sigma"]), int(p.get("rescale", 1)),
+                          int(p.get("noise_kind", SMAT_NOISE_GAUSSIAN)))
+
+
+def rng_key(seed: int, step: int, tensor_id: int = 0, elem_offset: int = 0) -> smat_rng_key:
+    return smat_rng_key(int(seed), int(step), int(tensor_id), int(elem_offset))
+
+
+# ------------------------------------------------------------------ single tensor
+def smat_simulate(theta, theta0, out, params, seed: int, step: int, tensor_id: int = 0, elem_offset: int = 0,
+                  stream=None) -> None:
+    """theta~ of one flat tensor into `out` (see include/smat.h)."""
+    n = theta.numel()
+    if theta0.numel() != n or out.numel() != n:
+        raise SmatError(SMAT_ERR_INVALID, "theta, theta0 and out differ in size")
+    _check(lib().smat_simulate(_dev_ptr(theta, "theta"), _dev_ptr(theta0, "theta0"), dtype_code(theta0),
+                               _dev_ptr(out, "out"), dtype_code(out), n, op_params(params),
+                               rng_key(seed, step, tensor_id, elem_offset), _stream_handle(stream)))
+
+
+def smat_backward_accum(grad_sim, grad_theta, params, lam: float, seed: int, step: int, tensor_id: int = 0,
+                        elem_offset: int = 0, stream=None) -> None:
+    """grad_theta += lam * t * m * grad_sim in place (see include/smat.h)."""
+    n = grad_theta.numel()
+    if grad_sim.numel() != n:
+        raise SmatError(SMAT_ERR_INVALID, "grad_sim and grad_theta differ in size")
+    _check(lib().smat_backward_accum(_dev_ptr(grad_sim, "grad_sim"), dtype_code(grad_sim),
+                                     _dev_ptr(grad_theta, "grad_theta"), n, op_params(params), float(lam),
+                                     rng_key(seed, step, tensor_id, elem_offset), _stream_handle(stream)))
+
+
+def smat_debug_draws(n: int, params, seed: int, step: int, tensor_id: int = 0, elem_offset: int = 0,
+                     mask_words=None, noise_words=None, kept=None, z=None, stream=None) -> None:
+    """Raw per-element draws into the given GPU tensors (uint32 viewed as int32, uint8, fp32)."""
+    for name, t in (("mask_words", mask_words), ("noise_words", noise_words), ("kept", kept), ("z", z)):
+        if t is not None and t.numel() != n:
+            raise SmatError(SMAT_ERR_INVALID, f"{name} must hold n elements")
+    _check(lib().smat_debug_draws(rng_key(seed, step, tensor_id, elem_offset), int(n), op_params(params),
+                                  _dev_ptr(mask_words, "mask_words"), _dev_ptr(noise_words, "noise_words"),
+                                  _dev_ptr(kept, "kept"), _dev_ptr(z, "z"), _stream_handle(stream)))
+
+
+# ------------------------------------------------------------------ tensor-list plans
+class Plan:
+    """A tensor list bound to libsmat (smat_plan_* calls); holds references to its tensors."""
+
+    def __init__(self, thetas: Sequence, outs: Sequence, theta0s: Optional[Sequence] = None,
+                 grad_sims: Optional[Sequence] = None, grad_thetas: Optional[Sequence] = None,
+                 tensor_ids: Optional[Sequence[int]] = None, elem_offsets: Optional[Sequence[int]] = None,
+                 offload: bool = False, theta0_hosts: Optional[Sequence] = None, stream=None,
+                 dtypes: Optional[tuple] = None):
+        torch = _torch()
+        count = len(thetas)
+        self.count = count
+        self._refs = [thetas, outs, theta0s, grad_sims, grad_thetas, theta0_hosts]
+        ids = list(tensor_ids) if tensor_ids is not None else list(range(count))
+        offs = list(elem_offsets) if elem_offsets is not None else [0] * count
+        descs = (smat_tensor_desc * max(count, 1))()
+        for i in range(count):
+            d = descs[i]
+            d.theta = _dev_ptr(thetas[i], "theta")
+            d.out = _dev_ptr(outs[i], "out")
+            d.theta0 = _dev_ptr(theta0s[i], "theta0") if theta0s is not None else None
+            d.grad_sim = _dev_ptr(grad_sims[i], "grad_sim") if grad_sims is not None else None
+            d.grad_theta = _dev_ptr(grad_thetas[i], "grad_theta") if grad_thetas is not None else None
+            if theta0_hosts is not None:
+                h = theta0_hosts[i]
+                if h.is_cuda or not h.is_pinned() or not h.is_contiguous():
+                    raise SmatError(SMAT_ERR_INVALID, "theta0_hosts must be contiguous pinned host tensors")
+                d.theta0_host = c_void_p(h.data_ptr()) if h.numel() else None
+            d.n = thetas[i].numel()
+            d.tensor_id = ids[i]
+            d.elem_offset = offs[i]
+        if dtypes is None:
+            t0_dt = dtype_code(theta0s[0] if theta0s is not None else outs[0]) if count else SMAT_BF16
+            out_dt = dtype_code(outs[0]) if count else SMAT_BF16
+            g_dt = dtype_code(grad_sims[0]) if (count and grad_sims is not None) else SMAT_BF16
+        else:
+            t0_dt, out_dt, g_dt = dtypes
+        self.dtypes = (t0_dt, out_dt, g_dt)
+        plan = c_void_p()
+        _check(lib().smat_plan_create(descs, count, t0_dt, out_dt, g_dt, 1 if offload else 0, ctypes.byref(plan)))
+        self._plan = plan
+        nbytes = c_size_t()
+        _check(lib().smat_plan_workspace_bytes(plan, ctypes.byref(nbytes)))
+        dev = thetas[0].device if count else torch.device("cuda")
+        self.workspace = torch.empty(nbytes.value, dtype=torch.uint8, device=dev)
+        _check(lib().smat_plan_bind_workspace(plan, c_void_p(self.workspace.data_ptr()), nbytes.value,
+                                              _stream_handle(stream)))
+
+    def set_params(self, params: Sequence, stream=None) -> None:
+        arr = (smat_op_params * max(self.count, 1))(*[op_params(p) for p in params])
+        if len(params) != self.count:
+            raise SmatError(SMAT_ERR_INVALID, "one parameter record per tensor")
+        _check(lib().smat_plan_set_params(self._plan, arr, _stream_handle(stream)))
+
+    def simulate(self, seed: int, step: int, stream=None) -> None:
+        _check(lib().smat_simulate_multi(self._plan, int(seed), int(step), _stream_handle(stream)))
+
+    def backward_accum(self, seed: int, step: int, lam: float, stream=None) -> None:
+        _check(lib().smat_backward_accum_multi(self._plan, int(seed), int(step), float(lam), _stream_handle(stream)))
+
+    def switch_storage(self, to: int, stream=None) -> None:
+        _check(lib().smat_switch_storage(self._plan, int(to), _stream_handle(stream)))
+
+    @property
+    def state(self) -> int:
+        st = c_int32()
+        _check(lib().smat_plan_state(self._plan, ctypes.byref(st)))
+        return st.value
+
+    def active_ptrs(self):
+        """(host list of active pointers, device address of the active pointer table)."""
+        host = (c_void_p * max(self.count, 1))()
+        dev = c_void_p()
+        _check(lib().smat_plan_active_ptrs(self._plan, host, ctypes.byref(dev)))
+        return [host[i] or 0 for i in range(self.count)], dev.value or 0
+
+    def close(self) -> None:
+        if getattr(self, "_plan", None):
+            _check(lib().smat_plan_destroy(self._plan))
+            self._plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

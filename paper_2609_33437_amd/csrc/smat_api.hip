@@ -1,0 +1,491 @@
+// C ABI of libsmat: argument checks, per-tensor constants, tensor-list plans, the storage
+// switch and the offload prefetch.  Kernels live in smat_kernels.hip.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "smat.h"
+#include "smat_launch.h"
+
+using smat::ParamRec;
+using smat::TensorRec;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+smat_status fail(smat_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+#define SMAT_HIP(call)                                                                   \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess) return fail(SMAT_ERR_HIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr uint32_t kMaxStep = 1u << 30;
+
+bool valid_dtype(int d) { return d == SMAT_F32 || d == SMAT_BF16; }
+size_t dtype_bytes(int d) { return d == SMAT_F32 ? 4 : 2; }
+size_t quad_align(int d) { return d == SMAT_F32 ? 16 : 8; }
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool overlap(const void* a, size_t abytes, const void* b, size_t bbytes) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + bbytes && y < x + abytes;
+}
+
+// Per-tensor constants of one step (Sec. 4.1): the keep threshold on a 32-bit word, the
+// coefficient t = s/keep (rescale) or s of the task vector, and which draws are needed.
+smat_status make_param(const smat_op_params& p, ParamRec* out, const char* where) {
+  if (!std::isfinite(p.s)) return fail(SMAT_ERR_INVALID, "%s: scale s must be finite", where);
+  if (!std::isfinite(p.keep) || p.keep < 0.f || p.keep > 1.f)
+    return fail(SMAT_ERR_INVALID, "%s: keep must lie in [0, 1] (got %g)", where, (double)p.keep);
+  if (!std::isfinite(p.sigma) || p.sigma < 0.f)
+    return fail(SMAT_ERR_INVALID, "%s: sigma must be finite and >= 0 (got %g)", where, (double)p.sigma);
+  if (p.noise_kind != SMAT_NOISE_GAUSSIAN && p.noise_kind != SMAT_NOISE_UNIFORM)
+    return fail(SMAT_ERR_INVALID, "%s: unknown noise kind %d", where, p.noise_kind);
+  ParamRec r{};
+  if (p.keep >= 1.f) {
+    r.t = p.s;
+  } else if (p.keep <= 0.f) {
+    r.flags |= smat::kFlagDropAll;
+  } else {
+    r.flags |= smat::kFlagMask;
+    r.thr = (uint32_t)std::floor((double)p.keep * 4294967296.0);
+    r.t = p.rescale ? (float)((double)p.s / (double)p.keep) : p.s;
+  }
+  if (p.sigma > 0.f) {
+    r.flags |= smat::kFlagNoise;
+    if (p.noise_kind == SMAT_NOISE_UNIFORM) r.flags |= smat::kFlagUniform;
+    r.sigma = p.sigma;
+  }
+  *out = r;
+  return SMAT_OK;
+}
+
+uint32_t sim_flags(const float* theta, const void* theta0, int t0_dt, const void* out, int out_dt,
+                   uint64_t elem_offset) {
+  return (elem_offset % 4 == 0 && aligned(theta, 16) && aligned(theta0, quad_align(t0_dt)) &&
+          aligned(out, quad_align(out_dt)))
+             ? smat::kVecSim
+             : 0u;
+}
+
+uint32_t bwd_flags(const void* grad_sim, int g_dt, const float* grad_theta, uint64_t elem_offset) {
+  return (elem_offset % 4 == 0 && aligned(grad_sim, quad_align(g_dt)) && aligned(grad_theta, 16)) ? smat::kVecBwd
+                                                                                                  : 0u;
+}
+
+smat_status check_simulate_ptrs(const float* theta, const void* theta0, int t0_dt, const void* out, int out_dt,
+                                int64_t n, const char* where) {
+  if (!theta || !out || !theta0) return fail(SMAT_ERR_INVALID, "%s: null pointer with n > 0", where);
+  const size_t nb = (size_t)n;
+  if (overlap(out, nb * dtype_bytes(out_dt), theta, nb * 4))
+    return fail(SMAT_ERR_INVALID, "%s: out must not overlap theta", where);
+  if (out == theta0) {
+    if (t0_dt != out_dt) return fail(SMAT_ERR_INVALID, "%s: in-place out == theta0 needs equal dtypes", where);
+  } else if (overlap(out, nb * dtype_bytes(out_dt), theta0, nb * dtype_bytes(t0_dt))) {
+    return fail(SMAT_ERR_INVALID, "%s: out overlaps theta0 without being the same buffer", where);
+  }
+  return SMAT_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace
+
+// ------------------------------------------------------------------ single tensor
+extern "C" smat_status smat_simulate(const float* theta, const void* theta0, smat_dtype theta0_dtype, void* out,
+                                     smat_dtype out_dtype, int64_t n, smat_op_params p, smat_rng_key key,
+                                     hipStream_t stream) {
+  if (!valid_dtype(theta0_dtype) || !valid_dtype(out_dtype))
+    return fail(SMAT_ERR_DTYPE, "smat_simulate: unsupported dtype");
+  if (n < 0) return fail(SMAT_ERR_INVALID, "smat_simulate: n < 0");
+  if (key.step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_simulate: step must be < 2^30");
+  ParamRec prm;
+  smat_status st = make_param(p, &prm, "smat_simulate");
+  if (st != SMAT_OK) return st;
+  if (n == 0) return SMAT_OK;
+  if (key.elem_offset > UINT64_MAX - (uint64_t)n) return fail(SMAT_ERR_INVALID, "smat_simulate: elem_offset + n overflows");
+  st = check_simulate_ptrs(theta, theta0, theta0_dtype, out, out_dtype, n, "smat_simulate");
+  if (st != SMAT_OK) return st;
+  TensorRec rec{};
+  rec.theta = theta;
+  rec.theta0 = theta0;
+  rec.out = out;
+  rec.n = n;
+  rec.elem_offset = key.elem_offset;
+  rec.tensor_id = key.tensor_id;
+  rec.sflags = sim_flags(theta, theta0, theta0_dtype, out, out_dtype, key.elem_offset);
+  SMAT_HIP(smat::launch_simulate_one(rec, prm, theta0_dtype, out_dtype, key.seed, key.step, stream));
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_backward_accum(const void* grad_sim, smat_dtype grad_dtype, float* grad_theta, int64_t n,
+                                           smat_op_params p, float lambda, smat_rng_key key, hipStream_t stream) {
+  if (!valid_dtype(grad_dtype)) return fail(SMAT_ERR_DTYPE, "smat_backward_accum: unsupported dtype");
+  if (n < 0) return fail(SMAT_ERR_INVALID, "smat_backward_accum: n < 0");
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_backward_accum: lambda must be finite");
+  if (key.step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_backward_accum: step must be < 2^30");
+  ParamRec prm;
+  smat_status st = make_param(p, &prm, "smat_backward_accum");
+  if (st != SMAT_OK) return st;
+  if (n == 0) return SMAT_OK;
+  if (key.elem_offset > UINT64_MAX - (uint64_t)n)
+    return fail(SMAT_ERR_INVALID, "smat_backward_accum: elem_offset + n overflows");
+  if (!grad_sim || !grad_theta) return fail(SMAT_ERR_INVALID, "smat_backward_accum: null pointer with n > 0");
+  if (overlap(grad_sim, (size_t)n * dtype_bytes(grad_dtype), grad_theta, (size_t)n * 4))
+    return fail(SMAT_ERR_INVALID, "smat_backward_accum: grad_sim must not overlap grad_theta");
+  TensorRec rec{};
+  rec.grad_sim = grad_sim;
+  rec.grad_theta = grad_theta;
+  rec.n = n;
+  rec.elem_offset = key.elem_offset;
+  rec.tensor_id = key.tensor_id;
+  rec.sflags = bwd_flags(grad_sim, grad_dtype, grad_theta, key.elem_offset);
+  SMAT_HIP(smat::launch_backward_one(rec, prm, grad_dtype, lambda, key.seed, key.step, stream));
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_debug_draws(smat_rng_key key, int64_t n, smat_op_params p, uint32_t* mask_words,
+                                        uint32_t* noise_words, uint8_t* kept, float* z, hipStream_t stream) {
+  if (n < 0) return fail(SMAT_ERR_INVALID, "smat_debug_draws: n < 0");
+  if (key.step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_debug_draws: step must be < 2^30");
+  ParamRec prm;
+  smat_status st = make_param(p, &prm, "smat_debug_draws");
+  if (st != SMAT_OK) return st;
+  if (n == 0 || (!mask_words && !noise_words && !kept && !z)) return SMAT_OK;
+  if (key.elem_offset > UINT64_MAX - (uint64_t)n) return fail(SMAT_ERR_INVALID, "smat_debug_draws: elem_offset + n overflows");
+  SMAT_HIP(smat::launch_debug_draws(key.seed, key.step, key.tensor_id, key.elem_offset, n, prm, mask_words,
+                                    noise_words, kept, z, stream));
+  return SMAT_OK;
+}
+
+// ------------------------------------------------------------------ plans
+struct smat_plan {
+  int32_t count = 0;
+  int t0_dt = 0, out_dt = 0, g_dt = 0;
+  bool offload = false;
+  bool has_grads = false;
+  std::vector<smat_tensor_desc> descs;
+  std::vector<TensorRec> recs;
+  std::vector<uint2> chunks;
+  std::vector<void*> expert_ptrs, sim_ptrs;
+
+  // workspace layout: [recs][chunks][active table][expert table][simulated table][params]
+  size_t off_recs = 0, off_chunks = 0, off_active = 0, off_expert = 0, off_sim = 0, off_params = 0, ws_bytes = 0;
+  char* ws = nullptr;
+
+  // pinned staging for the asynchronous uploads: the static tables once, the params every step
+  // through two alternating slots, so a new upload only waits for the one before the last
+  char* static_staging = nullptr;
+  ParamRec* params_staging[2] = {nullptr, nullptr};
+  hipEvent_t ev_static = nullptr;
+  hipEvent_t ev_params[2] = {nullptr, nullptr};
+  bool params_pending[2] = {false, false};
+  int params_slot = 0;
+  bool params_set = false;
+
+  int32_t state = SMAT_EXPERT;
+  bool fresh = false;  // the buffers hold theta~ of a simulate issued since the last restore
+
+  // offload mode: theta0 prefetch from pinned host memory on a copy stream
+  hipStream_t copy_stream = nullptr;
+  hipEvent_t ev_release = nullptr, ev_prefetch = nullptr;
+  bool prefetch_pending = false;
+};
+
+namespace {
+
+smat_status release(smat_plan* p) {
+  // wait for the plan's own work that still reads its pinned staging or owns its events
+  for (hipEvent_t e : {p->ev_static, p->ev_params[0], p->ev_params[1], p->ev_prefetch})
+    if (e) (void)hipEventSynchronize(e);
+  if (p->static_staging) (void)hipHostFree(p->static_staging);
+  for (ParamRec* s : p->params_staging)
+    if (s) (void)hipHostFree(s);
+  for (hipEvent_t e : {p->ev_static, p->ev_params[0], p->ev_params[1], p->ev_release, p->ev_prefetch})
+    if (e) (void)hipEventDestroy(e);
+  if (p->copy_stream) (void)hipStreamDestroy(p->copy_stream);
+  delete p;
+  return SMAT_OK;
+}
+
+smat_status enqueue_prefetch(smat_plan* p, hipStream_t stream) {
+  // the buffers are free once `stream` reaches this point (the model no longer reads theta~)
+  SMAT_HIP(hipEventRecord(p->ev_release, stream));
+  SMAT_HIP(hipStreamWaitEvent(p->copy_stream, p->ev_release, 0));
+  for (int32_t i = 0; i < p->count; ++i) {
+    const smat_tensor_desc& d = p->descs[i];
+    if (d.n == 0) continue;
+    SMAT_HIP(hipMemcpyAsync(d.out, d.theta0_host, (size_t)d.n * dtype_bytes(p->out_dt), hipMemcpyHostToDevice,
+                            p->copy_stream));
+  }
+  SMAT_HIP(hipEventRecord(p->ev_prefetch, p->copy_stream));
+  p->prefetch_pending = true;
+  return SMAT_OK;
+}
+
+}  // namespace
+
+extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t count, smat_dtype theta0_dtype,
+                                        smat_dtype out_dtype, smat_dtype grad_dtype, int32_t offload,
+                                        smat_plan** out_plan) {
+  if (!out_plan) return fail(SMAT_ERR_INVALID, "smat_plan_create: out_plan is null");
+  *out_plan = nullptr;
+  if (!valid_dtype(theta0_dtype) || !valid_dtype(out_dtype) || !valid_dtype(grad_dtype))
+    return fail(SMAT_ERR_DTYPE, "smat_plan_create: unsupported dtype");
+  if (count < 0 || (count > 0 && !descs)) return fail(SMAT_ERR_INVALID, "smat_plan_create: bad tensor list");
+  if (offload != 0 && offload != 1) return fail(SMAT_ERR_INVALID, "smat_plan_create: offload must be 0 or 1");
+  if (offload && theta0_dtype != out_dtype)
+    return fail(SMAT_ERR_INVALID, "smat_plan_create: offload mode keeps theta0 in the buffer, dtypes must match");
+
+  smat_plan* p = new smat_plan();
+  p->count = count;
+  p->t0_dt = theta0_dtype;
+  p->out_dt = out_dtype;
+  p->g_dt = grad_dtype;
+  p->offload = offload != 0;
+  p->descs.assign(descs, descs + count);
+  p->has_grads = true;
+
+  std::vector<std::pair<uint32_t, std::pair<uint64_t, uint64_t>>> ranges;
+  for (int32_t i = 0; i < count; ++i) {
+    const smat_tensor_desc& d = p->descs[i];
+    char where[64];
+    std::snprintf(where, sizeof(where), "smat_plan_create: tensor %d", i);
+    smat_status st = SMAT_OK;
+    if (d.n < 0 || d.reserved != 0) st = fail(SMAT_ERR_INVALID, "%s: n < 0 or reserved != 0", where);
+    else if (d.elem_offset > UINT64_MAX - (uint64_t)d.n) st = fail(SMAT_ERR_INVALID, "%s: elem_offset + n overflows", where);
+    else if (d.n > 0 && p->offload && (!d.theta0_host || (d.theta0 && d.theta0 != d.out)))
+      st = fail(SMAT_ERR_INVALID, "%s: offload mode needs theta0_host and theta0 == NULL or == out", where);
+    else if (d.n > 0 && !p->offload && d.theta0_host)
+      st = fail(SMAT_ERR_INVALID, "%s: theta0_host is only used in offload mode", where);
+    else if (d.n > 0)
+      st = check_simulate_ptrs(d.theta, p->offload ? d.out : d.theta0, theta0_dtype, d.out, out_dtype, d.n, where);
+    if (st == SMAT_OK && d.n > 0) {
+      if (!d.grad_sim || !d.grad_theta) {
+        if (d.grad_sim || d.grad_theta) st = fail(SMAT_ERR_INVALID, "%s: give both gradient pointers or neither", where);
+        p->has_grads = false;
+      } else if (overlap(d.grad_sim, (size_t)d.n * dtype_bytes(grad_dtype), d.grad_theta, (size_t)d.n * 4)) {
+        st = fail(SMAT_ERR_INVALID, "%s: grad_sim must not overlap grad_theta", where);
+      }
+    }
+    if (st != SMAT_OK) {
+      delete p;
+      return st;
+    }
+    if (d.n > 0) ranges.push_back({d.tensor_id, {d.elem_offset, d.elem_offset + (uint64_t)d.n}});
+  }
+  // the same tensor_id may appear for disjoint shards of one tensor, never for overlapping ranges
+  // (they would reuse the same draws); with ranges sorted by start, any overlap shows between neighbours
+  std::sort(ranges.begin(), ranges.end());
+  for (size_t i = 1; i < ranges.size(); ++i) {
+    if (ranges[i].first == ranges[i - 1].first && ranges[i].second.first < ranges[i - 1].second.second) {
+      delete p;
+      return fail(SMAT_ERR_INVALID, "smat_plan_create: tensor_id %u given twice for overlapping elements",
+                  ranges[i].first);
+    }
+  }
+
+  p->recs.resize(count);
+  p->expert_ptrs.resize(count);
+  p->sim_ptrs.resize(count);
+  uint64_t nchunks = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const smat_tensor_desc& d = p->descs[i];
+    TensorRec& r = p->recs[i];
+    r.theta = d.theta;
+    r.theta0 = p->offload ? d.out : d.theta0;
+    r.out = d.out;
+    r.grad_sim = d.grad_sim;
+    r.grad_theta = d.grad_theta;
+    r.n = d.n;
+    r.elem_offset = d.elem_offset;
+    r.tensor_id = d.tensor_id;
+    if (d.n > 0) {
+      r.sflags = sim_flags(r.theta, r.theta0, theta0_dtype, r.out, out_dtype, d.elem_offset);
+      if (d.grad_sim && d.grad_theta) r.sflags |= bwd_flags(d.grad_sim, grad_dtype, d.grad_theta, d.elem_offset);
+    }
+    p->expert_ptrs[i] = const_cast<float*>(d.theta);
+    p->sim_ptrs[i] = d.out;
+    nchunks += (uint64_t)((d.n + smat::kChunk - 1) / smat::kChunk);
+  }
+  if (nchunks > 0x7FFFFFFFull) {
+    delete p;
+    return fail(SMAT_ERR_INVALID, "smat_plan_create: tensor list too large for one launch");
+  }
+  p->chunks.reserve(nchunks);
+  for (int32_t i = 0; i < count; ++i) {
+    const uint32_t nc = (uint32_t)((p->descs[i].n + smat::kChunk - 1) / smat::kChunk);
+    for (uint32_t c = 0; c < nc; ++c) p->chunks.push_back(make_uint2((uint32_t)i, c));
+  }
+
+  size_t off = 0;
+  p->off_recs = off;
+  off = align256(off + sizeof(TensorRec) * count);
+  p->off_chunks = off;
+  off = align256(off + sizeof(uint2) * p->chunks.size());
+  p->off_active = off;
+  off = align256(off + sizeof(void*) * count);
+  p->off_expert = off;
+  off = align256(off + sizeof(void*) * count);
+  p->off_sim = off;
+  off = align256(off + sizeof(void*) * count);
+  p->off_params = off;
+  off = align256(off + sizeof(ParamRec) * count);
+  p->ws_bytes = std::max<size_t>(off, 256);
+  *out_plan = p;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_plan_workspace_bytes(const smat_plan* plan, size_t* bytes) {
+  if (!plan || !bytes) return fail(SMAT_ERR_INVALID, "smat_plan_workspace_bytes: null argument");
+  *bytes = plan->ws_bytes;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_plan_bind_workspace(smat_plan* p, void* workspace, size_t bytes, hipStream_t stream) {
+  if (!p || !workspace) return fail(SMAT_ERR_INVALID, "smat_plan_bind_workspace: null argument");
+  if (p->ws) return fail(SMAT_ERR_STATE, "smat_plan_bind_workspace: workspace already bound");
+  if (!aligned(workspace, 256)) return fail(SMAT_ERR_INVALID, "smat_plan_bind_workspace: workspace not 256-byte aligned");
+  if (bytes < p->ws_bytes)
+    return fail(SMAT_ERR_INVALID, "smat_plan_bind_workspace: workspace of %zu bytes, need %zu", bytes, p->ws_bytes);
+
+  const size_t static_bytes = p->off_params;
+  SMAT_HIP(hipHostMalloc((void**)&p->static_staging, std::max<size_t>(static_bytes, 256), hipHostMallocDefault));
+  for (ParamRec*& s : p->params_staging)
+    SMAT_HIP(hipHostMalloc((void**)&s, sizeof(ParamRec) * std::max(p->count, 1), hipHostMallocDefault));
+  std::memset(p->static_staging, 0, static_bytes);
+  std::memcpy(p->static_staging + p->off_recs, p->recs.data(), sizeof(TensorRec) * p->count);
+  std::memcpy(p->static_staging + p->off_chunks, p->chunks.data(), sizeof(uint2) * p->chunks.size());
+  std::memcpy(p->static_staging + p->off_active, p->expert_ptrs.data(), sizeof(void*) * p->count);
+  std::memcpy(p->static_staging + p->off_expert, p->expert_ptrs.data(), sizeof(void*) * p->count);
+  std::memcpy(p->static_staging + p->off_sim, p->sim_ptrs.data(), sizeof(void*) * p->count);
+  SMAT_HIP(hipEventCreateWithFlags(&p->ev_static, hipEventDisableTiming));
+  for (hipEvent_t& e : p->ev_params) SMAT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  if (static_bytes > 0)
+    SMAT_HIP(hipMemcpyAsync(workspace, p->static_staging, static_bytes, hipMemcpyHostToDevice, stream));
+  SMAT_HIP(hipEventRecord(p->ev_static, stream));
+  p->ws = static_cast<char*>(workspace);
+  if (p->offload) {
+    SMAT_HIP(hipStreamCreateWithFlags(&p->copy_stream, hipStreamNonBlocking));
+    SMAT_HIP(hipEventCreateWithFlags(&p->ev_release, hipEventDisableTiming));
+    SMAT_HIP(hipEventCreateWithFlags(&p->ev_prefetch, hipEventDisableTiming));
+    smat_status st = enqueue_prefetch(p, stream);
+    if (st != SMAT_OK) return st;
+  }
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_plan_set_params(smat_plan* p, const smat_op_params* per_tensor, hipStream_t stream) {
+  if (!p || (p->count > 0 && !per_tensor)) return fail(SMAT_ERR_INVALID, "smat_plan_set_params: null argument");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_set_params: no workspace bound");
+  std::vector<ParamRec> recs(p->count);
+  for (int32_t i = 0; i < p->count; ++i) {
+    char where[64];
+    std::snprintf(where, sizeof(where), "smat_plan_set_params: tensor %d", i);
+    smat_status st = make_param(per_tensor[i], &recs[i], where);
+    if (st != SMAT_OK) return st;
+  }
+  const int slot = p->params_slot;
+  if (p->params_pending[slot]) SMAT_HIP(hipEventSynchronize(p->ev_params[slot]));  // slot still being read
+  std::memcpy(p->params_staging[slot], recs.data(), sizeof(ParamRec) * p->count);
+  if (p->count > 0)
+    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_params, p->params_staging[slot], sizeof(ParamRec) * p->count,
+                            hipMemcpyHostToDevice, stream));
+  SMAT_HIP(hipEventRecord(p->ev_params[slot], stream));
+  p->params_pending[slot] = true;
+  p->params_slot = slot ^ 1;
+  p->params_set = true;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_simulate_multi(smat_plan* p, uint64_t seed, uint32_t step, hipStream_t stream) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_simulate_multi: null plan");
+  if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_simulate_multi: step must be < 2^30");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_simulate_multi: no workspace bound");
+  if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_simulate_multi: parameters never set");
+  if (p->state != SMAT_EXPERT)
+    return fail(SMAT_ERR_STATE, "smat_simulate_multi: the simulated storage is active (restore the expert first)");
+  if (p->offload && p->prefetch_pending) SMAT_HIP(hipStreamWaitEvent(stream, p->ev_prefetch, 0));
+  if (!p->chunks.empty())
+    SMAT_HIP(smat::launch_simulate_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                         reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                         reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
+                                         (uint32_t)p->chunks.size(), p->t0_dt, p->out_dt, seed, step, stream));
+  p->fresh = true;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_backward_accum_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
+                                                 hipStream_t stream) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: null plan");
+  if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: step must be < 2^30");
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: lambda must be finite");
+  if (!p->has_grads) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: plan has no gradient pointers");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: no workspace bound");
+  if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: parameters never set");
+  if (!p->chunks.empty())
+    SMAT_HIP(smat::launch_backward_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                         reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                         reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
+                                         (uint32_t)p->chunks.size(), p->g_dt, lambda, seed, step, stream));
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_switch_storage(smat_plan* p, int32_t to, hipStream_t stream) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_switch_storage: null plan");
+  if (to != SMAT_EXPERT && to != SMAT_SIMULATED) return fail(SMAT_ERR_INVALID, "smat_switch_storage: bad target %d", to);
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_switch_storage: no workspace bound");
+  const size_t table = sizeof(void*) * p->count;
+  if (to == SMAT_SIMULATED) {
+    if (p->state == SMAT_SIMULATED) return fail(SMAT_ERR_STATE, "smat_switch_storage: simulated storage already active");
+    if (!p->fresh) return fail(SMAT_ERR_STATE, "smat_switch_storage: no simulate since the last restore");
+    if (table) SMAT_HIP(hipMemcpyAsync(p->ws + p->off_active, p->ws + p->off_sim, table, hipMemcpyDeviceToDevice, stream));
+    p->state = SMAT_SIMULATED;
+    return SMAT_OK;
+  }
+  if (p->state == SMAT_EXPERT) return SMAT_OK;  // restoring is idempotent
+  if (table) SMAT_HIP(hipMemcpyAsync(p->ws + p->off_active, p->ws + p->off_expert, table, hipMemcpyDeviceToDevice, stream));
+  p->state = SMAT_EXPERT;
+  p->fresh = false;
+  if (p->offload) return enqueue_prefetch(p, stream);
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_plan_state(const smat_plan* p, int32_t* state) {
+  if (!p || !state) return fail(SMAT_ERR_INVALID, "smat_plan_state: null argument");
+  *state = p->state;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_plan_active_ptrs(const smat_plan* p, void** host_out, void** dev_table) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_plan_active_ptrs: null plan");
+  if (host_out) {
+    const std::vector<void*>& src = p->state == SMAT_SIMULATED ? p->sim_ptrs : p->expert_ptrs;
+    std::copy(src.begin(), src.end(), host_out);
+  }
+  if (dev_table) *dev_table = p->ws ? p->ws + p->off_active : nullptr;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_plan_destroy(smat_plan* p) {
+  if (!p) return SMAT_OK;
+  return release(p);
+}
+
+extern "C" const char* smat_last_error(void) { return g_last_error.c_str(); }

@@ -1,0 +1,219 @@
+// Device-side building blocks of the SMAT transform for gfx950, plus the
+// per-tensor records that the host API uploads and the kernels read.
+//
+// Random words: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11).  Key =
+// 64-bit seed, counter = (g_lo, g_hi, tensor_id, 4*step + stream) for the
+// 4-element group g = e >> 2 of global element e.  The kernels work on such
+// groups ("quads"), so one Philox call feeds four elements.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace smat {
+
+// ---------------------------------------------------------------- records
+// Per-step flags of a tensor (ParamRec::flags).
+enum : uint32_t {
+  kFlagMask = 1u,     // draw the mask: kept iff word < thr
+  kFlagDropAll = 2u,  // keep == 0: every coordinate dropped, no draw
+  kFlagNoise = 4u,    // sigma > 0: draw the noise
+  kFlagUniform = 8u,  // uniform noise instead of Gaussian
+};
+// Static flags of a tensor (TensorRec::sflags): pointers aligned for quad vectors and
+// elem_offset a multiple of 4, so quads line up with Philox groups.
+enum : uint32_t { kVecSim = 1u, kVecBwd = 2u };
+
+struct alignas(16) TensorRec {
+  const float* theta;
+  const void* theta0;
+  void* out;
+  const void* grad_sim;
+  float* grad_theta;
+  int64_t n;
+  uint64_t elem_offset;
+  uint32_t tensor_id;
+  uint32_t sflags;
+};
+static_assert(sizeof(TensorRec) == 64, "TensorRec layout");
+
+struct alignas(16) ParamRec {
+  uint32_t thr;   // floor(keep * 2^32) when kFlagMask
+  float t;        // coefficient of the task vector for kept coordinates: s/keep or s
+  float sigma;    // noise RMS
+  uint32_t flags;
+};
+static_assert(sizeof(ParamRec) == 16, "ParamRec layout");
+
+// Work decomposition: a block of kBlock threads handles one chunk of kChunk elements of one
+// tensor; each thread handles kUnroll quads per iteration.
+constexpr int kBlock = 256;
+constexpr int kUnroll = 2;
+constexpr int kIters = 8;
+constexpr int64_t kChunk = (int64_t)kBlock * 4 * kUnroll * kIters;  // 16384 elements
+
+constexpr uint32_t kStreamMask = 0u;
+constexpr uint32_t kStreamNoise = 1u;
+
+// ---------------------------------------------------------------- Philox4x32-10
+struct Words {
+  uint32_t w0, w1, w2, w3;
+};
+
+// a ^ b ^ key in one VALU op: gfx950's three-input bitwise op with truth table 0x96 (xor3).
+// The key is wave-uniform and rides in an SGPR.
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t key) {
+  uint32_t r;
+  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(key));
+  return r;
+}
+
+__device__ __forceinline__ Words philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                               uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)c0 * 0xD2511F53u;
+    const uint64_t p1 = (uint64_t)c2 * 0xCD9E8D57u;
+    const uint32_t n0 = xor3((uint32_t)(p1 >> 32), c1, k0);
+    const uint32_t n2 = xor3((uint32_t)(p0 >> 32), c3, k1);
+    c0 = n0;
+    c1 = (uint32_t)p1;
+    c2 = n2;
+    c3 = (uint32_t)p0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return {c0, c1, c2, c3};
+}
+
+// Words of group g of a tensor in one stream.
+__device__ __forceinline__ Words group_words(uint64_t g, uint32_t tensor_id, uint32_t c3, uint32_t k0,
+                                             uint32_t k1) {
+  return philox4x32_10((uint32_t)g, (uint32_t)(g >> 32), tensor_id, c3, k0, k1);
+}
+
+__device__ __forceinline__ uint32_t pick(const Words& w, uint32_t lane) {
+  const uint32_t lo = (lane & 1u) ? w.w1 : w.w0;
+  const uint32_t hi = (lane & 1u) ? w.w3 : w.w2;
+  return (lane & 2u) ? hi : lo;
+}
+
+// ---------------------------------------------------------------- noise
+// Box-Muller on 24-bit uniforms: u1 = ((a >> 8) + 1) 2^-24 in (0, 1], u2 = (b >> 8) 2^-24 in [0, 1).
+// r = sqrt(-2 ln u1) with the hardware log2; cos/sin take revolutions (v_cos_f32/v_sin_f32 compute
+// cos/sin of 2*pi*x), so 2*pi*u2 never has to be formed.
+__device__ __forceinline__ void box_muller(uint32_t a, uint32_t b, float& zc, float& zs) {
+  const float u1 = (float)((a >> 8) + 1u) * 0x1p-24f;
+  const float u2 = (float)(b >> 8) * 0x1p-24f;
+  const float r = __builtin_amdgcn_sqrtf(-1.38629436111989061883f * __builtin_amdgcn_logf(u1));
+  zc = r * __builtin_amdgcn_cosf(u2);
+  zs = r * __builtin_amdgcn_sinf(u2);
+}
+
+// Unit-variance uniform value sqrt(3) (2u - 1), u = ((w >> 8) + 1/2) 2^-24.  The odd integer
+// 2 (w >> 8) + 1 - 2^24 is exact in fp32, so 2u - 1 is formed without rounding.
+__device__ __forceinline__ float uniform_unit(uint32_t w) {
+  const int32_t k = (int32_t)((w >> 8) << 1) + 1 - (1 << 24);
+  return 1.73205080756887729353f * ((float)k * 0x1p-24f);
+}
+
+// The four unit noise values of a quad.
+__device__ __forceinline__ void quad_noise(const Words& w, bool uniform, float z[4]) {
+  if (uniform) {
+    z[0] = uniform_unit(w.w0);
+    z[1] = uniform_unit(w.w1);
+    z[2] = uniform_unit(w.w2);
+    z[3] = uniform_unit(w.w3);
+  } else {
+    box_muller(w.w0, w.w1, z[0], z[1]);
+    box_muller(w.w2, w.w3, z[2], z[3]);
+  }
+}
+
+// The unit noise value of lane `lane` of a quad, computed exactly as quad_noise does.
+__device__ __forceinline__ float lane_noise(const Words& w, uint32_t lane, bool uniform) {
+  if (uniform) return uniform_unit(pick(w, lane));
+  float zc, zs;
+  if (lane & 2u)
+    box_muller(w.w2, w.w3, zc, zs);
+  else
+    box_muller(w.w0, w.w1, zc, zs);
+  return (lane & 1u) ? zs : zc;
+}
+
+// ---------------------------------------------------------------- element arithmetic
+// theta~ before noise: the exact-endpoint lerp theta0 + t (theta - theta0) for kept coordinates
+// (t = 0 gives theta0, t = 1 gives theta bit for bit), theta0 for dropped ones.
+__device__ __forceinline__ float sim_value(float th, float b, bool kept, float t) {
+  return kept ? __builtin_fmaf(t, th, __builtin_fmaf(-t, b, b)) : b;
+}
+
+// ---------------------------------------------------------------- memory
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+struct Bf16 {};  // storage tag: bfloat16 stored as 16-bit words
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 v = {(__bf16)a, (__bf16)b};  // v_cvt_pk_bf16_f32: round to nearest even
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ uint16_t to_bf16(float a) { return __builtin_bit_cast(uint16_t, (__bf16)a); }
+
+// Global-address-space views of the tensors.  Pointers read from the record table are generic;
+// naming the global space lets the compiler emit global_load/store with an SGPR base instead of
+// flat accesses.
+#define SMAT_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ const SMAT_GLOBAL T* gload_ptr(const void* p) {
+  return (const SMAT_GLOBAL T*)p;
+}
+template <typename T>
+__device__ __forceinline__ SMAT_GLOBAL T* gstore_ptr(void* p) {
+  return (SMAT_GLOBAL T*)p;
+}
+
+// Streaming (nontemporal) quad loads/stores: every byte is touched once per pass.
+template <typename T>
+struct QuadIO;
+
+template <>
+struct QuadIO<float> {
+  static __device__ __forceinline__ void load(const void* base, uint32_t q, float v[4]) {
+    const f32x4 x = __builtin_nontemporal_load(gload_ptr<f32x4>(base) + q);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  }
+  static __device__ __forceinline__ void store(void* base, uint32_t q, const float v[4]) {
+    const f32x4 x = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(x, gstore_ptr<f32x4>(base) + q);
+  }
+  static __device__ __forceinline__ float load1(const void* base, uint32_t i) { return gload_ptr<float>(base)[i]; }
+  static __device__ __forceinline__ void store1(void* base, uint32_t i, float v) { gstore_ptr<float>(base)[i] = v; }
+};
+
+template <>
+struct QuadIO<Bf16> {
+  static __device__ __forceinline__ void load(const void* base, uint32_t q, float v[4]) {
+    const u32x2 x = __builtin_nontemporal_load(gload_ptr<u32x2>(base) + q);
+    v[0] = bf16_to_f32(x.x & 0xFFFFu);
+    v[1] = __uint_as_float(x.x & 0xFFFF0000u);
+    v[2] = bf16_to_f32(x.y & 0xFFFFu);
+    v[3] = __uint_as_float(x.y & 0xFFFF0000u);
+  }
+  static __device__ __forceinline__ void store(void* base, uint32_t q, const float v[4]) {
+    const u32x2 x = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+    __builtin_nontemporal_store(x, gstore_ptr<u32x2>(base) + q);
+  }
+  static __device__ __forceinline__ float load1(const void* base, uint32_t i) {
+    return bf16_to_f32(gload_ptr<uint16_t>(base)[i]);
+  }
+  static __device__ __forceinline__ void store1(void* base, uint32_t i, float v) {
+    gstore_ptr<uint16_t>(base)[i] = to_bf16(v);
+  }
+};
+
+}  // namespace smat

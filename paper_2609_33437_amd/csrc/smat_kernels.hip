@@ -1,0 +1,297 @@
+// HIP kernels of the SMAT per-step transform for gfx950.
+//
+// simulate:  theta~ = theta0 + t m (theta - theta0) + sigma z      (Sec. 4.1, Eq. smat-state/smat-mask)
+// backward:  grad_theta += lambda t m g~ on kept coordinates       (Sec. 4.2, Eq. smat-gradient)
+//
+// Both are purely HBM-bound streams (no contraction, so no MFMA).  The unit of work is a quad
+// of 4 consecutive elements = one Philox group, so a thread draws one 128-bit Philox output per
+// stream per quad and never stores a draw.  Consecutive lanes take consecutive quads, so every
+// load/store instruction of a wave covers one contiguous span (16 B per lane for fp32, 8 B per
+// lane for bf16), issued as nontemporal streaming accesses.  A block walks one chunk of
+// kChunk elements of one tensor; the ragged-list kernels find their (tensor, chunk) pair in a
+// table built once per tensor list, so huge matrices and tiny vectors share one launch.
+#include "smat_launch.h"
+
+namespace smat {
+
+template <typename T>
+struct StorageBytes;
+template <>
+struct StorageBytes<float> {
+  static constexpr int value = 4;
+};
+template <>
+struct StorageBytes<Bf16> {
+  static constexpr int value = 2;
+};
+
+// ---------------------------------------------------------------- simulate
+template <typename T0, typename TO>
+__device__ __forceinline__ void simulate_range(const TensorRec& R, const ParamRec& P, int64_t begin, int64_t end,
+                                               uint64_t seed, uint32_t step) {
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  const uint32_t cmask = (step << 2) | kStreamMask;
+  const uint32_t cnoise = (step << 2) | kStreamNoise;
+  const uint32_t tensor_id = R.tensor_id;
+  const uint32_t flags = P.flags;
+  const bool use_mask = (flags & kFlagMask) != 0;
+  const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
+  const bool use_noise = (flags & kFlagNoise) != 0;
+  const bool uniform = (flags & kFlagUniform) != 0;
+  const float t = P.t, sigma = P.sigma;
+  const uint32_t thr = P.thr;
+
+  const uint32_t len = (uint32_t)(end - begin);
+  const float* th = R.theta + begin;
+  const void* t0 = static_cast<const char*>(R.theta0) + begin * StorageBytes<T0>::value;
+  void* out = static_cast<char*>(R.out) + begin * StorageBytes<TO>::value;
+  const uint64_t e0 = R.elem_offset + (uint64_t)begin;
+
+  // one element by itself: ragged tails and tensors whose pointers or offset break quad alignment
+  auto one = [&](uint32_t i) {
+    const uint64_t e = e0 + i;
+    const uint64_t g = e >> 2;
+    const uint32_t lane = (uint32_t)e & 3u;
+    bool kept = all_kept;
+    if (use_mask) kept = pick(group_words(g, tensor_id, cmask, k0, k1), lane) < thr;
+    float y = sim_value(QuadIO<float>::load1(th, i), QuadIO<T0>::load1(t0, i), kept, t);
+    if (use_noise) y = __builtin_fmaf(sigma, lane_noise(group_words(g, tensor_id, cnoise, k0, k1), lane, uniform), y);
+    QuadIO<TO>::store1(out, i, y);
+  };
+
+  if (R.sflags & kVecSim) {
+    const uint64_t g0 = e0 >> 2;  // e0 is a multiple of 4 here
+    const uint32_t nq = len >> 2;
+    for (uint32_t q0 = threadIdx.x; q0 < nq; q0 += kBlock * kUnroll) {
+      float a[kUnroll][4], b[kUnroll][4];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t q = q0 + u * kBlock;
+        if (q < nq) {
+          QuadIO<float>::load(th, q, a[u]);
+          QuadIO<T0>::load(t0, q, b[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t q = q0 + u * kBlock;
+        if (q < nq) {
+          const uint64_t g = g0 + q;
+          bool kept[4] = {all_kept, all_kept, all_kept, all_kept};
+          if (use_mask) {
+            const Words w = group_words(g, tensor_id, cmask, k0, k1);
+            kept[0] = w.w0 < thr;
+            kept[1] = w.w1 < thr;
+            kept[2] = w.w2 < thr;
+            kept[3] = w.w3 < thr;
+          }
+          float y[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) y[j] = sim_value(a[u][j], b[u][j], kept[j], t);
+          if (use_noise) {
+            float z[4];
+            quad_noise(group_words(g, tensor_id, cnoise, k0, k1), uniform, z);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) y[j] = __builtin_fmaf(sigma, z[j], y[j]);
+          }
+          QuadIO<TO>::store(out, q, y);
+        }
+      }
+    }
+    const uint32_t done = nq << 2;
+    if (threadIdx.x < len - done) one(done + threadIdx.x);
+  } else {
+    for (uint32_t i = threadIdx.x; i < len; i += kBlock) one(i);
+  }
+}
+
+// ---------------------------------------------------------------- backward
+template <typename TG>
+__device__ __forceinline__ void backward_range(const TensorRec& R, const ParamRec& P, int64_t begin, int64_t end,
+                                               uint64_t seed, uint32_t step, float lambda) {
+  const uint32_t flags = P.flags;
+  if (flags & kFlagDropAll) return;  // every coordinate dropped: the gradient is left as it is
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  const uint32_t cmask = (step << 2) | kStreamMask;
+  const uint32_t tensor_id = R.tensor_id;
+  const bool use_mask = (flags & kFlagMask) != 0;
+  const uint32_t thr = P.thr;
+  const float c = lambda * P.t;
+
+  const uint32_t len = (uint32_t)(end - begin);
+  const void* gs = static_cast<const char*>(R.grad_sim) + begin * StorageBytes<TG>::value;
+  float* gt = R.grad_theta + begin;
+  const uint64_t e0 = R.elem_offset + (uint64_t)begin;
+
+  auto one = [&](uint32_t i) {
+    const uint64_t e = e0 + i;
+    bool kept = true;
+    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
+    if (kept) QuadIO<float>::store1(gt, i, __builtin_fmaf(c, QuadIO<TG>::load1(gs, i), QuadIO<float>::load1(gt, i)));
+  };
+
+  if (R.sflags & kVecBwd) {
+    const uint64_t g0 = e0 >> 2;
+    const uint32_t nq = len >> 2;
+    for (uint32_t q0 = threadIdx.x; q0 < nq; q0 += kBlock * kUnroll) {
+      float a[kUnroll][4], b[kUnroll][4];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t q = q0 + u * kBlock;
+        if (q < nq) {
+          QuadIO<TG>::load(gs, q, a[u]);
+          QuadIO<float>::load(gt, q, b[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t q = q0 + u * kBlock;
+        if (q < nq) {
+          bool kept[4] = {true, true, true, true};
+          if (use_mask) {
+            const Words w = group_words(g0 + q, tensor_id, cmask, k0, k1);
+            kept[0] = w.w0 < thr;
+            kept[1] = w.w1 < thr;
+            kept[2] = w.w2 < thr;
+            kept[3] = w.w3 < thr;
+          }
+          float o[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[j] = kept[j] ? __builtin_fmaf(c, a[u][j], b[u][j]) : b[u][j];
+          QuadIO<float>::store(gt, q, o);
+        }
+      }
+    }
+    const uint32_t done = nq << 2;
+    if (threadIdx.x < len - done) one(done + threadIdx.x);
+  } else {
+    for (uint32_t i = threadIdx.x; i < len; i += kBlock) one(i);
+  }
+}
+
+// ---------------------------------------------------------------- kernels
+template <typename T0, typename TO>
+__global__ __launch_bounds__(kBlock) void k_simulate_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step) {
+  const int64_t begin = (int64_t)blockIdx.x * kChunk;
+  const int64_t end = begin + kChunk < R.n ? begin + kChunk : R.n;
+  simulate_range<T0, TO>(R, P, begin, end, seed, step);
+}
+
+template <typename TG>
+__global__ __launch_bounds__(kBlock) void k_backward_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step,
+                                                         float lambda) {
+  const int64_t begin = (int64_t)blockIdx.x * kChunk;
+  const int64_t end = begin + kChunk < R.n ? begin + kChunk : R.n;
+  backward_range<TG>(R, P, begin, end, seed, step, lambda);
+}
+
+template <typename T0, typename TO>
+__global__ __launch_bounds__(kBlock) void k_simulate_multi(const TensorRec* __restrict__ recs,
+                                                           const ParamRec* __restrict__ prms,
+                                                           const uint2* __restrict__ chunks, uint64_t seed,
+                                                           uint32_t step) {
+  const uint2 ch = chunks[blockIdx.x];  // (tensor index, chunk index within the tensor)
+  const TensorRec R = recs[ch.x];
+  const ParamRec P = prms[ch.x];
+  const int64_t begin = (int64_t)ch.y * kChunk;
+  const int64_t end = begin + kChunk < R.n ? begin + kChunk : R.n;
+  simulate_range<T0, TO>(R, P, begin, end, seed, step);
+}
+
+template <typename TG>
+__global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __restrict__ recs,
+                                                           const ParamRec* __restrict__ prms,
+                                                           const uint2* __restrict__ chunks, uint64_t seed,
+                                                           uint32_t step, float lambda) {
+  const uint2 ch = chunks[blockIdx.x];
+  const TensorRec R = recs[ch.x];
+  const ParamRec P = prms[ch.x];
+  const int64_t begin = (int64_t)ch.y * kChunk;
+  const int64_t end = begin + kChunk < R.n ? begin + kChunk : R.n;
+  backward_range<TG>(R, P, begin, end, seed, step, lambda);
+}
+
+__global__ __launch_bounds__(kBlock) void k_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id,
+                                                        uint64_t elem_offset, int64_t n, ParamRec P,
+                                                        uint32_t* mask_words, uint32_t* noise_words,
+                                                        uint8_t* kept, float* z) {
+  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  const uint64_t e = elem_offset + (uint64_t)i;
+  const uint32_t lane = (uint32_t)e & 3u;
+  const Words wm = group_words(e >> 2, tensor_id, (step << 2) | kStreamMask, k0, k1);
+  const Words wn = group_words(e >> 2, tensor_id, (step << 2) | kStreamNoise, k0, k1);
+  if (mask_words) mask_words[i] = pick(wm, lane);
+  if (noise_words) noise_words[i] = pick(wn, lane);
+  if (kept) {
+    bool k = (P.flags & (kFlagMask | kFlagDropAll)) == 0;
+    if (P.flags & kFlagMask) k = pick(wm, lane) < P.thr;
+    kept[i] = k ? 1 : 0;
+  }
+  if (z) z[i] = lane_noise(wn, lane, false);
+}
+
+// ---------------------------------------------------------------- launchers
+static inline uint32_t blocks_for(int64_t n, int64_t per_block) { return (uint32_t)((n + per_block - 1) / per_block); }
+
+hipError_t launch_simulate_one(const TensorRec& rec, const ParamRec& prm, int theta0_dtype, int out_dtype,
+                               uint64_t seed, uint32_t step, hipStream_t stream) {
+  const dim3 grid(blocks_for(rec.n, kChunk)), block(kBlock);
+  if (theta0_dtype == 1 && out_dtype == 1)
+    k_simulate_one<Bf16, Bf16><<<grid, block, 0, stream>>>(rec, prm, seed, step);
+  else if (theta0_dtype == 1 && out_dtype == 0)
+    k_simulate_one<Bf16, float><<<grid, block, 0, stream>>>(rec, prm, seed, step);
+  else if (theta0_dtype == 0 && out_dtype == 1)
+    k_simulate_one<float, Bf16><<<grid, block, 0, stream>>>(rec, prm, seed, step);
+  else
+    k_simulate_one<float, float><<<grid, block, 0, stream>>>(rec, prm, seed, step);
+  return hipGetLastError();
+}
+
+hipError_t launch_backward_one(const TensorRec& rec, const ParamRec& prm, int grad_dtype, float lambda,
+                               uint64_t seed, uint32_t step, hipStream_t stream) {
+  const dim3 grid(blocks_for(rec.n, kChunk)), block(kBlock);
+  if (grad_dtype == 1)
+    k_backward_one<Bf16><<<grid, block, 0, stream>>>(rec, prm, seed, step, lambda);
+  else
+    k_backward_one<float><<<grid, block, 0, stream>>>(rec, prm, seed, step, lambda);
+  return hipGetLastError();
+}
+
+hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks,
+                                 uint32_t nchunks, int theta0_dtype, int out_dtype, uint64_t seed,
+                                 uint32_t step, hipStream_t stream) {
+  const dim3 grid(nchunks), block(kBlock);
+  if (theta0_dtype == 1 && out_dtype == 1)
+    k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
+  else if (theta0_dtype == 1 && out_dtype == 0)
+    k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
+  else if (theta0_dtype == 0 && out_dtype == 1)
+    k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
+  else
+    k_simulate_multi<float, float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
+  return hipGetLastError();
+}
+
+hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks,
+                                 uint32_t nchunks, int grad_dtype, float lambda, uint64_t seed,
+                                 uint32_t step, hipStream_t stream) {
+  const dim3 grid(nchunks), block(kBlock);
+  if (grad_dtype == 1)
+    k_backward_multi<Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+  else
+    k_backward_multi<float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+  return hipGetLastError();
+}
+
+hipError_t launch_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t elem_offset,
+                              int64_t n, const ParamRec& prm, uint32_t* mask_words, uint32_t* noise_words,
+                              uint8_t* kept, float* z, hipStream_t stream) {
+  const dim3 grid(blocks_for(n, kBlock)), block(kBlock);
+  k_debug_draws<<<grid, block, 0, stream>>>(seed, step, tensor_id, elem_offset, n, prm, mask_words, noise_words,
+                                            kept, z);
+  return hipGetLastError();
+}
+
+}  // namespace smat

@@ -1,0 +1,145 @@
+"""The C ABI library loads on the CPU, exports every function include/smat.h declares, and the
+Python binding's structs match the C layout.  Only host-side argument checks are called here:
+they return before any HIP call, so no GPU is needed."""
+import ctypes
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+import paper_2609_33437_amd as smat
+from paper_2609_33437_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "smat.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:smat_status|const char\*)\s+(smat_[a-z_]+)\(", text, re.M)))
+
+
+def test_header_declares_the_binding_exports():
+    assert _declared() == sorted(_lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    for name in _declared():
+        assert hasattr(lib, name), name
+    res = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True)
+    if res.returncode == 0:
+        exported = set(re.findall(r" T (smat_[a-z_]+)$", res.stdout, re.M))
+        assert exported == set(_declared())
+
+
+def test_struct_layout_matches_c(tmp_path):
+    gcc = shutil.which("gcc")
+    if gcc is None or not os.path.exists("/opt/rocm/include/hip/hip_runtime_api.h"):
+        pytest.skip("gcc or HIP headers missing")
+    src = tmp_path / "layout.c"
+    src.write_text("""
+#include <stdio.h>
+#include <stddef.h>
+#include "smat.h"
+int main(void) {
+  printf("%zu %zu %zu\\n", sizeof(smat_op_params), sizeof(smat_rng_key), sizeof(smat_tensor_desc));
+  printf("%zu %zu %zu %zu\\n", offsetof(smat_tensor_desc, n), offsetof(smat_tensor_desc, tensor_id),
+         offsetof(smat_tensor_desc, elem_offset), offsetof(smat_rng_key, elem_offset));
+  return 0;
+}
+""")
+    exe = tmp_path / "layout"
+    subprocess.run([gcc, "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+                    str(src), "-o", str(exe)], check=True, capture_output=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()
+    want = [ctypes.sizeof(_lib.smat_op_params), ctypes.sizeof(_lib.smat_rng_key), ctypes.sizeof(_lib.smat_tensor_desc),
+            _lib.smat_tensor_desc.n.offset, _lib.smat_tensor_desc.tensor_id.offset,
+            _lib.smat_tensor_desc.elem_offset.offset, _lib.smat_rng_key.elem_offset.offset]
+    assert [int(x) for x in out] == want
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+@pytest.mark.parametrize("bad", [dict(keep=1.5), dict(keep=-0.5), dict(sigma=-1.0), dict(sigma=float("inf")),
+                                 dict(s=float("nan")), dict(noise_kind=9)])
+def test_invalid_params_rejected_before_launch(bad):
+    lib = smat.lib()
+    p = _lib.op_params(dict(dict(s=0.5, keep=0.5, sigma=1e-3), **bad))
+    key = _lib.rng_key(0, 0)
+    st = lib.smat_simulate(ctypes.c_void_p(16), ctypes.c_void_p(4096), 1, ctypes.c_void_p(8192), 1, 4, p, key, None)
+    assert st == _lib.SMAT_ERR_INVALID
+    assert lib.smat_last_error().decode()
+
+
+def test_argument_errors_without_gpu():
+    lib = smat.lib()
+    ok = _lib.op_params(dict(s=0.5, keep=0.5, sigma=1e-3))
+    key = _lib.rng_key(0, 0)
+    P = ctypes.c_void_p
+    # dtype, negative size, null pointers, step range, aliasing
+    assert lib.smat_simulate(P(16), P(4096), 7, P(8192), 1, 4, ok, key, None) == _lib.SMAT_ERR_DTYPE
+    assert lib.smat_simulate(P(16), P(4096), 1, P(8192), 1, -1, ok, key, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_simulate(None, P(4096), 1, P(8192), 1, 4, ok, key, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_simulate(P(16), P(4096), 1, P(8192), 1, 4, ok, _lib.rng_key(0, 1 << 30), None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_simulate(P(4096), P(65536), 1, P(4096), 1, 4, ok, key, None) == _lib.SMAT_ERR_INVALID  # out == theta
+    assert lib.smat_simulate(P(4096), P(65536), 1, P(65538), 1, 4, ok, key, None) == _lib.SMAT_ERR_INVALID  # partial overlap
+    assert lib.smat_simulate(P(4096), P(65536), 0, P(65536), 1, 4, ok, key, None) == _lib.SMAT_ERR_INVALID  # in place, dtypes differ
+    assert lib.smat_backward_accum(P(4096), 1, P(4100), 4, ok, 1.0, key, None) == _lib.SMAT_ERR_INVALID      # overlap
+    assert lib.smat_backward_accum(P(4096), 1, P(65536), 4, ok, float("nan"), key, None) == _lib.SMAT_ERR_INVALID
+    # n == 0 is a no-op even with null pointers
+    assert lib.smat_simulate(None, None, 1, None, 1, 0, ok, key, None) == _lib.SMAT_OK
+
+
+def _desc(theta, out, t0, gs, gt, n, tid, off=0, host=None):
+    d = _lib.smat_tensor_desc()
+    d.theta, d.out, d.theta0, d.grad_sim, d.grad_theta = theta, out, t0, gs, gt
+    d.theta0_host = host
+    d.n, d.tensor_id, d.elem_offset = n, tid, off
+    return d
+
+
+def test_plan_create_validation_without_gpu():
+    lib = smat.lib()
+    A = 1 << 20
+
+    def plan(descs, offload=0, dts=(1, 1, 1)):
+        arr = (_lib.smat_tensor_desc * len(descs))(*descs)
+        p = ctypes.c_void_p()
+        st = lib.smat_plan_create(arr, len(descs), dts[0], dts[1], dts[2], offload, ctypes.byref(p))
+        if st == _lib.SMAT_OK:
+            nb = ctypes.c_size_t()
+            assert lib.smat_plan_workspace_bytes(p, ctypes.byref(nb)) == 0 and nb.value % 256 == 0
+            s = ctypes.c_int32(-1)
+            assert lib.smat_plan_state(p, ctypes.byref(s)) == 0 and s.value == _lib.SMAT_EXPERT
+            assert lib.smat_plan_destroy(p) == 0
+        return st
+
+    good = [_desc(1 * A, 2 * A, 3 * A, 4 * A, 5 * A, 1000, 0), _desc(6 * A, 7 * A, 8 * A, 9 * A, 10 * A, 5, 1)]
+    assert plan(good) == _lib.SMAT_OK
+    # shards of one tensor may share a tensor id when their element ranges are disjoint
+    shards = [_desc(1 * A, 2 * A, 3 * A, 4 * A, 5 * A, 1000, 7, 0), _desc(6 * A, 7 * A, 8 * A, 9 * A, 10 * A, 5, 7, 1000)]
+    assert plan(shards) == _lib.SMAT_OK
+    overlapping = [_desc(1 * A, 2 * A, 3 * A, 4 * A, 5 * A, 1000, 7, 0), _desc(6 * A, 7 * A, 8 * A, 9 * A, 10 * A, 5, 7, 999)]
+    assert plan(overlapping) == _lib.SMAT_ERR_INVALID
+    assert plan([_desc(1 * A, 1 * A, 3 * A, None, None, 10, 0)]) == _lib.SMAT_ERR_INVALID        # out over theta
+    assert plan([_desc(1 * A, 2 * A, 3 * A, 4 * A, None, 10, 0)]) == _lib.SMAT_ERR_INVALID       # half the grads
+    assert plan(good, dts=(1, 1, 5)) == _lib.SMAT_ERR_DTYPE
+    assert plan(good, offload=1) == _lib.SMAT_ERR_INVALID                                         # no host copy
+    assert plan([_desc(1 * A, 2 * A, None, None, None, 10, 0, 0, 11 * A)], offload=1) == _lib.SMAT_OK
+    assert plan([_desc(1 * A, 2 * A, None, None, None, 10, 0, 0, 11 * A)], offload=1, dts=(0, 1, 1)) == _lib.SMAT_ERR_INVALID
+    # a plan without gradient pointers is valid for simulate-only use
+    assert plan([_desc(1 * A, 2 * A, 3 * A, None, None, 10, 0)]) == _lib.SMAT_OK
+    # calls on an unbound plan fail with a state error and never launch
+    arr = (_lib.smat_tensor_desc * 2)(*good)
+    p = ctypes.c_void_p()
+    assert lib.smat_plan_create(arr, 2, 1, 1, 1, 0, ctypes.byref(p)) == 0
+    assert lib.smat_simulate_multi(p, 0, 0, None) == _lib.SMAT_ERR_STATE
+    assert lib.smat_switch_storage(p, 1, None) == _lib.SMAT_ERR_STATE
+    assert lib.smat_switch_storage(p, 5, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_plan_destroy(p) == 0
+    assert lib.smat_plan_destroy(None) == 0

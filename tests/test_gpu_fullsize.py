@@ -1,0 +1,76 @@
+"""Full-size parity on the 125M-, 1.5B-, 7B- and VLM-shaped tensor lists, launched exactly as the
+benchmark launches them (one plan, one simulate and one backward launch over the whole list).
+The oracle checks sampled windows of every tensor: the first and last elements (ragged tail)
+and one random window, each computed from its global element index."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_33437_amd as smat
+import workloads
+from tolerances import check_grad, check_theta_tilde, ordered
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+W = 256
+
+
+def windows(n, rng):
+    if n <= 4 * W:
+        return [(0, n)]
+    r = int(rng.integers(W, n - 2 * W))
+    return [(0, W), (r, r + W), (n - W - 3, n)]
+
+
+def host(t):
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16), "bf16"
+    return t.numpy().copy(), "f32"
+
+
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
+def test_fullsize_sampled(name):
+    cfg = workloads.config(name)
+    print(f"[{name}] generating {cfg.count} tensors, {cfg.numel} params", flush=True)
+    inp = workloads.make_inputs(cfg, device=DEV)
+    outs = [torch.empty(t.numel(), dtype=torch.bfloat16, device=DEV) for t in inp.theta]
+    step = 3
+    params = workloads.step_params(cfg, inp.settings, step)
+    rng = np.random.default_rng(cfg.index)
+    wins = [windows(t.numel(), rng) for t in inp.theta]
+    # inputs of the sampled windows, taken before the kernels run
+    samples = []
+    for i, ws in enumerate(wins):
+        th, t0, gs, gt = (inp.theta[i].view(-1), inp.theta0[i].view(-1), inp.grad_sim[i].view(-1),
+                          inp.grad_theta[i].view(-1))
+        samples.append([(a, b, host(th[a:b])[0], host(t0[a:b])[0], host(gs[a:b])[0], host(gt[a:b])[0])
+                        for a, b in ws])
+    with smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta) as plan:
+        plan.set_params(params)
+        plan.simulate(cfg.smat_seed, step)
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        plan.backward_accum(cfg.smat_seed, step, cfg.lam)
+        plan.switch_storage(smat.SMAT_EXPERT)
+        torch.cuda.synchronize()
+    print(f"[{name}] kernels done, checking {sum(len(w) for w in wins)} windows", flush=True)
+    worst = 0
+    for i, ws in enumerate(samples):
+        p = params[i]
+        for a, b, th, t0, gs, g_old in ws:
+            y, kept, eps = oracle.simulate_f64(th, t0, "bf16", p, cfg.smat_seed, step, i, a)
+            coef = np.where(kept, oracle.coefficient(p["s"], p["keep"], p["rescale"]), 0.0)
+            got = host(outs[i][a:b])[0]
+            ok, strict = check_theta_tilde(got, "bf16", y, th, oracle.as_f64(t0, "bf16"), coef, eps, p["sigma"])
+            assert ok.all(), f"{name} tensor {i} [{a},{b}): theta~ mismatch"
+            dist = np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))
+            worst = max(worst, int(dist[strict].max(initial=0)))
+            want = oracle.backward_accum(gs, "bf16", g_old, p, cfg.lam, cfg.smat_seed, step, i, a)
+            gotg = host(inp.grad_theta[i].view(-1)[a:b])[0]
+            assert check_grad(gotg, want, g_old, np.abs(cfg.lam * coef * oracle.as_f64(gs, "bf16"))).all(), \
+                f"{name} tensor {i} [{a},{b}): grad mismatch"
+            np.testing.assert_array_equal(gotg.view(np.uint32)[~kept], g_old.view(np.uint32)[~kept])
+    assert worst <= 1
+    del inp, outs
+    torch.cuda.empty_cache()

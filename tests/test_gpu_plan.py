@@ -1,0 +1,269 @@
+"""GPU parity of the ragged tensor-list entry points (smat_plan_*, smat_simulate_multi,
+smat_backward_accum_multi, smat_switch_storage) against the CPU oracle: element by element on a
+small ragged list, invariance to list order and to sharding, the storage switch and its offload
+prefetch, the periodic schedule and resume from (seed, step)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_33437_amd as smat
+import workloads
+from tolerances import check_grad, check_theta_tilde, ordered
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def host(t):
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16), "bf16"
+    return t.numpy().copy(), "f32"
+
+
+def bits(t):
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
+@pytest.fixture(scope="module")
+def mini():
+    cfg = workloads.config("mini")
+    inp = workloads.make_inputs(cfg, device="cpu")
+    return cfg, inp
+
+
+def to_dev(inp):
+    th = [t.to(DEV) for t in inp.theta]
+    t0 = [t.to(DEV) for t in inp.theta0]
+    gs = [t.to(DEV) for t in inp.grad_sim]
+    gt = [t.to(DEV) for t in inp.grad_theta]
+    out = [torch.empty(t.numel(), dtype=torch.bfloat16, device=DEV) for t in th]
+    return th, t0, gs, gt, out
+
+
+def check_list(cfg, inp, params, outs, gts, step, lam, check_grads=True):
+    for i in range(cfg.count):
+        th, _ = host(inp.theta[i])
+        t0, t0_dt = host(inp.theta0[i])
+        p = params[i]
+        y, kept, eps = oracle.simulate_f64(th.ravel(), t0.ravel(), t0_dt, p, cfg.smat_seed, step, i)
+        coef = np.where(kept, oracle.coefficient(p["s"], p["keep"], p["rescale"]), 0.0)
+        got, out_dt = host(outs[i])
+        ok, strict = check_theta_tilde(got, out_dt, y, th.ravel(), oracle.as_f64(t0.ravel(), t0_dt), coef, eps,
+                                       p["sigma"])
+        assert ok.all(), f"tensor {i}: {np.count_nonzero(~ok)} theta~ mismatches"
+        assert np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))[strict].max(initial=0) <= 1
+        if check_grads:
+            gsn, gs_dt = host(inp.grad_sim[i])
+            g_old, _ = host(inp.grad_theta[i])
+            want = oracle.backward_accum(gsn.ravel(), gs_dt, g_old.ravel(), p, lam, cfg.smat_seed, step, i)
+            gotg, _ = host(gts[i])
+            assert check_grad(gotg.ravel(), want, g_old.ravel(), np.abs(lam * coef * oracle.as_f64(gsn.ravel(), gs_dt))).all()
+            np.testing.assert_array_equal(gotg.ravel().view(np.uint32)[~kept], g_old.ravel().view(np.uint32)[~kept])
+
+
+def test_mini_list_parity(mini):
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    step = 3
+    params = workloads.step_params(cfg, inp.settings, step)
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        plan.set_params(params)
+        plan.simulate(cfg.smat_seed, step)
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        plan.backward_accum(cfg.smat_seed, step, cfg.lam)
+        plan.switch_storage(smat.SMAT_EXPERT)
+        torch.cuda.synchronize()
+    check_list(cfg, inp, params, out, gt, step, cfg.lam)
+    # the expert storage is never written
+    for a, b in zip(th, inp.theta):
+        assert torch.equal(bits(a.cpu()), bits(b))
+
+
+def test_single_and_multi_entry_points_agree(mini):
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    params = workloads.step_params(cfg, inp.settings, 0)
+    with smat.Plan(th, out, t0) as plan:
+        plan.set_params(params)
+        plan.simulate(cfg.smat_seed, 0)
+    for i in range(cfg.count):
+        one = torch.empty_like(out[i])
+        smat.smat_simulate(th[i], t0[i], one, params[i], cfg.smat_seed, 0, i)
+        torch.cuda.synchronize()
+        assert torch.equal(bits(one), bits(out[i]))
+
+
+def test_order_invariance(mini):
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    params = workloads.step_params(cfg, inp.settings, 5)
+    perm = list(reversed(range(cfg.count)))
+    out2 = [torch.empty_like(o) for o in out]
+    gt2 = [g.clone() for g in gt]
+    with smat.Plan(th, out, t0, gs, gt) as a, \
+            smat.Plan([th[j] for j in perm], [out2[j] for j in perm], [t0[j] for j in perm],
+                      [gs[j] for j in perm], [gt2[j] for j in perm], tensor_ids=perm) as b:
+        a.set_params(params)
+        b.set_params([params[j] for j in perm])
+        for plan in (a, b):
+            plan.simulate(cfg.smat_seed, 5)
+            plan.backward_accum(cfg.smat_seed, 5, 0.5)
+        torch.cuda.synchronize()
+    for i in range(cfg.count):
+        assert torch.equal(bits(out[i]), bits(out2[i]))
+        assert torch.equal(bits(gt[i]), bits(gt2[i]))
+
+
+@pytest.mark.parametrize("cut_rule", ["aligned", "odd"])
+def test_shard_invariance(mini, cut_rule):
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    params = workloads.step_params(cfg, inp.settings, 7)
+    with smat.Plan(th, out, t0, gs, gt) as whole:
+        whole.set_params(params)
+        whole.simulate(cfg.smat_seed, 7)
+        whole.backward_accum(cfg.smat_seed, 7, 0.25)
+    # every tensor in two shards that share its tensor_id, the second with elem_offset = cut
+    sh_th, sh_out, sh_t0, sh_gs, sh_gt, ids, offs, sh_p = [], [], [], [], [], [], [], []
+    out2 = [torch.empty_like(o) for o in out]
+    gt2 = [g.clone() for g in to_dev(inp)[3]]
+    for i in range(cfg.count):
+        n = th[i].numel()
+        cut = (n // 2) & ~7 if cut_rule == "aligned" else n // 2 + 1
+        cut = min(max(cut, 0), n)
+        for lo, hi in ((0, cut), (cut, n)):
+            sh_th.append(th[i].view(-1)[lo:hi])
+            sh_out.append(out2[i][lo:hi])
+            sh_t0.append(t0[i].view(-1)[lo:hi])
+            sh_gs.append(gs[i].view(-1)[lo:hi])
+            sh_gt.append(gt2[i].view(-1)[lo:hi])
+            ids.append(i)
+            offs.append(lo)
+            sh_p.append(params[i])
+    with smat.Plan(sh_th, sh_out, sh_t0, sh_gs, sh_gt, tensor_ids=ids, elem_offsets=offs) as sharded:
+        sharded.set_params(sh_p)
+        sharded.simulate(cfg.smat_seed, 7)
+        sharded.backward_accum(cfg.smat_seed, 7, 0.25)
+        torch.cuda.synchronize()
+    for i in range(cfg.count):
+        assert torch.equal(bits(out[i]), bits(out2[i]))
+        assert torch.equal(bits(gt[i]), bits(gt2[i]))
+
+
+def test_switch_states_and_active_table(mini):
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    params = workloads.step_params(cfg, inp.settings, 0)
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        plan.set_params(params)
+        with pytest.raises(smat.SmatError):
+            plan.switch_storage(smat.SMAT_SIMULATED)          # nothing simulated yet
+        plan.simulate(1, 0)
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        assert plan.state == smat.SMAT_SIMULATED
+        host_ptrs, dev_table = plan.active_ptrs()
+        assert host_ptrs == [o.data_ptr() for o in out]
+        off = dev_table - plan.workspace.data_ptr()
+        torch.cuda.synchronize()
+        table = plan.workspace[off:off + 8 * cfg.count].cpu().view(torch.int64).tolist()
+        assert table == [o.data_ptr() for o in out]
+        with pytest.raises(smat.SmatError):
+            plan.simulate(1, 1)                               # buffers in use
+        with pytest.raises(smat.SmatError):
+            plan.switch_storage(smat.SMAT_SIMULATED)          # double switch
+        plan.backward_accum(1, 0, 1.0)
+        plan.switch_storage(smat.SMAT_EXPERT)
+        plan.switch_storage(smat.SMAT_EXPERT)                 # idempotent
+        host_ptrs, _ = plan.active_ptrs()
+        assert host_ptrs == [t.data_ptr() for t in th]
+        torch.cuda.synchronize()
+        table = plan.workspace[off:off + 8 * cfg.count].cpu().view(torch.int64).tolist()
+        assert table == [t.data_ptr() for t in th]
+        with pytest.raises(smat.SmatError):
+            plan.switch_storage(smat.SMAT_SIMULATED)          # stale buffer after restore
+        with pytest.raises(smat.SmatError):
+            plan.switch_storage(3)
+
+
+def test_offload_prefetch_matches_resident(mini):
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    hosts = [t.contiguous().pin_memory() for t in inp.theta0]
+    bufs = [torch.full((t.numel(),), 7.0, dtype=torch.bfloat16, device=DEV) for t in th]
+    with smat.Plan(th, out, t0) as res, smat.Plan(th, bufs, None, offload=True, theta0_hosts=hosts,
+                                                  dtypes=(smat.SMAT_BF16, smat.SMAT_BF16, smat.SMAT_BF16)) as off:
+        for step in (3, 7):
+            params = workloads.step_params(cfg, inp.settings, step)
+            res.set_params(params)
+            off.set_params(params)
+            res.simulate(cfg.smat_seed, step)
+            off.simulate(cfg.smat_seed, step)                 # waits for the prefetch of theta0 into bufs
+            off.switch_storage(smat.SMAT_SIMULATED)
+            torch.cuda.synchronize()
+            for a, b in zip(out, bufs):
+                assert torch.equal(bits(a), bits(b))
+            off.switch_storage(smat.SMAT_EXPERT)             # prefetch theta0 back into the buffers
+            torch.cuda.synchronize()
+            off_state = off.state
+            assert off_state == smat.SMAT_EXPERT
+        # let the copy stream finish before reading the buffers
+        off.close()
+        torch.cuda.synchronize()
+        for b, h in zip(bufs, inp.theta0):
+            assert torch.equal(bits(b.cpu()), bits(h.view(-1)))
+
+
+def test_periodic_schedule_and_resume(mini):
+    cfg, inp = mini
+    period, steps = 4, 12
+
+    def run(step_range, th, t0, gs, gt, out):
+        snaps = {}
+        with smat.Plan(th, out, t0, gs, gt) as plan:
+            for step in step_range:
+                if not oracle.is_simulated_step(step, period):
+                    continue
+                plan.set_params(workloads.step_params(cfg, inp.settings, step))
+                plan.simulate(cfg.smat_seed, step)
+                plan.switch_storage(smat.SMAT_SIMULATED)
+                plan.backward_accum(cfg.smat_seed, step, 1.0 / period)
+                plan.switch_storage(smat.SMAT_EXPERT)
+                torch.cuda.synchronize()
+                snaps[step] = [o.clone() for o in out]
+        return snaps
+
+    th, t0, gs, gt, out = to_dev(inp)
+    straight = run(range(steps), th, t0, gs, gt, out)
+    assert sorted(straight) == [3, 7, 11]
+    gt_straight = [g.clone() for g in gt]
+    th2, t02, gs2, gt2, out2 = to_dev(inp)
+    first = run(range(0, 6), th2, t02, gs2, gt2, out2)
+    second = run(range(6, steps), th2, t02, gs2, gt2, out2)    # a fresh plan resumes at step 6
+    resumed = {**first, **second}
+    assert sorted(resumed) == [3, 7, 11]
+    for s in straight:
+        for a, b in zip(straight[s], resumed[s]):
+            assert torch.equal(bits(a), bits(b))
+    for a, b in zip(gt_straight, gt2):
+        assert torch.equal(bits(a), bits(b))
+    # the simulated step 7 matches the oracle
+    params = workloads.step_params(cfg, inp.settings, 7)
+    check_list(cfg, inp, params, straight[7], None, 7, 0.25, check_grads=False)
+
+
+def test_empty_and_tiny_lists():
+    with smat.Plan([], [], []) as p:
+        p.set_params([])
+        p.simulate(0, 0)
+        p.switch_storage(smat.SMAT_SIMULATED)
+        p.switch_storage(smat.SMAT_EXPERT)
+    th = [torch.zeros(0, device=DEV), torch.ones(1, device=DEV)]
+    out = [torch.empty(0, dtype=torch.bfloat16, device=DEV), torch.empty(1, dtype=torch.bfloat16, device=DEV)]
+    t0 = [torch.zeros(0, dtype=torch.bfloat16, device=DEV), torch.zeros(1, dtype=torch.bfloat16, device=DEV)]
+    with smat.Plan(th, out, t0) as p:
+        p.set_params([dict(s=1.0, keep=1.0, sigma=0.0)] * 2)
+        p.simulate(0, 0)
+        torch.cuda.synchronize()
+    assert out[1].float().item() == 1.0

@@ -1,0 +1,68 @@
+"""Comparison rules of the GPU path against the oracle, derived from the kernels' fp32 arithmetic.
+
+theta~: the kernel forms t = fl(s/keep), fma(t, theta, fma(-t, theta0, theta0)), fma(sigma, z, .)
+in fp32 and rounds once to the output type.  Each fp32 step adds at most u = 2^-24 relative to its
+operands, so the fp32 value is within E = 3u (|theta0| + |t| (|theta| + |theta0|) + |eps|)
++ sigma * |z_gpu - z| of the exact value, and the final rounding adds half an ulp of the output
+type.  Away from cancellation this is "within 1 ulp of the oracle's correctly rounded value";
+near zero results the absolute bound E governs.
+
+grad: one fma in fp32 with c = fl(lambda * fl(s/keep)): |err| <= 3u (|g_old| + |lambda t g~|),
+well inside the 1e-6 relative bar, which is the bound the tests use.
+"""
+import numpy as np
+
+U = 2.0 ** -24
+Z_TOL = 2e-6          # absolute bound on the standard-normal draw
+GRAD_RTOL = 1e-6      # relative bound on the fp32 gradient accumulation
+
+
+def bf16_bits_to_f64(bits):
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def _ulp_bf16(x):
+    x = np.abs(np.asarray(x, dtype=np.float64))
+    e = np.frexp(x)[1]
+    return np.ldexp(1.0, np.maximum(e - 8, -133))
+
+
+def _ulp_f32(x):
+    x = np.abs(np.asarray(x, dtype=np.float64))
+    e = np.frexp(x)[1]
+    return np.ldexp(1.0, np.maximum(e - 24, -149))
+
+
+def ordered(bits16):
+    """bf16 bit patterns mapped to integers that are monotone in value."""
+    b = np.asarray(bits16, dtype=np.int64)
+    return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
+
+
+def check_theta_tilde(gpu, out_dtype, y, theta, theta0, t, eps, sigma):
+    """Returns (ok, strict).  gpu: uint16 bits (bf16) or float32 values; y: the oracle's
+    unrounded fp64 value; theta, theta0: fp64 inputs; t: fp64 coefficient (0 for dropped
+    coordinates); eps: the oracle's noise; sigma: the tensor's noise RMS.
+    ok: |gpu - y| <= half an output ulp + E.  strict: elements whose fp32 error bound E is below
+    half an output ulp of y; there the GPU value is within 1 ulp of the oracle's rounding of y."""
+    theta = np.asarray(theta, dtype=np.float64)
+    theta0 = np.asarray(theta0, dtype=np.float64)
+    E = 3 * U * (np.abs(theta0) + np.abs(t) * (np.abs(theta) + np.abs(theta0)) + np.abs(eps)) + Z_TOL * sigma
+    if out_dtype == "bf16":
+        g = bf16_bits_to_f64(gpu)
+        uy = _ulp_bf16(y)
+        half = 0.5 * np.maximum(_ulp_bf16(g), uy)
+    else:
+        g = np.asarray(gpu, dtype=np.float64)
+        uy = _ulp_f32(y)
+        half = 0.5 * np.maximum(_ulp_f32(g), uy)
+    ok = np.abs(g - y) <= half * (1 + 1e-12) + E
+    strict = E < 0.5 * uy
+    return ok, strict
+
+
+def check_grad(gpu, oracle, g_old, incr):
+    """gpu/oracle: float32 arrays; g_old: previous values; incr: |lambda t g~| in fp64."""
+    scale = np.maximum(np.abs(oracle.astype(np.float64)), np.abs(g_old.astype(np.float64)) + np.abs(incr))
+    return np.abs(gpu.astype(np.float64) - oracle.astype(np.float64)) <= GRAD_RTOL * scale
