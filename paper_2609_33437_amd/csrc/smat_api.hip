@@ -120,6 +120,7 @@ extern "C" smat_status smat_simulate(const float* theta, const void* theta0, sma
   if (st != SMAT_OK) return st;
   if (n == 0) return SMAT_OK;
   if (key.elem_offset > UINT64_MAX - (uint64_t)n) return fail(SMAT_ERR_INVALID, "smat_simulate: elem_offset + n overflows");
+  if ((n + smat::tile_elems(1) - 1) / smat::tile_elems(1) > 0x7FFFFFFF) return fail(SMAT_ERR_INVALID, "smat_simulate: n too large");
   st = check_simulate_ptrs(theta, theta0, theta0_dtype, out, out_dtype, n, "smat_simulate");
   if (st != SMAT_OK) return st;
   TensorRec rec{};
@@ -146,6 +147,7 @@ extern "C" smat_status smat_backward_accum(const void* grad_sim, smat_dtype grad
   if (n == 0) return SMAT_OK;
   if (key.elem_offset > UINT64_MAX - (uint64_t)n)
     return fail(SMAT_ERR_INVALID, "smat_backward_accum: elem_offset + n overflows");
+  if ((n + smat::tile_elems(1) - 1) / smat::tile_elems(1) > 0x7FFFFFFF) return fail(SMAT_ERR_INVALID, "smat_backward_accum: n too large");
   if (!grad_sim || !grad_theta) return fail(SMAT_ERR_INVALID, "smat_backward_accum: null pointer with n > 0");
   if (overlap(grad_sim, (size_t)n * dtype_bytes(grad_dtype), grad_theta, (size_t)n * 4))
     return fail(SMAT_ERR_INVALID, "smat_backward_accum: grad_sim must not overlap grad_theta");
@@ -324,7 +326,7 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
     p->sim_ptrs[i] = d.out;
     nchunks += (uint64_t)((d.n + smat::kChunk - 1) / smat::kChunk);
   }
-  if (nchunks > 0x7FFFFFFFull) {
+  if (nchunks * smat::tiles_per_chunk(1) > 0x7FFFFFFFull) {  // one block per tile must fit in one grid
     delete p;
     return fail(SMAT_ERR_INVALID, "smat_plan_create: tensor list too large for one launch");
   }

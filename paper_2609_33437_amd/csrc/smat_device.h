@@ -45,12 +45,21 @@ struct alignas(16) ParamRec {
 };
 static_assert(sizeof(ParamRec) == 16, "ParamRec layout");
 
-// Work decomposition: a block of kBlock threads handles one chunk of kChunk elements of one
-// tensor; each thread handles kUnroll quads per iteration.
-constexpr int kBlock = 256;
-constexpr int kUnroll = 2;
-constexpr int kIters = 8;
-constexpr int64_t kChunk = (int64_t)kBlock * 4 * kUnroll * kIters;  // 16384 elements
+// Work decomposition: a block of kBlock threads (one wave) handles one tile of Q quads per
+// thread (tile = 4 * kBlock * Q elements); thread x owns quads x, x + kBlock, ... of the tile,
+// so every load/store instruction of the wave covers one contiguous span and consecutive blocks
+// stream consecutive memory.  A tensor list is cut into chunks of kChunk elements; block b of a
+// list launch takes tile (b mod tiles-per-chunk) of chunk (b / tiles-per-chunk), which keeps
+// the chunk table small.  The simulate carries two Philox calls and Box-Muller per quad and
+// takes two quads per thread to overlap that work with its loads; the backward takes one.
+constexpr int kBlock = 64;
+constexpr int kSimQuads = 2;
+constexpr int kBwdQuads = 1;
+constexpr int64_t kChunk = 16384;
+constexpr int64_t tile_elems(int quads) { return 4 * kBlock * quads; }
+constexpr int tiles_per_chunk(int quads) { return (int)(kChunk / tile_elems(quads)); }
+static_assert(kChunk % tile_elems(kSimQuads) == 0 && kChunk % tile_elems(kBwdQuads) == 0, "tiles split chunks");
+constexpr int64_t kMaxTile = tile_elems(kSimQuads > kBwdQuads ? kSimQuads : kBwdQuads);
 
 constexpr uint32_t kStreamMask = 0u;
 constexpr uint32_t kStreamNoise = 1u;
@@ -60,12 +69,10 @@ struct Words {
   uint32_t w0, w1, w2, w3;
 };
 
-// a ^ b ^ key in one VALU op: gfx950's three-input bitwise op with truth table 0x96 (xor3).
-// The key is wave-uniform and rides in an SGPR.
+// a ^ b ^ key in one VALU op: gfx950's three-input bitwise op (v_bitop3_b32) with truth table
+// 0x96, i.e. xor3.  The compiler keeps the wave-uniform key in an SGPR.
 __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t key) {
-  uint32_t r;
-  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(key));
-  return r;
+  return __builtin_amdgcn_bitop3_b32(a, b, key, 0x96);
 }
 
 __device__ __forceinline__ Words philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
@@ -177,14 +184,19 @@ __device__ __forceinline__ SMAT_GLOBAL T* gstore_ptr(void* p) {
   return (SMAT_GLOBAL T*)p;
 }
 
-// Streaming (nontemporal) quad loads/stores: every byte is touched once per pass.
+// Streaming (nontemporal) quad loads/stores: every byte is touched once per pass.  A quad is
+// loaded raw (one 16 B or 8 B access) and unpacked separately, so a kernel can issue all its
+// loads, do its random draws while they are in flight, and only then wait for the data.
 template <typename T>
 struct QuadIO;
 
 template <>
 struct QuadIO<float> {
-  static __device__ __forceinline__ void load(const void* base, uint32_t q, float v[4]) {
-    const f32x4 x = __builtin_nontemporal_load(gload_ptr<f32x4>(base) + q);
+  typedef f32x4 Raw;
+  static __device__ __forceinline__ Raw load_raw(const void* base, uint32_t q) {
+    return __builtin_nontemporal_load(gload_ptr<f32x4>(base) + q);
+  }
+  static __device__ __forceinline__ void unpack(const Raw& x, float v[4]) {
     v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
   }
   static __device__ __forceinline__ void store(void* base, uint32_t q, const float v[4]) {
@@ -197,8 +209,11 @@ struct QuadIO<float> {
 
 template <>
 struct QuadIO<Bf16> {
-  static __device__ __forceinline__ void load(const void* base, uint32_t q, float v[4]) {
-    const u32x2 x = __builtin_nontemporal_load(gload_ptr<u32x2>(base) + q);
+  typedef u32x2 Raw;
+  static __device__ __forceinline__ Raw load_raw(const void* base, uint32_t q) {
+    return __builtin_nontemporal_load(gload_ptr<u32x2>(base) + q);
+  }
+  static __device__ __forceinline__ void unpack(const Raw& x, float v[4]) {
     v[0] = bf16_to_f32(x.x & 0xFFFFu);
     v[1] = __uint_as_float(x.x & 0xFFFF0000u);
     v[2] = bf16_to_f32(x.y & 0xFFFFu);

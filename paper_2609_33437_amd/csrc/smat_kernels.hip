@@ -7,9 +7,12 @@
 // of 4 consecutive elements = one Philox group, so a thread draws one 128-bit Philox output per
 // stream per quad and never stores a draw.  Consecutive lanes take consecutive quads, so every
 // load/store instruction of a wave covers one contiguous span (16 B per lane for fp32, 8 B per
-// lane for bf16), issued as nontemporal streaming accesses.  A block walks one chunk of
-// kChunk elements of one tensor; the ragged-list kernels find their (tensor, chunk) pair in a
-// table built once per tensor list, so huge matrices and tiny vectors share one launch.
+// lane for bf16), issued as nontemporal streaming accesses.  Each one-wave block handles one
+// tile of one or two quads per thread, and consecutive blocks take consecutive tiles, so the blocks in
+// flight stream one contiguous window of each array (measured on MI355X: looping blocks over
+// strided chunks or persistent grid-stride loops lose 10-30 % of the bandwidth).  The
+// ragged-list kernels find a block's (tensor, chunk) pair in a table built once per tensor
+// list, so huge matrices and tiny vectors share one launch.
 #include "smat_launch.h"
 
 namespace smat {
@@ -26,9 +29,11 @@ struct StorageBytes<Bf16> {
 };
 
 // ---------------------------------------------------------------- simulate
-template <typename T0, typename TO>
-__device__ __forceinline__ void simulate_range(const TensorRec& R, const ParamRec& P, int64_t begin, int64_t end,
-                                               uint64_t seed, uint32_t step) {
+// One tile of `len` (<= 4 kBlock Q) elements starting at element `begin` of a tensor.  Thread x
+// owns quads x + u kBlock (u < Q) of the tile.
+template <typename T0, typename TO, int Q>
+__device__ __forceinline__ void simulate_tile(const TensorRec& R, const ParamRec& P, int64_t begin, uint32_t len,
+                                              uint64_t seed, uint32_t step) {
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
   const uint32_t cnoise = (step << 2) | kStreamNoise;
@@ -41,13 +46,12 @@ __device__ __forceinline__ void simulate_range(const TensorRec& R, const ParamRe
   const float t = P.t, sigma = P.sigma;
   const uint32_t thr = P.thr;
 
-  const uint32_t len = (uint32_t)(end - begin);
   const float* th = R.theta + begin;
   const void* t0 = static_cast<const char*>(R.theta0) + begin * StorageBytes<T0>::value;
   void* out = static_cast<char*>(R.out) + begin * StorageBytes<TO>::value;
   const uint64_t e0 = R.elem_offset + (uint64_t)begin;
 
-  // one element by itself: ragged tails and tensors whose pointers or offset break quad alignment
+  // element by element: ragged tails and tensors whose pointers or offset break quad alignment
   auto one = [&](uint32_t i) {
     const uint64_t e = e0 + i;
     const uint64_t g = e >> 2;
@@ -59,56 +63,71 @@ __device__ __forceinline__ void simulate_range(const TensorRec& R, const ParamRe
     QuadIO<TO>::store1(out, i, y);
   };
 
-  if (R.sflags & kVecSim) {
-    const uint64_t g0 = e0 >> 2;  // e0 is a multiple of 4 here
-    const uint32_t nq = len >> 2;
-    for (uint32_t q0 = threadIdx.x; q0 < nq; q0 += kBlock * kUnroll) {
-      float a[kUnroll][4], b[kUnroll][4];
+  if (!(R.sflags & kVecSim)) {
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const uint32_t q = q0 + u * kBlock;
-        if (q < nq) {
-          QuadIO<float>::load(th, q, a[u]);
-          QuadIO<T0>::load(t0, q, b[u]);
-        }
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
+      for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) one(i);
+    }
+    return;
+  }
+  // whole quads: each is one Philox group, since e0 is a multiple of 4 on this path.
+  // Phase 1 issues every load (indices clamped into the tile, so no branch guards them), phase 2
+  // draws the mask and noise while the loads are in flight, phase 3 combines and stores.
+  const uint32_t nq = len >> 2;
+  if (nq > 0) {
+    typename QuadIO<float>::Raw ra[Q];
+    typename QuadIO<T0>::Raw rb[Q];
+#pragma unroll
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t q = u * kBlock + threadIdx.x;
+      const uint32_t qc = q < nq ? q : nq - 1;
+      ra[u] = QuadIO<float>::load_raw(th, qc);
+      rb[u] = QuadIO<T0>::load_raw(t0, qc);
+    }
+    bool kept[Q][4];
+    float z[Q][4];
+#pragma unroll
+    for (int u = 0; u < Q; ++u) {
+      const uint64_t g = (e0 >> 2) + u * kBlock + threadIdx.x;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
+      if (use_mask) {
+        const Words w = group_words(g, tensor_id, cmask, k0, k1);
+        kept[u][0] = w.w0 < thr;
+        kept[u][1] = w.w1 < thr;
+        kept[u][2] = w.w2 < thr;
+        kept[u][3] = w.w3 < thr;
       }
+      if (use_noise) quad_noise(group_words(g, tensor_id, cnoise, k0, k1), uniform, z[u]);
+    }
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const uint32_t q = q0 + u * kBlock;
-        if (q < nq) {
-          const uint64_t g = g0 + q;
-          bool kept[4] = {all_kept, all_kept, all_kept, all_kept};
-          if (use_mask) {
-            const Words w = group_words(g, tensor_id, cmask, k0, k1);
-            kept[0] = w.w0 < thr;
-            kept[1] = w.w1 < thr;
-            kept[2] = w.w2 < thr;
-            kept[3] = w.w3 < thr;
-          }
-          float y[4];
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t q = u * kBlock + threadIdx.x;
+      if (q < nq) {
+        float a[4], b[4], y[4];
+        QuadIO<float>::unpack(ra[u], a);
+        QuadIO<T0>::unpack(rb[u], b);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) y[j] = sim_value(a[u][j], b[u][j], kept[j], t);
-          if (use_noise) {
-            float z[4];
-            quad_noise(group_words(g, tensor_id, cnoise, k0, k1), uniform, z);
+        for (int j = 0; j < 4; ++j) y[j] = sim_value(a[j], b[j], kept[u][j], t);
+        if (use_noise) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) y[j] = __builtin_fmaf(sigma, z[j], y[j]);
-          }
-          QuadIO<TO>::store(out, q, y);
+          for (int j = 0; j < 4; ++j) y[j] = __builtin_fmaf(sigma, z[u][j], y[j]);
         }
+        QuadIO<TO>::store(out, q, y);
       }
     }
-    const uint32_t done = nq << 2;
-    if (threadIdx.x < len - done) one(done + threadIdx.x);
-  } else {
-    for (uint32_t i = threadIdx.x; i < len; i += kBlock) one(i);
+  }
+  // the last 1-3 elements of a tensor whose size is not a multiple of 4
+  if ((len & 3u) && threadIdx.x == (nq & (kBlock - 1))) {
+    for (uint32_t i = nq * 4u; i < len; ++i) one(i);
   }
 }
 
 // ---------------------------------------------------------------- backward
-template <typename TG>
-__device__ __forceinline__ void backward_range(const TensorRec& R, const ParamRec& P, int64_t begin, int64_t end,
-                                               uint64_t seed, uint32_t step, float lambda) {
+template <typename TG, int Q>
+__device__ __forceinline__ void backward_tile(const TensorRec& R, const ParamRec& P, int64_t begin, uint32_t len,
+                                              uint64_t seed, uint32_t step, float lambda) {
   const uint32_t flags = P.flags;
   if (flags & kFlagDropAll) return;  // every coordinate dropped: the gradient is left as it is
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
@@ -118,7 +137,6 @@ __device__ __forceinline__ void backward_range(const TensorRec& R, const ParamRe
   const uint32_t thr = P.thr;
   const float c = lambda * P.t;
 
-  const uint32_t len = (uint32_t)(end - begin);
   const void* gs = static_cast<const char*>(R.grad_sim) + begin * StorageBytes<TG>::value;
   float* gt = R.grad_theta + begin;
   const uint64_t e0 = R.elem_offset + (uint64_t)begin;
@@ -130,59 +148,75 @@ __device__ __forceinline__ void backward_range(const TensorRec& R, const ParamRe
     if (kept) QuadIO<float>::store1(gt, i, __builtin_fmaf(c, QuadIO<TG>::load1(gs, i), QuadIO<float>::load1(gt, i)));
   };
 
-  if (R.sflags & kVecBwd) {
-    const uint64_t g0 = e0 >> 2;
-    const uint32_t nq = len >> 2;
-    for (uint32_t q0 = threadIdx.x; q0 < nq; q0 += kBlock * kUnroll) {
-      float a[kUnroll][4], b[kUnroll][4];
+  if (!(R.sflags & kVecBwd)) {
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const uint32_t q = q0 + u * kBlock;
-        if (q < nq) {
-          QuadIO<TG>::load(gs, q, a[u]);
-          QuadIO<float>::load(gt, q, b[u]);
-        }
-      }
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
+      for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) one(i);
+    }
+    return;
+  }
+  // loads first (clamped, unguarded), the regenerated mask while they are in flight, then the update
+  const uint32_t nq = len >> 2;
+  if (nq > 0) {
+    typename QuadIO<TG>::Raw ra[Q];
+    typename QuadIO<float>::Raw rb[Q];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const uint32_t q = q0 + u * kBlock;
-        if (q < nq) {
-          bool kept[4] = {true, true, true, true};
-          if (use_mask) {
-            const Words w = group_words(g0 + q, tensor_id, cmask, k0, k1);
-            kept[0] = w.w0 < thr;
-            kept[1] = w.w1 < thr;
-            kept[2] = w.w2 < thr;
-            kept[3] = w.w3 < thr;
-          }
-          float o[4];
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t q = u * kBlock + threadIdx.x;
+      const uint32_t qc = q < nq ? q : nq - 1;
+      ra[u] = QuadIO<TG>::load_raw(gs, qc);
+      rb[u] = QuadIO<float>::load_raw(gt, qc);
+    }
+    bool kept[Q][4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) o[j] = kept[j] ? __builtin_fmaf(c, a[u][j], b[u][j]) : b[u][j];
-          QuadIO<float>::store(gt, q, o);
-        }
+    for (int u = 0; u < Q; ++u) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kept[u][j] = true;
+      if (use_mask) {
+        const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, cmask, k0, k1);
+        kept[u][0] = w.w0 < thr;
+        kept[u][1] = w.w1 < thr;
+        kept[u][2] = w.w2 < thr;
+        kept[u][3] = w.w3 < thr;
       }
     }
-    const uint32_t done = nq << 2;
-    if (threadIdx.x < len - done) one(done + threadIdx.x);
-  } else {
-    for (uint32_t i = threadIdx.x; i < len; i += kBlock) one(i);
+#pragma unroll
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t q = u * kBlock + threadIdx.x;
+      if (q < nq) {
+        float a[4], b[4], o[4];
+        QuadIO<TG>::unpack(ra[u], a);
+        QuadIO<float>::unpack(rb[u], b);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = kept[u][j] ? __builtin_fmaf(c, a[j], b[j]) : b[j];
+        QuadIO<float>::store(gt, q, o);
+      }
+    }
+  }
+  if ((len & 3u) && threadIdx.x == (nq & (kBlock - 1))) {
+    for (uint32_t i = nq * 4u; i < len; ++i) one(i);
   }
 }
 
 // ---------------------------------------------------------------- kernels
+__device__ __forceinline__ uint32_t tile_len(int64_t n, int64_t begin, int64_t tile) {
+  return (uint32_t)(n - begin < tile ? n - begin : tile);
+}
+
 template <typename T0, typename TO>
 __global__ __launch_bounds__(kBlock) void k_simulate_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step) {
-  const int64_t begin = (int64_t)blockIdx.x * kChunk;
-  const int64_t end = begin + kChunk < R.n ? begin + kChunk : R.n;
-  simulate_range<T0, TO>(R, P, begin, end, seed, step);
+  constexpr int64_t tile = tile_elems(kSimQuads);
+  const int64_t begin = (int64_t)blockIdx.x * tile;
+  simulate_tile<T0, TO, kSimQuads>(R, P, begin, tile_len(R.n, begin, tile), seed, step);
 }
 
 template <typename TG>
 __global__ __launch_bounds__(kBlock) void k_backward_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step,
                                                          float lambda) {
-  const int64_t begin = (int64_t)blockIdx.x * kChunk;
-  const int64_t end = begin + kChunk < R.n ? begin + kChunk : R.n;
-  backward_range<TG>(R, P, begin, end, seed, step, lambda);
+  constexpr int64_t tile = tile_elems(kBwdQuads);
+  const int64_t begin = (int64_t)blockIdx.x * tile;
+  backward_tile<TG, kBwdQuads>(R, P, begin, tile_len(R.n, begin, tile), seed, step, lambda);
 }
 
 template <typename T0, typename TO>
@@ -190,12 +224,14 @@ __global__ __launch_bounds__(kBlock) void k_simulate_multi(const TensorRec* __re
                                                            const ParamRec* __restrict__ prms,
                                                            const uint2* __restrict__ chunks, uint64_t seed,
                                                            uint32_t step) {
-  const uint2 ch = chunks[blockIdx.x];  // (tensor index, chunk index within the tensor)
+  constexpr int64_t tile = tile_elems(kSimQuads);
+  constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
+  const uint2 ch = chunks[blockIdx.x / tpc];  // (tensor index, chunk index within the tensor)
   const TensorRec R = recs[ch.x];
+  const int64_t begin = (int64_t)ch.y * kChunk + (int64_t)(blockIdx.x % tpc) * tile;
+  if (begin >= R.n) return;  // unused tile of a tensor's last chunk
   const ParamRec P = prms[ch.x];
-  const int64_t begin = (int64_t)ch.y * kChunk;
-  const int64_t end = begin + kChunk < R.n ? begin + kChunk : R.n;
-  simulate_range<T0, TO>(R, P, begin, end, seed, step);
+  simulate_tile<T0, TO, kSimQuads>(R, P, begin, tile_len(R.n, begin, tile), seed, step);
 }
 
 template <typename TG>
@@ -203,19 +239,23 @@ __global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __re
                                                            const ParamRec* __restrict__ prms,
                                                            const uint2* __restrict__ chunks, uint64_t seed,
                                                            uint32_t step, float lambda) {
-  const uint2 ch = chunks[blockIdx.x];
+  constexpr int64_t tile = tile_elems(kBwdQuads);
+  constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
+  const uint2 ch = chunks[blockIdx.x / tpc];
   const TensorRec R = recs[ch.x];
+  const int64_t begin = (int64_t)ch.y * kChunk + (int64_t)(blockIdx.x % tpc) * tile;
+  if (begin >= R.n) return;
   const ParamRec P = prms[ch.x];
-  const int64_t begin = (int64_t)ch.y * kChunk;
-  const int64_t end = begin + kChunk < R.n ? begin + kChunk : R.n;
-  backward_range<TG>(R, P, begin, end, seed, step, lambda);
+  backward_tile<TG, kBwdQuads>(R, P, begin, tile_len(R.n, begin, tile), seed, step, lambda);
 }
 
-__global__ __launch_bounds__(kBlock) void k_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id,
+constexpr int kDebugBlock = 256;
+
+__global__ __launch_bounds__(kDebugBlock) void k_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id,
                                                         uint64_t elem_offset, int64_t n, ParamRec P,
                                                         uint32_t* mask_words, uint32_t* noise_words,
                                                         uint8_t* kept, float* z) {
-  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  const int64_t i = (int64_t)blockIdx.x * kDebugBlock + threadIdx.x;
   if (i >= n) return;
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint64_t e = elem_offset + (uint64_t)i;
@@ -237,7 +277,7 @@ static inline uint32_t blocks_for(int64_t n, int64_t per_block) { return (uint32
 
 hipError_t launch_simulate_one(const TensorRec& rec, const ParamRec& prm, int theta0_dtype, int out_dtype,
                                uint64_t seed, uint32_t step, hipStream_t stream) {
-  const dim3 grid(blocks_for(rec.n, kChunk)), block(kBlock);
+  const dim3 grid(blocks_for(rec.n, tile_elems(kSimQuads))), block(kBlock);
   if (theta0_dtype == 1 && out_dtype == 1)
     k_simulate_one<Bf16, Bf16><<<grid, block, 0, stream>>>(rec, prm, seed, step);
   else if (theta0_dtype == 1 && out_dtype == 0)
@@ -251,7 +291,7 @@ hipError_t launch_simulate_one(const TensorRec& rec, const ParamRec& prm, int th
 
 hipError_t launch_backward_one(const TensorRec& rec, const ParamRec& prm, int grad_dtype, float lambda,
                                uint64_t seed, uint32_t step, hipStream_t stream) {
-  const dim3 grid(blocks_for(rec.n, kChunk)), block(kBlock);
+  const dim3 grid(blocks_for(rec.n, tile_elems(kBwdQuads))), block(kBlock);
   if (grad_dtype == 1)
     k_backward_one<Bf16><<<grid, block, 0, stream>>>(rec, prm, seed, step, lambda);
   else
@@ -262,7 +302,7 @@ hipError_t launch_backward_one(const TensorRec& rec, const ParamRec& prm, int gr
 hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks,
                                  uint32_t nchunks, int theta0_dtype, int out_dtype, uint64_t seed,
                                  uint32_t step, hipStream_t stream) {
-  const dim3 grid(nchunks), block(kBlock);
+  const dim3 grid(nchunks * tiles_per_chunk(kSimQuads)), block(kBlock);
   if (theta0_dtype == 1 && out_dtype == 1)
     k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
   else if (theta0_dtype == 1 && out_dtype == 0)
@@ -277,7 +317,7 @@ hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, co
 hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks,
                                  uint32_t nchunks, int grad_dtype, float lambda, uint64_t seed,
                                  uint32_t step, hipStream_t stream) {
-  const dim3 grid(nchunks), block(kBlock);
+  const dim3 grid(nchunks * tiles_per_chunk(kBwdQuads)), block(kBlock);
   if (grad_dtype == 1)
     k_backward_multi<Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
   else
@@ -288,7 +328,7 @@ hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, co
 hipError_t launch_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t elem_offset,
                               int64_t n, const ParamRec& prm, uint32_t* mask_words, uint32_t* noise_words,
                               uint8_t* kept, float* z, hipStream_t stream) {
-  const dim3 grid(blocks_for(n, kBlock)), block(kBlock);
+  const dim3 grid(blocks_for(n, kDebugBlock)), block(kDebugBlock);
   k_debug_draws<<<grid, block, 0, stream>>>(seed, step, tensor_id, elem_offset, n, prm, mask_words, noise_words,
                                             kept, z);
   return hipGetLastError();

@@ -38,9 +38,9 @@ def compare_simulate(theta, theta0, out, p, seed, step, tid, off=0):
     ok, strict = check_theta_tilde(got, out_dt, y, th, oracle.as_f64(t0, t0_dt), coef, eps, p["sigma"])
     bad = np.flatnonzero(~ok)
     assert bad.size == 0, f"{bad.size} mismatches, first at {bad[:5]}: gpu={got[bad[:5]]} y={y[bad[:5]]}"
-    if got.size >= 1000:
-        assert strict.mean() > 0.99   # the 1-ulp rule covers nearly every element
     if out_dt == "bf16":
+        if got.size >= 1000:
+            assert strict.mean() > 0.99   # the 1-ulp rule covers nearly every element
         want = oracle.round_to_bf16_bits(y)
         return np.abs(ordered(got) - ordered(want))[strict]
     return None
