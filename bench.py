@@ -60,6 +60,12 @@ def parse_args():
     ap.add_argument("--cpu-sample", type=int, default=1 << 27, help="most elements the CPU oracle baseline visits")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU work budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--summarize", metavar="DIR",
+                    help="turn rocprofv3 CSV output under DIR (prof_trace/, prof_fetch/, prof_write/) into the "
+                         "summaries under profiles/ and exit")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain elementwise copy of 2^28 fp32 values (1 GiB read, 1 GiB written) "
+                         "three times, whose HBM counters scale the kernels' counter readings")
     return ap.parse_args()
 
 
@@ -100,8 +106,91 @@ def cpu_baseline(cfg, inp, params, step, max_elems, budget_s, torch, np):
                       f"random order (simulate + backward, fp64 NumPy, one process), {secs:.1f} s of work"}
 
 
+TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_trace -o c4 -- "
+             "python3 bench.py --steps 20 --warmup 5 --no-cpu-baseline --calibrate-copy")
+PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d gpurun_out/prof_{tag} -o c4 --kernel-include-regex "
+           "'k_simulate_multi|k_backward_multi|elementwise' -- "
+           "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --calibrate-copy")
+COPY_GRID = 1 << 26   # threads of the calibration copy (2^28 fp32 values, 4 per thread)
+COPY_BYTES = 1 << 30  # read and written by one calibration dispatch
+
+
+def summarize(root: str) -> int:
+    """Write profiles/ summaries from rocprofv3 CSV output (kernel stats, FETCH_SIZE, WRITE_SIZE)."""
+    import csv
+    import statistics
+
+    def kind(name: str, grid: int):
+        if "k_simulate_multi" in name:
+            return "simulate"
+        if "k_backward_multi" in name:
+            return "backward"
+        if "MulFunctor" in name and grid == COPY_GRID:
+            return "copy"
+        return None
+
+    out_dir = os.path.join(ROOT, "profiles")
+    os.makedirs(out_dir, exist_ok=True)
+    stats = list(csv.DictReader(open(os.path.join(root, "prof_trace", "c4_kernel_stats.csv"))))
+    lines = ["# Kernel time on the 7B-shaped list (c4), rocprofv3 kernel trace", "",
+             f"Command (from the repository root, on one MI355X): `{TRACE_CMD}`", "",
+             "Each step launches one simulate and one backward over the 290-tensor list "
+             "(7,504,924,672 parameters); 5 warmup + 20 timed steps = 25 calls each.  The other kernels are "
+             "torch's input generation and the copy calibration.", "",
+             "| kernel | calls | average ms | min ms | max ms | share of GPU time |", "|---|---|---|---|---|---|"]
+    for r in stats[:12]:
+        name = r["Name"].replace("(anonymous namespace)", "{anon}").split("(")[0].replace("void ", "")
+        lines.append(f"| `{name[:80]}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.4f} | "
+                     f"{float(r['MinNs']) / 1e6:.4f} | {float(r['MaxNs']) / 1e6:.4f} | {float(r['Percentage']):.2f}% |")
+    avg = {kind(r["Name"], 0): float(r["AverageNs"]) / 1e6 for r in stats if kind(r["Name"], 0)}
+    with open(os.path.join(out_dir, "kernels_c4_7b_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+    vals = {}
+    for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        rows = csv.DictReader(open(os.path.join(root, f"prof_{tag}", "c4_counter_collection.csv")))
+        for r in rows:
+            k = kind(r["Kernel_Name"], int(r["Grid_Size"]))
+            if k and r["Counter_Name"] == ctr:
+                vals.setdefault((k, tag), []).append(float(r["Counter_Value"]))
+    fetch_factor = statistics.median(vals[("copy", "fetch")]) * 1024 / COPY_BYTES
+    write_factor = statistics.median(vals[("copy", "write")]) * 1024 / COPY_BYTES
+    P = 7504924672
+    algo = {"simulate": (P * 6, P * 2), "backward": (P * 6, P * 4)}
+    md = ["# HBM traffic per launch on the 7B-shaped list (c4), rocprofv3 counters", "",
+          f"Commands: `{PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with `WRITE_SIZE` "
+          "(`prof_write`).", "",
+          "Counters are KiB per dispatch.  Scale: a plain elementwise copy of 2^28 fp32 values (1 GiB read, "
+          f"1 GiB written) reads FETCH_SIZE = {fetch_factor:.4f} x and WRITE_SIZE = {write_factor:.4f} x its "
+          "true bytes; kernel readings are divided by these factors.", "",
+          "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | read GB (scaled) | written GB (scaled) | algorithmic read GB "
+          "| algorithmic written GB | traffic / algorithmic |", "|---|---|---|---|---|---|---|---|"]
+    for k in ("simulate", "backward"):
+        fk = statistics.median(vals[(k, "fetch")])
+        wk = statistics.median(vals[(k, "write")])
+        rd = fk * 1024 / fetch_factor
+        wr = wk * 1024 / write_factor
+        ar, aw = algo[k]
+        md.append(f"| {k} | {fk:.0f} | {wk:.0f} | {rd / 1e9:.3f} | {wr / 1e9:.3f} | {ar / 1e9:.3f} | {aw / 1e9:.3f} | "
+                  f"{(rd + wr) / (ar + aw):.4f} |")
+        rec = {"kernel": k, "workload": "c4", "kernel_sha": kernel_hash(),
+               "fetch_kib_per_dispatch": fk, "write_kib_per_dispatch": wk,
+               "fetch_factor": fetch_factor, "write_factor": write_factor,
+               "bytes_per_launch": round(rd + wr), "algorithmic_bytes_per_launch": ar + aw,
+               "avg_launch_ms_trace": avg.get(k),
+               "commands": [PMC_CMD.format(ctr="FETCH_SIZE", tag="fetch"), PMC_CMD.format(ctr="WRITE_SIZE", tag="write")]}
+        with open(os.path.join(out_dir, f"traffic_{k}_c4.json"), "w") as f:
+            json.dump(rec, f, indent=1)
+    with open(os.path.join(out_dir, "traffic_c4_7b.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+    print("\n".join(lines + [""] + md))
+    return 0
+
+
 def main() -> int:
     args = parse_args()
+    if args.summarize:
+        return summarize(args.summarize)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the transform is elementwise "
               "and shards by elem_offset without communication, so no multi-GPU figure is produced.",
@@ -175,6 +264,15 @@ def main() -> int:
     step_gbps = (sim_bytes + bwd_bytes) / (ms_step * 1e6)
     sim_gbps = sim_bytes / (sim_avg * 1e6)
     bwd_gbps = bwd_bytes / (bwd_avg * 1e6)
+
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        log("ran the copy calibration kernel (1 GiB read + 1 GiB written) 3 times")
 
     dominant = "simulate" if sim_avg >= bwd_avg else "backward"
     dom_gbps, dom_bytes = (sim_gbps, sim_bytes) if dominant == "simulate" else (bwd_gbps, bwd_bytes)
