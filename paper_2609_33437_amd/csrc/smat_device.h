@@ -37,6 +37,23 @@ struct alignas(16) TensorRec {
 };
 static_assert(sizeof(TensorRec) == 64, "TensorRec layout");
 
+// One chunk (kChunk elements, or the rest of a tensor) of a tensor list, self-contained so that a
+// block reaches its data with a single scalar load: pointers already advanced to the chunk's first
+// element, that element's global index, the chunk length and the tensor's parameter slot.
+struct alignas(16) ChunkRec {
+  const float* theta;
+  const void* theta0;
+  void* out;
+  const void* grad_sim;
+  float* grad_theta;
+  uint64_t e0;
+  uint32_t len;
+  uint32_t tensor;  // index into the per-step parameter table
+  uint32_t tensor_id;
+  uint32_t sflags;
+};
+static_assert(sizeof(ChunkRec) == 64, "ChunkRec layout");
+
 struct alignas(16) ParamRec {
   uint32_t thr;   // floor(keep * 2^32) when kFlagMask
   float t;        // coefficient of the task vector for kept coordinates: s/keep or s
@@ -183,6 +200,16 @@ template <typename T>
 __device__ __forceinline__ SMAT_GLOBAL T* gstore_ptr(void* p) {
   return (SMAT_GLOBAL T*)p;
 }
+// Element q of a tile-local array as a wave-uniform base plus a 32-bit byte offset, which the
+// compiler turns into the SGPR-base + VGPR-offset form of global_load/store.
+template <typename T>
+__device__ __forceinline__ const SMAT_GLOBAL T* gload_at(const void* base, uint32_t q) {
+  return (const SMAT_GLOBAL T*)((const SMAT_GLOBAL char*)base + q * (uint32_t)sizeof(T));
+}
+template <typename T>
+__device__ __forceinline__ SMAT_GLOBAL T* gstore_at(void* base, uint32_t q) {
+  return (SMAT_GLOBAL T*)((SMAT_GLOBAL char*)base + q * (uint32_t)sizeof(T));
+}
 
 // Streaming (nontemporal) quad loads/stores: every byte is touched once per pass.  A quad is
 // loaded raw (one 16 B or 8 B access) and unpacked separately, so a kernel can issue all its
@@ -194,24 +221,24 @@ template <>
 struct QuadIO<float> {
   typedef f32x4 Raw;
   static __device__ __forceinline__ Raw load_raw(const void* base, uint32_t q) {
-    return __builtin_nontemporal_load(gload_ptr<f32x4>(base) + q);
+    return __builtin_nontemporal_load(gload_at<f32x4>(base, q));
   }
   static __device__ __forceinline__ void unpack(const Raw& x, float v[4]) {
     v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
   }
   static __device__ __forceinline__ void store(void* base, uint32_t q, const float v[4]) {
     const f32x4 x = {v[0], v[1], v[2], v[3]};
-    __builtin_nontemporal_store(x, gstore_ptr<f32x4>(base) + q);
+    __builtin_nontemporal_store(x, gstore_at<f32x4>(base, q));
   }
-  static __device__ __forceinline__ float load1(const void* base, uint32_t i) { return gload_ptr<float>(base)[i]; }
-  static __device__ __forceinline__ void store1(void* base, uint32_t i, float v) { gstore_ptr<float>(base)[i] = v; }
+  static __device__ __forceinline__ float load1(const void* base, uint32_t i) { return *gload_at<float>(base, i); }
+  static __device__ __forceinline__ void store1(void* base, uint32_t i, float v) { *gstore_at<float>(base, i) = v; }
 };
 
 template <>
 struct QuadIO<Bf16> {
   typedef u32x2 Raw;
   static __device__ __forceinline__ Raw load_raw(const void* base, uint32_t q) {
-    return __builtin_nontemporal_load(gload_ptr<u32x2>(base) + q);
+    return __builtin_nontemporal_load(gload_at<u32x2>(base, q));
   }
   static __device__ __forceinline__ void unpack(const Raw& x, float v[4]) {
     v[0] = bf16_to_f32(x.x & 0xFFFFu);
@@ -221,13 +248,13 @@ struct QuadIO<Bf16> {
   }
   static __device__ __forceinline__ void store(void* base, uint32_t q, const float v[4]) {
     const u32x2 x = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-    __builtin_nontemporal_store(x, gstore_ptr<u32x2>(base) + q);
+    __builtin_nontemporal_store(x, gstore_at<u32x2>(base, q));
   }
   static __device__ __forceinline__ float load1(const void* base, uint32_t i) {
-    return bf16_to_f32(gload_ptr<uint16_t>(base)[i]);
+    return bf16_to_f32(*gload_at<uint16_t>(base, i));
   }
   static __device__ __forceinline__ void store1(void* base, uint32_t i, float v) {
-    gstore_ptr<uint16_t>(base)[i] = to_bf16(v);
+    *gstore_at<uint16_t>(base, i) = to_bf16(v);
   }
 };
 

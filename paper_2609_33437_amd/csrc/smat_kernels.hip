@@ -31,25 +31,43 @@ struct StorageBytes<Bf16> {
 // ---------------------------------------------------------------- simulate
 // One tile of `len` (<= 4 kBlock Q) elements starting at element `begin` of a tensor.  Thread x
 // owns quads x + u kBlock (u < Q) of the tile.
-template <typename T0, typename TO, int Q>
-__device__ __forceinline__ void simulate_tile(const TensorRec& R, const ParamRec& P, int64_t begin, uint32_t len,
-                                              uint64_t seed, uint32_t step) {
+// A tile handed to the element code: pointers at the tile's first element, its global index e0,
+// its length, the tensor id and the alignment flags.
+struct Tile {
+  const float* theta;
+  const void* theta0;
+  void* out;
+  const void* grad_sim;
+  float* grad_theta;
+  uint64_t e0;
+  uint32_t len;
+  uint32_t tensor_id;
+  uint32_t sflags;
+};
+
+template <typename T>
+__device__ __forceinline__ const void* advance(const void* p, int64_t elems) {
+  return static_cast<const char*>(p) + elems * StorageBytes<T>::value;
+}
+
+template <typename T0, typename TO, int Q, bool UNIFORM>
+__device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
   const uint32_t cnoise = (step << 2) | kStreamNoise;
-  const uint32_t tensor_id = R.tensor_id;
+  const uint32_t tensor_id = T.tensor_id;
+  const uint32_t len = T.len;
   const uint32_t flags = P.flags;
   const bool use_mask = (flags & kFlagMask) != 0;
   const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
   const bool use_noise = (flags & kFlagNoise) != 0;
-  const bool uniform = (flags & kFlagUniform) != 0;
   const float t = P.t, sigma = P.sigma;
   const uint32_t thr = P.thr;
 
-  const float* th = R.theta + begin;
-  const void* t0 = static_cast<const char*>(R.theta0) + begin * StorageBytes<T0>::value;
-  void* out = static_cast<char*>(R.out) + begin * StorageBytes<TO>::value;
-  const uint64_t e0 = R.elem_offset + (uint64_t)begin;
+  const float* th = T.theta;
+  const void* t0 = T.theta0;
+  void* out = T.out;
+  const uint64_t e0 = T.e0;
 
   // element by element: ragged tails and tensors whose pointers or offset break quad alignment
   auto one = [&](uint32_t i) {
@@ -59,11 +77,11 @@ __device__ __forceinline__ void simulate_tile(const TensorRec& R, const ParamRec
     bool kept = all_kept;
     if (use_mask) kept = pick(group_words(g, tensor_id, cmask, k0, k1), lane) < thr;
     float y = sim_value(QuadIO<float>::load1(th, i), QuadIO<T0>::load1(t0, i), kept, t);
-    if (use_noise) y = __builtin_fmaf(sigma, lane_noise(group_words(g, tensor_id, cnoise, k0, k1), lane, uniform), y);
+    if (use_noise) y = __builtin_fmaf(sigma, lane_noise(group_words(g, tensor_id, cnoise, k0, k1), lane, UNIFORM), y);
     QuadIO<TO>::store1(out, i, y);
   };
 
-  if (!(R.sflags & kVecSim)) {
+  if (!(T.sflags & kVecSim)) {
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
       const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
@@ -99,7 +117,7 @@ __device__ __forceinline__ void simulate_tile(const TensorRec& R, const ParamRec
         kept[u][2] = w.w2 < thr;
         kept[u][3] = w.w3 < thr;
       }
-      if (use_noise) quad_noise(group_words(g, tensor_id, cnoise, k0, k1), uniform, z[u]);
+      if (use_noise) quad_noise(group_words(g, tensor_id, cnoise, k0, k1), UNIFORM, z[u]);
     }
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
@@ -124,22 +142,33 @@ __device__ __forceinline__ void simulate_tile(const TensorRec& R, const ParamRec
   }
 }
 
+// The noise kind is fixed per tensor and step; dispatching on it once per block keeps the
+// compiler from computing both noise forms and selecting between them.
+template <typename T0, typename TO, int Q>
+__device__ __forceinline__ void simulate_tile(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
+  if (P.flags & kFlagUniform)
+    simulate_tile_kind<T0, TO, Q, true>(T, P, seed, step);
+  else
+    simulate_tile_kind<T0, TO, Q, false>(T, P, seed, step);
+}
+
 // ---------------------------------------------------------------- backward
 template <typename TG, int Q>
-__device__ __forceinline__ void backward_tile(const TensorRec& R, const ParamRec& P, int64_t begin, uint32_t len,
-                                              uint64_t seed, uint32_t step, float lambda) {
+__device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step,
+                                              float lambda) {
   const uint32_t flags = P.flags;
   if (flags & kFlagDropAll) return;  // every coordinate dropped: the gradient is left as it is
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
-  const uint32_t tensor_id = R.tensor_id;
+  const uint32_t tensor_id = T.tensor_id;
+  const uint32_t len = T.len;
   const bool use_mask = (flags & kFlagMask) != 0;
   const uint32_t thr = P.thr;
   const float c = lambda * P.t;
 
-  const void* gs = static_cast<const char*>(R.grad_sim) + begin * StorageBytes<TG>::value;
-  float* gt = R.grad_theta + begin;
-  const uint64_t e0 = R.elem_offset + (uint64_t)begin;
+  const void* gs = T.grad_sim;
+  float* gt = T.grad_theta;
+  const uint64_t e0 = T.e0;
 
   auto one = [&](uint32_t i) {
     const uint64_t e = e0 + i;
@@ -148,7 +177,7 @@ __device__ __forceinline__ void backward_tile(const TensorRec& R, const ParamRec
     if (kept) QuadIO<float>::store1(gt, i, __builtin_fmaf(c, QuadIO<TG>::load1(gs, i), QuadIO<float>::load1(gt, i)));
   };
 
-  if (!(R.sflags & kVecBwd)) {
+  if (!(T.sflags & kVecBwd)) {
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
       const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
@@ -205,10 +234,27 @@ __device__ __forceinline__ uint32_t tile_len(int64_t n, int64_t begin, int64_t t
 }
 
 template <typename T0, typename TO>
+__device__ __forceinline__ Tile tensor_tile(const TensorRec& R, int64_t begin, int64_t tile) {
+  return Tile{R.theta + begin, advance<T0>(R.theta0, begin), const_cast<void*>(advance<TO>(R.out, begin)),
+              R.grad_sim, R.grad_theta, R.elem_offset + (uint64_t)begin, tile_len(R.n, begin, tile), R.tensor_id,
+              R.sflags};
+}
+
+// Tile b of a list launch: tile (b mod tiles-per-chunk) of chunk (b / tiles-per-chunk); len 0 when the
+// tile lies past the end of a tensor's last chunk.
+template <typename T0, typename TO, typename TG>
+__device__ __forceinline__ Tile chunk_tile(const ChunkRec& C, uint32_t tile_in_chunk, int64_t tile) {
+  const int64_t begin = (int64_t)tile_in_chunk * tile;
+  const uint32_t len = begin < (int64_t)C.len ? tile_len(C.len, begin, tile) : 0u;
+  return Tile{C.theta + begin, advance<T0>(C.theta0, begin), const_cast<void*>(advance<TO>(C.out, begin)),
+              advance<TG>(C.grad_sim, begin), C.grad_theta + begin, C.e0 + (uint64_t)begin, len, C.tensor_id,
+              C.sflags};
+}
+
+template <typename T0, typename TO>
 __global__ __launch_bounds__(kBlock) void k_simulate_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step) {
   constexpr int64_t tile = tile_elems(kSimQuads);
-  const int64_t begin = (int64_t)blockIdx.x * tile;
-  simulate_tile<T0, TO, kSimQuads>(R, P, begin, tile_len(R.n, begin, tile), seed, step);
+  simulate_tile<T0, TO, kSimQuads>(tensor_tile<T0, TO>(R, (int64_t)blockIdx.x * tile, tile), P, seed, step);
 }
 
 template <typename TG>
@@ -216,37 +262,34 @@ __global__ __launch_bounds__(kBlock) void k_backward_one(TensorRec R, ParamRec P
                                                          float lambda) {
   constexpr int64_t tile = tile_elems(kBwdQuads);
   const int64_t begin = (int64_t)blockIdx.x * tile;
-  backward_tile<TG, kBwdQuads>(R, P, begin, tile_len(R.n, begin, tile), seed, step, lambda);
+  Tile T = tensor_tile<float, float>(R, begin, tile);
+  T.grad_sim = advance<TG>(R.grad_sim, begin);
+  T.grad_theta = R.grad_theta + begin;
+  backward_tile<TG, kBwdQuads>(T, P, seed, step, lambda);
 }
 
 template <typename T0, typename TO>
-__global__ __launch_bounds__(kBlock) void k_simulate_multi(const TensorRec* __restrict__ recs,
-                                                           const ParamRec* __restrict__ prms,
-                                                           const uint2* __restrict__ chunks, uint64_t seed,
+__global__ __launch_bounds__(kBlock) void k_simulate_multi(const ChunkRec* __restrict__ chunks,
+                                                           const ParamRec* __restrict__ prms, uint64_t seed,
                                                            uint32_t step) {
   constexpr int64_t tile = tile_elems(kSimQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
-  const uint2 ch = chunks[blockIdx.x / tpc];  // (tensor index, chunk index within the tensor)
-  const TensorRec R = recs[ch.x];
-  const int64_t begin = (int64_t)ch.y * kChunk + (int64_t)(blockIdx.x % tpc) * tile;
-  if (begin >= R.n) return;  // unused tile of a tensor's last chunk
-  const ParamRec P = prms[ch.x];
-  simulate_tile<T0, TO, kSimQuads>(R, P, begin, tile_len(R.n, begin, tile), seed, step);
+  const ChunkRec C = chunks[blockIdx.x / tpc];
+  const Tile T = chunk_tile<T0, TO, float>(C, blockIdx.x % tpc, tile);
+  if (T.len == 0) return;  // unused tile of a tensor's last chunk
+  simulate_tile<T0, TO, kSimQuads>(T, prms[C.tensor], seed, step);
 }
 
 template <typename TG>
-__global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __restrict__ recs,
-                                                           const ParamRec* __restrict__ prms,
-                                                           const uint2* __restrict__ chunks, uint64_t seed,
+__global__ __launch_bounds__(kBlock) void k_backward_multi(const ChunkRec* __restrict__ chunks,
+                                                           const ParamRec* __restrict__ prms, uint64_t seed,
                                                            uint32_t step, float lambda) {
   constexpr int64_t tile = tile_elems(kBwdQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
-  const uint2 ch = chunks[blockIdx.x / tpc];
-  const TensorRec R = recs[ch.x];
-  const int64_t begin = (int64_t)ch.y * kChunk + (int64_t)(blockIdx.x % tpc) * tile;
-  if (begin >= R.n) return;
-  const ParamRec P = prms[ch.x];
-  backward_tile<TG, kBwdQuads>(R, P, begin, tile_len(R.n, begin, tile), seed, step, lambda);
+  const ChunkRec C = chunks[blockIdx.x / tpc];
+  const Tile T = chunk_tile<float, float, TG>(C, blockIdx.x % tpc, tile);
+  if (T.len == 0) return;
+  backward_tile<TG, kBwdQuads>(T, prms[C.tensor], seed, step, lambda);
 }
 
 constexpr int kDebugBlock = 256;
@@ -299,29 +342,27 @@ hipError_t launch_backward_one(const TensorRec& rec, const ParamRec& prm, int gr
   return hipGetLastError();
 }
 
-hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks,
-                                 uint32_t nchunks, int theta0_dtype, int out_dtype, uint64_t seed,
-                                 uint32_t step, hipStream_t stream) {
+hipError_t launch_simulate_multi(const ChunkRec* chunks, const ParamRec* prms, uint32_t nchunks, int theta0_dtype,
+                                 int out_dtype, uint64_t seed, uint32_t step, hipStream_t stream) {
   const dim3 grid(nchunks * tiles_per_chunk(kSimQuads)), block(kBlock);
   if (theta0_dtype == 1 && out_dtype == 1)
-    k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
+    k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(chunks, prms, seed, step);
   else if (theta0_dtype == 1 && out_dtype == 0)
-    k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
+    k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(chunks, prms, seed, step);
   else if (theta0_dtype == 0 && out_dtype == 1)
-    k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
+    k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(chunks, prms, seed, step);
   else
-    k_simulate_multi<float, float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
+    k_simulate_multi<float, float><<<grid, block, 0, stream>>>(chunks, prms, seed, step);
   return hipGetLastError();
 }
 
-hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks,
-                                 uint32_t nchunks, int grad_dtype, float lambda, uint64_t seed,
-                                 uint32_t step, hipStream_t stream) {
+hipError_t launch_backward_multi(const ChunkRec* chunks, const ParamRec* prms, uint32_t nchunks, int grad_dtype,
+                                 float lambda, uint64_t seed, uint32_t step, hipStream_t stream) {
   const dim3 grid(nchunks * tiles_per_chunk(kBwdQuads)), block(kBlock);
   if (grad_dtype == 1)
-    k_backward_multi<Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+    k_backward_multi<Bf16><<<grid, block, 0, stream>>>(chunks, prms, seed, step, lambda);
   else
-    k_backward_multi<float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+    k_backward_multi<float><<<grid, block, 0, stream>>>(chunks, prms, seed, step, lambda);
   return hipGetLastError();
 }
 
