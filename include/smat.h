@@ -66,8 +66,10 @@ typedef enum smat_dtype {
 
 typedef enum smat_noise_kind {
   SMAT_NOISE_GAUSSIAN = 0, /* eps = sigma * z, z standard normal by Box-Muller */
-  SMAT_NOISE_UNIFORM = 1   /* eps = sigma * sqrt(3) * (2u - 1), u = ((w >> 8) + 1/2) 2^-24:
+  SMAT_NOISE_UNIFORM = 1,  /* eps = sigma * sqrt(3) * (2u - 1), u = ((w >> 8) + 1/2) 2^-24:
                               the paper's default U[-sqrt(3) sigma, sqrt(3) sigma] (Sec. 4.1) */
+  SMAT_NOISE_LAPLACE = 2   /* eps = -sigma sign(u - 1/2) ln(1 - 2|u - 1/2|) / sqrt(2), same u: Laplace noise
+                              of RMS sigma, compared with the other two in Sec. 4.1 */
 } smat_noise_kind;
 
 typedef enum smat_storage {

@@ -36,6 +36,9 @@ and noise in-kernel but gives no generator):
   [0, 1); r = sqrt(-2 ln u1); even lane r cos(2 pi u2), odd lane r sin(2 pi u2);
 * uniform noise (the paper's default, Sec. 4.1): eps = sigma sqrt(3) (2u - 1)
   with u = ((w >> 8) + 0.5) 2^-24, one word per element;
+* Laplace noise at the same RMS (compared in Sec. 4.1): with the same u,
+  eps = -sigma sign(u - 1/2) ln(1 - 2|u - 1/2|) / sqrt(2) (inverse CDF of a
+  Laplace law of scale sigma / sqrt(2), whose variance is sigma^2);
 * all arithmetic in fp64 from the stored input values, one final rounding to
   the output type (round to nearest even).
 """
@@ -59,6 +62,7 @@ STREAM_NOISE = 1
 
 NOISE_GAUSSIAN = 0
 NOISE_UNIFORM = 1
+NOISE_LAPLACE = 2
 
 EXPERT = 0
 SIMULATED = 1
@@ -175,6 +179,13 @@ def uniform_unit(seed: int, step: int, tensor_id: int, elem_offset: int, n: int)
     return math.sqrt(3.0) * (2.0 * u - 1.0)
 
 
+def laplace_unit(seed: int, step: int, tensor_id: int, elem_offset: int, n: int) -> np.ndarray:
+    """Zero-mean, unit-variance Laplace draw per element by inversion of its CDF."""
+    w = element_words(seed, step, tensor_id, elem_offset, n, STREAM_NOISE).astype(np.uint64)
+    u = ((w >> np.uint64(8)).astype(np.float64) + 0.5) * 2.0 ** -24 - 0.5   # in (-1/2, 1/2), never 0
+    return -np.sign(u) * np.log(1.0 - 2.0 * np.abs(u)) / math.sqrt(2.0)
+
+
 def noise(seed: int, step: int, tensor_id: int, elem_offset: int, n: int, sigma: float, kind: int) -> np.ndarray:
     """eps in fp64 (Sec. 4.1, "Perturb"); sigma == 0 gives exact zeros without drawing."""
     sg = float(np.float32(sigma))
@@ -184,6 +195,8 @@ def noise(seed: int, step: int, tensor_id: int, elem_offset: int, n: int, sigma:
         return sg * gaussian_z(seed, step, tensor_id, elem_offset, n)
     if kind == NOISE_UNIFORM:
         return sg * uniform_unit(seed, step, tensor_id, elem_offset, n)
+    if kind == NOISE_LAPLACE:
+        return sg * laplace_unit(seed, step, tensor_id, elem_offset, n)
     raise ValueError(f"unknown noise kind {kind}")
 
 
@@ -240,7 +253,7 @@ def validate_params(s: float, keep: float, sigma: float, rescale: int = 1, noise
         raise ValueError("keep must lie in [0, 1]")
     if not (math.isfinite(sigma) and sigma >= 0.0):
         raise ValueError("sigma must be finite and non-negative")
-    if noise_kind not in (NOISE_GAUSSIAN, NOISE_UNIFORM):
+    if noise_kind not in (NOISE_GAUSSIAN, NOISE_UNIFORM, NOISE_LAPLACE):
         raise ValueError("unknown noise kind")
 
 

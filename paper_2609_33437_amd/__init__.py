@@ -3,10 +3,10 @@
 `libsmat.so` (C ABI in include/smat.h) holds the HIP kernels; this package binds it with
 ctypes.  Build it with `python -m paper_2609_33437_amd.build`.
 """
-from ._lib import (EXPORTS, SMAT_BF16, SMAT_EXPERT, SMAT_F32, SMAT_NOISE_GAUSSIAN, SMAT_NOISE_UNIFORM,
+from ._lib import (EXPORTS, SMAT_BF16, SMAT_EXPERT, SMAT_F32, SMAT_NOISE_GAUSSIAN, SMAT_NOISE_LAPLACE, SMAT_NOISE_UNIFORM,
                    SMAT_SIMULATED, Plan, SmatError, lib, load_library, op_params, rng_key, smat_backward_accum,
                    smat_debug_draws, smat_simulate)
 
-__all__ = ["EXPORTS", "SMAT_BF16", "SMAT_EXPERT", "SMAT_F32", "SMAT_NOISE_GAUSSIAN", "SMAT_NOISE_UNIFORM",
+__all__ = ["EXPORTS", "SMAT_BF16", "SMAT_EXPERT", "SMAT_F32", "SMAT_NOISE_GAUSSIAN", "SMAT_NOISE_LAPLACE", "SMAT_NOISE_UNIFORM",
            "SMAT_SIMULATED", "Plan", "SmatError", "lib", "load_library", "op_params", "rng_key",
            "smat_backward_accum", "smat_debug_draws", "smat_simulate"]

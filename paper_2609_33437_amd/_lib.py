@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libsmat.so")
 
 SMAT_OK, SMAT_ERR_INVALID, SMAT_ERR_DTYPE, SMAT_ERR_STATE, SMAT_ERR_HIP = 0, 1, 2, 3, 4
 SMAT_F32, SMAT_BF16 = 0, 1
-SMAT_NOISE_GAUSSIAN, SMAT_NOISE_UNIFORM = 0, 1
+SMAT_NOISE_GAUSSIAN, SMAT_NOISE_UNIFORM, SMAT_NOISE_LAPLACE = 0, 1, 2
 SMAT_EXPERT, SMAT_SIMULATED = 0, 1
 
 STATUS_NAMES = {0: "SMAT_OK", 1: "SMAT_ERR_INVALID", 2: "SMAT_ERR_DTYPE", 3: "SMAT_ERR_STATE", 4: "SMAT_ERR_HIP"}

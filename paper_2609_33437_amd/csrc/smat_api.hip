@@ -56,7 +56,7 @@ smat_status make_param(const smat_op_params& p, ParamRec* out, const char* where
     return fail(SMAT_ERR_INVALID, "%s: keep must lie in [0, 1] (got %g)", where, (double)p.keep);
   if (!std::isfinite(p.sigma) || p.sigma < 0.f)
     return fail(SMAT_ERR_INVALID, "%s: sigma must be finite and >= 0 (got %g)", where, (double)p.sigma);
-  if (p.noise_kind != SMAT_NOISE_GAUSSIAN && p.noise_kind != SMAT_NOISE_UNIFORM)
+  if (p.noise_kind != SMAT_NOISE_GAUSSIAN && p.noise_kind != SMAT_NOISE_UNIFORM && p.noise_kind != SMAT_NOISE_LAPLACE)
     return fail(SMAT_ERR_INVALID, "%s: unknown noise kind %d", where, p.noise_kind);
   ParamRec r{};
   if (p.keep >= 1.f) {
@@ -71,6 +71,7 @@ smat_status make_param(const smat_op_params& p, ParamRec* out, const char* where
   if (p.sigma > 0.f) {
     r.flags |= smat::kFlagNoise;
     if (p.noise_kind == SMAT_NOISE_UNIFORM) r.flags |= smat::kFlagUniform;
+    if (p.noise_kind == SMAT_NOISE_LAPLACE) r.flags |= smat::kFlagLaplace;
     r.sigma = p.sigma;
   }
   *out = r;

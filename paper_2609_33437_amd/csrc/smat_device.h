@@ -19,7 +19,11 @@ enum : uint32_t {
   kFlagDropAll = 2u,  // keep == 0: every coordinate dropped, no draw
   kFlagNoise = 4u,    // sigma > 0: draw the noise
   kFlagUniform = 8u,  // uniform noise instead of Gaussian
+  kFlagLaplace = 16u, // Laplace noise instead of Gaussian
 };
+
+// Noise forms (smat_noise_kind).
+enum NoiseKind : int { kGaussian = 0, kUniform = 1, kLaplace = 2 };
 // Static flags of a tensor (TensorRec::sflags): pointers aligned for quad vectors and
 // elem_offset a multiple of 4, so quads line up with Philox groups.
 enum : uint32_t { kVecSim = 1u, kVecBwd = 2u };
@@ -141,13 +145,31 @@ __device__ __forceinline__ float uniform_unit(uint32_t w) {
   return 1.73205080756887729353f * ((float)k * 0x1p-24f);
 }
 
+// Unit-variance Laplace value by inverting its CDF at u = ((w >> 8) + 1/2) 2^-24:
+// z = -sign(u - 1/2) ln(1 - 2|u - 1/2|) / sqrt(2).  With d = 2 (w >> 8) + 1 - 2^24 (odd, nonzero),
+// u - 1/2 = d 2^-25 and 1 - 2|u - 1/2| = (2^24 - |d|) 2^-24, both exact in fp32; ln comes from the
+// hardware log2.
+__device__ __forceinline__ float laplace_unit(uint32_t w) {
+  const int32_t d = (int32_t)((w >> 8) << 1) + 1 - (1 << 24);
+  const uint32_t m = (uint32_t)(d < 0 ? -d : d);
+  const float v = (float)((1u << 24) - m) * 0x1p-24f;
+  const float mag = __builtin_amdgcn_logf(v) * -0.49012907173427356f;  // -ln(2) / sqrt(2)
+  return d < 0 ? -mag : mag;
+}
+
 // The four unit noise values of a quad.
-__device__ __forceinline__ void quad_noise(const Words& w, bool uniform, float z[4]) {
-  if (uniform) {
+template <int KIND>
+__device__ __forceinline__ void quad_noise(const Words& w, float z[4]) {
+  if (KIND == kUniform) {
     z[0] = uniform_unit(w.w0);
     z[1] = uniform_unit(w.w1);
     z[2] = uniform_unit(w.w2);
     z[3] = uniform_unit(w.w3);
+  } else if (KIND == kLaplace) {
+    z[0] = laplace_unit(w.w0);
+    z[1] = laplace_unit(w.w1);
+    z[2] = laplace_unit(w.w2);
+    z[3] = laplace_unit(w.w3);
   } else {
     box_muller(w.w0, w.w1, z[0], z[1]);
     box_muller(w.w2, w.w3, z[2], z[3]);
@@ -155,8 +177,10 @@ __device__ __forceinline__ void quad_noise(const Words& w, bool uniform, float z
 }
 
 // The unit noise value of lane `lane` of a quad, computed exactly as quad_noise does.
-__device__ __forceinline__ float lane_noise(const Words& w, uint32_t lane, bool uniform) {
-  if (uniform) return uniform_unit(pick(w, lane));
+template <int KIND>
+__device__ __forceinline__ float lane_noise(const Words& w, uint32_t lane) {
+  if (KIND == kUniform) return uniform_unit(pick(w, lane));
+  if (KIND == kLaplace) return laplace_unit(pick(w, lane));
   float zc, zs;
   if (lane & 2u)
     box_muller(w.w2, w.w3, zc, zs);

@@ -50,7 +50,7 @@ __device__ __forceinline__ const void* advance(const void* p, int64_t elems) {
   return static_cast<const char*>(p) + elems * StorageBytes<T>::value;
 }
 
-template <typename T0, typename TO, int Q, bool UNIFORM>
+template <typename T0, typename TO, int Q, int KIND>
 __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
@@ -77,7 +77,7 @@ __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec
     bool kept = all_kept;
     if (use_mask) kept = pick(group_words(g, tensor_id, cmask, k0, k1), lane) < thr;
     float y = sim_value(QuadIO<float>::load1(th, i), QuadIO<T0>::load1(t0, i), kept, t);
-    if (use_noise) y = __builtin_fmaf(sigma, lane_noise(group_words(g, tensor_id, cnoise, k0, k1), lane, UNIFORM), y);
+    if (use_noise) y = __builtin_fmaf(sigma, lane_noise<KIND>(group_words(g, tensor_id, cnoise, k0, k1), lane), y);
     QuadIO<TO>::store1(out, i, y);
   };
 
@@ -117,7 +117,7 @@ __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec
         kept[u][2] = w.w2 < thr;
         kept[u][3] = w.w3 < thr;
       }
-      if (use_noise) quad_noise(group_words(g, tensor_id, cnoise, k0, k1), UNIFORM, z[u]);
+      if (use_noise) quad_noise<KIND>(group_words(g, tensor_id, cnoise, k0, k1), z[u]);
     }
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
@@ -147,9 +147,11 @@ __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec
 template <typename T0, typename TO, int Q>
 __device__ __forceinline__ void simulate_tile(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
   if (P.flags & kFlagUniform)
-    simulate_tile_kind<T0, TO, Q, true>(T, P, seed, step);
+    simulate_tile_kind<T0, TO, Q, kUniform>(T, P, seed, step);
+  else if (P.flags & kFlagLaplace)
+    simulate_tile_kind<T0, TO, Q, kLaplace>(T, P, seed, step);
   else
-    simulate_tile_kind<T0, TO, Q, false>(T, P, seed, step);
+    simulate_tile_kind<T0, TO, Q, kGaussian>(T, P, seed, step);
 }
 
 // ---------------------------------------------------------------- backward
@@ -312,7 +314,7 @@ __global__ __launch_bounds__(kDebugBlock) void k_debug_draws(uint64_t seed, uint
     if (P.flags & kFlagMask) k = pick(wm, lane) < P.thr;
     kept[i] = k ? 1 : 0;
   }
-  if (z) z[i] = lane_noise(wn, lane, false);
+  if (z) z[i] = lane_noise<kGaussian>(wn, lane);
 }
 
 // ---------------------------------------------------------------- launchers

@@ -242,3 +242,27 @@ def test_errors_through_the_binding():
         smat.smat_simulate(x, y, x, dict(s=1.0, keep=1.0, sigma=0.0), 0, 0)   # out over theta
     with pytest.raises(smat.SmatError):
         smat.smat_backward_accum(x, x, dict(s=1.0, keep=1.0, sigma=0.0), 1.0, 0, 0)
+
+
+def test_laplace_noise_parity():
+    n = 1 << 20
+    g = torch.Generator(DEV).manual_seed(12)
+    theta = torch.randn(n, device=DEV, generator=g) * 0.02
+    # keep = 0, sigma = 1 and theta0 = 0: the output is the unit Laplace draw itself
+    zero = torch.zeros(n, device=DEV)
+    out = torch.empty(n, device=DEV, dtype=torch.float32)
+    p = dict(s=0.5, keep=0.0, sigma=1.0, rescale=1, noise_kind=oracle.NOISE_LAPLACE)
+    smat.smat_simulate(theta, zero, out, p, 21, 4, 9)
+    torch.cuda.synchronize()
+    want = oracle.laplace_unit(21, 4, 9, 0, n)
+    err = np.abs(out.cpu().numpy().astype(np.float64) - want)
+    print(f"max |z_gpu - z| over {n} Laplace draws: {err.max():.3e}")
+    assert err.max() <= Z_TOL
+    # the full transform with a mask, bf16 and f32 outputs
+    theta0 = (theta + torch.randn(n, device=DEV, generator=g) * 1e-3).to(torch.bfloat16)
+    p = dict(s=0.8, keep=0.4, sigma=2e-3, rescale=1, noise_kind=oracle.NOISE_LAPLACE)
+    for dt in (torch.bfloat16, torch.float32):
+        o = torch.empty(n, device=DEV, dtype=dt)
+        dist = compare_simulate(theta, theta0, o, p, 21, 5, 9, 8)
+        if dist is not None:
+            assert dist.max(initial=0) <= 1

@@ -137,3 +137,29 @@ def test_offset_consistency():
     fk = oracle.keep_mask(2, 5, 9, 0, 1000, 0.3)
     pk = oracle.keep_mask(2, 5, 9, 501, 499, 0.3)
     np.testing.assert_array_equal(fk[501:], pk)
+
+
+def test_laplace_noise_moments_ks_and_range():
+    z = oracle.laplace_unit(4, 2, 6, 0, N)
+    assert abs(z.mean()) <= 5 / math.sqrt(N)
+    # Var of a unit-variance Laplace sample variance: (E z^4 - 1)/N with E z^4 = 6
+    assert abs(z.var() - 1.0) <= 5 * math.sqrt(5.0 / N)
+    assert stats.kstest(z, "laplace", args=(0.0, 1 / math.sqrt(2))).pvalue > 1e-4
+    # the most extreme uniforms give |z| = ln(2^24) / sqrt(2), never infinity
+    assert np.all(np.abs(z) <= 24 * math.log(2) / math.sqrt(2) + 1e-12)
+    # the median word (u just above 1/2) gives a tiny positive value, its mirror the same negative one
+    eps = oracle.noise(4, 2, 6, 0, 1000, 0.5, oracle.NOISE_LAPLACE)
+    np.testing.assert_allclose(eps, 0.5 * z[:1000], rtol=1e-15)
+
+
+def test_laplace_inverse_cdf_special_values():
+    # u = (k + 1/2) 2^-24 for k = 2^23 (just above the median) maps to -ln(1 - 2^-24)/sqrt(2) > 0;
+    # k = 2^23 - 1 is its mirror image; k = 0 gives the most negative value
+    def z_of_k(k):
+        u = (k + 0.5) * 2.0 ** -24 - 0.5
+        return -math.copysign(1.0, u) * math.log(1 - 2 * abs(u)) / math.sqrt(2)
+    assert z_of_k(2 ** 23) == -z_of_k(2 ** 23 - 1) > 0
+    assert abs(z_of_k(0) + 24 * math.log(2) / math.sqrt(2)) < 1e-9
+    # the oracle uses exactly this map on the top 24 bits of each noise word
+    w = oracle.element_words(8, 1, 2, 0, 64, oracle.STREAM_NOISE)
+    np.testing.assert_allclose(oracle.laplace_unit(8, 1, 2, 0, 64), [z_of_k(int(x) >> 8) for x in w], rtol=1e-14)
