@@ -60,6 +60,9 @@ def parse_args():
     ap.add_argument("--cpu-sample", type=int, default=1 << 27, help="most elements the CPU oracle baseline visits")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU work budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--offload", action="store_true",
+                    help="theta0 in pinned host memory, copied into the simulated buffers at each restore; "
+                         "also reports the prefetch's host-link rate")
     ap.add_argument("--summarize", metavar="DIR",
                     help="turn rocprofv3 CSV output under DIR (prof_trace/, prof_fetch/, prof_write/) into the "
                          "summaries under profiles/ and exit")
@@ -216,7 +219,35 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"generated in {time.perf_counter() - t_gen:.1f} s")
 
-    plan = smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta)
+    prefetch = None
+    if args.offload:
+        if cfg.theta0_dtype != cfg.out_dtype:
+            print("offload mode needs theta0 and the buffers in one dtype", file=sys.stderr)
+            return 1
+        log("copying theta0 into pinned host memory")
+        hosts = [t.to("cpu").pin_memory() for t in inp.theta0]
+        inp.theta0 = hosts  # the device copies are released; the CPU baseline reads the host copies
+        torch.cuda.empty_cache()
+        plan = smat.Plan(inp.theta, outs, None, inp.grad_sim, inp.grad_theta, offload=True, theta0_hosts=hosts,
+                         dtypes=(smat.SMAT_BF16 if cfg.theta0_dtype == "bf16" else smat.SMAT_F32,) * 2 +
+                                (smat.SMAT_BF16 if cfg.grad_dtype == "bf16" else smat.SMAT_F32,))
+        # one prefetch on its own: restore (starts the copy) then a simulate that has to wait for it
+        plan.set_params(workloads.step_params(cfg, inp.settings, 0))
+        plan.simulate(cfg.smat_seed, 0)
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        torch.cuda.synchronize()
+        t_pf = time.perf_counter()
+        plan.switch_storage(smat.SMAT_EXPERT)
+        plan.close()  # waits for the plan's copy stream
+        pf_s = time.perf_counter() - t_pf
+        nb = sum(h.numel() * h.element_size() for h in hosts)
+        prefetch = {"bytes": nb, "seconds": round(pf_s, 4), "gbps": round(nb / pf_s / 1e9, 2)}
+        log(f"theta0 prefetch: {nb / 1e9:.2f} GB in {pf_s * 1e3:.1f} ms = {nb / pf_s / 1e9:.1f} GB/s")
+        plan = smat.Plan(inp.theta, outs, None, inp.grad_sim, inp.grad_theta, offload=True, theta0_hosts=hosts,
+                         dtypes=(smat.SMAT_BF16 if cfg.theta0_dtype == "bf16" else smat.SMAT_F32,) * 2 +
+                                (smat.SMAT_BF16 if cfg.grad_dtype == "bf16" else smat.SMAT_F32,))
+    else:
+        plan = smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta)
     K, W = args.steps, args.warmup
     # the hot path runs on simulated steps only: every step, or steps = 3 mod 4 for the periodic list
     step_ids = [k * cfg.period + cfg.period - 1 for k in range(W + K)]
@@ -307,6 +338,11 @@ def main() -> int:
         "roofline": roofline,
         "cpu_baseline": None,
     }
+    if cfg.period > 1:
+        result["config"]["ms_per_training_step_avg"] = round(ms_step / cfg.period, 4)
+    if prefetch is not None:
+        result["config"]["mode"] = "offload: theta0 in pinned host memory, copied into the buffers at each restore"
+        result["offload_prefetch"] = prefetch
     if not args.no_cpu_baseline:
         last = W + K - 1
         result["cpu_baseline"] = cpu_baseline(cfg, inp, params[last], step_ids[last], args.cpu_sample,

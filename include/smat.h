@@ -196,13 +196,13 @@ smat_status smat_backward_accum_multi(smat_plan* plan, uint64_t seed, uint32_t s
                                       hipStream_t stream);
 
 /* smat_switch_storage -- point the model at the simulated buffer (SMAT_SIMULATED) or back at the
- * expert storage (SMAT_EXPERT) (Sec. 4.3, "Parameter storage switching").  The plan keeps a
- * device table of the active pointer of every tensor (see smat_plan_active_ptrs) and rewrites it
- * on `stream`.  SMAT_SIMULATED requires a simulate since the last restore and is an error when
- * already active; SMAT_EXPERT is idempotent.  In offload mode, restoring the expert storage also
- * starts the theta0 prefetch into the buffers on the plan's copy stream once `stream` has
- * reached this point; the next simulate waits for it.  Expert storage is never written.
- * Errors: SMAT_ERR_INVALID (bad `to`), SMAT_ERR_STATE, SMAT_ERR_HIP. */
+ * expert storage (SMAT_EXPERT) (Sec. 4.3, "Parameter storage switching").  The plan holds one
+ * device table of per-tensor pointers for each storage; switching selects the active one (see
+ * smat_plan_active_ptrs) and moves no data.  SMAT_SIMULATED requires a simulate since the last
+ * restore and is an error when already active; SMAT_EXPERT is idempotent.  In offload mode,
+ * restoring the expert storage also starts the theta0 prefetch into the buffers on the plan's copy
+ * stream once `stream` has reached this point; the next simulate waits for it.  Expert storage is
+ * never written.  Errors: SMAT_ERR_INVALID (bad `to`), SMAT_ERR_STATE, SMAT_ERR_HIP. */
 smat_status smat_switch_storage(smat_plan* plan, int32_t to, hipStream_t stream);
 
 /* smat_plan_state -- the active storage (an smat_storage value) in *state. */
@@ -210,7 +210,8 @@ smat_status smat_plan_state(const smat_plan* plan, int32_t* state);
 
 /* smat_plan_active_ptrs -- the active pointer of every tensor.  host_out, if not NULL, receives
  * count pointers; *dev_table, if dev_table is not NULL, receives the device address of the
- * count-entry pointer table that smat_switch_storage maintains (inside the workspace). */
+ * count-entry pointer table of the active storage (inside the workspace; the address changes with
+ * each switch, the two tables themselves never do). */
 smat_status smat_plan_active_ptrs(const smat_plan* plan, void** host_out, void** dev_table);
 
 /* smat_plan_destroy -- wait for the plan's own pending uploads and prefetches, then free its host

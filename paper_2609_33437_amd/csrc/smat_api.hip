@@ -189,8 +189,8 @@ struct smat_plan {
   std::vector<ChunkRec> chunks;
   std::vector<void*> expert_ptrs, sim_ptrs;
 
-  // workspace layout: [chunk table][active table][expert table][simulated table][params]
-  size_t off_chunks = 0, off_active = 0, off_expert = 0, off_sim = 0, off_params = 0, ws_bytes = 0;
+  // workspace layout: [chunk table][expert pointer table][simulated pointer table][params]
+  size_t off_chunks = 0, off_expert = 0, off_sim = 0, off_params = 0, ws_bytes = 0;
   char* ws = nullptr;
 
   // pinned staging for the asynchronous uploads: the static tables once, the params every step
@@ -356,8 +356,6 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
   size_t off = 0;
   p->off_chunks = off;
   off = align256(off + sizeof(ChunkRec) * p->chunks.size());
-  p->off_active = off;
-  off = align256(off + sizeof(void*) * count);
   p->off_expert = off;
   off = align256(off + sizeof(void*) * count);
   p->off_sim = off;
@@ -388,7 +386,6 @@ extern "C" smat_status smat_plan_bind_workspace(smat_plan* p, void* workspace, s
     SMAT_HIP(hipHostMalloc((void**)&s, sizeof(ParamRec) * std::max(p->count, 1), hipHostMallocDefault));
   std::memset(p->static_staging, 0, static_bytes);
   std::memcpy(p->static_staging + p->off_chunks, p->chunks.data(), sizeof(ChunkRec) * p->chunks.size());
-  std::memcpy(p->static_staging + p->off_active, p->expert_ptrs.data(), sizeof(void*) * p->count);
   std::memcpy(p->static_staging + p->off_expert, p->expert_ptrs.data(), sizeof(void*) * p->count);
   std::memcpy(p->static_staging + p->off_sim, p->sim_ptrs.data(), sizeof(void*) * p->count);
   SMAT_HIP(hipEventCreateWithFlags(&p->ev_static, hipEventDisableTiming));
@@ -465,16 +462,15 @@ extern "C" smat_status smat_switch_storage(smat_plan* p, int32_t to, hipStream_t
   if (!p) return fail(SMAT_ERR_INVALID, "smat_switch_storage: null plan");
   if (to != SMAT_EXPERT && to != SMAT_SIMULATED) return fail(SMAT_ERR_INVALID, "smat_switch_storage: bad target %d", to);
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_switch_storage: no workspace bound");
-  const size_t table = sizeof(void*) * p->count;
+  // the pointer tables of both storages are prebuilt in the workspace: switching only changes which
+  // one is active, so it moves no data and launches nothing
   if (to == SMAT_SIMULATED) {
     if (p->state == SMAT_SIMULATED) return fail(SMAT_ERR_STATE, "smat_switch_storage: simulated storage already active");
     if (!p->fresh) return fail(SMAT_ERR_STATE, "smat_switch_storage: no simulate since the last restore");
-    if (table) SMAT_HIP(hipMemcpyAsync(p->ws + p->off_active, p->ws + p->off_sim, table, hipMemcpyDeviceToDevice, stream));
     p->state = SMAT_SIMULATED;
     return SMAT_OK;
   }
   if (p->state == SMAT_EXPERT) return SMAT_OK;  // restoring is idempotent
-  if (table) SMAT_HIP(hipMemcpyAsync(p->ws + p->off_active, p->ws + p->off_expert, table, hipMemcpyDeviceToDevice, stream));
   p->state = SMAT_EXPERT;
   p->fresh = false;
   if (p->offload) return enqueue_prefetch(p, stream);
@@ -493,7 +489,7 @@ extern "C" smat_status smat_plan_active_ptrs(const smat_plan* p, void** host_out
     const std::vector<void*>& src = p->state == SMAT_SIMULATED ? p->sim_ptrs : p->expert_ptrs;
     std::copy(src.begin(), src.end(), host_out);
   }
-  if (dev_table) *dev_table = p->ws ? p->ws + p->off_active : nullptr;
+  if (dev_table) *dev_table = p->ws ? p->ws + (p->state == SMAT_SIMULATED ? p->off_sim : p->off_expert) : nullptr;
   return SMAT_OK;
 }
 

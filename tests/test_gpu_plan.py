@@ -176,8 +176,9 @@ def test_switch_states_and_active_table(mini):
         plan.backward_accum(1, 0, 1.0)
         plan.switch_storage(smat.SMAT_EXPERT)
         plan.switch_storage(smat.SMAT_EXPERT)                 # idempotent
-        host_ptrs, _ = plan.active_ptrs()
+        host_ptrs, dev_table = plan.active_ptrs()
         assert host_ptrs == [t.data_ptr() for t in th]
+        off = dev_table - plan.workspace.data_ptr()
         torch.cuda.synchronize()
         table = plan.workspace[off:off + 8 * cfg.count].cpu().view(torch.int64).tolist()
         assert table == [t.data_ptr() for t in th]
