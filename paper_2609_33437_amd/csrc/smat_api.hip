@@ -12,7 +12,6 @@
 #include "smat.h"
 #include "smat_launch.h"
 
-using smat::ChunkRec;
 using smat::ParamRec;
 using smat::TensorRec;
 
@@ -186,11 +185,11 @@ struct smat_plan {
   bool has_grads = false;
   std::vector<smat_tensor_desc> descs;
   std::vector<TensorRec> recs;
-  std::vector<ChunkRec> chunks;
+  std::vector<uint2> chunks;  // (tensor index, chunk index within the tensor)
   std::vector<void*> expert_ptrs, sim_ptrs;
 
-  // workspace layout: [chunk table][expert pointer table][simulated pointer table][params]
-  size_t off_chunks = 0, off_expert = 0, off_sim = 0, off_params = 0, ws_bytes = 0;
+  // workspace layout: [tensor records][chunk table][expert pointer table][simulated pointer table][params]
+  size_t off_recs = 0, off_chunks = 0, off_expert = 0, off_sim = 0, off_params = 0, ws_bytes = 0;
   char* ws = nullptr;
 
   // pinned staging for the asynchronous uploads: the static tables once, the params every step
@@ -332,30 +331,17 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
     delete p;
     return fail(SMAT_ERR_INVALID, "smat_plan_create: tensor list too large for one launch");
   }
-  // one self-contained record per kChunk elements: pointers advanced to the chunk's first element
   p->chunks.reserve(nchunks);
-  const size_t t0b = dtype_bytes(theta0_dtype), ob = dtype_bytes(out_dtype), gb = dtype_bytes(grad_dtype);
   for (int32_t i = 0; i < count; ++i) {
-    const TensorRec& r = p->recs[i];
-    for (int64_t b = 0; b < r.n; b += smat::kChunk) {
-      ChunkRec c{};
-      c.theta = r.theta + b;
-      c.theta0 = static_cast<const char*>(r.theta0) + b * t0b;
-      c.out = static_cast<char*>(r.out) + b * ob;
-      c.grad_sim = r.grad_sim ? static_cast<const char*>(r.grad_sim) + b * gb : nullptr;
-      c.grad_theta = r.grad_theta ? r.grad_theta + b : nullptr;
-      c.e0 = r.elem_offset + (uint64_t)b;
-      c.len = (uint32_t)std::min<int64_t>(smat::kChunk, r.n - b);
-      c.tensor = (uint32_t)i;
-      c.tensor_id = r.tensor_id;
-      c.sflags = r.sflags;
-      p->chunks.push_back(c);
-    }
+    const uint32_t nc = (uint32_t)((p->descs[i].n + smat::kChunk - 1) / smat::kChunk);
+    for (uint32_t c = 0; c < nc; ++c) p->chunks.push_back(make_uint2((uint32_t)i, c));
   }
 
   size_t off = 0;
+  p->off_recs = off;
+  off = align256(off + sizeof(TensorRec) * count);
   p->off_chunks = off;
-  off = align256(off + sizeof(ChunkRec) * p->chunks.size());
+  off = align256(off + sizeof(uint2) * p->chunks.size());
   p->off_expert = off;
   off = align256(off + sizeof(void*) * count);
   p->off_sim = off;
@@ -385,7 +371,8 @@ extern "C" smat_status smat_plan_bind_workspace(smat_plan* p, void* workspace, s
   for (ParamRec*& s : p->params_staging)
     SMAT_HIP(hipHostMalloc((void**)&s, sizeof(ParamRec) * std::max(p->count, 1), hipHostMallocDefault));
   std::memset(p->static_staging, 0, static_bytes);
-  std::memcpy(p->static_staging + p->off_chunks, p->chunks.data(), sizeof(ChunkRec) * p->chunks.size());
+  std::memcpy(p->static_staging + p->off_recs, p->recs.data(), sizeof(TensorRec) * p->count);
+  std::memcpy(p->static_staging + p->off_chunks, p->chunks.data(), sizeof(uint2) * p->chunks.size());
   std::memcpy(p->static_staging + p->off_expert, p->expert_ptrs.data(), sizeof(void*) * p->count);
   std::memcpy(p->static_staging + p->off_sim, p->sim_ptrs.data(), sizeof(void*) * p->count);
   SMAT_HIP(hipEventCreateWithFlags(&p->ev_static, hipEventDisableTiming));
@@ -436,8 +423,9 @@ extern "C" smat_status smat_simulate_multi(smat_plan* p, uint64_t seed, uint32_t
     return fail(SMAT_ERR_STATE, "smat_simulate_multi: the simulated storage is active (restore the expert first)");
   if (p->offload && p->prefetch_pending) SMAT_HIP(hipStreamWaitEvent(stream, p->ev_prefetch, 0));
   if (!p->chunks.empty())
-    SMAT_HIP(smat::launch_simulate_multi(reinterpret_cast<const ChunkRec*>(p->ws + p->off_chunks),
+    SMAT_HIP(smat::launch_simulate_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
                                          reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                         reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
                                          (uint32_t)p->chunks.size(), p->t0_dt, p->out_dt, seed, step, stream));
   p->fresh = true;
   return SMAT_OK;
@@ -452,8 +440,9 @@ extern "C" smat_status smat_backward_accum_multi(smat_plan* p, uint64_t seed, ui
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: no workspace bound");
   if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: parameters never set");
   if (!p->chunks.empty())
-    SMAT_HIP(smat::launch_backward_multi(reinterpret_cast<const ChunkRec*>(p->ws + p->off_chunks),
+    SMAT_HIP(smat::launch_backward_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
                                          reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                         reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
                                          (uint32_t)p->chunks.size(), p->g_dt, lambda, seed, step, stream));
   return SMAT_OK;
 }

@@ -41,23 +41,6 @@ struct alignas(16) TensorRec {
 };
 static_assert(sizeof(TensorRec) == 64, "TensorRec layout");
 
-// One chunk (kChunk elements, or the rest of a tensor) of a tensor list, self-contained so that a
-// block reaches its data with a single scalar load: pointers already advanced to the chunk's first
-// element, that element's global index, the chunk length and the tensor's parameter slot.
-struct alignas(16) ChunkRec {
-  const float* theta;
-  const void* theta0;
-  void* out;
-  const void* grad_sim;
-  float* grad_theta;
-  uint64_t e0;
-  uint32_t len;
-  uint32_t tensor;  // index into the per-step parameter table
-  uint32_t tensor_id;
-  uint32_t sflags;
-};
-static_assert(sizeof(ChunkRec) == 64, "ChunkRec layout");
-
 struct alignas(16) ParamRec {
   uint32_t thr;   // floor(keep * 2^32) when kFlagMask
   float t;        // coefficient of the task vector for kept coordinates: s/keep or s

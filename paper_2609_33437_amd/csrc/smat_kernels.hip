@@ -242,15 +242,18 @@ __device__ __forceinline__ Tile tensor_tile(const TensorRec& R, int64_t begin, i
               R.sflags};
 }
 
-// Tile b of a list launch: tile (b mod tiles-per-chunk) of chunk (b / tiles-per-chunk); len 0 when the
-// tile lies past the end of a tensor's last chunk.
+// Tile b of a list launch: tile (b mod tiles-per-chunk) of chunk (b / tiles-per-chunk), the chunk
+// table giving (tensor index, chunk index within the tensor).  The chunk table (8 B per 16K
+// elements) and the tensor records (64 B per tensor) are small enough to stay in L2 while the
+// kernel streams the tensors.  len is 0 when the tile lies past the end of a tensor.
 template <typename T0, typename TO, typename TG>
-__device__ __forceinline__ Tile chunk_tile(const ChunkRec& C, uint32_t tile_in_chunk, int64_t tile) {
-  const int64_t begin = (int64_t)tile_in_chunk * tile;
-  const uint32_t len = begin < (int64_t)C.len ? tile_len(C.len, begin, tile) : 0u;
-  return Tile{C.theta + begin, advance<T0>(C.theta0, begin), const_cast<void*>(advance<TO>(C.out, begin)),
-              advance<TG>(C.grad_sim, begin), C.grad_theta + begin, C.e0 + (uint64_t)begin, len, C.tensor_id,
-              C.sflags};
+__device__ __forceinline__ Tile list_tile(const TensorRec& R, uint32_t chunk, uint32_t tile_in_chunk, int64_t tile) {
+  const int64_t begin = (int64_t)chunk * kChunk + (int64_t)tile_in_chunk * tile;
+  Tile T = tensor_tile<T0, TO>(R, begin, tile);
+  T.grad_sim = advance<TG>(R.grad_sim, begin);
+  T.grad_theta = R.grad_theta + begin;
+  if (begin >= R.n) T.len = 0;
+  return T;
 }
 
 template <typename T0, typename TO>
@@ -271,27 +274,29 @@ __global__ __launch_bounds__(kBlock) void k_backward_one(TensorRec R, ParamRec P
 }
 
 template <typename T0, typename TO>
-__global__ __launch_bounds__(kBlock) void k_simulate_multi(const ChunkRec* __restrict__ chunks,
-                                                           const ParamRec* __restrict__ prms, uint64_t seed,
+__global__ __launch_bounds__(kBlock) void k_simulate_multi(const TensorRec* __restrict__ recs,
+                                                           const ParamRec* __restrict__ prms,
+                                                           const uint2* __restrict__ chunks, uint64_t seed,
                                                            uint32_t step) {
   constexpr int64_t tile = tile_elems(kSimQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
-  const ChunkRec C = chunks[blockIdx.x / tpc];
-  const Tile T = chunk_tile<T0, TO, float>(C, blockIdx.x % tpc, tile);
+  const uint2 ch = chunks[blockIdx.x / tpc];
+  const Tile T = list_tile<T0, TO, float>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;  // unused tile of a tensor's last chunk
-  simulate_tile<T0, TO, kSimQuads>(T, prms[C.tensor], seed, step);
+  simulate_tile<T0, TO, kSimQuads>(T, prms[ch.x], seed, step);
 }
 
 template <typename TG>
-__global__ __launch_bounds__(kBlock) void k_backward_multi(const ChunkRec* __restrict__ chunks,
-                                                           const ParamRec* __restrict__ prms, uint64_t seed,
+__global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __restrict__ recs,
+                                                           const ParamRec* __restrict__ prms,
+                                                           const uint2* __restrict__ chunks, uint64_t seed,
                                                            uint32_t step, float lambda) {
   constexpr int64_t tile = tile_elems(kBwdQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
-  const ChunkRec C = chunks[blockIdx.x / tpc];
-  const Tile T = chunk_tile<float, float, TG>(C, blockIdx.x % tpc, tile);
+  const uint2 ch = chunks[blockIdx.x / tpc];
+  const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;
-  backward_tile<TG, kBwdQuads>(T, prms[C.tensor], seed, step, lambda);
+  backward_tile<TG, kBwdQuads>(T, prms[ch.x], seed, step, lambda);
 }
 
 constexpr int kDebugBlock = 256;
@@ -344,27 +349,27 @@ hipError_t launch_backward_one(const TensorRec& rec, const ParamRec& prm, int gr
   return hipGetLastError();
 }
 
-hipError_t launch_simulate_multi(const ChunkRec* chunks, const ParamRec* prms, uint32_t nchunks, int theta0_dtype,
-                                 int out_dtype, uint64_t seed, uint32_t step, hipStream_t stream) {
+hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
+                                 int theta0_dtype, int out_dtype, uint64_t seed, uint32_t step, hipStream_t stream) {
   const dim3 grid(nchunks * tiles_per_chunk(kSimQuads)), block(kBlock);
   if (theta0_dtype == 1 && out_dtype == 1)
-    k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(chunks, prms, seed, step);
+    k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
   else if (theta0_dtype == 1 && out_dtype == 0)
-    k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(chunks, prms, seed, step);
+    k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
   else if (theta0_dtype == 0 && out_dtype == 1)
-    k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(chunks, prms, seed, step);
+    k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
   else
-    k_simulate_multi<float, float><<<grid, block, 0, stream>>>(chunks, prms, seed, step);
+    k_simulate_multi<float, float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
   return hipGetLastError();
 }
 
-hipError_t launch_backward_multi(const ChunkRec* chunks, const ParamRec* prms, uint32_t nchunks, int grad_dtype,
-                                 float lambda, uint64_t seed, uint32_t step, hipStream_t stream) {
+hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
+                                 int grad_dtype, float lambda, uint64_t seed, uint32_t step, hipStream_t stream) {
   const dim3 grid(nchunks * tiles_per_chunk(kBwdQuads)), block(kBlock);
   if (grad_dtype == 1)
-    k_backward_multi<Bf16><<<grid, block, 0, stream>>>(chunks, prms, seed, step, lambda);
+    k_backward_multi<Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
   else
-    k_backward_multi<float><<<grid, block, 0, stream>>>(chunks, prms, seed, step, lambda);
+    k_backward_multi<float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
   return hipGetLastError();
 }
 
