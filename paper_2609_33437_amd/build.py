@@ -35,6 +35,14 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: the HIP toolchain is required to build libsmat")
 
 
+def hipcc_available() -> bool:
+    try:
+        hipcc()
+        return True
+    except RuntimeError:
+        return False
+
+
 def build(verbose: bool = False) -> str:
     """Compile every HIP source into libsmat.so (always recompiles); returns its path."""
     tmp = LIB + f".tmp{os.getpid()}"

@@ -268,3 +268,40 @@ def test_empty_and_tiny_lists():
         p.simulate(0, 0)
         torch.cuda.synchronize()
     assert out[1].float().item() == 1.0
+
+
+def test_offload_periodic_training_cycle_matches_resident(mini):
+    # 12 steps with t = 4: the simulated steps 3, 7, 11 run simulate -> switch(SIM) -> backward ->
+    # switch(EXPERT); in offload mode every restore refills the buffers with theta0 from pinned host
+    # memory while the ordinary steps run.  Both modes must give the same bytes at every simulated
+    # step, and the same accumulated gradient.
+    cfg, inp = mini
+    th, t0, gs, gt_res, out_res = to_dev(inp)
+    gt_off = [g.clone() for g in gt_res]
+    hosts = [t.contiguous().pin_memory() for t in inp.theta0]
+    bufs = [torch.empty(t.numel(), dtype=torch.bfloat16, device=DEV) for t in th]
+    dt = (smat.SMAT_BF16, smat.SMAT_BF16, smat.SMAT_BF16)
+    with smat.Plan(th, out_res, t0, gs, gt_res) as res, \
+            smat.Plan(th, bufs, None, gs, gt_off, offload=True, theta0_hosts=hosts, dtypes=dt) as off:
+        for step in range(12):
+            if not oracle.is_simulated_step(step, 4):
+                continue
+            params = workloads.step_params(cfg, inp.settings, step)
+            for plan in (res, off):
+                plan.set_params(params)
+                plan.simulate(cfg.smat_seed, step)
+                plan.switch_storage(smat.SMAT_SIMULATED)
+            torch.cuda.synchronize()
+            for a, b in zip(out_res, bufs):
+                assert torch.equal(bits(a), bits(b)), f"step {step}"
+            host_ptrs, _ = off.active_ptrs()
+            assert host_ptrs == [b.data_ptr() for b in bufs]
+            for plan in (res, off):
+                plan.backward_accum(cfg.smat_seed, step, 0.25)
+                plan.switch_storage(smat.SMAT_EXPERT)
+        torch.cuda.synchronize()
+    for a, b in zip(gt_res, gt_off):
+        assert torch.equal(bits(a), bits(b))
+    # after the last restore the buffers hold theta0 again
+    for b, h in zip(bufs, inp.theta0):
+        assert torch.equal(bits(b.cpu()), bits(h.view(-1)))
