@@ -134,8 +134,8 @@ smat_status smat_debug_draws(smat_rng_key key, int64_t n, smat_op_params p, uint
                              uint32_t* noise_words, uint8_t* kept, float* z, hipStream_t stream);
 
 /* ---------------------------------------------------------------- ragged tensor lists
- * A plan covers a fixed list of parameter tensors ("compatible tensors" handled by one
- * launch, Sec. 4.3 "Kernel fusion").  It holds host-side tables only; its device tables live
+ * A plan covers a fixed list of parameter tensors processed by one launch per operation
+ * (the grouping of tensors of Sec. 4.3, "Kernel fusion").  It holds host-side tables only; its device tables live
  * in a caller-allocated workspace.  One launch per operation covers the whole list, split
  * into equal-sized chunks so that thousands of small vectors and a few huge matrices share
  * the GPU evenly. */
