@@ -173,7 +173,8 @@ def test_closed_forms_exact():
 # sizes around quads and chunks; element offsets and base misalignment that force the per-element path
 @pytest.mark.parametrize("n,shift,off", [(1, 0, 0), (3, 0, 0), (4, 0, 0), (5, 0, 0), (4095, 0, 0),
                                           (16384, 0, 0), (16384 + 7, 0, 0), (3 * 16384 + 1, 0, 4),
-                                          (50000, 1, 0), (50000, 0, 2), (50001, 3, 5), (70000, 2, 2 ** 33 + 1)])
+                                          (50000, 1, 0), (50000, 0, 2), (50001, 3, 5), (70000, 2, 2 ** 33 + 1),
+                                          (70000, 0, 2 ** 34 + 4096)])
 @pytest.mark.parametrize("dts", [("bf16", "bf16", "bf16"), ("f32", "f32", "f32"), ("f32", "bf16", "bf16")])
 def test_ragged_and_misaligned(n, shift, off, dts):
     tmap = {"bf16": torch.bfloat16, "f32": torch.float32}
@@ -266,3 +267,40 @@ def test_laplace_noise_parity():
         dist = compare_simulate(theta, theta0, o, p, 21, 5, 9, 8)
         if dist is not None:
             assert dist.max(initial=0) <= 1
+
+
+def test_tensor_beyond_2_32_elements():
+    # one tensor of 2^32 + 1029 elements: 64-bit element indices in both entry points, the last
+    # chunk's ragged tail, and element offsets whose Philox group index exceeds 32 bits
+    n = (1 << 32) + 1029
+    theta = torch.empty(n, device=DEV, dtype=torch.float32)
+    theta0 = torch.empty(n, device=DEV, dtype=torch.bfloat16)
+    out = torch.empty(n, device=DEV, dtype=torch.bfloat16)
+    g = torch.Generator(DEV).manual_seed(13)
+    step_ = 1 << 28
+    for a in range(0, n, step_):   # fill in slices to bound the temporaries
+        b = min(n, a + step_)
+        theta[a:b].normal_(0.0, 0.02, generator=g)
+        theta0[a:b] = (theta[a:b] + torch.randn(b - a, device=DEV, generator=g) * 1e-3).to(torch.bfloat16)
+    p = dict(s=0.6, keep=0.3, sigma=1e-3, rescale=1, noise_kind=0)
+    seed, step, tid = 0x5EED1234, 9, 77
+    smat.smat_simulate(theta, theta0, out, p, seed, step, tid)
+    torch.cuda.synchronize()
+    windows = [(0, 4096), ((1 << 31) - 17, (1 << 31) + 4099), ((1 << 32) - 2048, n)]
+    for a, b in windows:
+        th = theta[a:b].cpu().numpy()
+        t0 = theta0[a:b].cpu().view(torch.int16).numpy().view(np.uint16)
+        got = out[a:b].cpu().view(torch.int16).numpy().view(np.uint16)
+        y, kept, eps = oracle.simulate_f64(th, t0, "bf16", p, seed, step, tid, a)
+        coef = np.where(kept, oracle.coefficient(0.6, 0.3, 1), 0.0)
+        ok, _ = check_theta_tilde(got, "bf16", y, th, oracle.as_f64(t0, "bf16"), coef, eps, 1e-3)
+        assert ok.all(), f"window [{a},{b})"
+    # the list entry point over the same tensor produces the same bytes
+    out2 = torch.empty_like(out)
+    with smat.Plan([theta], [out2], [theta0], tensor_ids=[tid]) as plan:
+        plan.set_params([p])
+        plan.simulate(seed, step)
+        torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), out2.view(torch.int16))
+    del theta, theta0, out, out2
+    torch.cuda.empty_cache()
