@@ -318,6 +318,63 @@ def backward_accum(grad_sim, grad_sim_dtype: str, grad_theta, p: dict, lam: floa
     return np.where(kept, new, gt)
 
 
+# ------------------------------------------------------------------ fused optimizer step
+def validate_adamw(hp: dict) -> None:
+    for k in ("lr", "beta1", "beta2", "eps", "weight_decay", "grad_scale"):
+        if not math.isfinite(hp[k]):
+            raise ValueError(f"{k} must be finite")
+    if not (0.0 <= hp["beta1"] < 1.0 and 0.0 <= hp["beta2"] < 1.0):
+        raise ValueError("betas must lie in [0, 1)")
+    if hp["eps"] <= 0.0 or hp["lr"] < 0.0 or hp["weight_decay"] < 0.0:
+        raise ValueError("eps must be > 0, lr and weight_decay >= 0")
+    if int(hp["step"]) < 1:
+        raise ValueError("step must be >= 1")
+
+
+def adamw_update(theta, exp_avg, exp_avg_sq, grad, hp: dict):
+    """One decoupled-weight-decay Adam step (Loshchilov & Hutter; Adam when weight_decay = 0) in fp64:
+    m1 = b1 m1 + (1 - b1) g, m2 = b2 m2 + (1 - b2) g^2,
+    theta = theta (1 - lr wd) - lr (m1 / (1 - b1^k)) / (sqrt(m2 / (1 - b2^k)) + eps).
+    Inputs are arrays (any float dtype, used exactly); returns the fp64 results."""
+    validate_adamw(hp)
+    f = lambda x: float(np.float32(x))
+    lr, b1, b2, eps, wd = f(hp["lr"]), f(hp["beta1"]), f(hp["beta2"]), f(hp["eps"]), f(hp["weight_decay"])
+    k = int(hp["step"])
+    th = np.asarray(theta).astype(np.float64)
+    m1 = b1 * np.asarray(exp_avg).astype(np.float64) + (1.0 - b1) * grad
+    m2 = b2 * np.asarray(exp_avg_sq).astype(np.float64) + (1.0 - b2) * grad * grad
+    bc1 = 1.0 - b1 ** k
+    bc2 = 1.0 - b2 ** k
+    new = th * (1.0 - lr * wd) - lr * (m1 / bc1) / (np.sqrt(m2 / bc2) + eps)
+    return new, m1, m2
+
+
+def simulated_gradient(grad_sim, grad_sim_dtype: str, p: dict, lam: float, seed: int, step: int, tensor_id: int,
+                       elem_offset: int = 0, grad_acc=None, grad_scale: float = 1.0) -> np.ndarray:
+    """grad_scale * (grad_acc + lambda * alpha * m (.) g~) in fp64 (Eq. smat-gradient, weighted by lambda)."""
+    validate_params(p["s"], p["keep"], p["sigma"], p.get("rescale", 1), p.get("noise_kind", 0))
+    g = as_f64(np.asarray(grad_sim).ravel(), grad_sim_dtype)
+    kept = keep_mask(seed, step, tensor_id, elem_offset, g.size, p["keep"])
+    m = mask_values(kept, p["keep"], p.get("rescale", 1))
+    out = float(np.float32(lam)) * float(np.float32(p["s"])) * m * g
+    if grad_acc is not None:
+        out = out + np.asarray(grad_acc).astype(np.float64).ravel()
+    return float(np.float32(grad_scale)) * out
+
+
+def adamw_fused(grad_sim, grad_sim_dtype: str, theta, exp_avg, exp_avg_sq, p: dict, lam: float, hp: dict,
+                seed: int, step: int, tensor_id: int, elem_offset: int = 0, grad_acc=None):
+    """The optimizer update of a simulated step fed directly by the simulated-loss gradient; the
+    expert storage and its optimizer state are updated (App. "Training and Scheduling Details",
+    "Implementation details": the optimizer runs on the restored storage, weight decay included).
+    Returns (theta, exp_avg, exp_avg_sq) as float32 arrays and the fp64 values before rounding."""
+    g = simulated_gradient(grad_sim, grad_sim_dtype, p, lam, seed, step, tensor_id, elem_offset, grad_acc,
+                           hp["grad_scale"])
+    th, m1, m2 = adamw_update(np.asarray(theta).ravel(), np.asarray(exp_avg).ravel(),
+                              np.asarray(exp_avg_sq).ravel(), g, hp)
+    return (th.astype(np.float32), m1.astype(np.float32), m2.astype(np.float32)), (th, m1, m2, g)
+
+
 # ------------------------------------------------------------------ ragged lists
 def simulate_multi(thetas: Sequence, theta0s: Sequence, theta0_dtype: str, out_dtype: str,
                    params: Sequence[dict], seed: int, step: int, tensor_ids: Sequence[int],
