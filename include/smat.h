@@ -133,6 +133,41 @@ smat_status smat_backward_accum(const void* grad_sim, smat_dtype grad_dtype, flo
 smat_status smat_debug_draws(smat_rng_key key, int64_t n, smat_op_params p, uint32_t* mask_words,
                              uint32_t* noise_words, uint8_t* kept, float* z, hipStream_t stream);
 
+/* Hyperparameters of the fused optimizer step: decoupled-weight-decay Adam (AdamW; Adam when
+ * weight_decay == 0), the optimizers of the paper's language and vision experiments (App.
+ * "Additional Experimental Settings", "Training").
+ *   lr >= 0, beta1 and beta2 in [0, 1), eps > 0, weight_decay >= 0, all finite
+ *   grad_scale  multiplies the gradient first (e.g. a norm-clipping factor the caller computed)
+ *   step        1-based optimizer step count k, for the bias corrections 1 - beta^k */
+typedef struct smat_adamw_params {
+  float lr;
+  float beta1;
+  float beta2;
+  float eps;
+  float weight_decay;
+  float grad_scale;
+  int32_t step;
+} smat_adamw_params;
+
+/* smat_adamw_fused -- the optimizer update of a simulated step fed directly by the gradient through
+ * the simulation (Sec. 4.2, Eq. smat-gradient, weighted by lambda), on the expert storage with its
+ * weight decay (App. "Training and Scheduling Details", "Implementation details").  With
+ *   g = grad_scale * (grad_acc + lambda * t * m (.) grad_sim)      (grad_acc == NULL: no accumulator)
+ * it applies m1 += (1 - b1)(g - m1), m2 = b2 m2 + (1 - b2) g^2,
+ *   theta = theta (1 - lr wd) - (lr / (1 - b1^k)) m1 / (sqrt(m2) / sqrt(1 - b2^k) + eps)
+ * in fp32.  It replaces smat_backward_accum followed by a separate optimizer pass and never writes a
+ * gradient: per element it moves 12 B of optimizer state in and out plus the gradient at theta~
+ * (and grad_acc), against 10 B more for the unfused pair.  Dropped coordinates enter with a zero
+ * simulated gradient (their moments still decay and weight decay still applies).
+ *   grad_sim            [n] gradient of the loss at theta~ (grad_dtype, device)
+ *   grad_acc            [n] fp32 gradient already accumulated for theta (device), or NULL
+ *   theta, exp_avg, exp_avg_sq  [n] fp32 expert weights and first/second moments (device), in place
+ * The arrays must not overlap.  The mask is regenerated from (key, p.keep) as in smat_simulate.
+ * Errors: SMAT_ERR_INVALID, SMAT_ERR_DTYPE, SMAT_ERR_HIP. */
+smat_status smat_adamw_fused(const void* grad_sim, smat_dtype grad_dtype, const float* grad_acc, float* theta,
+                             float* exp_avg, float* exp_avg_sq, int64_t n, smat_op_params p, float lambda,
+                             smat_adamw_params hp, smat_rng_key key, hipStream_t stream);
+
 /* ---------------------------------------------------------------- ragged tensor lists
  * A plan covers a fixed list of parameter tensors processed by one launch per operation
  * (the grouping of tensors of Sec. 4.3, "Kernel fusion").  It holds host-side tables only; its device tables live
@@ -194,6 +229,26 @@ smat_status smat_simulate_multi(smat_plan* plan, uint64_t seed, uint32_t step, h
  * SMAT_ERR_HIP. */
 smat_status smat_backward_accum_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda,
                                       hipStream_t stream);
+
+/* Optimizer state of one tensor of a plan (device pointers, [n] fp32 each). */
+typedef struct smat_adam_state {
+  float* exp_avg;
+  float* exp_avg_sq;
+} smat_adam_state;
+
+/* smat_plan_bind_adam_state -- hand the plan the optimizer state of every tensor (count entries in
+ * descriptor order) for smat_adamw_fused_multi; uploads a small table on `stream`.  May be called
+ * again to rebind.  Errors: SMAT_ERR_INVALID (null or overlapping arrays, plan without gradient
+ * pointers), SMAT_ERR_STATE (no workspace), SMAT_ERR_HIP. */
+smat_status smat_plan_bind_adam_state(smat_plan* plan, const smat_adam_state* per_tensor, hipStream_t stream);
+
+/* smat_adamw_fused_multi -- smat_adamw_fused over every tensor of the plan in one launch: theta is
+ * desc.theta (the expert storage, updated in place), grad_sim is desc.grad_sim and, when accumulate
+ * is nonzero, grad_acc is desc.grad_theta (read, not written).  Allowed only while the expert
+ * storage is active (the optimizer never sees the simulated buffer).  Errors: SMAT_ERR_INVALID,
+ * SMAT_ERR_STATE (no workspace, params or optimizer state, or simulated storage active), SMAT_ERR_HIP. */
+smat_status smat_adamw_fused_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda, smat_adamw_params hp,
+                                   int32_t accumulate, hipStream_t stream);
 
 /* smat_switch_storage -- point the model at the simulated buffer (SMAT_SIMULATED) or back at the
  * expert storage (SMAT_EXPERT) (Sec. 4.3, "Parameter storage switching").  The plan holds one

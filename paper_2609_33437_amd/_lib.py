@@ -25,6 +25,7 @@ EXPORTS = (
     "smat_simulate", "smat_backward_accum", "smat_debug_draws", "smat_plan_create", "smat_plan_workspace_bytes",
     "smat_plan_bind_workspace", "smat_plan_set_params", "smat_simulate_multi", "smat_backward_accum_multi",
     "smat_switch_storage", "smat_plan_state", "smat_plan_active_ptrs", "smat_plan_destroy", "smat_last_error",
+    "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi",
 )
 
 
@@ -40,6 +41,15 @@ class smat_tensor_desc(ctypes.Structure):
     _fields_ = [("theta", c_void_p), ("theta0", c_void_p), ("out", c_void_p), ("grad_sim", c_void_p),
                 ("grad_theta", c_void_p), ("theta0_host", c_void_p), ("n", c_int64), ("tensor_id", c_uint32),
                 ("reserved", c_uint32), ("elem_offset", c_uint64)]
+
+
+class smat_adamw_params(ctypes.Structure):
+    _fields_ = [("lr", c_float), ("beta1", c_float), ("beta2", c_float), ("eps", c_float),
+                ("weight_decay", c_float), ("grad_scale", c_float), ("step", c_int32)]
+
+
+class smat_adam_state(ctypes.Structure):
+    _fields_ = [("exp_avg", c_void_p), ("exp_avg_sq", c_void_p)]
 
 
 class SmatError(RuntimeError):
@@ -68,6 +78,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_plan_state": [P, POINTER(c_int32)],
         "smat_plan_active_ptrs": [P, POINTER(P), POINTER(P)],
         "smat_plan_destroy": [P],
+        "smat_adamw_fused": [P, c_int32, P, P, P, P, c_int64, smat_op_params, c_float, smat_adamw_params,
+                             smat_rng_key, P],
+        "smat_plan_bind_adam_state": [P, POINTER(smat_adam_state), P],
+        "smat_adamw_fused_multi": [P, c_uint64, c_uint32, c_float, smat_adamw_params, c_int32, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -136,6 +150,14 @@ def rng_key(seed: int, step: int, tensor_id: int = 0, elem_offset: int = 0) -> s
     return smat_rng_key(int(seed), int(step), int(tensor_id), int(elem_offset))
 
 
+def adamw_params(hp) -> smat_adamw_params:
+    """dict(lr, beta1, beta2, eps, weight_decay, grad_scale=1, step) or an smat_adamw_params."""
+    if isinstance(hp, smat_adamw_params):
+        return hp
+    return smat_adamw_params(float(hp["lr"]), float(hp["beta1"]), float(hp["beta2"]), float(hp["eps"]),
+                             float(hp["weight_decay"]), float(hp.get("grad_scale", 1.0)), int(hp["step"]))
+
+
 # ------------------------------------------------------------------ single tensor
 def smat_simulate(theta, theta0, out, params, seed: int, step: int, tensor_id: int = 0, elem_offset: int = 0,
                   stream=None) -> None:
@@ -168,6 +190,20 @@ def smat_debug_draws(n: int, params, seed: int, step: int, tensor_id: int = 0, e
     _check(lib().smat_debug_draws(rng_key(seed, step, tensor_id, elem_offset), int(n), op_params(params),
                                   _dev_ptr(mask_words, "mask_words"), _dev_ptr(noise_words, "noise_words"),
                                   _dev_ptr(kept, "kept"), _dev_ptr(z, "z"), _stream_handle(stream)))
+
+
+def smat_adamw_fused(grad_sim, theta, exp_avg, exp_avg_sq, params, lam: float, hp, seed: int, step: int,
+                     tensor_id: int = 0, elem_offset: int = 0, grad_acc=None, stream=None) -> None:
+    """One AdamW step of theta from grad_acc + lam * t * m * grad_sim, in place (see include/smat.h)."""
+    n = theta.numel()
+    for name, t in (("grad_sim", grad_sim), ("exp_avg", exp_avg), ("exp_avg_sq", exp_avg_sq), ("grad_acc", grad_acc)):
+        if t is not None and t.numel() != n:
+            raise SmatError(SMAT_ERR_INVALID, f"{name} differs in size from theta")
+    _check(lib().smat_adamw_fused(_dev_ptr(grad_sim, "grad_sim"), dtype_code(grad_sim), _dev_ptr(grad_acc, "grad_acc"),
+                                  _dev_ptr(theta, "theta"), _dev_ptr(exp_avg, "exp_avg"),
+                                  _dev_ptr(exp_avg_sq, "exp_avg_sq"), n, op_params(params), float(lam),
+                                  adamw_params(hp), rng_key(seed, step, tensor_id, elem_offset),
+                                  _stream_handle(stream)))
 
 
 # ------------------------------------------------------------------ tensor-list plans
@@ -229,6 +265,18 @@ class Plan:
 
     def backward_accum(self, seed: int, step: int, lam: float, stream=None) -> None:
         _check(lib().smat_backward_accum_multi(self._plan, int(seed), int(step), float(lam), _stream_handle(stream)))
+
+    def bind_adam_state(self, exp_avgs: Sequence, exp_avg_sqs: Sequence, stream=None) -> None:
+        if len(exp_avgs) != self.count or len(exp_avg_sqs) != self.count:
+            raise SmatError(SMAT_ERR_INVALID, "one optimizer state per tensor")
+        arr = (smat_adam_state * max(self.count, 1))(
+            *[smat_adam_state(_dev_ptr(a, "exp_avg"), _dev_ptr(b, "exp_avg_sq")) for a, b in zip(exp_avgs, exp_avg_sqs)])
+        self._refs.append((exp_avgs, exp_avg_sqs))
+        _check(lib().smat_plan_bind_adam_state(self._plan, arr, _stream_handle(stream)))
+
+    def adamw_fused(self, seed: int, step: int, lam: float, hp, accumulate: bool = False, stream=None) -> None:
+        _check(lib().smat_adamw_fused_multi(self._plan, int(seed), int(step), float(lam), adamw_params(hp),
+                                            1 if accumulate else 0, _stream_handle(stream)))
 
     def switch_storage(self, to: int, stream=None) -> None:
         _check(lib().smat_switch_storage(self._plan, int(to), _stream_handle(stream)))

@@ -12,6 +12,8 @@
 #include "smat.h"
 #include "smat_launch.h"
 
+using smat::AdamConsts;
+using smat::AdamRec;
 using smat::ParamRec;
 using smat::TensorRec;
 
@@ -106,6 +108,52 @@ smat_status check_simulate_ptrs(const float* theta, const void* theta0, int t0_d
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Per-call constants of the fused optimizer step, formed in fp64 and rounded once to fp32.
+smat_status make_adam(const smat_adamw_params& hp, AdamConsts* A, const char* where) {
+  if (!std::isfinite(hp.lr) || !std::isfinite(hp.beta1) || !std::isfinite(hp.beta2) || !std::isfinite(hp.eps) ||
+      !std::isfinite(hp.weight_decay) || !std::isfinite(hp.grad_scale))
+    return fail(SMAT_ERR_INVALID, "%s: optimizer hyperparameters must be finite", where);
+  if (hp.beta1 < 0.f || hp.beta1 >= 1.f || hp.beta2 < 0.f || hp.beta2 >= 1.f)
+    return fail(SMAT_ERR_INVALID, "%s: betas must lie in [0, 1)", where);
+  if (hp.eps <= 0.f || hp.lr < 0.f || hp.weight_decay < 0.f)
+    return fail(SMAT_ERR_INVALID, "%s: eps must be > 0, lr and weight_decay >= 0", where);
+  if (hp.step < 1) return fail(SMAT_ERR_INVALID, "%s: step must be >= 1", where);
+  const double b1 = hp.beta1, b2 = hp.beta2, lr = hp.lr;
+  const double bc1 = 1.0 - std::pow(b1, (double)hp.step), bc2 = 1.0 - std::pow(b2, (double)hp.step);
+  A->one_m_b1 = (float)(1.0 - b1);
+  A->b2 = hp.beta2;
+  A->one_m_b2 = (float)(1.0 - b2);
+  A->inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+  A->step_size = (float)(lr / bc1);
+  A->decay = (float)(1.0 - lr * (double)hp.weight_decay);
+  A->eps = hp.eps;
+  A->grad_scale = hp.grad_scale;
+  return SMAT_OK;
+}
+
+uint32_t adam_flags(const float* theta, const float* m1, const float* m2, const void* grad_sim, int g_dt,
+                    const float* grad_acc, uint64_t elem_offset) {
+  const bool base = elem_offset % 4 == 0 && aligned(theta, 16) && aligned(m1, 16) && aligned(m2, 16) &&
+                    aligned(grad_sim, quad_align(g_dt));
+  uint32_t f = base ? smat::kVecAdam : 0u;
+  if (base && grad_acc && aligned(grad_acc, 16)) f |= smat::kVecAdamAcc;
+  return f;
+}
+
+// theta, the two moments, grad_sim and (if given) grad_acc must be pairwise disjoint.
+smat_status check_adam_ptrs(const float* theta, const float* m1, const float* m2, const void* grad_sim, int g_dt,
+                            const float* grad_acc, int64_t n, const char* where) {
+  if (!theta || !m1 || !m2 || !grad_sim) return fail(SMAT_ERR_INVALID, "%s: null pointer with n > 0", where);
+  const size_t nb = (size_t)n;
+  const void* ptr[5] = {theta, m1, m2, grad_sim, grad_acc};
+  const size_t sz[5] = {nb * 4, nb * 4, nb * 4, nb * dtype_bytes(g_dt), nb * 4};
+  for (int i = 0; i < 5; ++i)
+    for (int j = i + 1; j < 5; ++j)
+      if (ptr[i] && ptr[j] && overlap(ptr[i], sz[i], ptr[j], sz[j]))
+        return fail(SMAT_ERR_INVALID, "%s: theta, moments and gradients must not overlap", where);
+  return SMAT_OK;
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ single tensor
@@ -177,6 +225,40 @@ extern "C" smat_status smat_debug_draws(smat_rng_key key, int64_t n, smat_op_par
   return SMAT_OK;
 }
 
+extern "C" smat_status smat_adamw_fused(const void* grad_sim, smat_dtype grad_dtype, const float* grad_acc, float* theta,
+                                        float* exp_avg, float* exp_avg_sq, int64_t n, smat_op_params p, float lambda,
+                                        smat_adamw_params hp, smat_rng_key key, hipStream_t stream) {
+  if (!valid_dtype(grad_dtype)) return fail(SMAT_ERR_DTYPE, "smat_adamw_fused: unsupported dtype");
+  if (n < 0) return fail(SMAT_ERR_INVALID, "smat_adamw_fused: n < 0");
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_adamw_fused: lambda must be finite");
+  if (key.step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_adamw_fused: step must be < 2^30");
+  ParamRec prm;
+  smat_status st = make_param(p, &prm, "smat_adamw_fused");
+  if (st != SMAT_OK) return st;
+  AdamConsts A;
+  st = make_adam(hp, &A, "smat_adamw_fused");
+  if (st != SMAT_OK) return st;
+  if (n == 0) return SMAT_OK;
+  if (key.elem_offset > UINT64_MAX - (uint64_t)n)
+    return fail(SMAT_ERR_INVALID, "smat_adamw_fused: elem_offset + n overflows");
+  if ((n + smat::tile_elems(1) - 1) / smat::tile_elems(1) > 0x7FFFFFFF)
+    return fail(SMAT_ERR_INVALID, "smat_adamw_fused: n too large");
+  st = check_adam_ptrs(theta, exp_avg, exp_avg_sq, grad_sim, grad_dtype, grad_acc, n, "smat_adamw_fused");
+  if (st != SMAT_OK) return st;
+  TensorRec rec{};
+  rec.theta = theta;
+  rec.grad_sim = grad_sim;
+  rec.grad_theta = const_cast<float*>(grad_acc);
+  rec.n = n;
+  rec.elem_offset = key.elem_offset;
+  rec.tensor_id = key.tensor_id;
+  rec.sflags = adam_flags(theta, exp_avg, exp_avg_sq, grad_sim, grad_dtype, grad_acc, key.elem_offset);
+  const AdamRec sr{exp_avg, exp_avg_sq};
+  SMAT_HIP(smat::launch_adamw_one(rec, sr, prm, A, grad_dtype, grad_acc != nullptr, lambda, key.seed, key.step,
+                                  stream));
+  return SMAT_OK;
+}
+
 // ------------------------------------------------------------------ plans
 struct smat_plan {
   int32_t count = 0;
@@ -205,6 +287,13 @@ struct smat_plan {
   int32_t state = SMAT_EXPERT;
   bool fresh = false;  // the buffers hold theta~ of a simulate issued since the last restore
 
+  // fused optimizer step: per-tensor moment pointers, uploaded with the tensor records' flags
+  size_t off_adam = 0;
+  std::vector<AdamRec> adam;
+  char* adam_staging = nullptr;
+  hipEvent_t ev_adam = nullptr;
+  bool adam_bound = false;
+
   // offload mode: theta0 prefetch from pinned host memory on a copy stream
   hipStream_t copy_stream = nullptr;
   hipEvent_t ev_release = nullptr, ev_prefetch = nullptr;
@@ -215,12 +304,13 @@ namespace {
 
 smat_status release(smat_plan* p) {
   // wait for the plan's own work that still reads its pinned staging or owns its events
-  for (hipEvent_t e : {p->ev_static, p->ev_params[0], p->ev_params[1], p->ev_prefetch})
+  for (hipEvent_t e : {p->ev_static, p->ev_params[0], p->ev_params[1], p->ev_prefetch, p->ev_adam})
     if (e) (void)hipEventSynchronize(e);
   if (p->static_staging) (void)hipHostFree(p->static_staging);
+  if (p->adam_staging) (void)hipHostFree(p->adam_staging);
   for (ParamRec* s : p->params_staging)
     if (s) (void)hipHostFree(s);
-  for (hipEvent_t e : {p->ev_static, p->ev_params[0], p->ev_params[1], p->ev_release, p->ev_prefetch})
+  for (hipEvent_t e : {p->ev_static, p->ev_params[0], p->ev_params[1], p->ev_release, p->ev_prefetch, p->ev_adam})
     if (e) (void)hipEventDestroy(e);
   if (p->copy_stream) (void)hipStreamDestroy(p->copy_stream);
   delete p;
@@ -348,6 +438,8 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
   off = align256(off + sizeof(void*) * count);
   p->off_params = off;
   off = align256(off + sizeof(ParamRec) * count);
+  p->off_adam = off;
+  off = align256(off + sizeof(AdamRec) * count);
   p->ws_bytes = std::max<size_t>(off, 256);
   *out_plan = p;
   return SMAT_OK;
@@ -444,6 +536,70 @@ extern "C" smat_status smat_backward_accum_multi(smat_plan* p, uint64_t seed, ui
                                          reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
                                          reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
                                          (uint32_t)p->chunks.size(), p->g_dt, lambda, seed, step, stream));
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_state* per_tensor, hipStream_t stream) {
+  if (!p || (p->count > 0 && !per_tensor)) return fail(SMAT_ERR_INVALID, "smat_plan_bind_adam_state: null argument");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_bind_adam_state: no workspace bound");
+  if (!p->has_grads) return fail(SMAT_ERR_INVALID, "smat_plan_bind_adam_state: plan has no gradient pointers");
+  std::vector<AdamRec> adam(p->count);
+  std::vector<TensorRec> recs = p->recs;
+  for (int32_t i = 0; i < p->count; ++i) {
+    const TensorRec& r = recs[i];
+    adam[i] = AdamRec{per_tensor[i].exp_avg, per_tensor[i].exp_avg_sq};
+    if (r.n == 0) continue;
+    char where[64];
+    std::snprintf(where, sizeof(where), "smat_plan_bind_adam_state: tensor %d", i);
+    smat_status st = check_adam_ptrs(r.theta, adam[i].exp_avg, adam[i].exp_avg_sq, r.grad_sim, p->g_dt, r.grad_theta,
+                                     r.n, where);
+    if (st != SMAT_OK) return st;
+    if (overlap(adam[i].exp_avg, (size_t)r.n * 4, r.out, (size_t)r.n * dtype_bytes(p->out_dt)) ||
+        overlap(adam[i].exp_avg_sq, (size_t)r.n * 4, r.out, (size_t)r.n * dtype_bytes(p->out_dt)))
+      return fail(SMAT_ERR_INVALID, "%s: moments must not overlap the simulated buffer", where);
+    recs[i].sflags = (r.sflags & ~(smat::kVecAdam | smat::kVecAdamAcc)) |
+                     adam_flags(r.theta, adam[i].exp_avg, adam[i].exp_avg_sq, r.grad_sim, p->g_dt, r.grad_theta,
+                                r.elem_offset);
+  }
+  const size_t rec_bytes = sizeof(TensorRec) * p->count, adam_bytes = sizeof(AdamRec) * p->count;
+  if (!p->adam_staging) {
+    SMAT_HIP(hipHostMalloc((void**)&p->adam_staging, std::max<size_t>(rec_bytes + adam_bytes, 256), hipHostMallocDefault));
+    SMAT_HIP(hipEventCreateWithFlags(&p->ev_adam, hipEventDisableTiming));
+  } else {
+    SMAT_HIP(hipEventSynchronize(p->ev_adam));  // the previous upload has left the staging buffer
+  }
+  std::memcpy(p->adam_staging, recs.data(), rec_bytes);
+  std::memcpy(p->adam_staging + rec_bytes, adam.data(), adam_bytes);
+  if (p->count > 0) {
+    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_recs, p->adam_staging, rec_bytes, hipMemcpyHostToDevice, stream));
+    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_adam, p->adam_staging + rec_bytes, adam_bytes, hipMemcpyHostToDevice, stream));
+  }
+  SMAT_HIP(hipEventRecord(p->ev_adam, stream));
+  p->recs = recs;
+  p->adam = adam;
+  p->adam_bound = true;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_adamw_fused_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
+                                              smat_adamw_params hp, int32_t accumulate, hipStream_t stream) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi: null plan");
+  if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi: step must be < 2^30");
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi: lambda must be finite");
+  AdamConsts A;
+  smat_status st = make_adam(hp, &A, "smat_adamw_fused_multi");
+  if (st != SMAT_OK) return st;
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: no workspace bound");
+  if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: parameters never set");
+  if (!p->adam_bound) return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: optimizer state never bound");
+  if (p->state != SMAT_EXPERT)
+    return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: restore the expert storage before the optimizer step");
+  if (!p->chunks.empty())
+    SMAT_HIP(smat::launch_adamw_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                      reinterpret_cast<const AdamRec*>(p->ws + p->off_adam),
+                                      reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                      reinterpret_cast<const uint2*>(p->ws + p->off_chunks), (uint32_t)p->chunks.size(),
+                                      A, p->g_dt, accumulate != 0, lambda, seed, step, stream));
   return SMAT_OK;
 }
 

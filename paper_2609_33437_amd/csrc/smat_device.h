@@ -49,6 +49,27 @@ struct alignas(16) ParamRec {
 };
 static_assert(sizeof(ParamRec) == 16, "ParamRec layout");
 
+// Optimizer state of one tensor for the fused optimizer step, and the per-call constants of that
+// step (all formed on the host in fp64 and rounded once to fp32).
+struct alignas(16) AdamRec {
+  float* exp_avg;
+  float* exp_avg_sq;
+};
+static_assert(sizeof(AdamRec) == 16, "AdamRec layout");
+
+struct AdamConsts {
+  float one_m_b1;      // 1 - beta1
+  float b2;            // beta2
+  float one_m_b2;      // 1 - beta2
+  float inv_sqrt_bc2;  // 1 / sqrt(1 - beta2^k)
+  float step_size;     // lr / (1 - beta1^k)
+  float decay;         // 1 - lr * weight_decay
+  float eps;
+  float grad_scale;
+};
+// Static flag: theta, the moments, grad_sim (and grad_theta when accumulating) aligned for quads.
+enum : uint32_t { kVecAdam = 4u, kVecAdamAcc = 8u };
+
 // Work decomposition: a block of kBlock threads (one wave) handles one tile of Q quads per
 // thread (tile = 4 * kBlock * Q elements); thread x owns quads x, x + kBlock, ... of the tile,
 // so every load/store instruction of the wave covers one contiguous span and consecutive blocks
@@ -59,10 +80,13 @@ static_assert(sizeof(ParamRec) == 16, "ParamRec layout");
 constexpr int kBlock = 64;
 constexpr int kSimQuads = 2;
 constexpr int kBwdQuads = 1;
+constexpr int kAdamQuads = 1;
 constexpr int64_t kChunk = 16384;
 constexpr int64_t tile_elems(int quads) { return 4 * kBlock * quads; }
 constexpr int tiles_per_chunk(int quads) { return (int)(kChunk / tile_elems(quads)); }
-static_assert(kChunk % tile_elems(kSimQuads) == 0 && kChunk % tile_elems(kBwdQuads) == 0, "tiles split chunks");
+static_assert(kChunk % tile_elems(kSimQuads) == 0 && kChunk % tile_elems(kBwdQuads) == 0 &&
+                  kChunk % tile_elems(kAdamQuads) == 0,
+              "tiles split chunks");
 constexpr int64_t kMaxTile = tile_elems(kSimQuads > kBwdQuads ? kSimQuads : kBwdQuads);
 
 constexpr uint32_t kStreamMask = 0u;

@@ -45,7 +45,8 @@ def test_struct_layout_matches_c(tmp_path):
 #include <stddef.h>
 #include "smat.h"
 int main(void) {
-  printf("%zu %zu %zu\\n", sizeof(smat_op_params), sizeof(smat_rng_key), sizeof(smat_tensor_desc));
+  printf("%zu %zu %zu %zu %zu\\n", sizeof(smat_op_params), sizeof(smat_rng_key), sizeof(smat_tensor_desc),
+         sizeof(smat_adamw_params), sizeof(smat_adam_state));
   printf("%zu %zu %zu %zu\\n", offsetof(smat_tensor_desc, n), offsetof(smat_tensor_desc, tensor_id),
          offsetof(smat_tensor_desc, elem_offset), offsetof(smat_rng_key, elem_offset));
   return 0;
@@ -56,6 +57,7 @@ int main(void) {
                     str(src), "-o", str(exe)], check=True, capture_output=True)
     out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()
     want = [ctypes.sizeof(_lib.smat_op_params), ctypes.sizeof(_lib.smat_rng_key), ctypes.sizeof(_lib.smat_tensor_desc),
+            ctypes.sizeof(_lib.smat_adamw_params), ctypes.sizeof(_lib.smat_adam_state),
             _lib.smat_tensor_desc.n.offset, _lib.smat_tensor_desc.tensor_id.offset,
             _lib.smat_tensor_desc.elem_offset.offset, _lib.smat_rng_key.elem_offset.offset]
     assert [int(x) for x in out] == want
@@ -143,3 +145,26 @@ def test_plan_create_validation_without_gpu():
     assert lib.smat_switch_storage(p, 5, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_plan_destroy(p) == 0
     assert lib.smat_plan_destroy(None) == 0
+
+
+@pytest.mark.parametrize("bad", [dict(beta1=1.0), dict(beta2=-0.5), dict(eps=0.0), dict(lr=-1.0), dict(step=0),
+                                 dict(weight_decay=float("nan")), dict(grad_scale=float("inf"))])
+def test_invalid_adamw_hyperparameters_rejected_before_launch(bad):
+    lib = smat.lib()
+    hp = _lib.adamw_params(dict(dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1), **bad))
+    p = _lib.op_params(dict(s=0.5, keep=0.5, sigma=0.0))
+    P = ctypes.c_void_p
+    st = lib.smat_adamw_fused(P(1 << 20), 1, None, P(2 << 20), P(3 << 20), P(4 << 20), 4, p, 1.0, hp,
+                              _lib.rng_key(0, 0), None)
+    assert st == _lib.SMAT_ERR_INVALID
+
+
+def test_adamw_overlap_rejected_without_gpu():
+    lib = smat.lib()
+    hp = _lib.adamw_params(dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1))
+    p = _lib.op_params(dict(s=0.5, keep=0.5, sigma=0.0))
+    P = ctypes.c_void_p
+    # exp_avg overlaps theta
+    st = lib.smat_adamw_fused(P(1 << 20), 1, None, P(2 << 20), P((2 << 20) + 8), P(4 << 20), 4, p, 1.0, hp,
+                              _lib.rng_key(0, 0), None)
+    assert st == _lib.SMAT_ERR_INVALID

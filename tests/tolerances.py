@@ -66,3 +66,28 @@ def check_grad(gpu, oracle, g_old, incr):
     """gpu/oracle: float32 arrays; g_old: previous values; incr: |lambda t g~| in fp64."""
     scale = np.maximum(np.abs(oracle.astype(np.float64)), np.abs(g_old.astype(np.float64)) + np.abs(incr))
     return np.abs(gpu.astype(np.float64) - oracle.astype(np.float64)) <= GRAD_RTOL * scale
+
+
+def check_adam(gpu, old, oracle_f64, hp, gmag=None):
+    """Fused optimizer step: gpu = (theta, m1, m2) float32 arrays; old = (theta, m1, m2) before the
+    step; oracle_f64 = (theta, m1, m2, g) from the oracle in fp64.  Bounds from the kernel's fp32
+    sequence (g: <= 5u|g| from t, c = lambda t, the product and grad_scale; m1 = fma(1-b1, g-m1, m1):
+    8u(|m1_old| + |g|); m2 is a sum of non-negative terms: 16u m2; theta = fma(-lr/bc1, m1/denom,
+    theta (1 - lr wd)): 4u(|theta_old| + |theta|) + 24u (lr/bc1)(|m1_old| + |g|)/denom).
+    gmag: magnitude of the gradient's terms (|grad_scale| (|acc| + |lambda t m g~|)); defaults to |g|.
+    With an accumulator the kernel's error scales with it rather than with |g|, which may cancel.
+    Returns three boolean arrays."""
+    th_o, m1_o, m2_o, g = oracle_f64
+    ga = np.abs(g) if gmag is None else np.asarray(gmag, dtype=np.float64)
+    th0, m10, m20 = (np.asarray(x, dtype=np.float64) for x in old)
+    k = int(hp["step"])
+    b1, b2 = float(np.float32(hp["beta1"])), float(np.float32(hp["beta2"]))
+    step_size = float(np.float32(hp["lr"])) / (1 - b1 ** k)
+    denom = np.sqrt(m2_o / (1 - b2 ** k)) + float(np.float32(hp["eps"]))
+    tiny = 1e-37
+    gt, g1, g2 = (np.asarray(x, dtype=np.float64) for x in gpu)
+    ok_m1 = np.abs(g1 - m1_o) <= 8 * U * (np.abs(m10) + ga) + tiny
+    ok_m2 = np.abs(g2 - m2_o) <= 16 * U * (m2_o + (1 - b2) * ga * ga) + tiny
+    ok_th = np.abs(gt - th_o) <= (4 * U * (np.abs(th0) + np.abs(th_o))
+                                  + 24 * U * step_size * (np.abs(m10) + ga) / denom + tiny)
+    return ok_th, ok_m1, ok_m2
