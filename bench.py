@@ -60,6 +60,9 @@ def parse_args():
     ap.add_argument("--cpu-sample", type=int, default=1 << 27, help="most elements the CPU oracle baseline visits")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU work budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--adamw", action="store_true",
+                    help="also time a simulated training step whose optimizer update is fused with the gradient "
+                         "through the simulation, against backward-accumulate + torch's AdamW on the same list")
     ap.add_argument("--offload", action="store_true",
                     help="theta0 in pinned host memory, copied into the simulated buffers at each restore; "
                          "also reports the prefetch's host-link rate")
@@ -188,6 +191,92 @@ def summarize(root: str) -> int:
         f.write("\n".join(md) + "\n")
     print("\n".join(lines + [""] + md))
     return 0
+
+
+def bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat):
+    """Simulated training step with the optimizer: (a) simulate, switch, fused AdamW on the expert
+    storage; (b) simulate, switch, backward-accumulate, switch, torch.optim.AdamW over the same tensors."""
+    hp = dict(lr=2e-5, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-3, grad_scale=1.0, step=1)
+    P = cfg.numel
+    res = {}
+    m1 = [torch.zeros(t.numel(), device="cuda") for t in inp.theta]
+    m2 = [torch.zeros(t.numel(), device="cuda") for t in inp.theta]
+    plan = smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta)
+    plan.bind_adam_state(m1, m2)
+
+    def fused(k, ev=None):
+        plan.set_params(params[k])
+        plan.simulate(seed, step_ids[k])
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        plan.switch_storage(smat.SMAT_EXPERT)
+        if ev:
+            ev[0].record()
+        plan.adamw_fused(seed, step_ids[k], cfg.lam, dict(hp, step=k + 1))
+        if ev:
+            ev[1].record()
+
+    for k in range(W):
+        fused(k)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for k in range(K):
+        fused(W + k, evs[k])
+    b.record()
+    torch.cuda.synchronize()
+    kern = sum(e[0].elapsed_time(e[1]) for e in evs) / K
+    nb = {"bf16": 2, "f32": 4}
+    fused_bytes = P * (nb[cfg.grad_dtype] + 24)
+    res["fused"] = {"ms_per_step": round(a.elapsed_time(b) / K, 4), "optimizer_kernel_ms": round(kern, 4),
+                    "optimizer_kernel_gbps": round(fused_bytes / (kern * 1e6), 1),
+                    "optimizer_bytes_per_param": fused_bytes / P}
+    plan.close()
+    del m1, m2
+    torch.cuda.empty_cache()
+
+    params_t = [torch.nn.Parameter(t) for t in inp.theta]   # share the expert storage
+    for prm, g in zip(params_t, inp.grad_theta):
+        prm.grad = g
+    kind = "fused"
+    try:
+        opt = torch.optim.AdamW(params_t, lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
+                                weight_decay=hp["weight_decay"], fused=True)
+    except (RuntimeError, ValueError):
+        kind = "foreach"
+        opt = torch.optim.AdamW(params_t, lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
+                                weight_decay=hp["weight_decay"], foreach=True)
+    plan = smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta)
+
+    def unfused(k, ev=None):
+        plan.set_params(params[k])
+        plan.simulate(seed, step_ids[k])
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        if ev:
+            ev[0].record()
+        plan.backward_accum(seed, step_ids[k], cfg.lam)
+        plan.switch_storage(smat.SMAT_EXPERT)
+        opt.step()
+        if ev:
+            ev[1].record()
+
+    for k in range(W):
+        unfused(k)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+    a.record()
+    for k in range(K):
+        unfused(W + k, evs[k])
+    b.record()
+    torch.cuda.synchronize()
+    kern = sum(e[0].elapsed_time(e[1]) for e in evs) / K
+    res["unfused"] = {"ms_per_step": round(a.elapsed_time(b) / K, 4), "backward_plus_optimizer_ms": round(kern, 4),
+                      "optimizer": f"torch.optim.AdamW({kind}=True)"}
+    res["speedup_of_gradient_plus_optimizer"] = round(kern / res["fused"]["optimizer_kernel_ms"], 3)
+    plan.close()
+    log(f"adamw: fused optimizer {res['fused']['optimizer_kernel_ms']:.3f} ms vs backward + torch AdamW "
+        f"{kern:.3f} ms")
+    return res
 
 
 def main() -> int:
@@ -343,6 +432,9 @@ def main() -> int:
     if prefetch is not None:
         result["config"]["mode"] = "offload: theta0 in pinned host memory, copied into the buffers at each restore"
         result["offload_prefetch"] = prefetch
+    if args.adamw:
+        plan.close()
+        result["adamw_step"] = bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat)
     if not args.no_cpu_baseline:
         last = W + K - 1
         result["cpu_baseline"] = cpu_baseline(cfg, inp, params[last], step_ids[last], args.cpu_sample,
