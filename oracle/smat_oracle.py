@@ -375,7 +375,35 @@ def adamw_fused(grad_sim, grad_sim_dtype: str, theta, exp_avg, exp_avg_sq, p: di
     return (th.astype(np.float32), m1.astype(np.float32), m2.astype(np.float32)), (th, m1, m2, g)
 
 
+def grad_sqnorm(grad_sim, grad_sim_dtype: str, p: dict, lam: float, seed: int, step: int, tensor_id: int,
+                elem_offset: int = 0, grad_acc=None) -> float:
+    """Squared L2 norm of the expert gradient [grad_acc +] lambda * alpha * m (.) g~ of one tensor,
+    in fp64 (the quantity gradient-norm clipping measures before the optimizer step)."""
+    g = simulated_gradient(grad_sim, grad_sim_dtype, p, lam, seed, step, tensor_id, elem_offset, grad_acc)
+    return float(np.dot(g, g))
+
+
+def clip_coefficient(total_norm: float, max_norm: float) -> float:
+    """Norm clipping with the rule of torch.nn.utils.clip_grad_norm_ (L2 norm): the gradient is
+    multiplied by min(1, max_norm / (total_norm + 1e-6))."""
+    if not (math.isfinite(max_norm) and max_norm > 0.0):
+        raise ValueError("max_norm must be finite and > 0")
+    return min(1.0, max_norm / (total_norm + 1e-6))
+
+
 # ------------------------------------------------------------------ ragged lists
+def grad_sqnorm_multi(grad_sims: Sequence, grad_sim_dtype: str, params: Sequence[dict], lam: float, seed: int,
+                      step: int, tensor_ids: Sequence[int], elem_offsets: Optional[Sequence[int]] = None,
+                      grad_accs: Optional[Sequence] = None) -> float:
+    """Squared L2 norm of the expert gradient over a list of tensors (or shards of tensors), in fp64."""
+    offs = elem_offsets if elem_offsets is not None else [0] * len(grad_sims)
+    total = 0.0
+    for i in range(len(grad_sims)):
+        total += grad_sqnorm(grad_sims[i], grad_sim_dtype, params[i], lam, seed, step, tensor_ids[i], offs[i],
+                             None if grad_accs is None else grad_accs[i])
+    return total
+
+
 def simulate_multi(thetas: Sequence, theta0s: Sequence, theta0_dtype: str, out_dtype: str,
                    params: Sequence[dict], seed: int, step: int, tensor_ids: Sequence[int],
                    elem_offsets: Optional[Sequence[int]] = None) -> List[np.ndarray]:
