@@ -24,7 +24,8 @@ if ROOT not in sys.path:
 
 METRIC = "fused simulate+backward params/s and achieved HBM GB/s (% of peak), 7B-shaped"
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
-KERNEL_SOURCES = ("paper_2609_33437_amd/csrc/smat_kernels.hip", "paper_2609_33437_amd/csrc/smat_device.h")
+KERNEL_SOURCES = ("paper_2609_33437_amd/csrc/smat_kernels.hip", "paper_2609_33437_amd/csrc/smat_device.h",
+                  "paper_2609_33437_amd/csrc/smat_tile.h")
 
 
 def log(msg: str) -> None:
@@ -69,6 +70,12 @@ def parse_args():
     ap.add_argument("--summarize", metavar="DIR",
                     help="turn rocprofv3 CSV output under DIR (prof_trace/, prof_fetch/, prof_write/) into the "
                          "summaries under profiles/ and exit")
+    ap.add_argument("--train", action="store_true",
+                    help="time SMAT inside a bf16 training loop of a Llama-1B-shaped synthetic decoder against "
+                         "plain fine-tuning (AdamW, clipping at 1), print that comparison as the JSON line and exit")
+    ap.add_argument("--train-batch", type=int, default=8)
+    ap.add_argument("--train-seq", type=int, default=512)
+    ap.add_argument("--train-reps", type=int, default=3)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain elementwise copy of 2^28 fp32 values (1 GiB read, 1 GiB written) "
                          "three times, whose HBM counters scale the kernels' counter readings")
@@ -231,6 +238,40 @@ def bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat):
     res["fused"] = {"ms_per_step": round(a.elapsed_time(b) / K, 4), "optimizer_kernel_ms": round(kern, 4),
                     "optimizer_kernel_gbps": round(fused_bytes / (kern * 1e6), 1),
                     "optimizer_bytes_per_param": fused_bytes / P}
+
+    # the same with norm clipping at 1: norm pass (reads g~ only), factor kept on the GPU
+    coef = torch.ones(1, dtype=torch.float32, device="cuda")
+
+    def clipped(k, ev=None):
+        plan.set_params(params[k])
+        plan.simulate(seed, step_ids[k])
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        plan.switch_storage(smat.SMAT_EXPERT)
+        if ev:
+            ev[0].record()
+        plan.grad_norm(seed, step_ids[k], cfg.lam, False, 1.0, None, coef)
+        if ev:
+            ev[1].record()
+        plan.adamw_fused(seed, step_ids[k], cfg.lam, dict(hp, step=W + K + k + 1), grad_scale_dev=coef)
+        if ev:
+            ev[2].record()
+
+    for k in range(W):
+        clipped(k)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    a.record()
+    for k in range(K):
+        clipped(W + k, evs[k])
+    b.record()
+    torch.cuda.synchronize()
+    norm_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / K
+    clip_kern = sum(e[0].elapsed_time(e[2]) for e in evs) / K
+    norm_bytes = P * nb[cfg.grad_dtype]
+    res["fused_clipped"] = {"ms_per_step": round(a.elapsed_time(b) / K, 4),
+                            "norm_plus_optimizer_ms": round(clip_kern, 4), "grad_norm_ms": round(norm_ms, 4),
+                            "grad_norm_gbps": round(norm_bytes / (norm_ms * 1e6), 1),
+                            "grad_norm_bytes_per_param": norm_bytes / P}
     plan.close()
     del m1, m2
     torch.cuda.empty_cache()
@@ -248,6 +289,8 @@ def bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat):
                                 weight_decay=hp["weight_decay"], foreach=True)
     plan = smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta)
 
+    clip_now = [False]
+
     def unfused(k, ev=None):
         plan.set_params(params[k])
         plan.simulate(seed, step_ids[k])
@@ -256,6 +299,8 @@ def bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat):
             ev[0].record()
         plan.backward_accum(seed, step_ids[k], cfg.lam)
         plan.switch_storage(smat.SMAT_EXPERT)
+        if clip_now[0]:
+            torch.nn.utils.clip_grad_norm_(params_t, 1.0)
         opt.step()
         if ev:
             ev[1].record()
@@ -273,10 +318,140 @@ def bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat):
     res["unfused"] = {"ms_per_step": round(a.elapsed_time(b) / K, 4), "backward_plus_optimizer_ms": round(kern, 4),
                       "optimizer": f"torch.optim.AdamW({kind}=True)"}
     res["speedup_of_gradient_plus_optimizer"] = round(kern / res["fused"]["optimizer_kernel_ms"], 3)
+    clip_now[0] = True
+    for k in range(W):
+        unfused(k)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+    a.record()
+    for k in range(K):
+        unfused(W + k, evs[k])
+    b.record()
+    torch.cuda.synchronize()
+    kern_c = sum(e[0].elapsed_time(e[1]) for e in evs) / K
+    res["unfused_clipped"] = {"ms_per_step": round(a.elapsed_time(b) / K, 4),
+                              "backward_clip_optimizer_ms": round(kern_c, 4),
+                              "clip": "torch.nn.utils.clip_grad_norm_(max_norm=1)"}
+    res["speedup_with_clipping"] = round(kern_c / res["fused_clipped"]["norm_plus_optimizer_ms"], 3)
     plan.close()
     log(f"adamw: fused optimizer {res['fused']['optimizer_kernel_ms']:.3f} ms vs backward + torch AdamW "
-        f"{kern:.3f} ms")
+        f"{kern:.3f} ms; with clipping {res['fused_clipped']['norm_plus_optimizer_ms']:.3f} ms "
+        f"(norm {norm_ms:.3f} ms) vs {kern_c:.3f} ms")
     return res
+
+
+def bench_train(args, torch, smat) -> int:
+    """SMAT in a training loop against plain fine-tuning (FT), the measurement behind the method's
+    training-time table (App. "Implementation and Measurement Details"): same model, data and AdamW
+    (lr 2e-5, weight decay 1e-3, gradient clipping at 1, App. "Training and Scheduling Details"),
+    bf16 autocast over fp32 master weights.  Variants, timed in interleaved blocks of whole cycles:
+      ft          forward, backward, clip, AdamW (torch, fused)
+      smat        SMAT with t = 4: on simulated steps theta~ in the buffers, then the expert gradient
+                  lambda alpha m g~ (backward-accumulate), clip and torch AdamW on the expert storage
+      smat_fused  as smat, but the simulated step's clip and AdamW update are the library's norm pass
+                  and fused optimizer kernel, fed by g~ directly."""
+    from paper_2609_33437_amd.training import SimulatedMergeTraining
+    from workloads.model import LLAMA_1B, make_decoder, parameter_count, token_batches
+
+    shape = LLAMA_1B
+    B, S, t = args.train_batch, args.train_seq, 4
+    K = max(t, (args.steps // t) * t)
+    W = max(t, -(-args.warmup // t) * t)
+    clip = 1.0
+    log(f"building the decoder ({parameter_count(shape) / 1e9:.2f}B params), batch {B} x {S} tokens")
+    model = make_decoder(shape, 0, "cuda")
+    batches = token_batches(shape, B, S, 8, 1, "cuda")
+    params = list(model.parameters())
+    opt = torch.optim.AdamW(params, lr=2e-5, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-3, fused=True)
+    w = SimulatedMergeTraining.from_module(model, keep=0.5, alpha_min=0.2, sigma=2e-3, period=t, seed=0x7A11,
+                                           offload=args.offload)
+    extra = sum(b.numel() * b.element_size() + g.numel() * g.element_size() + a.numel() * a.element_size()
+                for b, g, a in zip(w.buffers, w.grad_sim, w.grad_theta))
+    if not args.offload:
+        extra += sum(x.numel() * x.element_size() for x in w.theta0)
+    hooks = {"begin": [], "end": []}
+    counter = [0]
+
+    def step(mode, timed):
+        k = counter[0]
+        counter[0] += 1
+        opt.zero_grad(set_to_none=True)
+        sim = False
+        if mode != "ft":
+            if timed:
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                e[0].record()
+            sim = w.begin(k)
+            if timed and sim:
+                e[1].record()
+                hooks["begin"].append(e)
+        with torch.autocast("cuda", dtype=torch.bfloat16):
+            loss = model.loss(batches[k % len(batches)])
+        loss.backward()
+        if sim:
+            if timed:
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                e[0].record()
+            if mode == "smat_fused":
+                w.end(opt, fused=True, max_norm=clip)
+            else:
+                w.end()
+                torch.nn.utils.clip_grad_norm_(params, clip)
+                opt.step()
+            if timed:
+                e[1].record()
+                hooks["end"].append(e)
+            return
+        torch.nn.utils.clip_grad_norm_(params, clip)
+        opt.step()
+
+    modes = ("ft", "smat", "smat_fused")
+    for mode in modes:
+        log(f"warmup {W} steps: {mode}")
+        for _ in range(W):
+            step(mode, False)
+    torch.cuda.synchronize()
+    times = {m: [] for m in modes}
+    for r in range(args.train_reps):
+        for mode in modes:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            for _ in range(K):
+                step(mode, True)
+            b.record()
+            torch.cuda.synchronize()
+            times[mode].append(a.elapsed_time(b) / K)
+            log(f"rep {r} {mode}: {times[mode][-1]:.3f} ms/step")
+    med = {m: sorted(v)[len(v) // 2] for m, v in times.items()}
+    begin_ms = sum(x[0].elapsed_time(x[1]) for x in hooks["begin"]) / max(1, len(hooks["begin"]))
+    w.close()
+    tokens = B * S
+    result = {
+        "metric": "training step time, SMAT (t = 4) vs plain fine-tuning, Llama-1B-shaped synthetic decoder",
+        "unit": "ms/step",
+        "higher_is_better": False,
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "reps": args.train_reps,
+        "dtype": "bf16 autocast, fp32 master weights",
+        "data": "synthetic",
+        "ms_per_step": {m: round(v, 3) for m, v in med.items()},
+        "ms_per_step_all_reps": {m: [round(x, 3) for x in v] for m, v in times.items()},
+        "overhead_vs_ft": {m: round(med[m] / med["ft"] - 1.0, 4) for m in modes[1:]},
+        "tokens_per_s": {m: round(tokens / (med[m] * 1e-3), 1) for m in modes},
+        "begin_ms_per_simulated_step": round(begin_ms, 3),
+        "config": {"workload": f"decoder d={shape.d} L={shape.layers} heads={shape.heads} ffn={shape.ffn} "
+                               f"vocab={shape.vocab} tied, {parameter_count(shape)} params",
+                   "batch": B, "seq_len": S, "optimizer": "torch.optim.AdamW(fused=True) lr 2e-5 wd 1e-3",
+                   "clip": clip, "period": t, "keep": 0.5, "alpha_min": 0.2, "sigma": 2e-3, "noise": "uniform",
+                   "buffers": "bf16", "theta0": "pinned host (offload)" if args.offload else "resident bf16",
+                   "smat_extra_bytes": extra},
+        "paper_h800_llama_1b_s_per_step": {"ft": 0.0687, "smat": 0.0700},
+    }
+    print(json.dumps(result))
+    return 0
 
 
 def main() -> int:
@@ -298,6 +473,8 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     smat.lib()  # fail loudly if the HIP library is missing
+    if args.train:
+        return bench_train(args, torch, smat)
     cfg = workloads.config(args.config)
     dt = {"bf16": torch.bfloat16, "f32": torch.float32}
     nbytes = {"bf16": 2, "f32": 4}

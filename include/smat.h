@@ -162,11 +162,15 @@ typedef struct smat_adamw_params {
  *   grad_sim            [n] gradient of the loss at theta~ (grad_dtype, device)
  *   grad_acc            [n] fp32 gradient already accumulated for theta (device), or NULL
  *   theta, exp_avg, exp_avg_sq  [n] fp32 expert weights and first/second moments (device), in place
+ *   grad_scale_dev      device pointer to one fp32 factor that further multiplies grad_scale (read by
+ *                       the kernel when it runs, e.g. the clipping factor smat_grad_norm_multi wrote
+ *                       earlier on the same stream), or NULL for none
  * The arrays must not overlap.  The mask is regenerated from (key, p.keep) as in smat_simulate.
  * Errors: SMAT_ERR_INVALID, SMAT_ERR_DTYPE, SMAT_ERR_HIP. */
 smat_status smat_adamw_fused(const void* grad_sim, smat_dtype grad_dtype, const float* grad_acc, float* theta,
                              float* exp_avg, float* exp_avg_sq, int64_t n, smat_op_params p, float lambda,
-                             smat_adamw_params hp, smat_rng_key key, hipStream_t stream);
+                             smat_adamw_params hp, smat_rng_key key, const float* grad_scale_dev,
+                             hipStream_t stream);
 
 /* ---------------------------------------------------------------- ragged tensor lists
  * A plan covers a fixed list of parameter tensors processed by one launch per operation
@@ -244,11 +248,30 @@ smat_status smat_plan_bind_adam_state(smat_plan* plan, const smat_adam_state* pe
 
 /* smat_adamw_fused_multi -- smat_adamw_fused over every tensor of the plan in one launch: theta is
  * desc.theta (the expert storage, updated in place), grad_sim is desc.grad_sim and, when accumulate
- * is nonzero, grad_acc is desc.grad_theta (read, not written).  Allowed only while the expert
- * storage is active (the optimizer never sees the simulated buffer).  Errors: SMAT_ERR_INVALID,
- * SMAT_ERR_STATE (no workspace, params or optimizer state, or simulated storage active), SMAT_ERR_HIP. */
+ * is nonzero, grad_acc is desc.grad_theta (read, not written); grad_scale_dev as in
+ * smat_adamw_fused.  Allowed only while the expert storage is active (the optimizer never sees the
+ * simulated buffer).  Errors: SMAT_ERR_INVALID, SMAT_ERR_STATE (no workspace, params or optimizer
+ * state, or simulated storage active), SMAT_ERR_HIP. */
 smat_status smat_adamw_fused_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda, smat_adamw_params hp,
-                                   int32_t accumulate, hipStream_t stream);
+                                   int32_t accumulate, const float* grad_scale_dev, hipStream_t stream);
+
+/* smat_grad_norm_multi -- squared L2 norm of the expert gradient of a simulated step over every
+ * tensor of the plan, for gradient-norm clipping ahead of the optimizer update (App. "Training and
+ * Scheduling Details": the language models train with clipping at 1):
+ *   sumsq = sum over tensors and elements of g^2,  g = [grad_acc +] lambda t m (.) grad_sim
+ * (Eq. smat-gradient weighted by lambda; grad_acc = desc.grad_theta when accumulate is 1), with the
+ * mask regenerated as in smat_backward_accum_multi.  Reads grad_sim (and grad_acc) only: 2 B per
+ * element for bf16 gradients.  Outputs, written on `stream` by the last of three small launches:
+ *   sumsq       device fp64 scalar, or NULL
+ *   clip_coef   device fp32 scalar min(1, max_norm / (sqrt(sumsq) + 1e-6)), the factor
+ *               torch.nn.utils.clip_grad_norm_ applies, or NULL; then max_norm must be finite and > 0.
+ *               Pass it as grad_scale_dev of smat_adamw_fused_multi to clip without a host sync.
+ * At least one output must be given.  Per-chunk fp32 partial sums (in the plan's workspace) are
+ * added in fp64 in a fixed order: the result is the same on every call.  Any storage may be active.
+ * Norm calls on one plan share those partials: calls that overlap (on different streams) race.
+ * Errors: SMAT_ERR_INVALID, SMAT_ERR_STATE (no workspace or params), SMAT_ERR_HIP. */
+smat_status smat_grad_norm_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda, int32_t accumulate,
+                                 float max_norm, double* sumsq, float* clip_coef, hipStream_t stream);
 
 /* smat_switch_storage -- point the model at the simulated buffer (SMAT_SIMULATED) or back at the
  * expert storage (SMAT_EXPERT) (Sec. 4.3, "Parameter storage switching").  The plan holds one

@@ -25,7 +25,7 @@ EXPORTS = (
     "smat_simulate", "smat_backward_accum", "smat_debug_draws", "smat_plan_create", "smat_plan_workspace_bytes",
     "smat_plan_bind_workspace", "smat_plan_set_params", "smat_simulate_multi", "smat_backward_accum_multi",
     "smat_switch_storage", "smat_plan_state", "smat_plan_active_ptrs", "smat_plan_destroy", "smat_last_error",
-    "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi",
+    "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi", "smat_grad_norm_multi",
 )
 
 
@@ -79,9 +79,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_plan_active_ptrs": [P, POINTER(P), POINTER(P)],
         "smat_plan_destroy": [P],
         "smat_adamw_fused": [P, c_int32, P, P, P, P, c_int64, smat_op_params, c_float, smat_adamw_params,
-                             smat_rng_key, P],
+                             smat_rng_key, P, P],
         "smat_plan_bind_adam_state": [P, POINTER(smat_adam_state), P],
-        "smat_adamw_fused_multi": [P, c_uint64, c_uint32, c_float, smat_adamw_params, c_int32, P],
+        "smat_adamw_fused_multi": [P, c_uint64, c_uint32, c_float, smat_adamw_params, c_int32, P, P],
+        "smat_grad_norm_multi": [P, c_uint64, c_uint32, c_float, c_int32, c_float, P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -136,6 +137,15 @@ def _dev_ptr(t, what: str):
     if not t.is_contiguous():
         raise SmatError(SMAT_ERR_INVALID, f"{what} must be contiguous")
     return c_void_p(t.data_ptr()) if t.numel() else None
+
+
+def _scalar_ptr(t, what: str, dtype: str):
+    """Device pointer of a one-element GPU tensor of the given dtype (None passes NULL)."""
+    if t is None:
+        return None
+    if str(t.dtype) != f"torch.{dtype}" or t.numel() != 1:
+        raise SmatError(SMAT_ERR_INVALID, f"{what} must be a one-element {dtype} tensor")
+    return _dev_ptr(t, what)
 
 
 def op_params(p) -> smat_op_params:
@@ -193,8 +203,10 @@ def smat_debug_draws(n: int, params, seed: int, step: int, tensor_id: int = 0, e
 
 
 def smat_adamw_fused(grad_sim, theta, exp_avg, exp_avg_sq, params, lam: float, hp, seed: int, step: int,
-                     tensor_id: int = 0, elem_offset: int = 0, grad_acc=None, stream=None) -> None:
-    """One AdamW step of theta from grad_acc + lam * t * m * grad_sim, in place (see include/smat.h)."""
+                     tensor_id: int = 0, elem_offset: int = 0, grad_acc=None, grad_scale_dev=None,
+                     stream=None) -> None:
+    """One AdamW step of theta from grad_acc + lam * t * m * grad_sim, in place (see include/smat.h).
+    grad_scale_dev: optional one-element fp32 GPU tensor multiplying the gradient (read on the GPU)."""
     n = theta.numel()
     for name, t in (("grad_sim", grad_sim), ("exp_avg", exp_avg), ("exp_avg_sq", exp_avg_sq), ("grad_acc", grad_acc)):
         if t is not None and t.numel() != n:
@@ -203,7 +215,7 @@ def smat_adamw_fused(grad_sim, theta, exp_avg, exp_avg_sq, params, lam: float, h
                                   _dev_ptr(theta, "theta"), _dev_ptr(exp_avg, "exp_avg"),
                                   _dev_ptr(exp_avg_sq, "exp_avg_sq"), n, op_params(params), float(lam),
                                   adamw_params(hp), rng_key(seed, step, tensor_id, elem_offset),
-                                  _stream_handle(stream)))
+                                  _scalar_ptr(grad_scale_dev, "grad_scale_dev", "float32"), _stream_handle(stream)))
 
 
 # ------------------------------------------------------------------ tensor-list plans
@@ -274,9 +286,20 @@ class Plan:
         self._refs.append((exp_avgs, exp_avg_sqs))
         _check(lib().smat_plan_bind_adam_state(self._plan, arr, _stream_handle(stream)))
 
-    def adamw_fused(self, seed: int, step: int, lam: float, hp, accumulate: bool = False, stream=None) -> None:
+    def adamw_fused(self, seed: int, step: int, lam: float, hp, accumulate: bool = False, grad_scale_dev=None,
+                    stream=None) -> None:
         _check(lib().smat_adamw_fused_multi(self._plan, int(seed), int(step), float(lam), adamw_params(hp),
-                                            1 if accumulate else 0, _stream_handle(stream)))
+                                            1 if accumulate else 0,
+                                            _scalar_ptr(grad_scale_dev, "grad_scale_dev", "float32"),
+                                            _stream_handle(stream)))
+
+    def grad_norm(self, seed: int, step: int, lam: float, accumulate: bool = False, max_norm: float = 0.0,
+                  sumsq=None, clip_coef=None, stream=None) -> None:
+        """smat_grad_norm_multi: the squared norm of the expert gradient into `sumsq` (one-element
+        fp64 GPU tensor) and/or the clipping factor for `max_norm` into `clip_coef` (fp32)."""
+        _check(lib().smat_grad_norm_multi(self._plan, int(seed), int(step), float(lam), 1 if accumulate else 0,
+                                          float(max_norm), _scalar_ptr(sumsq, "sumsq", "float64"),
+                                          _scalar_ptr(clip_coef, "clip_coef", "float32"), _stream_handle(stream)))
 
     def switch_storage(self, to: int, stream=None) -> None:
         _check(lib().smat_switch_storage(self._plan, int(to), _stream_handle(stream)))

@@ -227,7 +227,8 @@ extern "C" smat_status smat_debug_draws(smat_rng_key key, int64_t n, smat_op_par
 
 extern "C" smat_status smat_adamw_fused(const void* grad_sim, smat_dtype grad_dtype, const float* grad_acc, float* theta,
                                         float* exp_avg, float* exp_avg_sq, int64_t n, smat_op_params p, float lambda,
-                                        smat_adamw_params hp, smat_rng_key key, hipStream_t stream) {
+                                        smat_adamw_params hp, smat_rng_key key, const float* grad_scale_dev,
+                                        hipStream_t stream) {
   if (!valid_dtype(grad_dtype)) return fail(SMAT_ERR_DTYPE, "smat_adamw_fused: unsupported dtype");
   if (n < 0) return fail(SMAT_ERR_INVALID, "smat_adamw_fused: n < 0");
   if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_adamw_fused: lambda must be finite");
@@ -255,7 +256,7 @@ extern "C" smat_status smat_adamw_fused(const void* grad_sim, smat_dtype grad_dt
   rec.sflags = adam_flags(theta, exp_avg, exp_avg_sq, grad_sim, grad_dtype, grad_acc, key.elem_offset);
   const AdamRec sr{exp_avg, exp_avg_sq};
   SMAT_HIP(smat::launch_adamw_one(rec, sr, prm, A, grad_dtype, grad_acc != nullptr, lambda, key.seed, key.step,
-                                  stream));
+                                  grad_scale_dev, stream));
   return SMAT_OK;
 }
 
@@ -271,7 +272,9 @@ struct smat_plan {
   std::vector<void*> expert_ptrs, sim_ptrs;
 
   // workspace layout: [tensor records][chunk table][expert pointer table][simulated pointer table][params]
+  // [optimizer state table][gradient-norm partials: one float per chunk][their fp64 block sums]
   size_t off_recs = 0, off_chunks = 0, off_expert = 0, off_sim = 0, off_params = 0, ws_bytes = 0;
+  size_t off_partials = 0, off_sums = 0;
   char* ws = nullptr;
 
   // pinned staging for the asynchronous uploads: the static tables once, the params every step
@@ -440,6 +443,10 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
   off = align256(off + sizeof(ParamRec) * count);
   p->off_adam = off;
   off = align256(off + sizeof(AdamRec) * count);
+  p->off_partials = off;
+  off = align256(off + sizeof(float) * p->chunks.size());
+  p->off_sums = off;
+  off = align256(off + sizeof(double) * smat::kNormSums);
   p->ws_bytes = std::max<size_t>(off, 256);
   *out_plan = p;
   return SMAT_OK;
@@ -582,7 +589,8 @@ extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_s
 }
 
 extern "C" smat_status smat_adamw_fused_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
-                                              smat_adamw_params hp, int32_t accumulate, hipStream_t stream) {
+                                              smat_adamw_params hp, int32_t accumulate, const float* grad_scale_dev,
+                                              hipStream_t stream) {
   if (!p) return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi: null plan");
   if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi: step must be < 2^30");
   if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi: lambda must be finite");
@@ -599,7 +607,29 @@ extern "C" smat_status smat_adamw_fused_multi(smat_plan* p, uint64_t seed, uint3
                                       reinterpret_cast<const AdamRec*>(p->ws + p->off_adam),
                                       reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
                                       reinterpret_cast<const uint2*>(p->ws + p->off_chunks), (uint32_t)p->chunks.size(),
-                                      A, p->g_dt, accumulate != 0, lambda, seed, step, stream));
+                                      A, p->g_dt, accumulate != 0, lambda, seed, step, grad_scale_dev, stream));
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_grad_norm_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
+                                            int32_t accumulate, float max_norm, double* sumsq, float* clip_coef,
+                                            hipStream_t stream) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: null plan");
+  if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: step must be < 2^30");
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: lambda must be finite");
+  if (accumulate != 0 && accumulate != 1) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: accumulate must be 0 or 1");
+  if (!sumsq && !clip_coef) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: no output");
+  if (clip_coef && !(std::isfinite(max_norm) && max_norm > 0.f))
+    return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: max_norm must be finite and > 0");
+  if (!p->has_grads) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: plan has no gradient pointers");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_grad_norm_multi: no workspace bound");
+  if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_grad_norm_multi: parameters never set");
+  SMAT_HIP(smat::launch_sqnorm_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                     reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                     reinterpret_cast<const uint2*>(p->ws + p->off_chunks), (uint32_t)p->chunks.size(),
+                                     reinterpret_cast<float*>(p->ws + p->off_partials),
+                                     reinterpret_cast<double*>(p->ws + p->off_sums), p->g_dt, accumulate != 0, lambda,
+                                     seed, step, sumsq, clip_coef, max_norm, stream));
   return SMAT_OK;
 }
 

@@ -14,42 +14,13 @@
 // ragged-list kernels find a block's (tensor, chunk) pair in a table built once per tensor
 // list, so huge matrices and tiny vectors share one launch.
 #include "smat_launch.h"
+#include "smat_tile.h"
 
 namespace smat {
-
-template <typename T>
-struct StorageBytes;
-template <>
-struct StorageBytes<float> {
-  static constexpr int value = 4;
-};
-template <>
-struct StorageBytes<Bf16> {
-  static constexpr int value = 2;
-};
 
 // ---------------------------------------------------------------- simulate
 // One tile of `len` (<= 4 kBlock Q) elements starting at element `begin` of a tensor.  Thread x
 // owns quads x + u kBlock (u < Q) of the tile.
-// A tile handed to the element code: pointers at the tile's first element, its global index e0,
-// its length, the tensor id and the alignment flags.
-struct Tile {
-  const float* theta;
-  const void* theta0;
-  void* out;
-  const void* grad_sim;
-  float* grad_theta;
-  uint64_t e0;
-  uint32_t len;
-  uint32_t tensor_id;
-  uint32_t sflags;
-};
-
-template <typename T>
-__device__ __forceinline__ const void* advance(const void* p, int64_t elems) {
-  return static_cast<const char*>(p) + elems * StorageBytes<T>::value;
-}
-
 template <typename T0, typename TO, int Q, int KIND>
 __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
@@ -230,138 +201,7 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
   }
 }
 
-// ---------------------------------------------------------------- fused optimizer step
-// The optimizer update of a simulated step fed directly by the simulated-loss gradient
-// g = grad_scale * ([grad_acc +] lambda t m g~) (Eq. smat-gradient weighted by lambda), with
-// decoupled-weight-decay Adam on the expert storage: m1 += (1 - b1)(g - m1),
-// m2 = b2 m2 + (1 - b2) g^2, theta = theta (1 - lr wd) - (lr / bc1) m1 / (sqrt(m2) / sqrt(bc2) + eps).
-// Dropped coordinates enter the update with a zero simulated gradient.  Per element: 12 B of
-// state read and written plus the gradient at theta~ (and grad_acc when accumulating).
-__device__ __forceinline__ void adam_element(float g, float& th, float& m1, float& m2, const AdamConsts& A) {
-  m1 = __builtin_fmaf(A.one_m_b1, g - m1, m1);
-  m2 = __builtin_fmaf(A.one_m_b2, g * g, A.b2 * m2);
-  const float denom = __builtin_fmaf(__builtin_sqrtf(m2), A.inv_sqrt_bc2, A.eps);
-  th = __builtin_fmaf(-A.step_size, m1 / denom, th * A.decay);
-}
-
-template <typename TG, int Q, bool ACC>
-__device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p, const ParamRec& P,
-                                           const AdamConsts& A, uint64_t seed, uint32_t step, float lambda) {
-  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-  const uint32_t cmask = (step << 2) | kStreamMask;
-  const uint32_t flags = P.flags;
-  const bool use_mask = (flags & kFlagMask) != 0;
-  const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
-  const uint32_t thr = P.thr;
-  const float c = lambda * P.t;
-  const uint32_t len = T.len, tensor_id = T.tensor_id;
-  float* th = const_cast<float*>(T.theta);
-  const void* gs = T.grad_sim;
-  const float* ga = T.grad_theta;
-  const uint64_t e0 = T.e0;
-
-  // simulated gradient of one element: kept -> [acc +] c g~, dropped -> [acc or] 0, then grad_scale
-  auto grad = [&](bool kept, float gsim, float acc) {
-    const float gv = ACC ? (kept ? __builtin_fmaf(c, gsim, acc) : acc) : (kept ? c * gsim : 0.0f);
-    return A.grad_scale * gv;
-  };
-  auto one = [&](uint32_t i) {
-    const uint64_t e = e0 + i;
-    bool kept = all_kept;
-    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
-    const float g = grad(kept, QuadIO<TG>::load1(gs, i), ACC ? QuadIO<float>::load1(ga, i) : 0.0f);
-    float t = QuadIO<float>::load1(th, i), a = QuadIO<float>::load1(m1p, i), b = QuadIO<float>::load1(m2p, i);
-    adam_element(g, t, a, b, A);
-    QuadIO<float>::store1(th, i, t);
-    QuadIO<float>::store1(m1p, i, a);
-    QuadIO<float>::store1(m2p, i, b);
-  };
-
-  const uint32_t vec = ACC ? kVecAdamAcc : kVecAdam;
-  if (!(T.sflags & vec)) {
-#pragma unroll
-    for (int u = 0; u < Q; ++u) {
-      const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
-      for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) one(i);
-    }
-    return;
-  }
-  const uint32_t nq = len >> 2;
-  if (nq > 0) {
-    typename QuadIO<TG>::Raw rg[Q];
-    typename QuadIO<float>::Raw racc[Q], rt[Q], r1[Q], r2[Q];
-#pragma unroll
-    for (int u = 0; u < Q; ++u) {
-      const uint32_t q = u * kBlock + threadIdx.x;
-      const uint32_t qc = q < nq ? q : nq - 1;
-      rg[u] = QuadIO<TG>::load_raw(gs, qc);
-      if (ACC) racc[u] = QuadIO<float>::load_raw(ga, qc);
-      rt[u] = QuadIO<float>::load_raw(th, qc);
-      r1[u] = QuadIO<float>::load_raw(m1p, qc);
-      r2[u] = QuadIO<float>::load_raw(m2p, qc);
-    }
-    bool kept[Q][4];
-#pragma unroll
-    for (int u = 0; u < Q; ++u) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
-      if (use_mask) {
-        const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, cmask, k0, k1);
-        kept[u][0] = w.w0 < thr;
-        kept[u][1] = w.w1 < thr;
-        kept[u][2] = w.w2 < thr;
-        kept[u][3] = w.w3 < thr;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < Q; ++u) {
-      const uint32_t q = u * kBlock + threadIdx.x;
-      if (q < nq) {
-        float gsim[4], acc[4] = {0.f, 0.f, 0.f, 0.f}, t[4], a[4], b[4];
-        QuadIO<TG>::unpack(rg[u], gsim);
-        if (ACC) QuadIO<float>::unpack(racc[u], acc);
-        QuadIO<float>::unpack(rt[u], t);
-        QuadIO<float>::unpack(r1[u], a);
-        QuadIO<float>::unpack(r2[u], b);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) adam_element(grad(kept[u][j], gsim[j], acc[j]), t[j], a[j], b[j], A);
-        QuadIO<float>::store(th, q, t);
-        QuadIO<float>::store(m1p, q, a);
-        QuadIO<float>::store(m2p, q, b);
-      }
-    }
-  }
-  if ((len & 3u) && threadIdx.x == (nq & (kBlock - 1))) {
-    for (uint32_t i = nq * 4u; i < len; ++i) one(i);
-  }
-}
-
 // ---------------------------------------------------------------- kernels
-__device__ __forceinline__ uint32_t tile_len(int64_t n, int64_t begin, int64_t tile) {
-  return (uint32_t)(n - begin < tile ? n - begin : tile);
-}
-
-template <typename T0, typename TO>
-__device__ __forceinline__ Tile tensor_tile(const TensorRec& R, int64_t begin, int64_t tile) {
-  return Tile{R.theta + begin, advance<T0>(R.theta0, begin), const_cast<void*>(advance<TO>(R.out, begin)),
-              R.grad_sim, R.grad_theta, R.elem_offset + (uint64_t)begin, tile_len(R.n, begin, tile), R.tensor_id,
-              R.sflags};
-}
-
-// Tile b of a list launch: tile (b mod tiles-per-chunk) of chunk (b / tiles-per-chunk), the chunk
-// table giving (tensor index, chunk index within the tensor).  The chunk table (8 B per 16K
-// elements) and the tensor records (64 B per tensor) are small enough to stay in L2 while the
-// kernel streams the tensors.  len is 0 when the tile lies past the end of a tensor.
-template <typename T0, typename TO, typename TG>
-__device__ __forceinline__ Tile list_tile(const TensorRec& R, uint32_t chunk, uint32_t tile_in_chunk, int64_t tile) {
-  const int64_t begin = (int64_t)chunk * kChunk + (int64_t)tile_in_chunk * tile;
-  Tile T = tensor_tile<T0, TO>(R, begin, tile);
-  T.grad_sim = advance<TG>(R.grad_sim, begin);
-  T.grad_theta = R.grad_theta + begin;
-  if (begin >= R.n) T.len = 0;
-  return T;
-}
-
 template <typename T0, typename TO>
 __global__ __launch_bounds__(kBlock) void k_simulate_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step) {
   constexpr int64_t tile = tile_elems(kSimQuads);
@@ -403,34 +243,6 @@ __global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __re
   const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;
   backward_tile<TG, kBwdQuads>(T, prms[ch.x], seed, step, lambda);
-}
-
-template <typename TG, bool ACC>
-__global__ __launch_bounds__(kBlock) void k_adamw_one(TensorRec R, AdamRec S, ParamRec P, AdamConsts A, uint64_t seed,
-                                                      uint32_t step, float lambda) {
-  constexpr int64_t tile = tile_elems(kAdamQuads);
-  const int64_t begin = (int64_t)blockIdx.x * tile;
-  Tile T = tensor_tile<float, float>(R, begin, tile);
-  T.grad_sim = advance<TG>(R.grad_sim, begin);
-  T.grad_theta = R.grad_theta ? R.grad_theta + begin : nullptr;
-  adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, P, A, seed, step, lambda);
-}
-
-template <typename TG, bool ACC>
-__global__ __launch_bounds__(kBlock) void k_adamw_multi(const TensorRec* __restrict__ recs,
-                                                        const AdamRec* __restrict__ states,
-                                                        const ParamRec* __restrict__ prms,
-                                                        const uint2* __restrict__ chunks, AdamConsts A, uint64_t seed,
-                                                        uint32_t step, float lambda) {
-  constexpr int64_t tile = tile_elems(kAdamQuads);
-  constexpr uint32_t tpc = tiles_per_chunk(kAdamQuads);
-  const uint2 ch = chunks[blockIdx.x / tpc];
-  const TensorRec R = recs[ch.x];
-  const int64_t begin = (int64_t)ch.y * kChunk + (int64_t)(blockIdx.x % tpc) * tile;
-  const Tile T = list_tile<float, float, TG>(R, ch.y, blockIdx.x % tpc, tile);
-  if (T.len == 0) return;
-  const AdamRec S = states[ch.x];
-  adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, prms[ch.x], A, seed, step, lambda);
 }
 
 constexpr int kDebugBlock = 256;
@@ -504,36 +316,6 @@ hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, co
     k_backward_multi<Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
   else
     k_backward_multi<float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
-  return hipGetLastError();
-}
-
-hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const ParamRec& prm, const AdamConsts& A,
-                            int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
-                            hipStream_t stream) {
-  const dim3 grid(blocks_for(rec.n, tile_elems(kAdamQuads))), block(kBlock);
-  if (grad_dtype == 1 && accumulate)
-    k_adamw_one<Bf16, true><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda);
-  else if (grad_dtype == 1)
-    k_adamw_one<Bf16, false><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda);
-  else if (accumulate)
-    k_adamw_one<float, true><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda);
-  else
-    k_adamw_one<float, false><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda);
-  return hipGetLastError();
-}
-
-hipError_t launch_adamw_multi(const TensorRec* recs, const AdamRec* states, const ParamRec* prms, const uint2* chunks,
-                              uint32_t nchunks, const AdamConsts& A, int grad_dtype, bool accumulate, float lambda,
-                              uint64_t seed, uint32_t step, hipStream_t stream) {
-  const dim3 grid(nchunks * tiles_per_chunk(kAdamQuads)), block(kBlock);
-  if (grad_dtype == 1 && accumulate)
-    k_adamw_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda);
-  else if (grad_dtype == 1)
-    k_adamw_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda);
-  else if (accumulate)
-    k_adamw_multi<float, true><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda);
-  else
-    k_adamw_multi<float, false><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda);
   return hipGetLastError();
 }
 

@@ -19,10 +19,18 @@ hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, co
                                  int grad_dtype, float lambda, uint64_t seed, uint32_t step, hipStream_t stream);
 hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const ParamRec& prm, const AdamConsts& A,
                             int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
-                            hipStream_t stream);
+                            const float* dev_scale, hipStream_t stream);
 hipError_t launch_adamw_multi(const TensorRec* recs, const AdamRec* states, const ParamRec* prms, const uint2* chunks,
                               uint32_t nchunks, const AdamConsts& A, int grad_dtype, bool accumulate, float lambda,
-                              uint64_t seed, uint32_t step, hipStream_t stream);
+                              uint64_t seed, uint32_t step, const float* dev_scale, hipStream_t stream);
+// Squared norm of the simulated step's expert gradient over the list: per-chunk fp32 partials
+// (nchunks floats), their fp64 block sums (at most kNormSums doubles), then sumsq and/or the
+// clipping factor.
+constexpr uint32_t kNormSums = 256;
+hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
+                               float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
+                               uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
+                               hipStream_t stream);
 hipError_t launch_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t elem_offset,
                               int64_t n, const ParamRec& prm, uint32_t* mask_words, uint32_t* noise_words,
                               uint8_t* kept, float* z, hipStream_t stream);

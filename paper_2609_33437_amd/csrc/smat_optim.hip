@@ -1,0 +1,342 @@
+// HIP kernels of the optimizer side of a simulated step for gfx950: the AdamW update fed directly
+// by the gradient through the simulation, and the squared norm of that gradient for clipping.
+// Both are HBM-bound streams built like the simulate/backward kernels (quads of 4 elements = one
+// Philox group, the mask regenerated in registers, loads issued before the draws).
+#include "smat_launch.h"
+#include "smat_tile.h"
+
+namespace smat {
+
+// ---------------------------------------------------------------- fused optimizer step
+// The optimizer update of a simulated step fed directly by the simulated-loss gradient
+// g = grad_scale * ([grad_acc +] lambda t m g~) (Eq. smat-gradient weighted by lambda), with
+// decoupled-weight-decay Adam on the expert storage: m1 += (1 - b1)(g - m1),
+// m2 = b2 m2 + (1 - b2) g^2, theta = theta (1 - lr wd) - (lr / bc1) m1 / (sqrt(m2) / sqrt(bc2) + eps).
+// Dropped coordinates enter the update with a zero simulated gradient.  Per element: 12 B of
+// state read and written plus the gradient at theta~ (and grad_acc when accumulating).
+__device__ __forceinline__ void adam_element(float g, float& th, float& m1, float& m2, const AdamConsts& A) {
+  m1 = __builtin_fmaf(A.one_m_b1, g - m1, m1);
+  m2 = __builtin_fmaf(A.one_m_b2, g * g, A.b2 * m2);
+  const float denom = __builtin_fmaf(__builtin_sqrtf(m2), A.inv_sqrt_bc2, A.eps);
+  th = __builtin_fmaf(-A.step_size, m1 / denom, th * A.decay);
+}
+
+template <typename TG, int Q, bool ACC>
+__device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p, const ParamRec& P,
+                                           const AdamConsts& A, uint64_t seed, uint32_t step, float lambda) {
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  const uint32_t cmask = (step << 2) | kStreamMask;
+  const uint32_t flags = P.flags;
+  const bool use_mask = (flags & kFlagMask) != 0;
+  const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
+  const uint32_t thr = P.thr;
+  const float c = lambda * P.t;
+  const uint32_t len = T.len, tensor_id = T.tensor_id;
+  float* th = const_cast<float*>(T.theta);
+  const void* gs = T.grad_sim;
+  const float* ga = T.grad_theta;
+  const uint64_t e0 = T.e0;
+
+  // simulated gradient of one element: kept -> [acc +] c g~, dropped -> [acc or] 0, then grad_scale
+  auto grad = [&](bool kept, float gsim, float acc) {
+    const float gv = ACC ? (kept ? __builtin_fmaf(c, gsim, acc) : acc) : (kept ? c * gsim : 0.0f);
+    return A.grad_scale * gv;
+  };
+  auto one = [&](uint32_t i) {
+    const uint64_t e = e0 + i;
+    bool kept = all_kept;
+    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
+    const float g = grad(kept, QuadIO<TG>::load1(gs, i), ACC ? QuadIO<float>::load1(ga, i) : 0.0f);
+    float t = QuadIO<float>::load1(th, i), a = QuadIO<float>::load1(m1p, i), b = QuadIO<float>::load1(m2p, i);
+    adam_element(g, t, a, b, A);
+    QuadIO<float>::store1(th, i, t);
+    QuadIO<float>::store1(m1p, i, a);
+    QuadIO<float>::store1(m2p, i, b);
+  };
+
+  const uint32_t vec = ACC ? kVecAdamAcc : kVecAdam;
+  if (!(T.sflags & vec)) {
+#pragma unroll
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
+      for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) one(i);
+    }
+    return;
+  }
+  const uint32_t nq = len >> 2;
+  if (nq > 0) {
+    typename QuadIO<TG>::Raw rg[Q];
+    typename QuadIO<float>::Raw racc[Q], rt[Q], r1[Q], r2[Q];
+#pragma unroll
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t q = u * kBlock + threadIdx.x;
+      const uint32_t qc = q < nq ? q : nq - 1;
+      rg[u] = QuadIO<TG>::load_raw(gs, qc);
+      if (ACC) racc[u] = QuadIO<float>::load_raw(ga, qc);
+      rt[u] = QuadIO<float>::load_raw(th, qc);
+      r1[u] = QuadIO<float>::load_raw(m1p, qc);
+      r2[u] = QuadIO<float>::load_raw(m2p, qc);
+    }
+    bool kept[Q][4];
+#pragma unroll
+    for (int u = 0; u < Q; ++u) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
+      if (use_mask) {
+        const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, cmask, k0, k1);
+        kept[u][0] = w.w0 < thr;
+        kept[u][1] = w.w1 < thr;
+        kept[u][2] = w.w2 < thr;
+        kept[u][3] = w.w3 < thr;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < Q; ++u) {
+      const uint32_t q = u * kBlock + threadIdx.x;
+      if (q < nq) {
+        float gsim[4], acc[4] = {0.f, 0.f, 0.f, 0.f}, t[4], a[4], b[4];
+        QuadIO<TG>::unpack(rg[u], gsim);
+        if (ACC) QuadIO<float>::unpack(racc[u], acc);
+        QuadIO<float>::unpack(rt[u], t);
+        QuadIO<float>::unpack(r1[u], a);
+        QuadIO<float>::unpack(r2[u], b);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) adam_element(grad(kept[u][j], gsim[j], acc[j]), t[j], a[j], b[j], A);
+        QuadIO<float>::store(th, q, t);
+        QuadIO<float>::store(m1p, q, a);
+        QuadIO<float>::store(m2p, q, b);
+      }
+    }
+  }
+  if ((len & 3u) && threadIdx.x == (nq & (kBlock - 1))) {
+    for (uint32_t i = nq * 4u; i < len; ++i) one(i);
+  }
+}
+
+template <typename TG, bool ACC>
+__global__ __launch_bounds__(kBlock) void k_adamw_one(TensorRec R, AdamRec S, ParamRec P, AdamConsts A, uint64_t seed,
+                                                      uint32_t step, float lambda, const float* dev_scale) {
+  constexpr int64_t tile = tile_elems(kAdamQuads);
+  if (dev_scale) A.grad_scale *= *dev_scale;
+  const int64_t begin = (int64_t)blockIdx.x * tile;
+  Tile T = tensor_tile<float, float>(R, begin, tile);
+  T.grad_sim = advance<TG>(R.grad_sim, begin);
+  T.grad_theta = R.grad_theta ? R.grad_theta + begin : nullptr;
+  adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, P, A, seed, step, lambda);
+}
+
+template <typename TG, bool ACC>
+__global__ __launch_bounds__(kBlock) void k_adamw_multi(const TensorRec* __restrict__ recs,
+                                                        const AdamRec* __restrict__ states,
+                                                        const ParamRec* __restrict__ prms,
+                                                        const uint2* __restrict__ chunks, AdamConsts A, uint64_t seed,
+                                                        uint32_t step, float lambda, const float* dev_scale) {
+  constexpr int64_t tile = tile_elems(kAdamQuads);
+  if (dev_scale) A.grad_scale *= *dev_scale;
+  constexpr uint32_t tpc = tiles_per_chunk(kAdamQuads);
+  const uint2 ch = chunks[blockIdx.x / tpc];
+  const TensorRec R = recs[ch.x];
+  const int64_t begin = (int64_t)ch.y * kChunk + (int64_t)(blockIdx.x % tpc) * tile;
+  const Tile T = list_tile<float, float, TG>(R, ch.y, blockIdx.x % tpc, tile);
+  if (T.len == 0) return;
+  const AdamRec S = states[ch.x];
+  adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, prms[ch.x], A, seed, step, lambda);
+}
+
+// ---------------------------------------------------------------- gradient norm
+// Squared L2 norm of the expert gradient g = [grad_acc +] lambda t m g~ of a simulated step
+// (Eq. smat-gradient weighted by lambda): what norm clipping measures before the optimizer step.
+// It reads only g~ (2 B per element in bf16) and, when accumulating, grad_acc.  A block of
+// kNormBlock threads reduces one chunk: thread x owns quads x + u kNormBlock, issues all of its
+// loads first, then draws each quad's mask and adds its squares while later loads are in flight.
+// Each block writes one fp32 partial; the partials are then added in fp64 in a fixed order (at
+// most kNormSums blocks over contiguous ranges, then one block), so the result does not depend
+// on scheduling and is the same from run to run.
+constexpr int kNormBlock = 256;
+constexpr int kNormQuads = (int)(kChunk / (4 * kNormBlock));
+static_assert(kNormQuads * 4 * kNormBlock == kChunk, "norm blocks split chunks");
+constexpr int kSumBlock = 256;
+static_assert(kNormSums <= (uint32_t)kSumBlock, "the final block holds one block sum per thread");
+
+template <typename TG, bool ACC>
+__device__ __forceinline__ float chunk_sqnorm(const TensorRec& R, const ParamRec& P, uint32_t chunk, uint64_t seed,
+                                              uint32_t step, float lambda) {
+  const uint32_t flags = P.flags;
+  if (!ACC && (flags & kFlagDropAll)) return 0.0f;
+  const int64_t begin = (int64_t)chunk * kChunk;
+  const uint32_t len = tile_len(R.n, begin, kChunk);
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  const uint32_t cmask = (step << 2) | kStreamMask;
+  const bool use_mask = (flags & kFlagMask) != 0;
+  const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
+  const uint32_t thr = P.thr, tensor_id = R.tensor_id;
+  const float c = lambda * P.t;
+  const void* gs = advance<TG>(R.grad_sim, begin);
+  const float* ga = R.grad_theta + begin;
+  const uint64_t e0 = R.elem_offset + (uint64_t)begin;
+
+  auto gval = [&](bool kept, float gsim, float acc) {
+    return ACC ? (kept ? __builtin_fmaf(c, gsim, acc) : acc) : (kept ? c * gsim : 0.0f);
+  };
+  float s = 0.0f;
+  auto one = [&](uint32_t i) {
+    const uint64_t e = e0 + i;
+    bool kept = all_kept;
+    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
+    const float g = gval(kept, QuadIO<TG>::load1(gs, i), ACC ? QuadIO<float>::load1(ga, i) : 0.0f);
+    s = __builtin_fmaf(g, g, s);
+  };
+
+  if (!(R.sflags & kVecBwd)) {
+    for (int u = 0; u < kNormQuads; ++u) {
+      const uint32_t i0 = (u * kNormBlock + threadIdx.x) * 4u;
+      for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) one(i);
+    }
+    return s;
+  }
+  const uint32_t nq = len >> 2;
+  if (nq > 0) {
+    typename QuadIO<TG>::Raw rg[kNormQuads];
+    typename QuadIO<float>::Raw ra[kNormQuads];
+#pragma unroll
+    for (int u = 0; u < kNormQuads; ++u) {
+      const uint32_t q = u * kNormBlock + threadIdx.x;
+      const uint32_t qc = q < nq ? q : nq - 1;
+      rg[u] = QuadIO<TG>::load_raw(gs, qc);
+      if (ACC) ra[u] = QuadIO<float>::load_raw(ga, qc);
+    }
+#pragma unroll
+    for (int u = 0; u < kNormQuads; ++u) {
+      const uint32_t q = u * kNormBlock + threadIdx.x;
+      if (q < nq) {
+        bool kept[4] = {all_kept, all_kept, all_kept, all_kept};
+        if (use_mask) {
+          const Words w = group_words((e0 >> 2) + q, tensor_id, cmask, k0, k1);
+          kept[0] = w.w0 < thr;
+          kept[1] = w.w1 < thr;
+          kept[2] = w.w2 < thr;
+          kept[3] = w.w3 < thr;
+        }
+        float a[4], b[4] = {0.f, 0.f, 0.f, 0.f};
+        QuadIO<TG>::unpack(rg[u], a);
+        if (ACC) QuadIO<float>::unpack(ra[u], b);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float g = gval(kept[j], a[j], b[j]);
+          s = __builtin_fmaf(g, g, s);
+        }
+      }
+    }
+  }
+  if ((len & 3u) && threadIdx.x == (nq & (kNormBlock - 1))) {
+    for (uint32_t i = nq * 4u; i < len; ++i) one(i);
+  }
+  return s;
+}
+
+// Sum over the block, the same value in every thread: a butterfly within each wave, then the
+// waves' sums in a fixed order.
+template <typename T, int BLOCK>
+__device__ __forceinline__ T block_sum(T v) {
+  __shared__ T part[BLOCK / 64];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+  __syncthreads();
+  T t = part[0];
+#pragma unroll
+  for (int w = 1; w < BLOCK / 64; ++w) t += part[w];
+  return t;
+}
+
+template <typename TG, bool ACC>
+__global__ __launch_bounds__(kNormBlock) void k_sqnorm_multi(const TensorRec* __restrict__ recs,
+                                                             const ParamRec* __restrict__ prms,
+                                                             const uint2* __restrict__ chunks, float* partials,
+                                                             uint64_t seed, uint32_t step, float lambda) {
+  const uint2 ch = chunks[blockIdx.x];
+  const float s = block_sum<float, kNormBlock>(chunk_sqnorm<TG, ACC>(recs[ch.x], prms[ch.x], ch.y, seed, step, lambda));
+  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+}
+
+// Block b adds partials [b per, (b + 1) per) in fp64.
+__global__ __launch_bounds__(kSumBlock) void k_sum_partials(const float* __restrict__ partials, uint32_t n,
+                                                            uint32_t per, double* sums) {
+  const uint32_t lo = blockIdx.x * per, hi = lo + per < n ? lo + per : n;
+  double s = 0.0;
+  for (uint32_t i = lo + threadIdx.x; i < hi; i += kSumBlock) s += (double)partials[i];
+  s = block_sum<double, kSumBlock>(s);
+  if (threadIdx.x == 0) sums[blockIdx.x] = s;
+}
+
+// Total of the m block sums; the squared norm and/or the clipping factor min(1, max_norm /
+// (norm + 1e-6)), the rule of torch.nn.utils.clip_grad_norm_ for the L2 norm.
+__global__ __launch_bounds__(kSumBlock) void k_sqnorm_finalize(const double* __restrict__ sums, uint32_t m,
+                                                               double* sumsq, float* clip_coef, float max_norm) {
+  const double s = block_sum<double, kSumBlock>(threadIdx.x < m ? sums[threadIdx.x] : 0.0);
+  if (threadIdx.x == 0) {
+    if (sumsq) *sumsq = s;
+    if (clip_coef) {
+      const double c = (double)max_norm / (sqrt(s) + 1e-6);
+      *clip_coef = (float)(c < 1.0 ? c : 1.0);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+static inline uint32_t blocks_for(int64_t n, int64_t per_block) { return (uint32_t)((n + per_block - 1) / per_block); }
+
+hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const ParamRec& prm, const AdamConsts& A,
+                            int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
+                            const float* dev_scale, hipStream_t stream) {
+  const dim3 grid(blocks_for(rec.n, tile_elems(kAdamQuads))), block(kBlock);
+  if (grad_dtype == 1 && accumulate)
+    k_adamw_one<Bf16, true><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda, dev_scale);
+  else if (grad_dtype == 1)
+    k_adamw_one<Bf16, false><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda, dev_scale);
+  else if (accumulate)
+    k_adamw_one<float, true><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda, dev_scale);
+  else
+    k_adamw_one<float, false><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda, dev_scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_adamw_multi(const TensorRec* recs, const AdamRec* states, const ParamRec* prms, const uint2* chunks,
+                              uint32_t nchunks, const AdamConsts& A, int grad_dtype, bool accumulate, float lambda,
+                              uint64_t seed, uint32_t step, const float* dev_scale, hipStream_t stream) {
+  const dim3 grid(nchunks * tiles_per_chunk(kAdamQuads)), block(kBlock);
+  if (grad_dtype == 1 && accumulate)
+    k_adamw_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda, dev_scale);
+  else if (grad_dtype == 1)
+    k_adamw_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda, dev_scale);
+  else if (accumulate)
+    k_adamw_multi<float, true><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda, dev_scale);
+  else
+    k_adamw_multi<float, false><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda, dev_scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
+                               float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
+                               uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
+                               hipStream_t stream) {
+  if (nchunks > 0) {
+    const dim3 grid(nchunks), block(kNormBlock);
+    if (grad_dtype == 1 && accumulate)
+      k_sqnorm_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
+    else if (grad_dtype == 1)
+      k_sqnorm_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
+    else if (accumulate)
+      k_sqnorm_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
+    else
+      k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
+  }
+  // m <= kNormSums blocks, each adding `per` consecutive partials
+  const uint32_t per = (nchunks + kNormSums - 1) / kNormSums;
+  const uint32_t m = per ? (nchunks + per - 1) / per : 0;
+  if (m > 0) k_sum_partials<<<dim3(m), dim3(kSumBlock), 0, stream>>>(partials, nchunks, per, sums);
+  k_sqnorm_finalize<<<dim3(1), dim3(kSumBlock), 0, stream>>>(sums, m, sumsq, clip_coef, max_norm);
+  return hipGetLastError();
+}
+
+}  // namespace smat

@@ -160,6 +160,7 @@ class SimulatedMergeTraining:
         self.alpha: Optional[float] = None      # the scale of the current (or last) simulated step
         self._step: Optional[int] = None        # set between begin() and end()
         self._adam_key = None
+        self._clip = None                       # GPU scalars (sumsq, clipping factor) of the fused update
 
     @classmethod
     def from_module(cls, model: torch.nn.Module, keep: float = 0.5, alpha_min: float = 0.2, sigma: float = 2e-3,
@@ -219,14 +220,19 @@ class SimulatedMergeTraining:
         self._step = None
 
     def end(self, optimizer: Optional[torch.optim.Optimizer] = None, fused: bool = False,
-            grad_scale: float = 1.0) -> None:
+            grad_scale: float = 1.0, max_norm: Optional[float] = None) -> Optional[torch.Tensor]:
         """Call after the backward pass of a simulated step.  Without `fused`, leaves
-        param.grad = lam * alpha * m (.) g~ on the expert storage for the caller's optimizer.step().
-        With `fused`, applies the update of `optimizer` (torch Adam/AdamW) directly; its
-        hyperparameters and step count come from that optimizer, `grad_scale` multiplies the
-        gradient first (e.g. a clipping factor), and the caller must not call optimizer.step()."""
+        param.grad = lam * alpha * m (.) g~ on the expert storage for the caller's optimizer.step()
+        (and its own clipping).  With `fused`, applies the update of `optimizer` (torch Adam/AdamW)
+        directly; its hyperparameters and step count come from that optimizer, `grad_scale`
+        multiplies the gradient, and the caller must not call optimizer.step().  With `max_norm`
+        the fused update first clips the expert gradient to that L2 norm as
+        torch.nn.utils.clip_grad_norm_ would (smat_grad_norm_multi, factor kept on the GPU); the
+        gradient's total norm is then returned as a GPU scalar."""
         if self._step is None:
             raise SmatError(SMAT_ERR_STATE, "end() without an open simulated step")
+        if max_norm is not None and not fused:
+            raise SmatError(SMAT_ERR_INVALID, "max_norm applies to the fused update; clip param.grad otherwise")
         step = self._step
         self._collect_grad_sim()
         if fused:
@@ -234,14 +240,14 @@ class SimulatedMergeTraining:
                 raise SmatError(SMAT_ERR_INVALID, "the fused update needs the optimizer that owns the moments")
             hp = adam_hparams(optimizer, self.params)   # validate before touching any state
             self._restore()
-            self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step)
-            return
+            return self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step, max_norm)
         for g in self.grad_theta:
             g.zero_()
         self.plan.backward_accum(self.seed, step, self.lam)
         self._restore()
         for p, g in zip(self.params, self.grad_theta):
             p.grad = g
+        return None
 
     def abort(self) -> None:
         """Leave an open simulated step without any update (e.g. after an exception or a skipped
@@ -249,7 +255,7 @@ class SimulatedMergeTraining:
         if self._step is not None:
             self._restore()
 
-    def _fused_adam(self, optimizer, hp: dict, step: int) -> None:
+    def _fused_adam(self, optimizer, hp: dict, step: int, max_norm: Optional[float]) -> Optional[torch.Tensor]:
         exp_avg, exp_avg_sq, counts = [], [], []
         for p in self.params:
             st = optimizer.state[p]
@@ -267,9 +273,18 @@ class SimulatedMergeTraining:
         if key != self._adam_key:
             self.plan.bind_adam_state(exp_avg, exp_avg_sq)
             self._adam_key = key
-        self.plan.adamw_fused(self.seed, step, self.lam, hp)
+        coef = norm = None
+        if max_norm is not None:
+            if self._clip is None:
+                dev = self.master[0].device
+                self._clip = (torch.zeros(1, dtype=torch.float64, device=dev), torch.ones(1, dtype=torch.float32, device=dev))
+            sumsq, coef = self._clip
+            self.plan.grad_norm(self.seed, step, self.lam, False, float(max_norm), sumsq, coef)
+            norm = sumsq.sqrt()
+        self.plan.adamw_fused(self.seed, step, self.lam, hp, grad_scale_dev=coef)
         for c in counts:
             c.add_(1)
+        return norm
 
     def close(self) -> None:
         if self.plan is not None:

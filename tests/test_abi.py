@@ -155,7 +155,7 @@ def test_invalid_adamw_hyperparameters_rejected_before_launch(bad):
     p = _lib.op_params(dict(s=0.5, keep=0.5, sigma=0.0))
     P = ctypes.c_void_p
     st = lib.smat_adamw_fused(P(1 << 20), 1, None, P(2 << 20), P(3 << 20), P(4 << 20), 4, p, 1.0, hp,
-                              _lib.rng_key(0, 0), None)
+                              _lib.rng_key(0, 0), None, None)
     assert st == _lib.SMAT_ERR_INVALID
 
 
@@ -166,5 +166,30 @@ def test_adamw_overlap_rejected_without_gpu():
     P = ctypes.c_void_p
     # exp_avg overlaps theta
     st = lib.smat_adamw_fused(P(1 << 20), 1, None, P(2 << 20), P((2 << 20) + 8), P(4 << 20), 4, p, 1.0, hp,
-                              _lib.rng_key(0, 0), None)
+                              _lib.rng_key(0, 0), None, None)
     assert st == _lib.SMAT_ERR_INVALID
+
+
+def test_grad_norm_argument_errors_without_gpu():
+    lib = smat.lib()
+    A = 1 << 20
+    P = ctypes.c_void_p
+    arr = (_lib.smat_tensor_desc * 1)(_desc(1 * A, 2 * A, 3 * A, 4 * A, 5 * A, 1000, 0))
+    plan = P()
+    assert lib.smat_plan_create(arr, 1, 1, 1, 1, 0, ctypes.byref(plan)) == 0
+    out = P(6 * A)
+    assert lib.smat_grad_norm_multi(None, 0, 0, 1.0, 0, 1.0, out, None, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 0, 1.0, None, None, None) == _lib.SMAT_ERR_INVALID   # no output
+    for bad in (0.0, -1.0, float("nan"), float("inf")):
+        assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 0, bad, None, out, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_grad_norm_multi(plan, 0, 0, float("inf"), 0, 1.0, out, None, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 2, 1.0, out, None, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_grad_norm_multi(plan, 0, 1 << 30, 1.0, 0, 1.0, out, None, None) == _lib.SMAT_ERR_INVALID
+    # a valid call on a plan without workspace is a state error and launches nothing
+    assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 0, 1.0, out, None, None) == _lib.SMAT_ERR_STATE
+    assert lib.smat_plan_destroy(plan) == 0
+    # a plan without gradient pointers has no norm to take
+    arr = (_lib.smat_tensor_desc * 1)(_desc(1 * A, 2 * A, 3 * A, None, None, 1000, 0))
+    assert lib.smat_plan_create(arr, 1, 1, 1, 1, 0, ctypes.byref(plan)) == 0
+    assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 0, 1.0, out, None, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_plan_destroy(plan) == 0

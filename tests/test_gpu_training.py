@@ -15,7 +15,7 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 from paper_2609_33437_amd.training import SimulatedMergeTraining
-from tolerances import check_adam, check_grad, check_theta_tilde, ordered
+from tolerances import SQNORM_ULPS, U, check_adam, check_grad, check_sqnorm, check_theta_tilde, ordered
 from workloads.model import TINY, make_decoder, token_batches
 
 pytestmark = pytest.mark.gpu
@@ -134,6 +134,40 @@ def test_fused_adamw_step_matches_oracle(torch_fused):
     model.loss(batches[0]).backward()
     opt.step()
     assert all(int(float(opt.state[p]["step"])) == 5 for p in w.params)
+    w.close()
+
+
+def test_fused_clipped_step_matches_oracle():
+    """end(fused=True, max_norm) clips the expert gradient to max_norm before the AdamW update, with
+    the factor computed and applied on the GPU; the returned norm is the gradient's total norm."""
+    model = make_decoder(TINY, 37, DEV)
+    w = wrap(model)
+    opt = torch.optim.AdamW(w.params, lr=1e-3, betas=(0.9, 0.95), weight_decay=1e-3)
+    gen = torch.Generator(DEV).manual_seed(2)
+    for p in w.params:                                   # a state as after a few steps
+        opt.state[p] = dict(step=torch.tensor(3.0), exp_avg=torch.randn(p.shape, device=DEV, generator=gen) * 1e-3,
+                            exp_avg_sq=torch.rand(p.shape, device=DEV, generator=gen) * 1e-6)
+    assert w.begin(3)
+    model.loss(token_batches(TINY, 2, 16, 1, 5, DEV)[0]).backward()
+    old = [(host(m)[0], host(opt.state[p]["exp_avg"])[0], host(opt.state[p]["exp_avg_sq"])[0])
+           for p, m in zip(w.params, w.master)]
+    g_sim = [host(g)[0] for g in w.grad_sim]
+    ops = [op(w, i) for i in range(len(w.params))]
+    sq = sum(oracle.grad_sqnorm(g_sim[i], "f32", ops[i], w.lam, SEED, 3, i) for i in range(len(g_sim)))
+    max_norm = 0.25 * float(np.sqrt(sq))
+    norm = w.end(opt, fused=True, max_norm=max_norm)
+    torch.cuda.synchronize()
+    assert check_sqnorm(float(norm.item()) ** 2, sq, sq * (1 + 1e-6))
+    coef = float(w._clip[1].item())
+    assert abs(coef - oracle.clip_coefficient(np.sqrt(sq), max_norm)) <= (0.5 * SQNORM_ULPS + 2) * U * coef
+    hp = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=1e-3, grad_scale=coef, step=4)
+    for i, p in enumerate(w.params):
+        st = opt.state[p]
+        _, f64 = oracle.adamw_fused(g_sim[i], "f32", *old[i], ops[i], w.lam, hp, SEED, 3, i)
+        gmag = coef * np.abs(oracle.simulated_gradient(g_sim[i], "f32", ops[i], w.lam, SEED, 3, i))
+        got = (host(p.data)[0], host(st["exp_avg"])[0], host(st["exp_avg_sq"])[0])
+        for name, ok in zip(("theta", "exp_avg", "exp_avg_sq"), check_adam(got, old[i], f64, hp, gmag)):
+            assert ok.all(), f"{w.names[i]} {name}: {np.count_nonzero(~ok)} mismatches"
     w.close()
 
 

@@ -91,3 +91,18 @@ def check_adam(gpu, old, oracle_f64, hp, gmag=None):
     ok_th = np.abs(gt - th_o) <= (4 * U * (np.abs(th0) + np.abs(th_o))
                                   + 24 * U * step_size * (np.abs(m10) + ga) / denom + tiny)
     return ok_th, ok_m1, ok_m2
+
+
+# Squared gradient norm (smat_grad_norm_multi).  Per element the kernel forms g = fl(c g~) or
+# fl(fma(c, g~, acc)) with c = fl(lambda fl(s/keep)): |g' - g| <= 3u m, m = |lambda t g~| + |acc|,
+# so |g'^2 - g^2| <= 6u m^2 (first order).  The squares are added by one fp32 fma chain per thread
+# (at most 4 kNormQuads = 64 terms, 63 for the thread that also takes a tensor's 1-3 tail
+# elements), then 6 butterfly levels within the wave and 2 across the block's four waves: a sum of
+# non-negative terms through at most 72 roundings, within 72u of the exact total.  The later fp64
+# additions are negligible.  Hence |sumsq_gpu - sumsq| <= 78u * sum(m^2); the tests use 80u.
+SQNORM_ULPS = 80
+
+
+def check_sqnorm(gpu, oracle_sumsq, m2_sum):
+    """gpu: the kernel's sumsq; oracle_sumsq: exact value (fp64); m2_sum: sum of m^2 as above."""
+    return abs(float(gpu) - float(oracle_sumsq)) <= SQNORM_ULPS * U * float(m2_sum) + 1e-300
