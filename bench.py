@@ -124,6 +124,11 @@ TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_trace -
 PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d gpurun_out/prof_{tag} -o c4 --kernel-include-regex "
            "'k_simulate_multi|k_backward_multi|elementwise' -- "
            "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --calibrate-copy")
+OPT_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_opt_trace -o c4 -- "
+                 "python3 bench.py --adamw --steps 10 --warmup 2 --no-cpu-baseline")
+OPT_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d gpurun_out/prof_opt_{tag} -o c4 --kernel-include-regex "
+               "'k_adamw_multi|k_sqnorm_multi|elementwise' -- "
+               "python3 bench.py --adamw --steps 2 --warmup 1 --no-cpu-baseline --calibrate-copy")
 COPY_GRID = 1 << 26   # threads of the calibration copy (2^28 fp32 values, 4 per thread)
 COPY_BYTES = 1 << 30  # read and written by one calibration dispatch
 
@@ -197,7 +202,64 @@ def summarize(root: str) -> int:
     with open(os.path.join(out_dir, "traffic_c4_7b.md"), "w") as f:
         f.write("\n".join(md) + "\n")
     print("\n".join(lines + [""] + md))
+    if os.path.isdir(os.path.join(root, "prof_opt_trace")):
+        summarize_optimizer(root, out_dir, fetch_factor, write_factor)
     return 0
+
+
+def summarize_optimizer(root: str, out_dir: str, fetch_factor: float, write_factor: float) -> None:
+    """profiles/ summaries of the optimizer-side kernels (fused AdamW, gradient norm) on c4."""
+    import csv
+    import statistics
+
+    def kind(name: str):
+        if "k_adamw_multi" in name:
+            return "adamw"
+        if "k_sqnorm_multi" in name:
+            return "grad_norm"
+        return None
+
+    stats = list(csv.DictReader(open(os.path.join(root, "prof_opt_trace", "c4_kernel_stats.csv"))))
+    lines = ["# Optimizer-side kernel time on the 7B-shaped list (c4), rocprofv3 kernel trace", "",
+             f"Command (from the repository root, on one MI355X): `{OPT_TRACE_CMD}`", "",
+             "bench.py --adamw first runs the simulate + backward benchmark, then the fused AdamW step "
+             "(unclipped, then clipped at 1 after the gradient-norm pass), then backward-accumulate + "
+             "torch's fused AdamW (unclipped, then with torch.nn.utils.clip_grad_norm_).", "",
+             "| kernel | calls | average ms | min ms | max ms | share of GPU time |", "|---|---|---|---|---|---|"]
+    for r in stats[:16]:
+        name = r["Name"].replace("(anonymous namespace)", "{anon}").split("(")[0].replace("void ", "")
+        lines.append(f"| `{name[:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.4f} | "
+                     f"{float(r['MinNs']) / 1e6:.4f} | {float(r['MaxNs']) / 1e6:.4f} | {float(r['Percentage']):.2f}% |")
+    avg = {kind(r["Name"]): float(r["AverageNs"]) / 1e6 for r in stats if kind(r["Name"])}
+    with open(os.path.join(out_dir, "kernels_c4_7b_optimizer_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    vals = {}
+    for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        for r in csv.DictReader(open(os.path.join(root, f"prof_opt_{tag}", "c4_counter_collection.csv"))):
+            k = kind(r["Kernel_Name"])
+            if k and r["Counter_Name"] == ctr:
+                vals.setdefault((k, tag), []).append(float(r["Counter_Value"]))
+    P = 7504924672
+    algo = {"adamw": (P * 14, P * 12), "grad_norm": (P * 2, 0)}
+    md = ["# HBM traffic per launch of the optimizer-side kernels on c4, rocprofv3 counters", "",
+          f"Commands: `{OPT_PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with `WRITE_SIZE` "
+          "(`prof_opt_write`).", "",
+          f"Scaled by the copy calibration of the simulate/backward counter runs (FETCH_SIZE x {fetch_factor:.4f}, "
+          f"WRITE_SIZE x {write_factor:.4f}).  Algorithmic bytes per parameter: fused AdamW reads g~ (bf16, 2 B) and "
+          "theta, m1, m2 (12 B) and writes theta, m1, m2 (12 B); the norm pass reads g~ only (2 B).", "",
+          "| kernel | avg ms (trace) | FETCH_SIZE KiB | WRITE_SIZE KiB | read GB (scaled) | written GB (scaled) | "
+          "algorithmic GB | traffic / algorithmic | achieved GB/s (algorithmic / avg) |", "|---|---|---|---|---|---|---|---|---|"]
+    for k in ("adamw", "grad_norm"):
+        fk = statistics.median(vals[(k, "fetch")])
+        wk = statistics.median(vals[(k, "write")])
+        rd, wr = fk * 1024 / fetch_factor, wk * 1024 / write_factor
+        ar, aw = algo[k]
+        ms = avg.get(k)
+        md.append(f"| {k} | {ms:.4f} | {fk:.0f} | {wk:.0f} | {rd / 1e9:.3f} | {wr / 1e9:.3f} | {(ar + aw) / 1e9:.3f} | "
+                  f"{(rd + wr) / (ar + aw):.4f} | {(ar + aw) / (ms * 1e6):.0f} |")
+    with open(os.path.join(out_dir, "traffic_c4_7b_optimizer.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+    print("\n".join(lines + [""] + md))
 
 
 def bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat):
