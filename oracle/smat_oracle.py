@@ -425,6 +425,48 @@ def backward_accum_multi(grad_sims: Sequence, grad_sim_dtype: str, grad_thetas: 
                            tensor_ids[i], offs[i]) for i in range(len(grad_sims))]
 
 
+# ------------------------------------------------------------------ merging (evaluation side)
+def validate_merge_term(t: dict) -> None:
+    g, k = float(t["gamma"]), float(t["keep"])
+    if not math.isfinite(g):
+        raise ValueError("gamma must be finite")
+    if not (0.0 <= k <= 1.0):
+        raise ValueError("keep must lie in [0, 1]")
+    _check_key(int(t["seed"]), int(t["step"]), 0)
+
+
+def merge_f64(experts: Sequence, expert_dtype: str, theta0, theta0_dtype: str, terms: Sequence[dict],
+              tensor_id: int, elem_offset: int = 0) -> np.ndarray:
+    """Merged parameters in fp64 (Eq. merged-state):
+        theta_merge = theta0 + sum_j alpha_j m_j (.) (theta_j - theta0)
+    with a scalar weight alpha_j = gamma_j per expert (Task Arithmetic: all gamma_j = gamma; weight
+    averaging: gamma_j = 1/N) and DARE masks m_j (coordinate dropped with probability 1 - keep_j,
+    kept ones rescaled by 1/keep_j unless rescale is 0; keep_j = 1 leaves the task vector whole).
+    Expert j's mask is drawn like a training mask, from its own (seed, step) and the tensor's id and
+    element offsets, so one expert with (gamma = s, keep, seed, step) gives the simulated state of
+    that step without noise.  terms: one dict(gamma, keep, rescale=1, seed, step) per expert."""
+    if len(experts) != len(terms):
+        raise ValueError("one term per expert")
+    y = as_f64(np.asarray(theta0).ravel(), theta0_dtype)
+    t0 = y.copy()
+    n = t0.size
+    for x, t in zip(experts, terms):
+        validate_merge_term(t)
+        th = as_f64(np.asarray(x).ravel(), expert_dtype)
+        if th.size != n:
+            raise ValueError("an expert differs in size from theta0")
+        kept = keep_mask(int(t["seed"]), int(t["step"]), tensor_id, elem_offset, n, t["keep"])
+        m = mask_values(kept, t["keep"], t.get("rescale", 1))
+        y = y + float(np.float32(t["gamma"])) * m * (th - t0)
+    return y
+
+
+def merge(experts: Sequence, expert_dtype: str, theta0, theta0_dtype: str, out_dtype: str, terms: Sequence[dict],
+          tensor_id: int, elem_offset: int = 0) -> np.ndarray:
+    """merge_f64 rounded once to out_dtype (uint16 bits for bf16, float32 for f32)."""
+    return round_to(merge_f64(experts, expert_dtype, theta0, theta0_dtype, terms, tensor_id, elem_offset), out_dtype)
+
+
 # ------------------------------------------------------------------ schedule + switch
 def is_simulated_step(step: int, period: int = 4) -> bool:
     """Periodic scheduling: t-1 ordinary steps then one simulated step (Sec. 4.3).
