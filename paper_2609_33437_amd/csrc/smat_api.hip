@@ -272,7 +272,7 @@ struct smat_plan {
   std::vector<void*> expert_ptrs, sim_ptrs;
 
   // workspace layout: [tensor records][chunk table][expert pointer table][simulated pointer table][params]
-  // [optimizer state table][gradient-norm partials: one float per chunk][their fp64 block sums]
+  // [optimizer state table][gradient-norm partials: kNormPartialsPerChunk floats per chunk][their fp64 sums]
   size_t off_recs = 0, off_chunks = 0, off_expert = 0, off_sim = 0, off_params = 0, ws_bytes = 0;
   size_t off_partials = 0, off_sums = 0;
   char* ws = nullptr;
@@ -444,7 +444,7 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
   p->off_adam = off;
   off = align256(off + sizeof(AdamRec) * count);
   p->off_partials = off;
-  off = align256(off + sizeof(float) * p->chunks.size());
+  off = align256(off + sizeof(float) * smat::kNormPartialsPerChunk * p->chunks.size());
   p->off_sums = off;
   off = align256(off + sizeof(double) * smat::kNormSums);
   p->ws_bytes = std::max<size_t>(off, 256);

@@ -23,14 +23,41 @@ hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const Param
 hipError_t launch_adamw_multi(const TensorRec* recs, const AdamRec* states, const ParamRec* prms, const uint2* chunks,
                               uint32_t nchunks, const AdamConsts& A, int grad_dtype, bool accumulate, float lambda,
                               uint64_t seed, uint32_t step, const float* dev_scale, hipStream_t stream);
-// Squared norm of the simulated step's expert gradient over the list: per-chunk fp32 partials
-// (nchunks floats), their fp64 block sums (at most kNormSums doubles), then sumsq and/or the
-// clipping factor.
+// Squared norm of the simulated step's expert gradient over the list: one fp32 partial per
+// one-wave block of kNormQuads quads per thread (kNormPartialsPerChunk per chunk), their fp64 block
+// sums (at most kNormSums doubles), then sumsq and/or the clipping factor.
+constexpr int kNormQuads = 8;
+constexpr uint32_t kNormPartialsPerChunk = (uint32_t)tiles_per_chunk(kNormQuads);
 constexpr uint32_t kNormSums = 256;
 hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
                                uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
                                hipStream_t stream);
+// ---------------------------------------------------------------- N-expert merge
+// One expert's term on one tensor: its mask key (seed, step), threshold and coefficient
+// t = gamma/keep (rescaled) or gamma, and kFlagMask / kFlagDropAll.
+struct alignas(8) MergeRec {
+  uint64_t seed;
+  uint32_t step;
+  uint32_t thr;
+  float t;
+  uint32_t flags;
+};
+static_assert(sizeof(MergeRec) == 24, "MergeRec layout");
+constexpr int kMaxExperts = 16;
+constexpr int kMergeQuads = 2;
+constexpr uint32_t kVecMerge = 16u;  // TensorRec::sflags: theta0, out and every expert quad-aligned, offset % 4 == 0
+// Arguments of the one-tensor merge, passed by value (no device tables).
+struct MergeArgs {
+  const void* x[kMaxExperts];
+  MergeRec r[kMaxExperts];
+};
+hipError_t launch_merge_one(const TensorRec& rec, const MergeArgs& args, int nexp, int expert_dtype, int theta0_dtype,
+                            int out_dtype, hipStream_t stream);
+hipError_t launch_merge_multi(const TensorRec* recs, const void* const* experts, const MergeRec* terms,
+                              const uint2* chunks, uint32_t nchunks, int nexp, int expert_dtype, int theta0_dtype,
+                              int out_dtype, hipStream_t stream);
+
 hipError_t launch_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t elem_offset,
                               int64_t n, const ParamRec& prm, uint32_t* mask_words, uint32_t* noise_words,
                               uint8_t* kept, float* z, hipStream_t stream);

@@ -146,34 +146,31 @@ __global__ __launch_bounds__(kBlock) void k_adamw_multi(const TensorRec* __restr
 // ---------------------------------------------------------------- gradient norm
 // Squared L2 norm of the expert gradient g = [grad_acc +] lambda t m g~ of a simulated step
 // (Eq. smat-gradient weighted by lambda): what norm clipping measures before the optimizer step.
-// It reads only g~ (2 B per element in bf16) and, when accumulating, grad_acc.  A block of
-// kNormBlock threads reduces one chunk: thread x owns quads x + u kNormBlock, issues all of its
-// loads first, then draws each quad's mask and adds its squares while later loads are in flight.
-// Each block writes one fp32 partial; the partials are then added in fp64 in a fixed order (at
-// most kNormSums blocks over contiguous ranges, then one block), so the result does not depend
-// on scheduling and is the same from run to run.
-constexpr int kNormBlock = 256;
-constexpr int kNormQuads = (int)(kChunk / (4 * kNormBlock));
-static_assert(kNormQuads * 4 * kNormBlock == kChunk, "norm blocks split chunks");
+// It reads only g~ (2 B per element in bf16) and, when accumulating, grad_acc, so it carries twice
+// the Philox work per byte of the simulate.  Like the other streams, a one-wave block takes one
+// tile of kNormQuads quads per thread, issues its loads, draws the masks while they are in flight
+// and adds the squares; short-lived blocks let the chip overlap one block's draws with another's
+// loads.  Each block writes one fp32 partial (zero past a tensor's end); the partials are then added
+// in fp64 in a fixed order (at most kNormSums blocks over contiguous ranges, then one block), so the
+// result does not depend on scheduling and is the same from run to run.
 constexpr int kSumBlock = 256;
 static_assert(kNormSums <= (uint32_t)kSumBlock, "the final block holds one block sum per thread");
 
 template <typename TG, bool ACC>
-__device__ __forceinline__ float chunk_sqnorm(const TensorRec& R, const ParamRec& P, uint32_t chunk, uint64_t seed,
-                                              uint32_t step, float lambda) {
+__device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step,
+                                             float lambda) {
   const uint32_t flags = P.flags;
   if (!ACC && (flags & kFlagDropAll)) return 0.0f;
-  const int64_t begin = (int64_t)chunk * kChunk;
-  const uint32_t len = tile_len(R.n, begin, kChunk);
+  const uint32_t len = T.len;
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
   const bool use_mask = (flags & kFlagMask) != 0;
   const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
-  const uint32_t thr = P.thr, tensor_id = R.tensor_id;
+  const uint32_t thr = P.thr, tensor_id = T.tensor_id;
   const float c = lambda * P.t;
-  const void* gs = advance<TG>(R.grad_sim, begin);
-  const float* ga = R.grad_theta + begin;
-  const uint64_t e0 = R.elem_offset + (uint64_t)begin;
+  const void* gs = T.grad_sim;
+  const float* ga = T.grad_theta;
+  const uint64_t e0 = T.e0;
 
   auto gval = [&](bool kept, float gsim, float acc) {
     return ACC ? (kept ? __builtin_fmaf(c, gsim, acc) : acc) : (kept ? c * gsim : 0.0f);
@@ -187,9 +184,10 @@ __device__ __forceinline__ float chunk_sqnorm(const TensorRec& R, const ParamRec
     s = __builtin_fmaf(g, g, s);
   };
 
-  if (!(R.sflags & kVecBwd)) {
+  if (!(T.sflags & kVecBwd)) {
+#pragma unroll
     for (int u = 0; u < kNormQuads; ++u) {
-      const uint32_t i0 = (u * kNormBlock + threadIdx.x) * 4u;
+      const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
       for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) one(i);
     }
     return s;
@@ -200,35 +198,40 @@ __device__ __forceinline__ float chunk_sqnorm(const TensorRec& R, const ParamRec
     typename QuadIO<float>::Raw ra[kNormQuads];
 #pragma unroll
     for (int u = 0; u < kNormQuads; ++u) {
-      const uint32_t q = u * kNormBlock + threadIdx.x;
+      const uint32_t q = u * kBlock + threadIdx.x;
       const uint32_t qc = q < nq ? q : nq - 1;
       rg[u] = QuadIO<TG>::load_raw(gs, qc);
       if (ACC) ra[u] = QuadIO<float>::load_raw(ga, qc);
     }
+    bool kept[kNormQuads][4];
 #pragma unroll
     for (int u = 0; u < kNormQuads; ++u) {
-      const uint32_t q = u * kNormBlock + threadIdx.x;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
+      if (use_mask) {
+        const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, cmask, k0, k1);
+        kept[u][0] = w.w0 < thr;
+        kept[u][1] = w.w1 < thr;
+        kept[u][2] = w.w2 < thr;
+        kept[u][3] = w.w3 < thr;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kNormQuads; ++u) {
+      const uint32_t q = u * kBlock + threadIdx.x;
       if (q < nq) {
-        bool kept[4] = {all_kept, all_kept, all_kept, all_kept};
-        if (use_mask) {
-          const Words w = group_words((e0 >> 2) + q, tensor_id, cmask, k0, k1);
-          kept[0] = w.w0 < thr;
-          kept[1] = w.w1 < thr;
-          kept[2] = w.w2 < thr;
-          kept[3] = w.w3 < thr;
-        }
         float a[4], b[4] = {0.f, 0.f, 0.f, 0.f};
         QuadIO<TG>::unpack(rg[u], a);
         if (ACC) QuadIO<float>::unpack(ra[u], b);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float g = gval(kept[j], a[j], b[j]);
+          const float g = gval(kept[u][j], a[j], b[j]);
           s = __builtin_fmaf(g, g, s);
         }
       }
     }
   }
-  if ((len & 3u) && threadIdx.x == (nq & (kNormBlock - 1))) {
+  if ((len & 3u) && threadIdx.x == (nq & (kBlock - 1))) {
     for (uint32_t i = nq * 4u; i < len; ++i) one(i);
   }
   return s;
@@ -238,24 +241,33 @@ __device__ __forceinline__ float chunk_sqnorm(const TensorRec& R, const ParamRec
 // waves' sums in a fixed order.
 template <typename T, int BLOCK>
 __device__ __forceinline__ T block_sum(T v) {
-  __shared__ T part[BLOCK / 64];
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
-  __syncthreads();
-  T t = part[0];
+  if constexpr (BLOCK == 64) {
+    return v;
+  } else {
+    __shared__ T part[BLOCK / 64];
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+    __syncthreads();
+    T t = part[0];
 #pragma unroll
-  for (int w = 1; w < BLOCK / 64; ++w) t += part[w];
-  return t;
+    for (int w = 1; w < BLOCK / 64; ++w) t += part[w];
+    return t;
+  }
 }
 
 template <typename TG, bool ACC>
-__global__ __launch_bounds__(kNormBlock) void k_sqnorm_multi(const TensorRec* __restrict__ recs,
-                                                             const ParamRec* __restrict__ prms,
-                                                             const uint2* __restrict__ chunks, float* partials,
-                                                             uint64_t seed, uint32_t step, float lambda) {
-  const uint2 ch = chunks[blockIdx.x];
-  const float s = block_sum<float, kNormBlock>(chunk_sqnorm<TG, ACC>(recs[ch.x], prms[ch.x], ch.y, seed, step, lambda));
+__global__ __launch_bounds__(kBlock) void k_sqnorm_multi(const TensorRec* __restrict__ recs,
+                                                         const ParamRec* __restrict__ prms,
+                                                         const uint2* __restrict__ chunks, float* partials,
+                                                         uint64_t seed, uint32_t step, float lambda) {
+  constexpr int64_t tile = tile_elems(kNormQuads);
+  constexpr uint32_t tpc = tiles_per_chunk(kNormQuads);
+  const uint2 ch = chunks[blockIdx.x / tpc];
+  const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  float s = 0.0f;
+  if (T.len > 0) s = tile_sqnorm<TG, ACC>(T, prms[ch.x], seed, step, lambda);
+  s = block_sum<float, kBlock>(s);
   if (threadIdx.x == 0) partials[blockIdx.x] = s;
 }
 
@@ -320,8 +332,9 @@ hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, cons
                                float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
                                uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
                                hipStream_t stream) {
-  if (nchunks > 0) {
-    const dim3 grid(nchunks), block(kNormBlock);
+  const uint32_t npart = nchunks * kNormPartialsPerChunk;
+  if (npart > 0) {
+    const dim3 grid(npart), block(kBlock);
     if (grad_dtype == 1 && accumulate)
       k_sqnorm_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
     else if (grad_dtype == 1)
@@ -332,9 +345,9 @@ hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, cons
       k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
   }
   // m <= kNormSums blocks, each adding `per` consecutive partials
-  const uint32_t per = (nchunks + kNormSums - 1) / kNormSums;
-  const uint32_t m = per ? (nchunks + per - 1) / per : 0;
-  if (m > 0) k_sum_partials<<<dim3(m), dim3(kSumBlock), 0, stream>>>(partials, nchunks, per, sums);
+  const uint32_t per = (npart + kNormSums - 1) / kNormSums;
+  const uint32_t m = per ? (npart + per - 1) / per : 0;
+  if (m > 0) k_sum_partials<<<dim3(m), dim3(kSumBlock), 0, stream>>>(partials, npart, per, sums);
   k_sqnorm_finalize<<<dim3(1), dim3(kSumBlock), 0, stream>>>(sums, m, sumsq, clip_coef, max_norm);
   return hipGetLastError();
 }
