@@ -73,6 +73,10 @@ def parse_args():
     ap.add_argument("--train", action="store_true",
                     help="time SMAT inside a bf16 training loop of a Llama-1B-shaped synthetic decoder against "
                          "plain fine-tuning (AdamW, clipping at 1), print that comparison as the JSON line and exit")
+    ap.add_argument("--merge", action="store_true",
+                    help="time the N-expert merge (Task Arithmetic and DARE + Task Arithmetic) of seven bf16 "
+                         "experts shaped like the chosen list, print that as the JSON line and exit")
+    ap.add_argument("--experts", type=int, default=7)
     ap.add_argument("--train-batch", type=int, default=8)
     ap.add_argument("--train-seq", type=int, default=512)
     ap.add_argument("--train-reps", type=int, default=3)
@@ -402,6 +406,59 @@ def bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat):
     return res
 
 
+def bench_merge(args, torch, smat, workloads) -> int:
+    """N-expert merge (Eq. merged-state) over a list shaped like `--config`: N bf16 experts, bf16
+    theta0 and merged output; Task Arithmetic (gamma 0.3, no mask) and DARE + Task Arithmetic (drop
+    probability 0.3 on the linear weights), the paper's language-model merger settings."""
+    cfg = workloads.config(args.config)
+    N = args.experts
+    log(f"generating {N} experts shaped like {cfg.name}: {cfg.count} tensors, {cfg.numel} params each")
+    t0s, experts = workloads.make_experts(cfg, N, device="cuda")
+    outs = [torch.empty_like(t) for t in t0s]
+    torch.cuda.synchronize()
+    masked = [spec.kind == "linear" for spec in cfg.specs]
+    modes = {
+        "task_arithmetic": [[dict(gamma=0.3, keep=1.0, seed=0, step=0)] * N for _ in masked],
+        "dare_task_arithmetic": [[dict(gamma=0.3, keep=0.7 if m else 1.0, seed=0xDA4E + j, step=0) for j in range(N)]
+                                 for m in masked],
+    }
+    K, W = args.steps, args.warmup
+    P = cfg.numel
+    nbytes = P * (2 * N + 2 + 2)
+    res = {}
+    with smat.MergePlan(t0s, outs, experts) as plan:
+        for mode, terms in modes.items():
+            for _ in range(W):
+                plan.merge(terms)
+            torch.cuda.synchronize()
+            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+            for k in range(K):
+                evs[k][0].record()
+                plan.merge(terms)
+                evs[k][1].record()
+            torch.cuda.synchronize()
+            ms = sum(e[0].elapsed_time(e[1]) for e in evs) / K
+            res[mode] = {"ms": round(ms, 4), "gbps": round(nbytes / (ms * 1e6), 1),
+                         "frac": round(nbytes / (ms * 1e6) / PEAK_HBM_GBPS, 4)}
+            log(f"{mode}: {ms:.3f} ms = {nbytes / (ms * 1e6):.0f} GB/s")
+    dom = max(res, key=lambda m: res[m]["ms"])
+    result = {
+        "metric": f"N-expert merge params/s and achieved HBM GB/s, {cfg.name}-shaped",
+        "value": P / (res[dom]["ms"] * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": res[dom]["ms"], "higher_is_better": True,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.description}; {N} bf16 experts, bf16 theta0 and output",
+                   "params": P, "tensors": cfg.count, "experts": N, "bytes_per_param": 2 * N + 4},
+        "modes": res,
+        "roofline": {"bound": "hbm", "achieved": res[dom]["gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": res[dom]["frac"], "traffic": None, "kernel": f"merge ({dom})",
+                     "algorithmic_bytes_per_launch": nbytes, "avg_launch_ms": res[dom]["ms"]},
+    }
+    print(json.dumps(result))
+    return 0
+
+
 def bench_train(args, torch, smat) -> int:
     """SMAT in a training loop against plain fine-tuning (FT), the measurement behind the method's
     training-time table (App. "Implementation and Measurement Details"): same model, data and AdamW
@@ -537,6 +594,8 @@ def main() -> int:
     smat.lib()  # fail loudly if the HIP library is missing
     if args.train:
         return bench_train(args, torch, smat)
+    if args.merge:
+        return bench_merge(args, torch, smat, workloads)
     cfg = workloads.config(args.config)
     dt = {"bf16": torch.bfloat16, "f32": torch.float32}
     nbytes = {"bf16": 2, "f32": 4}

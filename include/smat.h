@@ -296,6 +296,74 @@ smat_status smat_plan_active_ptrs(const smat_plan* plan, void** host_out, void**
  * tables.  NULL is a no-op.  The workspace is not touched. */
 smat_status smat_plan_destroy(smat_plan* plan);
 
+/* ---------------------------------------------------------------- N-expert merge
+ * The merged parameters seen from any expert (Sec. 3, Eq. merged-state; App. "Additional
+ * Experimental Settings", mergers):
+ *   theta_merge = theta0 + sum_j alpha_j m_j (.) (theta_j - theta0)
+ * with one scalar weight alpha_j = gamma per expert (Task Arithmetic; gamma = 1/N gives weight
+ * averaging) and DARE masks m_j: a coordinate is dropped with probability 1 - keep_j and kept ones
+ * are scaled by 1/keep_j.  Expert j's mask is drawn exactly like a training mask (the smat_simulate
+ * mask stream) from its own (seed, step) and the tensor's id and global element index, so a
+ * one-expert merge with (gamma = s, keep, seed, step) equals smat_simulate with sigma = 0 bit for bit.
+ * Computed in fp32 as acc = theta0; acc = fma(t_j, theta_j, fma(-t_j, theta0, acc)) over kept
+ * coordinates of experts j = 0, 1, ... (t_j = gamma_j/keep_j with rescale, else gamma_j), rounded
+ * once to out_dtype (round to nearest even).  Per element it reads N experts and theta0 and writes
+ * out: 18 B for seven bf16 experts with bf16 theta0 and out. */
+typedef struct smat_merge_term {
+  float gamma;      /* weight of the expert's task vector; any finite value */
+  float keep;       /* DARE keep probability 1 - p in [0, 1]; 1 = whole task vector, 0 = expert left out */
+  int32_t rescale;  /* nonzero: kept coordinates scaled by 1/keep */
+  uint32_t step;    /* counter step of the expert's mask, < 2^30 */
+  uint64_t seed;    /* key of the expert's mask */
+} smat_merge_term;
+
+/* smat_merge -- one flat tensor: experts[0..n_experts) are n_experts device pointers (a host array)
+ * to [n] expert weights of expert_dtype; theta0 [n] of theta0_dtype; out [n] of out_dtype, which may
+ * be theta0 itself when the dtypes match but must not overlap any expert.  terms: n_experts host
+ * records.  1 <= n_experts <= 16.  Errors: SMAT_ERR_INVALID (sizes, null pointers, overlap, a bad
+ * term), SMAT_ERR_DTYPE, SMAT_ERR_HIP.  n == 0 is a no-op. */
+smat_status smat_merge(const void* const* experts, int32_t n_experts, smat_dtype expert_dtype, const void* theta0,
+                       smat_dtype theta0_dtype, void* out, smat_dtype out_dtype, int64_t n,
+                       const smat_merge_term* terms, uint32_t tensor_id, uint64_t elem_offset, hipStream_t stream);
+
+/* A merge plan: a fixed list of tensors, each with its n_experts expert tensors, merged by one launch
+ * per call.  Like smat_plan it keeps host tables only; its device tables live in a caller-allocated
+ * workspace. */
+typedef struct smat_merge_plan smat_merge_plan;
+
+typedef struct smat_merge_desc {
+  const void* theta0;    /* [n] base weights, device, theta0_dtype */
+  void* out;             /* [n] merged weights, device, out_dtype; may be theta0 when the dtypes match */
+  int64_t n;
+  uint32_t tensor_id;    /* mask counter word, as in smat_tensor_desc */
+  uint32_t reserved;     /* must be 0 */
+  uint64_t elem_offset;  /* global index of element 0 (shards of one tensor) */
+} smat_merge_desc;
+
+/* smat_merge_plan_create -- experts is a host array of count * n_experts device pointers, row i
+ * holding tensor i's experts in expert order.  Checks as smat_merge for every tensor; a tensor id may
+ * repeat only for disjoint element ranges.  Errors: SMAT_ERR_INVALID, SMAT_ERR_DTYPE. */
+smat_status smat_merge_plan_create(const smat_merge_desc* descs, int32_t count, const void* const* experts,
+                                   int32_t n_experts, smat_dtype expert_dtype, smat_dtype theta0_dtype,
+                                   smat_dtype out_dtype, smat_merge_plan** out_plan);
+
+/* smat_merge_plan_workspace_bytes -- device bytes the plan's tables need (256-byte aligned start). */
+smat_status smat_merge_plan_workspace_bytes(const smat_merge_plan* plan, size_t* bytes);
+
+/* smat_merge_plan_bind_workspace -- hand the plan its device workspace (caller-owned, outliving the
+ * plan) and upload its static tables on `stream`.  Errors as smat_plan_bind_workspace. */
+smat_status smat_merge_plan_bind_workspace(smat_merge_plan* plan, void* workspace, size_t bytes, hipStream_t stream);
+
+/* smat_merge_multi -- smat_merge over every tensor of the plan in one launch.  terms: count *
+ * n_experts host records, row i for tensor i (so the caller can leave tensors outside the DARE set
+ * unmasked with keep = 1), uploaded asynchronously on `stream`.  Errors: SMAT_ERR_INVALID (a bad
+ * term), SMAT_ERR_STATE (no workspace), SMAT_ERR_HIP. */
+smat_status smat_merge_multi(smat_merge_plan* plan, const smat_merge_term* terms, hipStream_t stream);
+
+/* smat_merge_plan_destroy -- wait for the plan's pending uploads, free its host tables.  NULL is a
+ * no-op. */
+smat_status smat_merge_plan_destroy(smat_merge_plan* plan);
+
 /* smat_last_error -- message of the last failure on the calling thread ("" if none). */
 const char* smat_last_error(void);
 

@@ -26,6 +26,8 @@ EXPORTS = (
     "smat_plan_bind_workspace", "smat_plan_set_params", "smat_simulate_multi", "smat_backward_accum_multi",
     "smat_switch_storage", "smat_plan_state", "smat_plan_active_ptrs", "smat_plan_destroy", "smat_last_error",
     "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi", "smat_grad_norm_multi",
+    "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
+    "smat_merge_multi", "smat_merge_plan_destroy",
 )
 
 
@@ -50,6 +52,15 @@ class smat_adamw_params(ctypes.Structure):
 
 class smat_adam_state(ctypes.Structure):
     _fields_ = [("exp_avg", c_void_p), ("exp_avg_sq", c_void_p)]
+
+
+class smat_merge_term(ctypes.Structure):
+    _fields_ = [("gamma", c_float), ("keep", c_float), ("rescale", c_int32), ("step", c_uint32), ("seed", c_uint64)]
+
+
+class smat_merge_desc(ctypes.Structure):
+    _fields_ = [("theta0", c_void_p), ("out", c_void_p), ("n", c_int64), ("tensor_id", c_uint32),
+                ("reserved", c_uint32), ("elem_offset", c_uint64)]
 
 
 class SmatError(RuntimeError):
@@ -83,6 +94,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_plan_bind_adam_state": [P, POINTER(smat_adam_state), P],
         "smat_adamw_fused_multi": [P, c_uint64, c_uint32, c_float, smat_adamw_params, c_int32, P, P],
         "smat_grad_norm_multi": [P, c_uint64, c_uint32, c_float, c_int32, c_float, P, P, P],
+        "smat_merge": [POINTER(P), c_int32, c_int32, P, c_int32, P, c_int32, c_int64, POINTER(smat_merge_term),
+                       c_uint32, c_uint64, P],
+        "smat_merge_plan_create": [POINTER(smat_merge_desc), c_int32, POINTER(P), c_int32, c_int32, c_int32, c_int32,
+                                   POINTER(P)],
+        "smat_merge_plan_workspace_bytes": [P, POINTER(c_size_t)],
+        "smat_merge_plan_bind_workspace": [P, P, c_size_t, P],
+        "smat_merge_multi": [P, POINTER(smat_merge_term), P],
+        "smat_merge_plan_destroy": [P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -320,6 +339,110 @@ class Plan:
     def close(self) -> None:
         if getattr(self, "_plan", None):
             _check(lib().smat_plan_destroy(self._plan))
+            self._plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+# ------------------------------------------------------------------ N-expert merge
+def merge_term(t) -> smat_merge_term:
+    """dict(gamma, keep=1, rescale=1, seed=0, step=0) or an smat_merge_term -> smat_merge_term."""
+    if isinstance(t, smat_merge_term):
+        return t
+    return smat_merge_term(float(t["gamma"]), float(t.get("keep", 1.0)), int(t.get("rescale", 1)),
+                           int(t.get("step", 0)), int(t.get("seed", 0)))
+
+
+def smat_merge(experts: Sequence, theta0, out, terms: Sequence, tensor_id: int = 0, elem_offset: int = 0,
+               stream=None) -> None:
+    """out = theta0 + sum_j gamma_j m_j (experts[j] - theta0) for one flat tensor (see include/smat.h)."""
+    n = out.numel()
+    if theta0.numel() != n or any(x.numel() != n for x in experts):
+        raise SmatError(SMAT_ERR_INVALID, "experts, theta0 and out differ in size")
+    if len(terms) != len(experts) or not experts:
+        raise SmatError(SMAT_ERR_INVALID, "one term per expert, at least one expert")
+    dts = {dtype_code(x) for x in experts}
+    if len(dts) != 1:
+        raise SmatError(SMAT_ERR_DTYPE, "all experts must share one dtype")
+    ptrs = (c_void_p * len(experts))(*[_dev_ptr(x, "expert") for x in experts])
+    arr = (smat_merge_term * len(terms))(*[merge_term(t) for t in terms])
+    _check(lib().smat_merge(ptrs, len(experts), dts.pop(), _dev_ptr(theta0, "theta0"), dtype_code(theta0),
+                            _dev_ptr(out, "out"), dtype_code(out), n, arr, int(tensor_id), int(elem_offset),
+                            _stream_handle(stream)))
+
+
+class MergePlan:
+    """A tensor list merged from N experts by one launch per call (smat_merge_plan_* calls).
+    experts[j][i] is expert j's version of tensor i; holds references to every tensor."""
+
+    def __init__(self, theta0s: Sequence, outs: Sequence, experts: Sequence[Sequence],
+                 tensor_ids: Optional[Sequence[int]] = None, elem_offsets: Optional[Sequence[int]] = None,
+                 stream=None):
+        torch = _torch()
+        count, nexp = len(theta0s), len(experts)
+        if nexp == 0 or any(len(e) != count for e in experts) or len(outs) != count:
+            raise SmatError(SMAT_ERR_INVALID, "experts[j] and outs must list every tensor")
+        self.count, self.nexp = count, nexp
+        self._refs = [theta0s, outs, experts]
+        ids = list(tensor_ids) if tensor_ids is not None else list(range(count))
+        offs = list(elem_offsets) if elem_offsets is not None else [0] * count
+        descs = (smat_merge_desc * max(count, 1))()
+        ptrs = (c_void_p * max(count * nexp, 1))()
+        for i in range(count):
+            n = theta0s[i].numel()
+            if outs[i].numel() != n or any(experts[j][i].numel() != n for j in range(nexp)):
+                raise SmatError(SMAT_ERR_INVALID, f"tensor {i}: experts, theta0 and out differ in size")
+            d = descs[i]
+            d.theta0 = _dev_ptr(theta0s[i], "theta0")
+            d.out = _dev_ptr(outs[i], "out")
+            d.n = n
+            d.tensor_id = ids[i]
+            d.elem_offset = offs[i]
+            for j in range(nexp):
+                ptrs[i * nexp + j] = _dev_ptr(experts[j][i], "expert")
+        if count:
+            dts = {dtype_code(experts[j][i]) for j in range(nexp) for i in range(count)}
+            if len(dts) != 1:
+                raise SmatError(SMAT_ERR_DTYPE, "all experts must share one dtype")
+            e_dt, t0_dt, out_dt = dts.pop(), dtype_code(theta0s[0]), dtype_code(outs[0])
+        else:
+            e_dt = t0_dt = out_dt = SMAT_BF16
+        plan = c_void_p()
+        _check(lib().smat_merge_plan_create(descs, count, ptrs, nexp, e_dt, t0_dt, out_dt, ctypes.byref(plan)))
+        self._plan = plan
+        nbytes = c_size_t()
+        _check(lib().smat_merge_plan_workspace_bytes(plan, ctypes.byref(nbytes)))
+        dev = theta0s[0].device if count else torch.device("cuda")
+        self.workspace = torch.empty(nbytes.value, dtype=torch.uint8, device=dev)
+        _check(lib().smat_merge_plan_bind_workspace(plan, c_void_p(self.workspace.data_ptr()), nbytes.value,
+                                                    _stream_handle(stream)))
+
+    def merge(self, terms: Sequence, stream=None) -> None:
+        """terms: one per expert (applied to every tensor), or a list per tensor of one per expert."""
+        if len(terms) and isinstance(terms[0], (list, tuple)):
+            if len(terms) != self.count or any(len(r) != self.nexp for r in terms):
+                raise SmatError(SMAT_ERR_INVALID, "one row of terms per tensor, one term per expert")
+            flat = [merge_term(t) for row in terms for t in row]
+        else:
+            if len(terms) != self.nexp:
+                raise SmatError(SMAT_ERR_INVALID, "one term per expert")
+            flat = [merge_term(t) for _ in range(self.count) for t in terms]
+        arr = (smat_merge_term * max(len(flat), 1))(*flat)
+        _check(lib().smat_merge_multi(self._plan, arr, _stream_handle(stream)))
+
+    def close(self) -> None:
+        if getattr(self, "_plan", None):
+            _check(lib().smat_merge_plan_destroy(self._plan))
             self._plan = None
 
     def __del__(self):

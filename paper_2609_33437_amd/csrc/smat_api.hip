@@ -673,4 +673,267 @@ extern "C" smat_status smat_plan_destroy(smat_plan* p) {
   return release(p);
 }
 
+// ------------------------------------------------------------------ N-expert merge
+namespace {
+
+using smat::MergeArgs;
+using smat::MergeRec;
+
+// One expert's term on one tensor (Eq. merged-state): weight gamma on the task vector, DARE keep
+// probability with its rescale, and the expert's mask key.
+smat_status make_merge(const smat_merge_term& m, MergeRec* out, const char* where) {
+  if (!std::isfinite(m.gamma)) return fail(SMAT_ERR_INVALID, "%s: gamma must be finite", where);
+  if (!std::isfinite(m.keep) || m.keep < 0.f || m.keep > 1.f)
+    return fail(SMAT_ERR_INVALID, "%s: keep must lie in [0, 1] (got %g)", where, (double)m.keep);
+  if (m.step >= kMaxStep) return fail(SMAT_ERR_INVALID, "%s: step must be < 2^30", where);
+  MergeRec r{};
+  r.seed = m.seed;
+  r.step = m.step;
+  if (m.keep >= 1.f) {
+    r.t = m.gamma;
+  } else if (m.keep <= 0.f) {
+    r.flags |= smat::kFlagDropAll;
+  } else {
+    r.flags |= smat::kFlagMask;
+    r.thr = (uint32_t)std::floor((double)m.keep * 4294967296.0);
+    r.t = m.rescale ? (float)((double)m.gamma / (double)m.keep) : m.gamma;
+  }
+  *out = r;
+  return SMAT_OK;
+}
+
+uint32_t merge_flags(const void* const* experts, int nexp, int e_dt, const void* theta0, int t0_dt, const void* out,
+                     int out_dt, uint64_t elem_offset) {
+  bool ok = elem_offset % 4 == 0 && aligned(theta0, quad_align(t0_dt)) && aligned(out, quad_align(out_dt));
+  for (int j = 0; j < nexp && ok; ++j) ok = aligned(experts[j], quad_align(e_dt));
+  return ok ? smat::kVecMerge : 0u;
+}
+
+smat_status check_merge_ptrs(const void* const* experts, int nexp, int e_dt, const void* theta0, int t0_dt,
+                             const void* out, int out_dt, int64_t n, const char* where) {
+  if (!theta0 || !out) return fail(SMAT_ERR_INVALID, "%s: null theta0 or out with n > 0", where);
+  const size_t nb = (size_t)n;
+  for (int j = 0; j < nexp; ++j) {
+    if (!experts[j]) return fail(SMAT_ERR_INVALID, "%s: expert %d is null", where, j);
+    if (overlap(out, nb * dtype_bytes(out_dt), experts[j], nb * dtype_bytes(e_dt)))
+      return fail(SMAT_ERR_INVALID, "%s: out overlaps expert %d", where, j);
+  }
+  if (out == theta0) {
+    if (t0_dt != out_dt) return fail(SMAT_ERR_INVALID, "%s: in-place out == theta0 needs equal dtypes", where);
+  } else if (overlap(out, nb * dtype_bytes(out_dt), theta0, nb * dtype_bytes(t0_dt))) {
+    return fail(SMAT_ERR_INVALID, "%s: out overlaps theta0 without being the same buffer", where);
+  }
+  return SMAT_OK;
+}
+
+}  // namespace
+
+extern "C" smat_status smat_merge(const void* const* experts, int32_t n_experts, smat_dtype expert_dtype,
+                                  const void* theta0, smat_dtype theta0_dtype, void* out, smat_dtype out_dtype,
+                                  int64_t n, const smat_merge_term* terms, uint32_t tensor_id, uint64_t elem_offset,
+                                  hipStream_t stream) {
+  if (!valid_dtype(expert_dtype) || !valid_dtype(theta0_dtype) || !valid_dtype(out_dtype))
+    return fail(SMAT_ERR_DTYPE, "smat_merge: unsupported dtype");
+  if (n_experts < 1 || n_experts > smat::kMaxExperts)
+    return fail(SMAT_ERR_INVALID, "smat_merge: n_experts must lie in [1, %d]", smat::kMaxExperts);
+  if (n < 0) return fail(SMAT_ERR_INVALID, "smat_merge: n < 0");
+  if (!terms || !experts) return fail(SMAT_ERR_INVALID, "smat_merge: null terms or experts");
+  MergeArgs A{};
+  for (int32_t j = 0; j < n_experts; ++j) {
+    char where[64];
+    std::snprintf(where, sizeof(where), "smat_merge: expert %d", j);
+    smat_status st = make_merge(terms[j], &A.r[j], where);
+    if (st != SMAT_OK) return st;
+    A.x[j] = experts[j];
+  }
+  if (n == 0) return SMAT_OK;
+  if (elem_offset > UINT64_MAX - (uint64_t)n) return fail(SMAT_ERR_INVALID, "smat_merge: elem_offset + n overflows");
+  if ((n + smat::tile_elems(1) - 1) / smat::tile_elems(1) > 0x7FFFFFFF) return fail(SMAT_ERR_INVALID, "smat_merge: n too large");
+  smat_status st = check_merge_ptrs(experts, n_experts, expert_dtype, theta0, theta0_dtype, out, out_dtype, n,
+                                    "smat_merge");
+  if (st != SMAT_OK) return st;
+  TensorRec rec{};
+  rec.theta0 = theta0;
+  rec.out = out;
+  rec.n = n;
+  rec.elem_offset = elem_offset;
+  rec.tensor_id = tensor_id;
+  rec.sflags = merge_flags(experts, n_experts, expert_dtype, theta0, theta0_dtype, out, out_dtype, elem_offset);
+  SMAT_HIP(smat::launch_merge_one(rec, A, n_experts, expert_dtype, theta0_dtype, out_dtype, stream));
+  return SMAT_OK;
+}
+
+struct smat_merge_plan {
+  int32_t count = 0, nexp = 0;
+  int e_dt = 0, t0_dt = 0, out_dt = 0;
+  std::vector<TensorRec> recs;
+  std::vector<uint2> chunks;
+  std::vector<const void*> experts;  // [count][nexp]
+  // workspace layout: [tensor records][chunk table][expert pointer table][terms]
+  size_t off_recs = 0, off_chunks = 0, off_experts = 0, off_terms = 0, ws_bytes = 0;
+  char* ws = nullptr;
+  char* static_staging = nullptr;
+  MergeRec* terms_staging[2] = {nullptr, nullptr};
+  hipEvent_t ev_static = nullptr;
+  hipEvent_t ev_terms[2] = {nullptr, nullptr};
+  bool terms_pending[2] = {false, false};
+  int slot = 0;
+};
+
+namespace {
+
+smat_status release_merge(smat_merge_plan* p) {
+  for (hipEvent_t e : {p->ev_static, p->ev_terms[0], p->ev_terms[1]})
+    if (e) (void)hipEventSynchronize(e);
+  if (p->static_staging) (void)hipHostFree(p->static_staging);
+  for (MergeRec* s : p->terms_staging)
+    if (s) (void)hipHostFree(s);
+  for (hipEvent_t e : {p->ev_static, p->ev_terms[0], p->ev_terms[1]})
+    if (e) (void)hipEventDestroy(e);
+  delete p;
+  return SMAT_OK;
+}
+
+}  // namespace
+
+extern "C" smat_status smat_merge_plan_create(const smat_merge_desc* descs, int32_t count, const void* const* experts,
+                                              int32_t n_experts, smat_dtype expert_dtype, smat_dtype theta0_dtype,
+                                              smat_dtype out_dtype, smat_merge_plan** out_plan) {
+  if (!out_plan) return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: out_plan is null");
+  *out_plan = nullptr;
+  if (!valid_dtype(expert_dtype) || !valid_dtype(theta0_dtype) || !valid_dtype(out_dtype))
+    return fail(SMAT_ERR_DTYPE, "smat_merge_plan_create: unsupported dtype");
+  if (n_experts < 1 || n_experts > smat::kMaxExperts)
+    return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: n_experts must lie in [1, %d]", smat::kMaxExperts);
+  if (count < 0 || (count > 0 && (!descs || !experts)))
+    return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: bad tensor list");
+  std::vector<std::pair<uint32_t, std::pair<uint64_t, uint64_t>>> ranges;
+  uint64_t nchunks = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const smat_merge_desc& d = descs[i];
+    char where[64];
+    std::snprintf(where, sizeof(where), "smat_merge_plan_create: tensor %d", i);
+    if (d.n < 0 || d.reserved != 0) return fail(SMAT_ERR_INVALID, "%s: n < 0 or reserved != 0", where);
+    if (d.elem_offset > UINT64_MAX - (uint64_t)d.n) return fail(SMAT_ERR_INVALID, "%s: elem_offset + n overflows", where);
+    if (d.n == 0) continue;
+    smat_status st = check_merge_ptrs(experts + (size_t)i * n_experts, n_experts, expert_dtype, d.theta0, theta0_dtype,
+                                      d.out, out_dtype, d.n, where);
+    if (st != SMAT_OK) return st;
+    ranges.push_back({d.tensor_id, {d.elem_offset, d.elem_offset + (uint64_t)d.n}});
+    nchunks += (uint64_t)((d.n + smat::kChunk - 1) / smat::kChunk);
+  }
+  // a tensor id may cover disjoint shards of one tensor, never overlapping ranges (same draws twice)
+  std::sort(ranges.begin(), ranges.end());
+  for (size_t i = 1; i < ranges.size(); ++i)
+    if (ranges[i].first == ranges[i - 1].first && ranges[i].second.first < ranges[i - 1].second.second)
+      return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: tensor_id %u given twice for overlapping elements",
+                  ranges[i].first);
+  if (nchunks * smat::tiles_per_chunk(1) > 0x7FFFFFFFull)
+    return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: tensor list too large for one launch");
+
+  smat_merge_plan* p = new smat_merge_plan();
+  p->count = count;
+  p->nexp = n_experts;
+  p->e_dt = expert_dtype;
+  p->t0_dt = theta0_dtype;
+  p->out_dt = out_dtype;
+  p->recs.resize(count);
+  p->experts.assign(experts, experts + (size_t)count * n_experts);
+  p->chunks.reserve(nchunks);
+  for (int32_t i = 0; i < count; ++i) {
+    const smat_merge_desc& d = descs[i];
+    TensorRec& r = p->recs[i];
+    r.theta0 = d.theta0;
+    r.out = d.out;
+    r.n = d.n;
+    r.elem_offset = d.elem_offset;
+    r.tensor_id = d.tensor_id;
+    if (d.n > 0)
+      r.sflags = merge_flags(experts + (size_t)i * n_experts, n_experts, expert_dtype, d.theta0, theta0_dtype, d.out,
+                             out_dtype, d.elem_offset);
+    const uint32_t nc = (uint32_t)((d.n + smat::kChunk - 1) / smat::kChunk);
+    for (uint32_t c = 0; c < nc; ++c) p->chunks.push_back(make_uint2((uint32_t)i, c));
+  }
+  const size_t cells = (size_t)count * n_experts;
+  size_t off = 0;
+  p->off_recs = off;
+  off = align256(off + sizeof(TensorRec) * count);
+  p->off_chunks = off;
+  off = align256(off + sizeof(uint2) * p->chunks.size());
+  p->off_experts = off;
+  off = align256(off + sizeof(void*) * cells);
+  p->off_terms = off;
+  off = align256(off + sizeof(MergeRec) * cells);
+  p->ws_bytes = std::max<size_t>(off, 256);
+  *out_plan = p;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_merge_plan_workspace_bytes(const smat_merge_plan* p, size_t* bytes) {
+  if (!p || !bytes) return fail(SMAT_ERR_INVALID, "smat_merge_plan_workspace_bytes: null argument");
+  *bytes = p->ws_bytes;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_merge_plan_bind_workspace(smat_merge_plan* p, void* workspace, size_t bytes,
+                                                      hipStream_t stream) {
+  if (!p || !workspace) return fail(SMAT_ERR_INVALID, "smat_merge_plan_bind_workspace: null argument");
+  if (p->ws) return fail(SMAT_ERR_STATE, "smat_merge_plan_bind_workspace: workspace already bound");
+  if (!aligned(workspace, 256))
+    return fail(SMAT_ERR_INVALID, "smat_merge_plan_bind_workspace: workspace not 256-byte aligned");
+  if (bytes < p->ws_bytes)
+    return fail(SMAT_ERR_INVALID, "smat_merge_plan_bind_workspace: workspace of %zu bytes, need %zu", bytes, p->ws_bytes);
+  const size_t static_bytes = p->off_terms;
+  const size_t cells = (size_t)p->count * p->nexp;
+  SMAT_HIP(hipHostMalloc((void**)&p->static_staging, std::max<size_t>(static_bytes, 256), hipHostMallocDefault));
+  for (MergeRec*& s : p->terms_staging)
+    SMAT_HIP(hipHostMalloc((void**)&s, sizeof(MergeRec) * std::max<size_t>(cells, 1), hipHostMallocDefault));
+  std::memset(p->static_staging, 0, static_bytes);
+  std::memcpy(p->static_staging + p->off_recs, p->recs.data(), sizeof(TensorRec) * p->count);
+  std::memcpy(p->static_staging + p->off_chunks, p->chunks.data(), sizeof(uint2) * p->chunks.size());
+  std::memcpy(p->static_staging + p->off_experts, p->experts.data(), sizeof(void*) * cells);
+  SMAT_HIP(hipEventCreateWithFlags(&p->ev_static, hipEventDisableTiming));
+  for (hipEvent_t& e : p->ev_terms) SMAT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  if (static_bytes > 0)
+    SMAT_HIP(hipMemcpyAsync(workspace, p->static_staging, static_bytes, hipMemcpyHostToDevice, stream));
+  SMAT_HIP(hipEventRecord(p->ev_static, stream));
+  p->ws = static_cast<char*>(workspace);
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_merge_multi(smat_merge_plan* p, const smat_merge_term* terms, hipStream_t stream) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_merge_multi: null plan");
+  const size_t cells = (size_t)p->count * p->nexp;
+  if (cells > 0 && !terms) return fail(SMAT_ERR_INVALID, "smat_merge_multi: null terms");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_merge_multi: no workspace bound");
+  std::vector<MergeRec> recs(cells);
+  for (size_t c = 0; c < cells; ++c) {
+    char where[80];
+    std::snprintf(where, sizeof(where), "smat_merge_multi: tensor %zu, expert %zu", c / p->nexp, c % p->nexp);
+    smat_status st = make_merge(terms[c], &recs[c], where);
+    if (st != SMAT_OK) return st;
+  }
+  const int slot = p->slot;
+  if (p->terms_pending[slot]) SMAT_HIP(hipEventSynchronize(p->ev_terms[slot]));  // slot still being read
+  std::memcpy(p->terms_staging[slot], recs.data(), sizeof(MergeRec) * cells);
+  if (cells > 0)
+    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_terms, p->terms_staging[slot], sizeof(MergeRec) * cells,
+                            hipMemcpyHostToDevice, stream));
+  SMAT_HIP(hipEventRecord(p->ev_terms[slot], stream));
+  p->terms_pending[slot] = true;
+  p->slot = slot ^ 1;
+  if (!p->chunks.empty())
+    SMAT_HIP(smat::launch_merge_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                      reinterpret_cast<const void* const*>(p->ws + p->off_experts),
+                                      reinterpret_cast<const MergeRec*>(p->ws + p->off_terms),
+                                      reinterpret_cast<const uint2*>(p->ws + p->off_chunks), (uint32_t)p->chunks.size(),
+                                      p->nexp, p->e_dt, p->t0_dt, p->out_dt, stream));
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_merge_plan_destroy(smat_merge_plan* p) {
+  if (!p) return SMAT_OK;
+  return release_merge(p);
+}
+
 extern "C" const char* smat_last_error(void) { return g_last_error.c_str(); }

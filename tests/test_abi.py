@@ -45,8 +45,10 @@ def test_struct_layout_matches_c(tmp_path):
 #include <stddef.h>
 #include "smat.h"
 int main(void) {
-  printf("%zu %zu %zu %zu %zu\\n", sizeof(smat_op_params), sizeof(smat_rng_key), sizeof(smat_tensor_desc),
-         sizeof(smat_adamw_params), sizeof(smat_adam_state));
+  printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(smat_op_params), sizeof(smat_rng_key), sizeof(smat_tensor_desc),
+         sizeof(smat_adamw_params), sizeof(smat_adam_state), sizeof(smat_merge_term), sizeof(smat_merge_desc));
+  printf("%zu %zu %zu\\n", offsetof(smat_merge_term, seed), offsetof(smat_merge_desc, n),
+         offsetof(smat_merge_desc, elem_offset));
   printf("%zu %zu %zu %zu\\n", offsetof(smat_tensor_desc, n), offsetof(smat_tensor_desc, tensor_id),
          offsetof(smat_tensor_desc, elem_offset), offsetof(smat_rng_key, elem_offset));
   return 0;
@@ -58,6 +60,8 @@ int main(void) {
     out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()
     want = [ctypes.sizeof(_lib.smat_op_params), ctypes.sizeof(_lib.smat_rng_key), ctypes.sizeof(_lib.smat_tensor_desc),
             ctypes.sizeof(_lib.smat_adamw_params), ctypes.sizeof(_lib.smat_adam_state),
+            ctypes.sizeof(_lib.smat_merge_term), ctypes.sizeof(_lib.smat_merge_desc),
+            _lib.smat_merge_term.seed.offset, _lib.smat_merge_desc.n.offset, _lib.smat_merge_desc.elem_offset.offset,
             _lib.smat_tensor_desc.n.offset, _lib.smat_tensor_desc.tensor_id.offset,
             _lib.smat_tensor_desc.elem_offset.offset, _lib.smat_rng_key.elem_offset.offset]
     assert [int(x) for x in out] == want
@@ -193,3 +197,58 @@ def test_grad_norm_argument_errors_without_gpu():
     assert lib.smat_plan_create(arr, 1, 1, 1, 1, 0, ctypes.byref(plan)) == 0
     assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 0, 1.0, out, None, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_plan_destroy(plan) == 0
+
+
+def test_merge_argument_errors_without_gpu():
+    lib = smat.lib()
+    P = ctypes.c_void_p
+    A = 1 << 20
+    T = _lib.smat_merge_term
+    good = (T * 2)(T(0.3, 0.7, 1, 0, 5), T(0.3, 1.0, 1, 0, 6))
+    ex = (P * 2)(P(1 * A), P(2 * A))
+    assert lib.smat_merge(ex, 2, 1, P(3 * A), 1, P(4 * A), 1, 0, good, 0, 0, None) == _lib.SMAT_OK      # n == 0
+    assert lib.smat_merge(ex, 0, 1, P(3 * A), 1, P(4 * A), 1, 4, good, 0, 0, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_merge(ex, 17, 1, P(3 * A), 1, P(4 * A), 1, 4, good, 0, 0, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_merge(ex, 2, 9, P(3 * A), 1, P(4 * A), 1, 4, good, 0, 0, None) == _lib.SMAT_ERR_DTYPE
+    for bad in (T(float("nan"), 1.0, 1, 0, 0), T(0.3, 1.5, 1, 0, 0), T(0.3, -0.1, 1, 0, 0), T(0.3, 0.5, 1, 1 << 30, 0)):
+        terms = (T * 2)(good[0], bad)
+        assert lib.smat_merge(ex, 2, 1, P(3 * A), 1, P(4 * A), 1, 4, terms, 0, 0, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_merge(ex, 2, 1, P(3 * A), 1, P(2 * A + 2), 1, 4, good, 0, 0, None) == _lib.SMAT_ERR_INVALID  # out over expert
+    assert lib.smat_merge(ex, 2, 1, P(3 * A), 1, P(3 * A + 2), 1, 4, good, 0, 0, None) == _lib.SMAT_ERR_INVALID  # out over theta0
+    assert lib.smat_merge(ex, 2, 1, P(3 * A), 0, P(3 * A), 1, 4, good, 0, 0, None) == _lib.SMAT_ERR_INVALID      # in place, dtypes differ
+    nul = (P * 2)(P(1 * A), None)
+    assert lib.smat_merge(nul, 2, 1, P(3 * A), 1, P(4 * A), 1, 4, good, 0, 0, None) == _lib.SMAT_ERR_INVALID
+
+
+def test_merge_plan_validation_without_gpu():
+    lib = smat.lib()
+    P = ctypes.c_void_p
+    A = 1 << 20
+    D = _lib.smat_merge_desc
+
+    def create(descs, ptrs, nexp=2, dts=(1, 1, 1)):
+        arr = (D * len(descs))(*descs)
+        ex = (P * len(ptrs))(*ptrs)
+        p = P()
+        st = lib.smat_merge_plan_create(arr, len(descs), ex, nexp, dts[0], dts[1], dts[2], ctypes.byref(p))
+        if st == _lib.SMAT_OK:
+            nb = ctypes.c_size_t()
+            assert lib.smat_merge_plan_workspace_bytes(p, ctypes.byref(nb)) == 0 and nb.value % 256 == 0
+            terms = (_lib.smat_merge_term * max(1, len(descs) * nexp))()
+            assert lib.smat_merge_multi(p, terms, None) == _lib.SMAT_ERR_STATE      # no workspace: nothing launched
+            assert lib.smat_merge_plan_destroy(p) == 0
+        return st
+
+    two = [D(P(1 * A), P(2 * A), 1000, 0, 0, 0), D(P(3 * A), P(4 * A), 10, 1, 0, 0)]
+    ptrs = [P(5 * A), P(6 * A), P(7 * A), P(8 * A)]
+    assert create(two, ptrs) == _lib.SMAT_OK
+    assert create(two, ptrs, nexp=0) == _lib.SMAT_ERR_INVALID
+    assert create(two, ptrs, dts=(1, 1, 4)) == _lib.SMAT_ERR_DTYPE
+    assert create([D(P(1 * A), P(2 * A), 1000, 0, 1, 0)], ptrs[:2]) == _lib.SMAT_ERR_INVALID        # reserved != 0
+    assert create([D(P(1 * A), P(5 * A + 8), 1000, 0, 0, 0)], ptrs[:2]) == _lib.SMAT_ERR_INVALID    # out over an expert
+    assert create([D(P(1 * A), P(1 * A), 1000, 0, 0, 0)], ptrs[:2]) == _lib.SMAT_OK                 # in place over theta0
+    overlapping = [D(P(1 * A), P(2 * A), 1000, 7, 0, 0), D(P(3 * A), P(4 * A), 10, 7, 0, 999)]
+    assert create(overlapping, ptrs) == _lib.SMAT_ERR_INVALID
+    shards = [D(P(1 * A), P(2 * A), 1000, 7, 0, 0), D(P(3 * A), P(4 * A), 10, 7, 0, 1000)]
+    assert create(shards, ptrs) == _lib.SMAT_OK
+    assert lib.smat_merge_plan_destroy(None) == 0

@@ -1,0 +1,191 @@
+"""GPU parity of the N-expert merge (smat_merge, smat_merge_plan_*, smat_merge_multi) against the
+oracle, through the C ABI: one expert equals the simulated state without noise bit for bit; 1 to 16
+experts in every dtype mix; ragged, misaligned and offset tensors; tensor lists with per-tensor
+terms; order, shard and in-place invariance; weight averaging; errors."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_33437_amd as smat
+import workloads
+from tolerances import check_merge, ordered
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+DT = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
+def host(t):
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16).ravel(), "bf16"
+    return t.numpy().ravel().copy(), "f32"
+
+
+def bits(t):
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
+def make(n, nexp, e_dt, t0_dt, seed, shift=0, scale=1e-3):
+    g = torch.Generator(DEV).manual_seed(seed)
+    base = torch.randn(n + 8, device=DEV, generator=g) * 0.02
+    t0 = base.to(DT[t0_dt])[shift:shift + n]
+    ex = [(base + torch.randn(n + 8, device=DEV, generator=g) * scale).to(DT[e_dt])[shift:shift + n]
+          for _ in range(nexp)]
+    return t0, ex
+
+
+def terms_for(nexp, keep=0.7, gamma=0.3, seed0=100, step0=3, rescale=1):
+    return [dict(gamma=gamma + 0.05 * j, keep=keep if j % 3 != 2 else 1.0, rescale=rescale, seed=seed0 + j,
+                 step=step0 + j) for j in range(nexp)]
+
+
+def oracle_check(out, ex, t0, terms, tid, off):
+    """Compare a GPU merge with the oracle under check_merge; returns the number of strict elements."""
+    exn = [host(x) for x in ex]
+    t0n, t0_dt = host(t0)
+    y = oracle.merge_f64([x for x, _ in exn], exn[0][1], t0n, t0_dt, terms, tid, off)
+    b = oracle.as_f64(t0n, t0_dt)
+    A = np.abs(b).copy()
+    used = 0
+    for (x, dt), t in zip(exn, terms):
+        kept = oracle.keep_mask(t["seed"], t["step"], tid, off, b.size, t["keep"])
+        tj = oracle.coefficient(t["gamma"], t["keep"], t.get("rescale", 1))
+        A += np.where(kept, abs(tj) * (np.abs(oracle.as_f64(x, dt)) + np.abs(b)), 0.0)
+        used += float(np.float32(t["keep"])) > 0
+    got, out_dt = host(out)
+    ok, strict = check_merge(got, out_dt, y, A, max(used, 1))
+    assert ok.all(), f"{np.count_nonzero(~ok)} mismatches of {ok.size}, first {np.flatnonzero(~ok)[:5]}"
+    if out_dt == "bf16":
+        assert np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))[strict].max(initial=0) <= 1
+    return int(strict.sum())
+
+
+@pytest.mark.parametrize("n,shift,off", [(1, 0, 0), (5, 0, 0), (4096, 0, 0), (100003, 0, 0), (50001, 1, 3),
+                                          (70000, 0, 2 ** 34 + 8)])
+@pytest.mark.parametrize("t0_dt,out_dt", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32")])
+@pytest.mark.parametrize("keep", [0.5, 1.0, 0.0])
+def test_one_expert_is_the_simulated_state_bit_for_bit(n, shift, off, t0_dt, out_dt, keep):
+    t0, (th,) = make(n, 1, "f32", t0_dt, n + shift)
+    out_m = torch.empty(n, dtype=DT[out_dt], device=DEV)
+    out_s = torch.empty(n, dtype=DT[out_dt], device=DEV)
+    smat.smat_merge([th], t0, out_m, [dict(gamma=0.6, keep=keep, seed=77, step=12)], 9, off)
+    smat.smat_simulate(th, t0, out_s, dict(s=0.6, keep=keep, sigma=0.0), 77, 12, 9, off)
+    torch.cuda.synchronize()
+    assert torch.equal(bits(out_m), bits(out_s))
+
+
+@pytest.mark.parametrize("nexp", [1, 3, 7, 16])
+@pytest.mark.parametrize("e_dt,t0_dt,out_dt", [("bf16", "bf16", "bf16"), ("f32", "bf16", "f32"),
+                                               ("bf16", "f32", "bf16"), ("f32", "f32", "f32")])
+@pytest.mark.parametrize("n,shift,off", [(7, 0, 0), (65539, 0, 0), (40001, 1, 2), (16384 * 3 + 1, 0, 2 ** 33)])
+def test_single_tensor_matches_oracle(nexp, e_dt, t0_dt, out_dt, n, shift, off):
+    t0, ex = make(n, nexp, e_dt, t0_dt, 1000 * nexp + n, shift)
+    out = torch.empty(n, dtype=DT[out_dt], device=DEV)
+    terms = terms_for(nexp)
+    smat.smat_merge(ex, t0, out, terms, 5, off)
+    torch.cuda.synchronize()
+    oracle_check(out, ex, t0, terms, 5, off)
+
+
+def test_weight_averaging_and_task_arithmetic():
+    n, nexp = 200003, 4
+    t0, ex = make(n, nexp, "f32", "f32", 3)
+    out = torch.empty(n, device=DEV)
+    smat.smat_merge(ex, t0, out, [dict(gamma=1.0 / nexp)] * nexp)
+    torch.cuda.synchronize()
+    # weight averaging is the mean of the experts, within the merge's derived bound (2N + 1) u A plus
+    # half an fp32 ulp, A = |theta0| + sum_j (1/N)(|x_j| + |theta0|)
+    stack = torch.stack([x.double() for x in ex])
+    mean = stack.mean(0)
+    A = t0.double().abs() + (stack.abs() + t0.double().abs()).sum(0) / nexp
+    u = 2.0 ** -24
+    assert bool(((out.double() - mean).abs() <= (2 * nexp + 1) * u * A + u * mean.abs()).all())
+    oracle_check(out, ex, t0, [dict(gamma=1.0 / nexp, keep=1.0, seed=0, step=0)] * nexp, 0, 0)
+
+
+def mini_lists(nexp, e_dt="bf16"):
+    cfg = workloads.config("mini")
+    inp = workloads.make_inputs(cfg, device="cpu")
+    t0 = [t.to(DEV).view(-1) for t in inp.theta0]
+    g = torch.Generator(DEV).manual_seed(11)
+    ex = [[(x.float() + torch.randn(x.numel(), device=DEV, generator=g) * 1e-3).to(DT[e_dt]) for x in t0]
+          for _ in range(nexp)]
+    masked = [s.keep < 1.0 for s in inp.settings]
+    return cfg, t0, ex, masked
+
+
+def per_tensor_terms(masked, nexp):
+    return [[dict(gamma=0.3, keep=0.7 if m else 1.0, seed=500 + j, step=2) for j in range(nexp)] for m in masked]
+
+
+@pytest.mark.parametrize("nexp", [1, 4, 7])
+def test_plan_matches_oracle(nexp):
+    cfg, t0, ex, masked = mini_lists(nexp)
+    outs = [torch.empty_like(x) for x in t0]
+    terms = per_tensor_terms(masked, nexp)
+    with smat.MergePlan(t0, outs, ex) as plan:
+        plan.merge(terms)
+        torch.cuda.synchronize()
+    for i in range(cfg.count):
+        oracle_check(outs[i], [e[i] for e in ex], t0[i], terms[i], i, 0)
+    # the single-tensor entry point gives the same bits
+    for i in (0, cfg.count - 1):
+        o = torch.empty_like(t0[i])
+        smat.smat_merge([e[i] for e in ex], t0[i], o, terms[i], i, 0)
+        torch.cuda.synchronize()
+        assert torch.equal(bits(o), bits(outs[i]))
+
+
+def test_plan_order_shard_and_in_place_invariance():
+    nexp = 3
+    cfg, t0, ex, masked = mini_lists(nexp)
+    terms = per_tensor_terms(masked, nexp)
+    outs = [torch.empty_like(x) for x in t0]
+    with smat.MergePlan(t0, outs, ex) as plan:
+        plan.merge(terms)
+    # reversed list order with the same tensor ids
+    order = list(range(cfg.count))[::-1]
+    outs_r = [torch.empty_like(t0[i]) for i in order]
+    with smat.MergePlan([t0[i] for i in order], outs_r, [[e[i] for i in order] for e in ex], tensor_ids=order) as plan:
+        plan.merge([terms[i] for i in order])
+    # the largest tensor as two shards (cut at an odd element: both sides take the element path)
+    big = max(range(cfg.count), key=lambda i: t0[i].numel())
+    n = t0[big].numel()
+    cut = n // 2 + 1
+    out_s = torch.empty_like(t0[big])
+    with smat.MergePlan([t0[big][:cut], t0[big][cut:]], [out_s[:cut], out_s[cut:]],
+                        [[e[big][:cut], e[big][cut:]] for e in ex], tensor_ids=[big, big], elem_offsets=[0, cut]) as plan:
+        plan.merge([terms[big], terms[big]])
+    # in place: out == theta0
+    t0_copy = [x.clone() for x in t0]
+    with smat.MergePlan(t0_copy, t0_copy, ex) as plan:
+        plan.merge(terms)
+    torch.cuda.synchronize()
+    for k, i in enumerate(order):
+        assert torch.equal(bits(outs_r[k]), bits(outs[i]))
+    assert torch.equal(bits(out_s), bits(outs[big]))
+    for a, b in zip(t0_copy, outs):
+        assert torch.equal(bits(a), bits(b))
+
+
+def test_errors():
+    t0, ex = make(100, 2, "bf16", "bf16", 1)
+    out = torch.empty(100, dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(smat.SmatError):
+        smat.smat_merge(ex, t0, out, [dict(gamma=0.3)])                       # one term per expert
+    with pytest.raises(smat.SmatError):
+        smat.smat_merge([ex[0], ex[1].float()], t0, out, [dict(gamma=0.3)] * 2)  # mixed expert dtypes
+    with pytest.raises(smat.SmatError):
+        smat.smat_merge(ex, t0, ex[0], [dict(gamma=0.3)] * 2)                 # out is an expert
+    with pytest.raises(smat.SmatError):
+        smat.smat_merge(ex * 9, t0, out, [dict(gamma=0.1)] * 18)              # more than 16 experts
+    with pytest.raises(smat.SmatError):
+        smat.smat_merge(ex, t0, out, [dict(gamma=0.3, keep=2.0)] * 2)
+    with smat.MergePlan([t0], [out], [[e] for e in ex]) as plan:
+        with pytest.raises(smat.SmatError):
+            plan.merge([dict(gamma=0.3)])                                      # one term per expert
+        plan.merge([dict(gamma=0.3)] * 2)
+    with smat.MergePlan([], [], [[], []]) as plan:                             # empty list
+        plan.merge([dict(gamma=0.3)] * 2)

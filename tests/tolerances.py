@@ -106,3 +106,24 @@ SQNORM_ULPS = 44
 def check_sqnorm(gpu, oracle_sumsq, m2_sum):
     """gpu: the kernel's sumsq; oracle_sumsq: exact value (fp64); m2_sum: sum of m^2 as above."""
     return abs(float(gpu) - float(oracle_sumsq)) <= SQNORM_ULPS * U * float(m2_sum) + 1e-300
+
+
+# N-expert merge (smat_merge): acc starts at theta0 and takes acc = fma(t, x, fma(-t, theta0, acc)) for
+# every kept expert coordinate: two roundings per expert, each at most u of the magnitude of the
+# running sum or of t theta0.  With A = |theta0| + sum_j |t_j| (|x_j| + |theta0|) (over kept
+# coordinates) bounding every partial sum, the fp32 value is within (2N + 1) u A of the exact merge;
+# the final rounding adds half an ulp of the output type.  For N = 1 this is the simulate's bound.
+def check_merge(gpu, out_dtype, y, A, nexp):
+    """Returns (ok, strict) like check_theta_tilde: gpu bf16 bits or fp32 values; y the oracle's fp64
+    merge; A the magnitude above (fp64 array); nexp the number of experts that contributed."""
+    E = (2 * nexp + 1) * U * np.asarray(A, dtype=np.float64)
+    if out_dtype == "bf16":
+        g = bf16_bits_to_f64(gpu)
+        uy = _ulp_bf16(y)
+        half = 0.5 * np.maximum(_ulp_bf16(g), uy)
+    else:
+        g = np.asarray(gpu, dtype=np.float64)
+        uy = _ulp_f32(y)
+        half = 0.5 * np.maximum(_ulp_f32(g), uy)
+    ok = np.abs(g - y) <= half * (1 + 1e-12) + E
+    return ok, E < 0.5 * uy

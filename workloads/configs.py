@@ -364,3 +364,27 @@ def make_inputs(cfg: Config, device="cpu", with_grads: bool = True) -> Inputs:
                 inp.grad_theta.append(torch.randn(shape, generator=gen, device=device, dtype=torch.float32) * 1e-3)
     inp.settings = static_settings(cfg, inp.sigmas)
     return inp
+
+
+def make_experts(cfg: Config, n_experts: int, device="cpu"):
+    """Seeded inputs of an N-expert merge shaped like `cfg`: theta0 (cfg.theta0_dtype, drawn as in
+    make_inputs) and n_experts fine-tuned versions theta0 + N(0, delta_std^2), stored in theta0's
+    dtype.  Returns (theta0 list, experts as a list over experts of lists over tensors)."""
+    import torch
+
+    dt = {"bf16": torch.bfloat16, "f32": torch.float32}
+    gen = torch.Generator(device=device)
+    gen.manual_seed(cfg.data_seed + 0xE0)
+    theta0s, experts = [], [[] for _ in range(n_experts)]
+    for spec in cfg.specs:
+        mean, std = _init_std(spec.kind)
+        base = torch.randn(spec.shape, generator=gen, device=device, dtype=torch.float32) * std + mean
+        t0 = base.to(dt[cfg.theta0_dtype])
+        del base
+        theta0s.append(t0)
+        for j in range(n_experts):
+            x = t0.to(torch.float32) + torch.randn(spec.shape, generator=gen, device=device,
+                                                   dtype=torch.float32) * cfg.delta_std
+            experts[j].append(x.to(dt[cfg.theta0_dtype]))
+            del x
+    return theta0s, experts
