@@ -26,28 +26,30 @@ METRIC = "fused simulate+backward params/s and achieved HBM GB/s (% of peak), 7B
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 KERNEL_SOURCES = ("paper_2609_33437_amd/csrc/smat_kernels.hip", "paper_2609_33437_amd/csrc/smat_device.h",
                   "paper_2609_33437_amd/csrc/smat_tile.h")
+MERGE_SOURCES = ("paper_2609_33437_amd/csrc/smat_merge.hip", "paper_2609_33437_amd/csrc/smat_device.h",
+                 "paper_2609_33437_amd/csrc/smat_tile.h", "paper_2609_33437_amd/csrc/smat_launch.h")
 
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_hash() -> str:
+def kernel_hash(sources=KERNEL_SOURCES) -> str:
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in sources:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(kernel: str, workload: str):
+def load_traffic(kernel: str, workload: str, sources=KERNEL_SOURCES):
     """HBM bytes per launch from committed rocprofv3 counter runs, if taken on the current kernels."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_sha") != kernel_hash():
+    if rec.get("kernel_sha") != kernel_hash(sources):
         return None
     return rec
 
@@ -133,6 +135,10 @@ OPT_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_opt
 OPT_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d gpurun_out/prof_opt_{tag} -o c4 --kernel-include-regex "
                "'k_adamw_multi|k_sqnorm_multi|elementwise' -- "
                "python3 bench.py --adamw --steps 2 --warmup 1 --no-cpu-baseline --calibrate-copy")
+MERGE_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_merge_trace -o c4 -- "
+                   "python3 bench.py --merge --steps 10 --warmup 2")
+MERGE_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d gpurun_out/prof_merge_{tag} -o c4 --kernel-include-regex "
+                 "'k_merge_multi' -- python3 bench.py --merge --steps 2 --warmup 1")
 COPY_GRID = 1 << 26   # threads of the calibration copy (2^28 fp32 values, 4 per thread)
 COPY_BYTES = 1 << 30  # read and written by one calibration dispatch
 
@@ -208,7 +214,65 @@ def summarize(root: str) -> int:
     print("\n".join(lines + [""] + md))
     if os.path.isdir(os.path.join(root, "prof_opt_trace")):
         summarize_optimizer(root, out_dir, fetch_factor, write_factor)
+    if os.path.isdir(os.path.join(root, "prof_merge_trace")):
+        summarize_merge(root, out_dir, fetch_factor, write_factor)
     return 0
+
+
+def summarize_merge(root: str, out_dir: str, fetch_factor: float, write_factor: float) -> None:
+    """profiles/ summaries of the N-expert merge on c4 (seven bf16 experts), scaled by the copy
+    calibration of the simulate/backward counter runs."""
+    import csv
+    import statistics
+
+    stats = list(csv.DictReader(open(os.path.join(root, "prof_merge_trace", "c4_kernel_stats.csv"))))
+    lines = ["# N-expert merge on the 7B-shaped list (c4, seven bf16 experts), rocprofv3 kernel trace", "",
+             f"Command (from the repository root, on one MI355X): `{MERGE_TRACE_CMD}`", "",
+             "bench.py --merge runs Task Arithmetic (no mask) and then DARE + Task Arithmetic (drop 0.3 on "
+             "the linear weights), 2 warmup + 10 timed merges each, through one merge plan; the other kernels "
+             "generate the inputs.", "",
+             "| kernel | calls | average ms | min ms | max ms | share of GPU time |", "|---|---|---|---|---|---|"]
+    for r in stats[:8]:
+        name = r["Name"].replace("(anonymous namespace)", "{anon}").split("(")[0].replace("void ", "")
+        lines.append(f"| `{name[:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.4f} | "
+                     f"{float(r['MinNs']) / 1e6:.4f} | {float(r['MaxNs']) / 1e6:.4f} | {float(r['Percentage']):.2f}% |")
+    with open(os.path.join(out_dir, "kernels_c4_7b_merge_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    # per-dispatch counters in launch order: the first 3 merges are Task Arithmetic, the next 3 DARE
+    vals = {}
+    for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        rows = [r for r in csv.DictReader(open(os.path.join(root, f"prof_merge_{tag}", "c4_counter_collection.csv")))
+                if r["Counter_Name"] == ctr]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        merges = [float(r["Counter_Value"]) for r in rows if "k_merge_multi" in r["Kernel_Name"]]
+        vals[tag] = (merges, fetch_factor if tag == "fetch" else write_factor)
+    P, N = 7504924672, 7
+    algo_r, algo_w = P * 2 * (N + 1), P * 2
+    md = ["# HBM traffic per launch of the N-expert merge on c4 (seven bf16 experts), rocprofv3 counters", "",
+          f"Commands: `{MERGE_PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with `WRITE_SIZE` "
+          "(`prof_merge_write`).", "",
+          f"Scaled by the plain-copy calibration of the simulate/backward counter runs (FETCH_SIZE x "
+          f"{vals['fetch'][1]:.4f}, WRITE_SIZE x {vals['write'][1]:.4f}).  Algorithmic bytes per parameter: seven experts and theta0 read (16 B), "
+          "the merged weights written (2 B).", "",
+          "| merge | FETCH_SIZE KiB | WRITE_SIZE KiB | read GB (scaled) | written GB (scaled) | algorithmic GB | "
+          "traffic / algorithmic |", "|---|---|---|---|---|---|---|"]
+    recs = {}
+    for k, sl in (("task_arithmetic", slice(0, 3)), ("dare_task_arithmetic", slice(3, 6))):
+        fk = statistics.median(vals["fetch"][0][sl])
+        wk = statistics.median(vals["write"][0][sl])
+        rd, wr = fk * 1024 / vals["fetch"][1], wk * 1024 / vals["write"][1]
+        md.append(f"| {k} | {fk:.0f} | {wk:.0f} | {rd / 1e9:.3f} | {wr / 1e9:.3f} | {(algo_r + algo_w) / 1e9:.3f} | "
+                  f"{(rd + wr) / (algo_r + algo_w):.4f} |")
+        recs[k] = round(rd + wr)
+    with open(os.path.join(out_dir, "traffic_c4_7b_merge.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+    rec = {"kernel": "merge", "workload": "c4", "kernel_sha": kernel_hash(MERGE_SOURCES),
+           "bytes_per_launch": recs, "algorithmic_bytes_per_launch": algo_r + algo_w,
+           "commands": [MERGE_PMC_CMD.format(ctr="FETCH_SIZE", tag="fetch"),
+                        MERGE_PMC_CMD.format(ctr="WRITE_SIZE", tag="write")]}
+    with open(os.path.join(out_dir, "traffic_merge_c4.json"), "w") as f:
+        json.dump(rec, f, indent=1)
+    print("\n".join(lines + [""] + md))
 
 
 def summarize_optimizer(root: str, out_dir: str, fetch_factor: float, write_factor: float) -> None:
@@ -442,6 +506,15 @@ def bench_merge(args, torch, smat, workloads) -> int:
                          "frac": round(nbytes / (ms * 1e6) / PEAK_HBM_GBPS, 4)}
             log(f"{mode}: {ms:.3f} ms = {nbytes / (ms * 1e6):.0f} GB/s")
     dom = max(res, key=lambda m: res[m]["ms"])
+    traffic = load_traffic("merge", cfg.name, MERGE_SOURCES) if N == 7 else None
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        log("ran the copy calibration kernel (1 GiB read + 1 GiB written) 3 times")
     result = {
         "metric": f"N-expert merge params/s and achieved HBM GB/s, {cfg.name}-shaped",
         "value": P / (res[dom]["ms"] * 1e-3),
@@ -452,7 +525,8 @@ def bench_merge(args, torch, smat, workloads) -> int:
                    "params": P, "tensors": cfg.count, "experts": N, "bytes_per_param": 2 * N + 4},
         "modes": res,
         "roofline": {"bound": "hbm", "achieved": res[dom]["gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": res[dom]["frac"], "traffic": None, "kernel": f"merge ({dom})",
+                     "frac": res[dom]["frac"], "traffic": traffic["bytes_per_launch"][dom] if traffic else None,
+                     "kernel": f"merge ({dom})",
                      "algorithmic_bytes_per_launch": nbytes, "avg_launch_ms": res[dom]["ms"]},
     }
     print(json.dumps(result))
