@@ -70,7 +70,7 @@ def parse_args():
                     help="theta0 in pinned host memory, copied into the simulated buffers at each restore; "
                          "also reports the prefetch's host-link rate")
     ap.add_argument("--summarize", metavar="DIR",
-                    help="turn rocprofv3 CSV output under DIR (prof_trace/, prof_fetch/, prof_write/) into the "
+                    help="turn rocprofv3 CSV output under DIR (trace/, fetch/, write/, and opt_*/, merge_*/ when present) into the "
                          "summaries under profiles/ and exit")
     ap.add_argument("--train", action="store_true",
                     help="time SMAT inside a bf16 training loop of a Llama-1B-shaped synthetic decoder against "
@@ -125,20 +125,23 @@ def cpu_baseline(cfg, inp, params, step, max_elems, budget_s, torch, np):
                       f"random order (simulate + backward, fp64 NumPy, one process), {secs:.1f} s of work"}
 
 
-TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_trace -o c4 -- "
-             "python3 bench.py --steps 20 --warmup 5 --no-cpu-baseline --calibrate-copy")
-PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d gpurun_out/prof_{tag} -o c4 --kernel-include-regex "
+# rocprofv3 passes behind profiles/.  Run from /tmp with TMPDIR=/tmp; $REPO is the repository root and
+# $REPO/rocprof the output root that `bench.py --summarize $REPO/rocprof` reads.
+PROF_NOTE = "run from /tmp with TMPDIR=/tmp; $REPO is the repository root"
+TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d $REPO/rocprof/trace -o c4 -- "
+             "python3 $REPO/bench.py --steps 20 --warmup 5 --no-cpu-baseline --calibrate-copy")
+PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d $REPO/rocprof/{tag} -o c4 --kernel-include-regex "
            "'k_simulate_multi|k_backward_multi|elementwise' -- "
-           "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --calibrate-copy")
-OPT_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_opt_trace -o c4 -- "
-                 "python3 bench.py --adamw --steps 10 --warmup 2 --no-cpu-baseline")
-OPT_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d gpurun_out/prof_opt_{tag} -o c4 --kernel-include-regex "
-               "'k_adamw_multi|k_sqnorm_multi|elementwise' -- "
-               "python3 bench.py --adamw --steps 2 --warmup 1 --no-cpu-baseline --calibrate-copy")
-MERGE_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_merge_trace -o c4 -- "
-                   "python3 bench.py --merge --steps 10 --warmup 2")
-MERGE_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d gpurun_out/prof_merge_{tag} -o c4 --kernel-include-regex "
-                 "'k_merge_multi' -- python3 bench.py --merge --steps 2 --warmup 1")
+           "python3 $REPO/bench.py --steps 2 --warmup 1 --no-cpu-baseline --calibrate-copy")
+OPT_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d $REPO/rocprof/opt_trace -o c4 -- "
+                 "python3 $REPO/bench.py --adamw --steps 10 --warmup 2 --no-cpu-baseline")
+OPT_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d $REPO/rocprof/opt_{tag} -o c4 --kernel-include-regex "
+               "'k_adamw_multi|k_sqnorm_multi' -- "
+               "python3 $REPO/bench.py --adamw --steps 2 --warmup 1 --no-cpu-baseline")
+MERGE_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d $REPO/rocprof/merge_trace -o c4 -- "
+                   "python3 $REPO/bench.py --merge --steps 10 --warmup 2")
+MERGE_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d $REPO/rocprof/merge_{tag} -o c4 --kernel-include-regex "
+                 "'k_merge_multi' -- python3 $REPO/bench.py --merge --steps 2 --warmup 1")
 COPY_GRID = 1 << 26   # threads of the calibration copy (2^28 fp32 values, 4 per thread)
 COPY_BYTES = 1 << 30  # read and written by one calibration dispatch
 
@@ -159,9 +162,9 @@ def summarize(root: str) -> int:
 
     out_dir = os.path.join(ROOT, "profiles")
     os.makedirs(out_dir, exist_ok=True)
-    stats = list(csv.DictReader(open(os.path.join(root, "prof_trace", "c4_kernel_stats.csv"))))
+    stats = list(csv.DictReader(open(os.path.join(root, "trace", "c4_kernel_stats.csv"))))
     lines = ["# Kernel time on the 7B-shaped list (c4), rocprofv3 kernel trace", "",
-             f"Command (from the repository root, on one MI355X): `{TRACE_CMD}`", "",
+             f"Command (on one MI355X; {PROF_NOTE}): `{TRACE_CMD}`", "",
              "Each step launches one simulate and one backward over the 290-tensor list "
              "(7,504,924,672 parameters); 5 warmup + 20 timed steps = 25 calls each.  The other kernels are "
              "torch's input generation and the copy calibration.", "",
@@ -176,7 +179,7 @@ def summarize(root: str) -> int:
 
     vals = {}
     for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
-        rows = csv.DictReader(open(os.path.join(root, f"prof_{tag}", "c4_counter_collection.csv")))
+        rows = csv.DictReader(open(os.path.join(root, tag, "c4_counter_collection.csv")))
         for r in rows:
             k = kind(r["Kernel_Name"], int(r["Grid_Size"]))
             if k and r["Counter_Name"] == ctr:
@@ -186,8 +189,8 @@ def summarize(root: str) -> int:
     P = 7504924672
     algo = {"simulate": (P * 6, P * 2), "backward": (P * 6, P * 4)}
     md = ["# HBM traffic per launch on the 7B-shaped list (c4), rocprofv3 counters", "",
-          f"Commands: `{PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with `WRITE_SIZE` "
-          "(`prof_write`).", "",
+          f"Commands ({PROF_NOTE}): `{PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with "
+          "`WRITE_SIZE` (output `rocprof/write`).", "",
           "Counters are KiB per dispatch.  Scale: a plain elementwise copy of 2^28 fp32 values (1 GiB read, "
           f"1 GiB written) reads FETCH_SIZE = {fetch_factor:.4f} x and WRITE_SIZE = {write_factor:.4f} x its "
           "true bytes; kernel readings are divided by these factors.", "",
@@ -212,9 +215,9 @@ def summarize(root: str) -> int:
     with open(os.path.join(out_dir, "traffic_c4_7b.md"), "w") as f:
         f.write("\n".join(md) + "\n")
     print("\n".join(lines + [""] + md))
-    if os.path.isdir(os.path.join(root, "prof_opt_trace")):
+    if os.path.isdir(os.path.join(root, "opt_trace")):
         summarize_optimizer(root, out_dir, fetch_factor, write_factor)
-    if os.path.isdir(os.path.join(root, "prof_merge_trace")):
+    if os.path.isdir(os.path.join(root, "merge_trace")):
         summarize_merge(root, out_dir, fetch_factor, write_factor)
     return 0
 
@@ -225,9 +228,9 @@ def summarize_merge(root: str, out_dir: str, fetch_factor: float, write_factor: 
     import csv
     import statistics
 
-    stats = list(csv.DictReader(open(os.path.join(root, "prof_merge_trace", "c4_kernel_stats.csv"))))
+    stats = list(csv.DictReader(open(os.path.join(root, "merge_trace", "c4_kernel_stats.csv"))))
     lines = ["# N-expert merge on the 7B-shaped list (c4, seven bf16 experts), rocprofv3 kernel trace", "",
-             f"Command (from the repository root, on one MI355X): `{MERGE_TRACE_CMD}`", "",
+             f"Command (on one MI355X; {PROF_NOTE}): `{MERGE_TRACE_CMD}`", "",
              "bench.py --merge runs Task Arithmetic (no mask) and then DARE + Task Arithmetic (drop 0.3 on "
              "the linear weights), 2 warmup + 10 timed merges each, through one merge plan; the other kernels "
              "generate the inputs.", "",
@@ -241,7 +244,7 @@ def summarize_merge(root: str, out_dir: str, fetch_factor: float, write_factor: 
     # per-dispatch counters in launch order: the first 3 merges are Task Arithmetic, the next 3 DARE
     vals = {}
     for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
-        rows = [r for r in csv.DictReader(open(os.path.join(root, f"prof_merge_{tag}", "c4_counter_collection.csv")))
+        rows = [r for r in csv.DictReader(open(os.path.join(root, f"merge_{tag}", "c4_counter_collection.csv")))
                 if r["Counter_Name"] == ctr]
         rows.sort(key=lambda r: int(r["Dispatch_Id"]))
         merges = [float(r["Counter_Value"]) for r in rows if "k_merge_multi" in r["Kernel_Name"]]
@@ -249,8 +252,8 @@ def summarize_merge(root: str, out_dir: str, fetch_factor: float, write_factor: 
     P, N = 7504924672, 7
     algo_r, algo_w = P * 2 * (N + 1), P * 2
     md = ["# HBM traffic per launch of the N-expert merge on c4 (seven bf16 experts), rocprofv3 counters", "",
-          f"Commands: `{MERGE_PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with `WRITE_SIZE` "
-          "(`prof_merge_write`).", "",
+          f"Commands ({PROF_NOTE}): `{MERGE_PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with "
+          "`WRITE_SIZE` (output `rocprof/merge_write`).", "",
           f"Scaled by the plain-copy calibration of the simulate/backward counter runs (FETCH_SIZE x "
           f"{vals['fetch'][1]:.4f}, WRITE_SIZE x {vals['write'][1]:.4f}).  Algorithmic bytes per parameter: seven experts and theta0 read (16 B), "
           "the merged weights written (2 B).", "",
@@ -287,9 +290,9 @@ def summarize_optimizer(root: str, out_dir: str, fetch_factor: float, write_fact
             return "grad_norm"
         return None
 
-    stats = list(csv.DictReader(open(os.path.join(root, "prof_opt_trace", "c4_kernel_stats.csv"))))
+    stats = list(csv.DictReader(open(os.path.join(root, "opt_trace", "c4_kernel_stats.csv"))))
     lines = ["# Optimizer-side kernel time on the 7B-shaped list (c4), rocprofv3 kernel trace", "",
-             f"Command (from the repository root, on one MI355X): `{OPT_TRACE_CMD}`", "",
+             f"Command (on one MI355X; {PROF_NOTE}): `{OPT_TRACE_CMD}`", "",
              "bench.py --adamw first runs the simulate + backward benchmark, then the fused AdamW step "
              "(unclipped, then clipped at 1 after the gradient-norm pass), then backward-accumulate + "
              "torch's fused AdamW (unclipped, then with torch.nn.utils.clip_grad_norm_).", "",
@@ -303,15 +306,15 @@ def summarize_optimizer(root: str, out_dir: str, fetch_factor: float, write_fact
         f.write("\n".join(lines) + "\n")
     vals = {}
     for tag, ctr in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
-        for r in csv.DictReader(open(os.path.join(root, f"prof_opt_{tag}", "c4_counter_collection.csv"))):
+        for r in csv.DictReader(open(os.path.join(root, f"opt_{tag}", "c4_counter_collection.csv"))):
             k = kind(r["Kernel_Name"])
             if k and r["Counter_Name"] == ctr:
                 vals.setdefault((k, tag), []).append(float(r["Counter_Value"]))
     P = 7504924672
     algo = {"adamw": (P * 14, P * 12), "grad_norm": (P * 2, 0)}
     md = ["# HBM traffic per launch of the optimizer-side kernels on c4, rocprofv3 counters", "",
-          f"Commands: `{OPT_PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with `WRITE_SIZE` "
-          "(`prof_opt_write`).", "",
+          f"Commands ({PROF_NOTE}): `{OPT_PMC_CMD.format(ctr='FETCH_SIZE', tag='fetch')}` and the same with "
+          "`WRITE_SIZE` (output `rocprof/opt_write`).", "",
           f"Scaled by the copy calibration of the simulate/backward counter runs (FETCH_SIZE x {fetch_factor:.4f}, "
           f"WRITE_SIZE x {write_factor:.4f}).  Algorithmic bytes per parameter: fused AdamW reads g~ (bf16, 2 B) and "
           "theta, m1, m2 (12 B) and writes theta, m1, m2 (12 B); the norm pass reads g~ only (2 B).", "",
