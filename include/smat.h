@@ -246,6 +246,15 @@ typedef struct smat_adam_state {
  * pointers), SMAT_ERR_STATE (no workspace), SMAT_ERR_HIP. */
 smat_status smat_plan_bind_adam_state(smat_plan* plan, const smat_adam_state* per_tensor, hipStream_t stream);
 
+/* smat_plan_set_grad_sim -- point the plan at new gradient-at-theta~ arrays (count device pointers
+ * in descriptor order, grad_dtype, same sizes), e.g. the tensors autograd produced this step, so the
+ * caller need not copy them into fixed buffers.  Uploads the tensor records on `stream`; later
+ * operations on that stream use the new arrays.  The arrays must not overlap theta, the simulated
+ * buffer or grad_theta, and must stay valid until the operations that read them have run.
+ * Errors: SMAT_ERR_INVALID (null, overlap, plan without gradient pointers), SMAT_ERR_STATE (no
+ * workspace), SMAT_ERR_HIP. */
+smat_status smat_plan_set_grad_sim(smat_plan* plan, const void* const* grad_sims, hipStream_t stream);
+
 /* smat_adamw_fused_multi -- smat_adamw_fused over every tensor of the plan in one launch: theta is
  * desc.theta (the expert storage, updated in place), grad_sim is desc.grad_sim and, when accumulate
  * is nonzero, grad_acc is desc.grad_theta (read, not written); grad_scale_dev as in

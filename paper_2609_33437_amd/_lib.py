@@ -27,7 +27,7 @@ EXPORTS = (
     "smat_switch_storage", "smat_plan_state", "smat_plan_active_ptrs", "smat_plan_destroy", "smat_last_error",
     "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi", "smat_grad_norm_multi",
     "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
-    "smat_merge_multi", "smat_merge_plan_destroy",
+    "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grad_sim",
 )
 
 
@@ -102,6 +102,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_merge_plan_bind_workspace": [P, P, c_size_t, P],
         "smat_merge_multi": [P, POINTER(smat_merge_term), P],
         "smat_merge_plan_destroy": [P],
+        "smat_plan_set_grad_sim": [P, POINTER(P), P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -296,6 +297,18 @@ class Plan:
 
     def backward_accum(self, seed: int, step: int, lam: float, stream=None) -> None:
         _check(lib().smat_backward_accum_multi(self._plan, int(seed), int(step), float(lam), _stream_handle(stream)))
+
+    def set_grad_sim(self, grad_sims: Sequence, stream=None) -> None:
+        """Point the plan at new gradient-at-theta~ tensors (smat_plan_set_grad_sim); holds them until
+        the next call."""
+        if len(grad_sims) != self.count:
+            raise SmatError(SMAT_ERR_INVALID, "one gradient per tensor")
+        for g, t in zip(grad_sims, self._refs[0]):
+            if g.numel() != t.numel() or dtype_code(g) != self.dtypes[2]:
+                raise SmatError(SMAT_ERR_INVALID, "gradients must match the plan's sizes and gradient dtype")
+        arr = (c_void_p * max(self.count, 1))(*[_dev_ptr(g, "grad_sim") for g in grad_sims])
+        _check(lib().smat_plan_set_grad_sim(self._plan, arr, _stream_handle(stream)))
+        self._grad_sim_refs = list(grad_sims)
 
     def bind_adam_state(self, exp_avgs: Sequence, exp_avg_sqs: Sequence, stream=None) -> None:
         if len(exp_avgs) != self.count or len(exp_avg_sqs) != self.count:

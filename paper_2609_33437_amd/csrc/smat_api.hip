@@ -588,6 +588,42 @@ extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_s
   return SMAT_OK;
 }
 
+extern "C" smat_status smat_plan_set_grad_sim(smat_plan* p, const void* const* grad_sims, hipStream_t stream) {
+  if (!p || (p->count > 0 && !grad_sims)) return fail(SMAT_ERR_INVALID, "smat_plan_set_grad_sim: null argument");
+  if (!p->has_grads) return fail(SMAT_ERR_INVALID, "smat_plan_set_grad_sim: plan has no gradient pointers");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_set_grad_sim: no workspace bound");
+  std::vector<TensorRec> recs = p->recs;
+  for (int32_t i = 0; i < p->count; ++i) {
+    TensorRec& r = recs[i];
+    if (r.n == 0) continue;
+    const void* g = grad_sims[i];
+    const size_t gb = (size_t)r.n * dtype_bytes(p->g_dt);
+    if (!g) return fail(SMAT_ERR_INVALID, "smat_plan_set_grad_sim: tensor %d: null grad_sim", i);
+    if (overlap(g, gb, r.grad_theta, (size_t)r.n * 4) || overlap(g, gb, r.out, (size_t)r.n * dtype_bytes(p->out_dt)) ||
+        overlap(g, gb, r.theta, (size_t)r.n * 4))
+      return fail(SMAT_ERR_INVALID, "smat_plan_set_grad_sim: tensor %d: grad_sim overlaps theta, out or grad_theta", i);
+    r.grad_sim = g;
+    r.sflags = (r.sflags & ~smat::kVecBwd) | bwd_flags(g, p->g_dt, r.grad_theta, r.elem_offset);
+    if (p->adam_bound)
+      r.sflags = (r.sflags & ~(smat::kVecAdam | smat::kVecAdamAcc)) |
+                 adam_flags(r.theta, p->adam[i].exp_avg, p->adam[i].exp_avg_sq, g, p->g_dt, r.grad_theta, r.elem_offset);
+  }
+  const size_t rec_bytes = sizeof(TensorRec) * p->count, adam_bytes = sizeof(AdamRec) * p->count;
+  if (!p->adam_staging) {
+    SMAT_HIP(hipHostMalloc((void**)&p->adam_staging, std::max<size_t>(rec_bytes + adam_bytes, 256), hipHostMallocDefault));
+    SMAT_HIP(hipEventCreateWithFlags(&p->ev_adam, hipEventDisableTiming));
+  } else {
+    SMAT_HIP(hipEventSynchronize(p->ev_adam));  // the previous table upload has left the staging buffer
+  }
+  std::memcpy(p->adam_staging, recs.data(), rec_bytes);
+  if (p->count > 0)
+    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_recs, p->adam_staging, rec_bytes, hipMemcpyHostToDevice, stream));
+  SMAT_HIP(hipEventRecord(p->ev_adam, stream));
+  for (int32_t i = 0; i < p->count; ++i) p->descs[i].grad_sim = recs[i].grad_sim;
+  p->recs = recs;
+  return SMAT_OK;
+}
+
 extern "C" smat_status smat_adamw_fused_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
                                               smat_adamw_params hp, int32_t accumulate, const float* grad_scale_dev,
                                               hipStream_t stream) {

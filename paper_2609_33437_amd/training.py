@@ -6,8 +6,8 @@ Each step computes one loss with one forward and one backward pass.  On a simula
 1. `begin(step)` draws one scale alpha ~ U[alpha_min, 1] for all tensors (Sec. 4.1, Scale),
    writes theta~ = theta0 + alpha m (.) (theta - theta0) + eps into one reusable buffer per
    parameter (smat_simulate_multi), and rebinds each parameter's `.data` to its buffer.  The
-   model's forward and backward then run on theta~, and the gradient at theta~ lands in a
-   preallocated buffer.
+   model's forward and backward then run on theta~; autograd's gradient tensors at theta~ are
+   handed to the library as they are (smat_plan_set_grad_sim), with no copy.
 2. `end(optimizer)` turns that gradient into the expert gradient lambda alpha m (.) g~
    (Eq. smat-gradient), with the mask regenerated (smat_backward_accum_multi).  It then rebinds
    `.data` to the expert storage, so that the optimizer, weight decay included, only sees the fp32
@@ -23,7 +23,7 @@ This module only rebinds tensors and sequences library calls.
 """
 from __future__ import annotations
 
-from typing import Callable, Iterable, List, Optional, Sequence, Tuple
+from typing import Iterable, List, Optional, Sequence, Tuple
 
 import numpy as np
 import torch
@@ -161,6 +161,8 @@ class SimulatedMergeTraining:
         self._step: Optional[int] = None        # set between begin() and end()
         self._adam_key = None
         self._clip = None                       # GPU scalars (sumsq, clipping factor) of the fused update
+        self._grads = None                      # gradients at theta~ the plan points at
+        self.names = [f"param{i}" for i in range(n)]
 
     @classmethod
     def from_module(cls, model: torch.nn.Module, keep: float = 0.5, alpha_min: float = 0.2, sigma: float = 2e-3,
@@ -198,19 +200,26 @@ class SimulatedMergeTraining:
                               for k, s in zip(self.keep, self.sigma)])
         self.plan.simulate(self.seed, step)
         self.plan.switch_storage(SMAT_SIMULATED)
-        for p, b, g in zip(self.params, self.buffers, self.grad_sim):
-            g.zero_()
+        self._grads = None      # last step's gradients, no longer read by any queued kernel
+        for p, b in zip(self.params, self.buffers):
             p.data = b
-            p.grad = g          # autograd accumulates into it in place
+            p.grad = None       # autograd creates the gradient at theta~ and keeps it as p.grad
         self._step = int(step)
         return True
 
     def _collect_grad_sim(self) -> None:
-        for p, g in zip(self.params, self.grad_sim):
-            if p.grad is None:
+        """Hand the plan the gradients at theta~ that autograd left in p.grad."""
+        grads = []
+        for i, (p, b) in enumerate(zip(self.params, self.buffers)):
+            g = p.grad
+            if g is None:                            # the parameter took no part in the loss
+                g = self.grad_sim[i]
                 g.zero_()
-            elif p.grad is not g:     # the caller replaced the gradient tensor
-                g.copy_(p.grad)
+            elif not g.is_contiguous() or g.dtype != b.dtype:
+                g = g.to(dtype=b.dtype, memory_format=torch.contiguous_format)
+            grads.append(g)
+        self.plan.set_grad_sim(grads)
+        self._grads = grads     # kept alive until the kernels that read them have been queued
 
     def _restore(self) -> None:
         self.plan.switch_storage(SMAT_EXPERT)
@@ -239,10 +248,13 @@ class SimulatedMergeTraining:
             if optimizer is None:
                 raise SmatError(SMAT_ERR_INVALID, "the fused update needs the optimizer that owns the moments")
             hp = adam_hparams(optimizer, self.params)   # validate before touching any state
+            wrapped = {id(p) for p in self.params}
+            if any(id(q) not in wrapped and q.grad is not None for g in optimizer.param_groups for q in g["params"]):
+                raise SmatError(SMAT_ERR_INVALID, "the optimizer holds parameters outside the wrapper that have "
+                                                  "gradients; the fused update would skip them")
             self._restore()
             return self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step, max_norm)
-        for g in self.grad_theta:
-            g.zero_()
+        torch._foreach_zero_(self.grad_theta)
         self.plan.backward_accum(self.seed, step, self.lam)
         self._restore()
         for p, g in zip(self.params, self.grad_theta):
@@ -282,7 +294,7 @@ class SimulatedMergeTraining:
             self.plan.grad_norm(self.seed, step, self.lam, False, float(max_norm), sumsq, coef)
             norm = sumsq.sqrt()
         self.plan.adamw_fused(self.seed, step, self.lam, hp, grad_scale_dev=coef)
-        for c in counts:
+        for c in counts:        # the optimizer's own step counts (CPU or GPU scalars)
             c.add_(1)
         return norm
 

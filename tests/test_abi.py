@@ -146,6 +146,9 @@ def test_plan_create_validation_without_gpu():
     assert lib.smat_plan_create(arr, 2, 1, 1, 1, 0, ctypes.byref(p)) == 0
     assert lib.smat_simulate_multi(p, 0, 0, None) == _lib.SMAT_ERR_STATE
     assert lib.smat_switch_storage(p, 1, None) == _lib.SMAT_ERR_STATE
+    grads = (ctypes.c_void_p * 2)(ctypes.c_void_p(11 * A), ctypes.c_void_p(12 * A))
+    assert lib.smat_plan_set_grad_sim(p, grads, None) == _lib.SMAT_ERR_STATE          # no workspace yet
+    assert lib.smat_plan_set_grad_sim(p, None, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_switch_storage(p, 5, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_plan_destroy(p) == 0
     assert lib.smat_plan_destroy(None) == 0

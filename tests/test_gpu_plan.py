@@ -305,3 +305,38 @@ def test_offload_periodic_training_cycle_matches_resident(mini):
     # after the last restore the buffers hold theta0 again
     for b, h in zip(bufs, inp.theta0):
         assert torch.equal(bits(b.cpu()), bits(h.view(-1)))
+
+
+def test_set_grad_sim_rebinds_the_gradient_arrays(mini):
+    """smat_plan_set_grad_sim points the backward and the fused step at new gradient tensors,
+    including ones whose alignment takes the element path, with results equal to a plan built on
+    them from the start."""
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    step = 5
+    params = workloads.step_params(cfg, inp.settings, step)
+    g = torch.Generator(DEV).manual_seed(3)
+    # new gradients: every other one at an odd element offset inside a larger buffer (misaligned)
+    new = []
+    for i, x in enumerate(gs):
+        buf = (torch.randn(x.numel() + 8, device=DEV, generator=g) * 1e-2).to(x.dtype)
+        new.append(buf[1:1 + x.numel()] if i % 2 else buf[:x.numel()])
+    gt_a = [x.clone() for x in gt]
+    gt_b = [x.clone() for x in gt]
+    with smat.Plan(th, out, t0, gs, gt_a) as plan:
+        plan.set_params(params)
+        plan.set_grad_sim(new)
+        plan.backward_accum(cfg.smat_seed, step, cfg.lam)
+    with smat.Plan(th, out, t0, new, gt_b) as plan:
+        plan.set_params(params)
+        plan.backward_accum(cfg.smat_seed, step, cfg.lam)
+    torch.cuda.synchronize()
+    for a, b in zip(gt_a, gt_b):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        with pytest.raises(smat.SmatError):
+            plan.set_grad_sim(new[:-1])                           # one per tensor
+        with pytest.raises(smat.SmatError):
+            plan.set_grad_sim([x.float() for x in new])           # the plan's gradient dtype
+        with pytest.raises(smat.SmatError):
+            plan.set_grad_sim([o for o in out])                   # overlaps the simulated buffer

@@ -86,7 +86,7 @@ def test_simulated_step_matches_oracle():
     assert torch.allclose(loss, ref_loss, rtol=1e-6, atol=0)
     for p, q in zip(w.params, ref.parameters()):
         torch.testing.assert_close(p.grad, q.grad, rtol=1e-5, atol=1e-7)
-    g_sim = [host(g)[0] for g in w.grad_sim]
+    g_sim = [host(p.grad)[0] for p in w.params]    # the gradients at theta~ autograd produced
     w.end()
     assert not w.active
     for i, (p, m) in enumerate(zip(w.params, masters)):
@@ -116,7 +116,7 @@ def test_fused_adamw_step_matches_oracle(torch_fused):
     # p.data is theta~ here; the update applies to the expert storage
     old = [(host(m)[0], host(opt.state[p]["exp_avg"])[0], host(opt.state[p]["exp_avg_sq"])[0])
            for p, m in zip(w.params, w.master)]
-    g_sim = [host(g)[0] for g in w.grad_sim]
+    g_sim = [host(p.grad)[0] for p in w.params]    # the gradients at theta~ autograd produced
     ops = [op(w, i) for i in range(len(w.params))]
     w.end(opt, fused=True)
     hp = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.05, grad_scale=1.0, step=4)
@@ -151,7 +151,7 @@ def test_fused_clipped_step_matches_oracle():
     model.loss(token_batches(TINY, 2, 16, 1, 5, DEV)[0]).backward()
     old = [(host(m)[0], host(opt.state[p]["exp_avg"])[0], host(opt.state[p]["exp_avg_sq"])[0])
            for p, m in zip(w.params, w.master)]
-    g_sim = [host(g)[0] for g in w.grad_sim]
+    g_sim = [host(p.grad)[0] for p in w.params]    # the gradients at theta~ autograd produced
     ops = [op(w, i) for i in range(len(w.params))]
     sq = sum(oracle.grad_sqnorm(g_sim[i], "f32", ops[i], w.lam, SEED, 3, i) for i in range(len(g_sim)))
     max_norm = 0.25 * float(np.sqrt(sq))
@@ -178,7 +178,7 @@ def test_fused_update_creates_missing_optimizer_state():
     masters = [p.detach().clone() for p in w.params]
     assert w.begin(0)
     model.loss(token_batches(TINY, 2, 8, 1, 1, DEV)[0]).backward()
-    g_sim = [host(g)[0] for g in w.grad_sim]
+    g_sim = [host(p.grad)[0] for p in w.params]    # the gradients at theta~ autograd produced
     ops = [op(w, i) for i in range(len(w.params))]
     w.end(opt, fused=True)
     hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, grad_scale=1.0, step=1)
@@ -258,6 +258,10 @@ def test_wrapper_errors():
         w.begin(7)                                 # one already open
     with pytest.raises(smat.SmatError):
         w.end(torch.optim.SGD(w.params, lr=0.1), fused=True)
+    extra = torch.nn.Parameter(torch.zeros(3, device=DEV))
+    extra.grad = torch.ones(3, device=DEV)
+    with pytest.raises(smat.SmatError):            # a parameter the fused update would skip
+        w.end(torch.optim.AdamW(w.params + [extra], lr=1e-3), fused=True)
     assert w.active                                # a rejected end() leaves the step open
     w.abort()
     assert not w.active and all(p.data_ptr() == m.data_ptr() for p, m in zip(w.params, w.master))
