@@ -561,8 +561,7 @@ def bench_train(args, torch, smat) -> int:
     opt = torch.optim.AdamW(params, lr=2e-5, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-3, fused=True)
     w = SimulatedMergeTraining.from_module(model, keep=0.5, alpha_min=0.2, sigma=2e-3, period=t, seed=0x7A11,
                                            offload=args.offload)
-    extra = sum(b.numel() * b.element_size() + g.numel() * g.element_size() + a.numel() * a.element_size()
-                for b, g, a in zip(w.buffers, w.grad_sim, w.grad_theta))
+    extra = sum(b.numel() * b.element_size() for b in w.buffers)   # resident state beyond FT's
     if not args.offload:
         extra += sum(x.numel() * x.element_size() for x in w.theta0)
     hooks = {"begin": [], "end": []}

@@ -186,8 +186,8 @@ typedef struct smat_tensor_desc {
   const void* theta0;       /* [n] frozen base in the plan's theta0 dtype; resident mode only
                                (NULL in offload mode, where the buffer `out` holds theta0) */
   void* out;                /* [n] reusable buffer for theta~ in the plan's out dtype */
-  const void* grad_sim;     /* [n] gradient at theta~ (grad dtype), or NULL if no backward */
-  float* grad_theta;        /* [n] fp32 gradient accumulator, or NULL if no backward */
+  const void* grad_sim;     /* [n] gradient at theta~ (grad dtype), or NULL (set later or never) */
+  float* grad_theta;        /* [n] fp32 gradient accumulator, or NULL (set later or never) */
   const void* theta0_host;  /* offload mode: [n] pinned host copy of theta0 (out dtype); else NULL */
   int64_t n;                /* element count, >= 0 */
   uint32_t tensor_id;       /* unique within the plan */
@@ -201,8 +201,10 @@ typedef struct smat_tensor_desc {
  *               Implementation"): theta0 lives in desc.theta0_host and is copied into the
  *               buffer `out` on a copy stream whenever the expert storage is restored, so each
  *               simulate runs in place over the buffer.  Requires theta0_dtype == out_dtype.
- * The caller owns *out_plan and must release it with smat_plan_destroy.
- * Errors: SMAT_ERR_INVALID (bad descriptor, duplicate tensor_id, aliasing), SMAT_ERR_DTYPE. */
+ * Each gradient pointer is given for every tensor or for none (smat_plan_set_grads can supply or
+ * replace them later).  The caller owns *out_plan and must release it with smat_plan_destroy.
+ * Errors: SMAT_ERR_INVALID (bad descriptor, duplicate tensor_id, aliasing, gradient pointers given
+ * for some tensors only), SMAT_ERR_DTYPE. */
 smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t count, smat_dtype theta0_dtype,
                              smat_dtype out_dtype, smat_dtype grad_dtype, int32_t offload,
                              smat_plan** out_plan);
@@ -229,8 +231,8 @@ smat_status smat_plan_set_params(smat_plan* plan, const smat_op_params* per_tens
 smat_status smat_simulate_multi(smat_plan* plan, uint64_t seed, uint32_t step, hipStream_t stream);
 
 /* smat_backward_accum_multi -- smat_backward_accum over every tensor of the plan in one launch.
- * Errors: SMAT_ERR_INVALID (lambda, step, plan without gradient pointers), SMAT_ERR_STATE,
- * SMAT_ERR_HIP. */
+ * Errors: SMAT_ERR_INVALID (lambda, step), SMAT_ERR_STATE (no workspace or params, gradient arrays
+ * not set), SMAT_ERR_HIP. */
 smat_status smat_backward_accum_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda,
                                       hipStream_t stream);
 
@@ -242,25 +244,28 @@ typedef struct smat_adam_state {
 
 /* smat_plan_bind_adam_state -- hand the plan the optimizer state of every tensor (count entries in
  * descriptor order) for smat_adamw_fused_multi; uploads a small table on `stream`.  May be called
- * again to rebind.  Errors: SMAT_ERR_INVALID (null or overlapping arrays, plan without gradient
- * pointers), SMAT_ERR_STATE (no workspace), SMAT_ERR_HIP. */
+ * again to rebind.  Errors: SMAT_ERR_INVALID (null or overlapping arrays), SMAT_ERR_STATE (no
+ * workspace), SMAT_ERR_HIP. */
 smat_status smat_plan_bind_adam_state(smat_plan* plan, const smat_adam_state* per_tensor, hipStream_t stream);
 
-/* smat_plan_set_grad_sim -- point the plan at new gradient-at-theta~ arrays (count device pointers
- * in descriptor order, grad_dtype, same sizes), e.g. the tensors autograd produced this step, so the
- * caller need not copy them into fixed buffers.  Uploads the tensor records on `stream`; later
- * operations on that stream use the new arrays.  The arrays must not overlap theta, the simulated
- * buffer or grad_theta, and must stay valid until the operations that read them have run.
- * Errors: SMAT_ERR_INVALID (null, overlap, plan without gradient pointers), SMAT_ERR_STATE (no
- * workspace), SMAT_ERR_HIP. */
-smat_status smat_plan_set_grad_sim(smat_plan* plan, const void* const* grad_sims, hipStream_t stream);
+/* smat_plan_set_grads -- point the plan at new gradient arrays: grad_sims (count device pointers
+ * in descriptor order, grad_dtype, e.g. the tensors autograd produced at theta~ this step) and/or
+ * grad_thetas (count fp32 device pointers); a NULL array keeps the current ones.  Lets a caller use
+ * fresh tensors every step instead of fixed buffers, and a plan created without gradient pointers
+ * gain them.  Uploads the tensor records on `stream`; later operations on that stream use the new
+ * arrays.  The arrays must not overlap theta, theta0, the simulated buffer, each other or bound
+ * optimizer moments, and must stay valid until the operations that read them have run.
+ * Errors: SMAT_ERR_INVALID (both NULL, a null entry, overlap), SMAT_ERR_STATE (no workspace),
+ * SMAT_ERR_HIP. */
+smat_status smat_plan_set_grads(smat_plan* plan, const void* const* grad_sims, float* const* grad_thetas,
+                                hipStream_t stream);
 
 /* smat_adamw_fused_multi -- smat_adamw_fused over every tensor of the plan in one launch: theta is
  * desc.theta (the expert storage, updated in place), grad_sim is desc.grad_sim and, when accumulate
  * is nonzero, grad_acc is desc.grad_theta (read, not written); grad_scale_dev as in
  * smat_adamw_fused.  Allowed only while the expert storage is active (the optimizer never sees the
  * simulated buffer).  Errors: SMAT_ERR_INVALID, SMAT_ERR_STATE (no workspace, params or optimizer
- * state, or simulated storage active), SMAT_ERR_HIP. */
+ * state, gradient arrays not set, or simulated storage active), SMAT_ERR_HIP. */
 smat_status smat_adamw_fused_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda, smat_adamw_params hp,
                                    int32_t accumulate, const float* grad_scale_dev, hipStream_t stream);
 
@@ -278,7 +283,8 @@ smat_status smat_adamw_fused_multi(smat_plan* plan, uint64_t seed, uint32_t step
  * At least one output must be given.  Per-chunk fp32 partial sums (in the plan's workspace) are
  * added in fp64 in a fixed order: the result is the same on every call.  Any storage may be active.
  * Norm calls on one plan share those partials: calls that overlap (on different streams) race.
- * Errors: SMAT_ERR_INVALID, SMAT_ERR_STATE (no workspace or params), SMAT_ERR_HIP. */
+ * Errors: SMAT_ERR_INVALID, SMAT_ERR_STATE (no workspace or params, gradient arrays not set),
+ * SMAT_ERR_HIP. */
 smat_status smat_grad_norm_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda, int32_t accumulate,
                                  float max_norm, double* sumsq, float* clip_coef, hipStream_t stream);
 

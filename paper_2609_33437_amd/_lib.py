@@ -27,7 +27,7 @@ EXPORTS = (
     "smat_switch_storage", "smat_plan_state", "smat_plan_active_ptrs", "smat_plan_destroy", "smat_last_error",
     "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi", "smat_grad_norm_multi",
     "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
-    "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grad_sim",
+    "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
 )
 
 
@@ -102,7 +102,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_merge_plan_bind_workspace": [P, P, c_size_t, P],
         "smat_merge_multi": [P, POINTER(smat_merge_term), P],
         "smat_merge_plan_destroy": [P],
-        "smat_plan_set_grad_sim": [P, POINTER(P), P],
+        "smat_plan_set_grads": [P, POINTER(P), POINTER(P), P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -298,17 +298,26 @@ class Plan:
     def backward_accum(self, seed: int, step: int, lam: float, stream=None) -> None:
         _check(lib().smat_backward_accum_multi(self._plan, int(seed), int(step), float(lam), _stream_handle(stream)))
 
-    def set_grad_sim(self, grad_sims: Sequence, stream=None) -> None:
-        """Point the plan at new gradient-at-theta~ tensors (smat_plan_set_grad_sim); holds them until
-        the next call."""
-        if len(grad_sims) != self.count:
-            raise SmatError(SMAT_ERR_INVALID, "one gradient per tensor")
-        for g, t in zip(grad_sims, self._refs[0]):
-            if g.numel() != t.numel() or dtype_code(g) != self.dtypes[2]:
-                raise SmatError(SMAT_ERR_INVALID, "gradients must match the plan's sizes and gradient dtype")
-        arr = (c_void_p * max(self.count, 1))(*[_dev_ptr(g, "grad_sim") for g in grad_sims])
-        _check(lib().smat_plan_set_grad_sim(self._plan, arr, _stream_handle(stream)))
-        self._grad_sim_refs = list(grad_sims)
+    def set_grads(self, grad_sims: Optional[Sequence] = None, grad_thetas: Optional[Sequence] = None,
+                  stream=None) -> None:
+        """Point the plan at new gradient tensors (smat_plan_set_grads); None keeps that kind as it
+        is.  Holds the tensors until they are replaced."""
+        arrays = []
+        for ts, what, dt in ((grad_sims, "grad_sim", self.dtypes[2]), (grad_thetas, "grad_theta", SMAT_F32)):
+            if ts is None:
+                arrays.append(None)
+                continue
+            if len(ts) != self.count:
+                raise SmatError(SMAT_ERR_INVALID, f"one {what} per tensor")
+            for g, th in zip(ts, self._refs[0]):
+                if g.numel() != th.numel() or dtype_code(g) != dt:
+                    raise SmatError(SMAT_ERR_INVALID, f"{what} must match the plan's sizes and dtype")
+            arrays.append((c_void_p * max(self.count, 1))(*[_dev_ptr(g, what) for g in ts]))
+        _check(lib().smat_plan_set_grads(self._plan, arrays[0], arrays[1], _stream_handle(stream)))
+        if grad_sims is not None:
+            self._refs[3] = list(grad_sims)
+        if grad_thetas is not None:
+            self._refs[4] = list(grad_thetas)
 
     def bind_adam_state(self, exp_avgs: Sequence, exp_avg_sqs: Sequence, stream=None) -> None:
         if len(exp_avgs) != self.count or len(exp_avg_sqs) != self.count:

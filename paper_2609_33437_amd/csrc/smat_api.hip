@@ -108,6 +108,27 @@ smat_status check_simulate_ptrs(const float* theta, const void* theta0, int t0_d
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Gradient arrays of one plan tensor (either may be absent) must not overlap each other, theta,
+// theta0, the simulated buffer or the optimizer moments.
+smat_status check_grad_ptrs(const float* theta, const void* theta0, int t0_dt, const void* out, int out_dt,
+                            const void* grad_sim, int g_dt, const float* grad_theta, const float* m1, const float* m2,
+                            int64_t n, const char* where) {
+  const size_t nb = (size_t)n;
+  const void* fixed[5] = {theta, theta0, out, m1, m2};
+  const size_t fsz[5] = {nb * 4, nb * dtype_bytes(t0_dt), nb * dtype_bytes(out_dt), nb * 4, nb * 4};
+  const void* grads[2] = {grad_sim, grad_theta};
+  const size_t gsz[2] = {nb * dtype_bytes(g_dt), nb * 4};
+  for (int g = 0; g < 2; ++g) {
+    if (!grads[g]) continue;
+    for (int f = 0; f < 5; ++f)
+      if (fixed[f] && overlap(grads[g], gsz[g], fixed[f], fsz[f]))
+        return fail(SMAT_ERR_INVALID, "%s: a gradient array overlaps theta, theta0, the buffer or a moment", where);
+  }
+  if (grad_sim && grad_theta && overlap(grad_sim, gsz[0], grad_theta, gsz[1]))
+    return fail(SMAT_ERR_INVALID, "%s: grad_sim must not overlap grad_theta", where);
+  return SMAT_OK;
+}
+
 // Per-call constants of the fused optimizer step, formed in fp64 and rounded once to fp32.
 smat_status make_adam(const smat_adamw_params& hp, AdamConsts* A, const char* where) {
   if (!std::isfinite(hp.lr) || !std::isfinite(hp.beta1) || !std::isfinite(hp.beta2) || !std::isfinite(hp.eps) ||
@@ -143,7 +164,7 @@ uint32_t adam_flags(const float* theta, const float* m1, const float* m2, const 
 // theta, the two moments, grad_sim and (if given) grad_acc must be pairwise disjoint.
 smat_status check_adam_ptrs(const float* theta, const float* m1, const float* m2, const void* grad_sim, int g_dt,
                             const float* grad_acc, int64_t n, const char* where) {
-  if (!theta || !m1 || !m2 || !grad_sim) return fail(SMAT_ERR_INVALID, "%s: null pointer with n > 0", where);
+  if (!theta || !m1 || !m2) return fail(SMAT_ERR_INVALID, "%s: null pointer with n > 0", where);
   const size_t nb = (size_t)n;
   const void* ptr[5] = {theta, m1, m2, grad_sim, grad_acc};
   const size_t sz[5] = {nb * 4, nb * 4, nb * 4, nb * dtype_bytes(g_dt), nb * 4};
@@ -244,6 +265,7 @@ extern "C" smat_status smat_adamw_fused(const void* grad_sim, smat_dtype grad_dt
     return fail(SMAT_ERR_INVALID, "smat_adamw_fused: elem_offset + n overflows");
   if ((n + smat::tile_elems(1) - 1) / smat::tile_elems(1) > 0x7FFFFFFF)
     return fail(SMAT_ERR_INVALID, "smat_adamw_fused: n too large");
+  if (!grad_sim) return fail(SMAT_ERR_INVALID, "smat_adamw_fused: null grad_sim with n > 0");
   st = check_adam_ptrs(theta, exp_avg, exp_avg_sq, grad_sim, grad_dtype, grad_acc, n, "smat_adamw_fused");
   if (st != SMAT_OK) return st;
   TensorRec rec{};
@@ -265,7 +287,7 @@ struct smat_plan {
   int32_t count = 0;
   int t0_dt = 0, out_dt = 0, g_dt = 0;
   bool offload = false;
-  bool has_grads = false;
+  bool has_gs = false, has_gt = false;  // gradient arrays (grad_sim, grad_theta) known for every tensor
   std::vector<smat_tensor_desc> descs;
   std::vector<TensorRec> recs;
   std::vector<uint2> chunks;  // (tensor index, chunk index within the tensor)
@@ -356,7 +378,7 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
   p->g_dt = grad_dtype;
   p->offload = offload != 0;
   p->descs.assign(descs, descs + count);
-  p->has_grads = true;
+  int gs_seen = -1, gt_seen = -1;  // whether the tensors so far give each gradient kind (-1: no tensor yet)
 
   std::vector<std::pair<uint32_t, std::pair<uint64_t, uint64_t>>> ranges;
   for (int32_t i = 0; i < count; ++i) {
@@ -373,12 +395,14 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
     else if (d.n > 0)
       st = check_simulate_ptrs(d.theta, p->offload ? d.out : d.theta0, theta0_dtype, d.out, out_dtype, d.n, where);
     if (st == SMAT_OK && d.n > 0) {
-      if (!d.grad_sim || !d.grad_theta) {
-        if (d.grad_sim || d.grad_theta) st = fail(SMAT_ERR_INVALID, "%s: give both gradient pointers or neither", where);
-        p->has_grads = false;
-      } else if (overlap(d.grad_sim, (size_t)d.n * dtype_bytes(grad_dtype), d.grad_theta, (size_t)d.n * 4)) {
-        st = fail(SMAT_ERR_INVALID, "%s: grad_sim must not overlap grad_theta", where);
-      }
+      const int gs = d.grad_sim != nullptr, gt = d.grad_theta != nullptr;
+      if ((gs_seen >= 0 && gs != gs_seen) || (gt_seen >= 0 && gt != gt_seen))
+        st = fail(SMAT_ERR_INVALID, "%s: give each gradient pointer for every tensor or for none", where);
+      else
+        st = check_grad_ptrs(d.theta, p->offload ? d.out : d.theta0, theta0_dtype, d.out, out_dtype, d.grad_sim,
+                             grad_dtype, d.grad_theta, nullptr, nullptr, d.n, where);
+      gs_seen = gs;
+      gt_seen = gt;
     }
     if (st != SMAT_OK) {
       delete p;
@@ -397,6 +421,8 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
     }
   }
 
+  p->has_gs = gs_seen != 0;  // vacuously true for a list of empty tensors
+  p->has_gt = gt_seen != 0;
   p->recs.resize(count);
   p->expert_ptrs.resize(count);
   p->sim_ptrs.resize(count);
@@ -414,7 +440,7 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
     r.tensor_id = d.tensor_id;
     if (d.n > 0) {
       r.sflags = sim_flags(r.theta, r.theta0, theta0_dtype, r.out, out_dtype, d.elem_offset);
-      if (d.grad_sim && d.grad_theta) r.sflags |= bwd_flags(d.grad_sim, grad_dtype, d.grad_theta, d.elem_offset);
+      if (d.grad_sim) r.sflags |= bwd_flags(d.grad_sim, grad_dtype, d.grad_theta, d.elem_offset);
     }
     p->expert_ptrs[i] = const_cast<float*>(d.theta);
     p->sim_ptrs[i] = d.out;
@@ -535,7 +561,8 @@ extern "C" smat_status smat_backward_accum_multi(smat_plan* p, uint64_t seed, ui
   if (!p) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: null plan");
   if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: step must be < 2^30");
   if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: lambda must be finite");
-  if (!p->has_grads) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: plan has no gradient pointers");
+  if (!p->has_gs || !p->has_gt)
+    return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: gradient arrays not set (smat_plan_set_grads)");
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: no workspace bound");
   if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: parameters never set");
   if (!p->chunks.empty())
@@ -549,7 +576,6 @@ extern "C" smat_status smat_backward_accum_multi(smat_plan* p, uint64_t seed, ui
 extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_state* per_tensor, hipStream_t stream) {
   if (!p || (p->count > 0 && !per_tensor)) return fail(SMAT_ERR_INVALID, "smat_plan_bind_adam_state: null argument");
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_bind_adam_state: no workspace bound");
-  if (!p->has_grads) return fail(SMAT_ERR_INVALID, "smat_plan_bind_adam_state: plan has no gradient pointers");
   std::vector<AdamRec> adam(p->count);
   std::vector<TensorRec> recs = p->recs;
   for (int32_t i = 0; i < p->count; ++i) {
@@ -588,25 +614,30 @@ extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_s
   return SMAT_OK;
 }
 
-extern "C" smat_status smat_plan_set_grad_sim(smat_plan* p, const void* const* grad_sims, hipStream_t stream) {
-  if (!p || (p->count > 0 && !grad_sims)) return fail(SMAT_ERR_INVALID, "smat_plan_set_grad_sim: null argument");
-  if (!p->has_grads) return fail(SMAT_ERR_INVALID, "smat_plan_set_grad_sim: plan has no gradient pointers");
-  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_set_grad_sim: no workspace bound");
+extern "C" smat_status smat_plan_set_grads(smat_plan* p, const void* const* grad_sims, float* const* grad_thetas,
+                                           hipStream_t stream) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_plan_set_grads: null plan");
+  if (!grad_sims && !grad_thetas) return fail(SMAT_ERR_INVALID, "smat_plan_set_grads: nothing to set");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_set_grads: no workspace bound");
   std::vector<TensorRec> recs = p->recs;
   for (int32_t i = 0; i < p->count; ++i) {
     TensorRec& r = recs[i];
     if (r.n == 0) continue;
-    const void* g = grad_sims[i];
-    const size_t gb = (size_t)r.n * dtype_bytes(p->g_dt);
-    if (!g) return fail(SMAT_ERR_INVALID, "smat_plan_set_grad_sim: tensor %d: null grad_sim", i);
-    if (overlap(g, gb, r.grad_theta, (size_t)r.n * 4) || overlap(g, gb, r.out, (size_t)r.n * dtype_bytes(p->out_dt)) ||
-        overlap(g, gb, r.theta, (size_t)r.n * 4))
-      return fail(SMAT_ERR_INVALID, "smat_plan_set_grad_sim: tensor %d: grad_sim overlaps theta, out or grad_theta", i);
-    r.grad_sim = g;
-    r.sflags = (r.sflags & ~smat::kVecBwd) | bwd_flags(g, p->g_dt, r.grad_theta, r.elem_offset);
+    char where[64];
+    std::snprintf(where, sizeof(where), "smat_plan_set_grads: tensor %d", i);
+    const void* gs = grad_sims ? grad_sims[i] : r.grad_sim;
+    float* gt = grad_thetas ? grad_thetas[i] : r.grad_theta;
+    if ((grad_sims && !gs) || (grad_thetas && !gt)) return fail(SMAT_ERR_INVALID, "%s: null gradient pointer", where);
+    smat_status st = check_grad_ptrs(r.theta, r.theta0, p->t0_dt, r.out, p->out_dt, gs, p->g_dt, gt,
+                                     p->adam_bound ? p->adam[i].exp_avg : nullptr,
+                                     p->adam_bound ? p->adam[i].exp_avg_sq : nullptr, r.n, where);
+    if (st != SMAT_OK) return st;
+    r.grad_sim = gs;
+    r.grad_theta = gt;
+    r.sflags &= ~(smat::kVecBwd | smat::kVecAdam | smat::kVecAdamAcc);
+    if (gs) r.sflags |= bwd_flags(gs, p->g_dt, gt, r.elem_offset);
     if (p->adam_bound)
-      r.sflags = (r.sflags & ~(smat::kVecAdam | smat::kVecAdamAcc)) |
-                 adam_flags(r.theta, p->adam[i].exp_avg, p->adam[i].exp_avg_sq, g, p->g_dt, r.grad_theta, r.elem_offset);
+      r.sflags |= adam_flags(r.theta, p->adam[i].exp_avg, p->adam[i].exp_avg_sq, gs, p->g_dt, gt, r.elem_offset);
   }
   const size_t rec_bytes = sizeof(TensorRec) * p->count, adam_bytes = sizeof(AdamRec) * p->count;
   if (!p->adam_staging) {
@@ -619,8 +650,13 @@ extern "C" smat_status smat_plan_set_grad_sim(smat_plan* p, const void* const* g
   if (p->count > 0)
     SMAT_HIP(hipMemcpyAsync(p->ws + p->off_recs, p->adam_staging, rec_bytes, hipMemcpyHostToDevice, stream));
   SMAT_HIP(hipEventRecord(p->ev_adam, stream));
-  for (int32_t i = 0; i < p->count; ++i) p->descs[i].grad_sim = recs[i].grad_sim;
+  for (int32_t i = 0; i < p->count; ++i) {
+    p->descs[i].grad_sim = recs[i].grad_sim;
+    p->descs[i].grad_theta = recs[i].grad_theta;
+  }
   p->recs = recs;
+  if (grad_sims) p->has_gs = true;
+  if (grad_thetas) p->has_gt = true;
   return SMAT_OK;
 }
 
@@ -636,6 +672,8 @@ extern "C" smat_status smat_adamw_fused_multi(smat_plan* p, uint64_t seed, uint3
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: no workspace bound");
   if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: parameters never set");
   if (!p->adam_bound) return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: optimizer state never bound");
+  if (!p->has_gs || (accumulate && !p->has_gt))
+    return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: gradient arrays not set (smat_plan_set_grads)");
   if (p->state != SMAT_EXPERT)
     return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi: restore the expert storage before the optimizer step");
   if (!p->chunks.empty())
@@ -657,7 +695,8 @@ extern "C" smat_status smat_grad_norm_multi(smat_plan* p, uint64_t seed, uint32_
   if (!sumsq && !clip_coef) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: no output");
   if (clip_coef && !(std::isfinite(max_norm) && max_norm > 0.f))
     return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: max_norm must be finite and > 0");
-  if (!p->has_grads) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi: plan has no gradient pointers");
+  if (!p->has_gs || (accumulate && !p->has_gt))
+    return fail(SMAT_ERR_STATE, "smat_grad_norm_multi: gradient arrays not set (smat_plan_set_grads)");
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_grad_norm_multi: no workspace bound");
   if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_grad_norm_multi: parameters never set");
   SMAT_HIP(smat::launch_sqnorm_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),

@@ -7,7 +7,7 @@ Each step computes one loss with one forward and one backward pass.  On a simula
    writes theta~ = theta0 + alpha m (.) (theta - theta0) + eps into one reusable buffer per
    parameter (smat_simulate_multi), and rebinds each parameter's `.data` to its buffer.  The
    model's forward and backward then run on theta~; autograd's gradient tensors at theta~ are
-   handed to the library as they are (smat_plan_set_grad_sim), with no copy.
+   handed to the library as they are (smat_plan_set_grads), with no copy.
 2. `end(optimizer)` turns that gradient into the expert gradient lambda alpha m (.) g~
    (Eq. smat-gradient), with the mask regenerated (smat_backward_accum_multi).  It then rebinds
    `.data` to the expert storage, so that the optimizer, weight decay included, only sees the fp32
@@ -144,18 +144,17 @@ class SimulatedMergeTraining:
             raise SmatError(SMAT_ERR_INVALID, "one sigma per parameter")
         self.alpha_min, self.period, self.lam, self.seed = float(alpha_min), int(period), float(lam), int(seed)
         self.noise_kind, self.rescale, self.offload = int(noise_kind), 1 if rescale else 0, bool(offload)
+        # the only resident state: one buffer per parameter (plus theta0 unless offloaded).  Gradient
+        # arrays are the step's own tensors, handed to the plan when they exist.
         self.buffers = [torch.empty(p.shape, dtype=buffer_dtype, device=dev) for p in self.params]
-        self.grad_sim = [torch.zeros_like(b) for b in self.buffers]
-        self.grad_theta = [torch.zeros_like(m) for m in self.master]
         dt = _lib.dtype_code(self.buffers[0])
         if self.offload:
             self.theta0_host = [t.detach().to("cpu", dtype=buffer_dtype).contiguous().pin_memory() for t in theta0]
-            self.plan = Plan(self.master, self.buffers, None, self.grad_sim, self.grad_theta, offload=True,
-                             theta0_hosts=self.theta0_host, dtypes=(dt, dt, dt))
+            self.plan = Plan(self.master, self.buffers, None, offload=True, theta0_hosts=self.theta0_host,
+                             dtypes=(dt, dt, dt))
         else:
             self.theta0 = [t.detach().to(device=dev, dtype=buffer_dtype).contiguous() for t in theta0]
-            self.plan = Plan(self.master, self.buffers, self.theta0, self.grad_sim, self.grad_theta,
-                             dtypes=(dt, dt, dt))
+            self.plan = Plan(self.master, self.buffers, self.theta0, dtypes=(dt, dt, dt))
         self._rng = np.random.default_rng(self.seed)
         self.alpha: Optional[float] = None      # the scale of the current (or last) simulated step
         self._step: Optional[int] = None        # set between begin() and end()
@@ -207,19 +206,17 @@ class SimulatedMergeTraining:
         self._step = int(step)
         return True
 
-    def _collect_grad_sim(self) -> None:
-        """Hand the plan the gradients at theta~ that autograd left in p.grad."""
+    def _grads_at_theta_tilde(self) -> List[torch.Tensor]:
+        """The gradients at theta~ that autograd left in p.grad (zeros for unused parameters)."""
         grads = []
-        for i, (p, b) in enumerate(zip(self.params, self.buffers)):
+        for p, b in zip(self.params, self.buffers):
             g = p.grad
             if g is None:                            # the parameter took no part in the loss
-                g = self.grad_sim[i]
-                g.zero_()
+                g = torch.zeros_like(b)
             elif not g.is_contiguous() or g.dtype != b.dtype:
                 g = g.to(dtype=b.dtype, memory_format=torch.contiguous_format)
             grads.append(g)
-        self.plan.set_grad_sim(grads)
-        self._grads = grads     # kept alive until the kernels that read them have been queued
+        return grads
 
     def _restore(self) -> None:
         self.plan.switch_storage(SMAT_EXPERT)
@@ -243,7 +240,7 @@ class SimulatedMergeTraining:
         if max_norm is not None and not fused:
             raise SmatError(SMAT_ERR_INVALID, "max_norm applies to the fused update; clip param.grad otherwise")
         step = self._step
-        self._collect_grad_sim()
+        grads = self._grads_at_theta_tilde()
         if fused:
             if optimizer is None:
                 raise SmatError(SMAT_ERR_INVALID, "the fused update needs the optimizer that owns the moments")
@@ -253,11 +250,16 @@ class SimulatedMergeTraining:
                 raise SmatError(SMAT_ERR_INVALID, "the optimizer holds parameters outside the wrapper that have "
                                                   "gradients; the fused update would skip them")
             self._restore()
+            self.plan.set_grads(grads, None)
+            self._grads = grads     # kept alive until the kernels that read them have been queued
             return self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step, max_norm)
-        torch._foreach_zero_(self.grad_theta)
+        # the expert gradient lands in fresh fp32 tensors, as an ordinary step's gradients do
+        expert = [torch.zeros_like(m) for m in self.master]
+        self.plan.set_grads(grads, expert)
+        self._grads = grads
         self.plan.backward_accum(self.seed, step, self.lam)
         self._restore()
-        for p, g in zip(self.params, self.grad_theta):
+        for p, g in zip(self.params, expert):
             p.grad = g
         return None
 

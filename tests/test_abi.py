@@ -133,7 +133,10 @@ def test_plan_create_validation_without_gpu():
     overlapping = [_desc(1 * A, 2 * A, 3 * A, 4 * A, 5 * A, 1000, 7, 0), _desc(6 * A, 7 * A, 8 * A, 9 * A, 10 * A, 5, 7, 999)]
     assert plan(overlapping) == _lib.SMAT_ERR_INVALID
     assert plan([_desc(1 * A, 1 * A, 3 * A, None, None, 10, 0)]) == _lib.SMAT_ERR_INVALID        # out over theta
-    assert plan([_desc(1 * A, 2 * A, 3 * A, 4 * A, None, 10, 0)]) == _lib.SMAT_ERR_INVALID       # half the grads
+    assert plan([_desc(1 * A, 2 * A, 3 * A, 4 * A, None, 10, 0)]) == _lib.SMAT_OK                # grad_sim only
+    mixed = [_desc(1 * A, 2 * A, 3 * A, 4 * A, 5 * A, 10, 0), _desc(6 * A, 7 * A, 8 * A, None, None, 10, 1)]
+    assert plan(mixed) == _lib.SMAT_ERR_INVALID                                                   # some tensors only
+    assert plan([_desc(1 * A, 2 * A, 3 * A, 1 * A + 8, None, 10, 0)]) == _lib.SMAT_ERR_INVALID   # grad over theta
     assert plan(good, dts=(1, 1, 5)) == _lib.SMAT_ERR_DTYPE
     assert plan(good, offload=1) == _lib.SMAT_ERR_INVALID                                         # no host copy
     assert plan([_desc(1 * A, 2 * A, None, None, None, 10, 0, 0, 11 * A)], offload=1) == _lib.SMAT_OK
@@ -147,8 +150,8 @@ def test_plan_create_validation_without_gpu():
     assert lib.smat_simulate_multi(p, 0, 0, None) == _lib.SMAT_ERR_STATE
     assert lib.smat_switch_storage(p, 1, None) == _lib.SMAT_ERR_STATE
     grads = (ctypes.c_void_p * 2)(ctypes.c_void_p(11 * A), ctypes.c_void_p(12 * A))
-    assert lib.smat_plan_set_grad_sim(p, grads, None) == _lib.SMAT_ERR_STATE          # no workspace yet
-    assert lib.smat_plan_set_grad_sim(p, None, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_plan_set_grads(p, grads, None, None) == _lib.SMAT_ERR_STATE        # no workspace yet
+    assert lib.smat_plan_set_grads(p, None, None, None) == _lib.SMAT_ERR_INVALID       # nothing to set
     assert lib.smat_switch_storage(p, 5, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_plan_destroy(p) == 0
     assert lib.smat_plan_destroy(None) == 0
@@ -195,10 +198,10 @@ def test_grad_norm_argument_errors_without_gpu():
     # a valid call on a plan without workspace is a state error and launches nothing
     assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 0, 1.0, out, None, None) == _lib.SMAT_ERR_STATE
     assert lib.smat_plan_destroy(plan) == 0
-    # a plan without gradient pointers has no norm to take
+    # a plan without gradient arrays has no norm to take until smat_plan_set_grads supplies them
     arr = (_lib.smat_tensor_desc * 1)(_desc(1 * A, 2 * A, 3 * A, None, None, 1000, 0))
     assert lib.smat_plan_create(arr, 1, 1, 1, 1, 0, ctypes.byref(plan)) == 0
-    assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 0, 1.0, out, None, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_grad_norm_multi(plan, 0, 0, 1.0, 0, 1.0, out, None, None) == _lib.SMAT_ERR_STATE
     assert lib.smat_plan_destroy(plan) == 0
 
 

@@ -307,36 +307,45 @@ def test_offload_periodic_training_cycle_matches_resident(mini):
         assert torch.equal(bits(b.cpu()), bits(h.view(-1)))
 
 
-def test_set_grad_sim_rebinds_the_gradient_arrays(mini):
-    """smat_plan_set_grad_sim points the backward and the fused step at new gradient tensors,
-    including ones whose alignment takes the element path, with results equal to a plan built on
-    them from the start."""
+def test_set_grads_rebinds_the_gradient_arrays(mini):
+    """smat_plan_set_grads points the backward at new gradient tensors, including ones whose
+    alignment takes the element path, with results equal to a plan built on them from the start; a
+    plan created without gradient arrays refuses the backward until they are set."""
     cfg, inp = mini
     th, t0, gs, gt, out = to_dev(inp)
     step = 5
     params = workloads.step_params(cfg, inp.settings, step)
     g = torch.Generator(DEV).manual_seed(3)
     # new gradients: every other one at an odd element offset inside a larger buffer (misaligned)
-    new = []
+    new, new_gt = [], []
     for i, x in enumerate(gs):
         buf = (torch.randn(x.numel() + 8, device=DEV, generator=g) * 1e-2).to(x.dtype)
         new.append(buf[1:1 + x.numel()] if i % 2 else buf[:x.numel()])
-    gt_a = [x.clone() for x in gt]
-    gt_b = [x.clone() for x in gt]
-    with smat.Plan(th, out, t0, gs, gt_a) as plan:
+        acc = torch.randn(x.numel() + 8, device=DEV, generator=g) * 1e-3
+        new_gt.append(acc[3:3 + x.numel()] if i % 3 == 0 else acc[:x.numel()])
+    gt_b = [x.clone() for x in new_gt]
+    with smat.Plan(th, out, t0, gs, gt) as plan:           # built on other arrays, then rebound
         plan.set_params(params)
-        plan.set_grad_sim(new)
+        plan.set_grads(new, None)
+        plan.set_grads(None, new_gt)
         plan.backward_accum(cfg.smat_seed, step, cfg.lam)
     with smat.Plan(th, out, t0, new, gt_b) as plan:
         plan.set_params(params)
         plan.backward_accum(cfg.smat_seed, step, cfg.lam)
+    with smat.Plan(th, out, t0) as plan:                    # no gradient arrays yet
+        plan.set_params(params)
+        with pytest.raises(smat.SmatError):
+            plan.backward_accum(cfg.smat_seed, step, cfg.lam)
+        plan.set_grads(new, [x.clone() for x in gt])
     torch.cuda.synchronize()
-    for a, b in zip(gt_a, gt_b):
+    for a, b in zip(new_gt, gt_b):
         assert torch.equal(a.view(torch.int32), b.view(torch.int32))
     with smat.Plan(th, out, t0, gs, gt) as plan:
         with pytest.raises(smat.SmatError):
-            plan.set_grad_sim(new[:-1])                           # one per tensor
+            plan.set_grads(new[:-1])                              # one per tensor
         with pytest.raises(smat.SmatError):
-            plan.set_grad_sim([x.float() for x in new])           # the plan's gradient dtype
+            plan.set_grads([x.float() for x in new])              # the plan's gradient dtype
         with pytest.raises(smat.SmatError):
-            plan.set_grad_sim([o for o in out])                   # overlaps the simulated buffer
+            plan.set_grads([o for o in out])                      # overlaps the simulated buffer
+        with pytest.raises(smat.SmatError):
+            plan.set_grads(None, [x.view(-1) for x in th])          # the expert storage itself
