@@ -90,8 +90,11 @@ def parse_args():
 
 def cpu_baseline(cfg, inp, params, step, max_elems, budget_s, torch, np):
     """The CPU oracle on a bounded sample of the same workload: a window of every tensor with size
-    proportional to the tensor, simulate (with its rounding) then backward, on one core, visited
-    in random order until `budget_s` seconds of work are done."""
+    proportional to the tensor, simulate (with its rounding) then backward, on a pool of threads
+    (one per host core; the oracle is vectorized NumPy, whose array loops run without the GIL).
+    Windows are visited in random order; no new window starts after `budget_s` seconds."""
+    import concurrent.futures as cf
+
     import oracle
 
     frac = min(1.0, max_elems / cfg.numel)
@@ -102,27 +105,62 @@ def cpu_baseline(cfg, inp, params, step, max_elems, budget_s, torch, np):
     def bits(x):
         return x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
 
-    done = tensors = 0
-    secs = 0.0
+    tasks = []
     for i in order:
         t = inp.theta[i]
         n = t.numel()
         m = max(1, int(round(n * frac)))
         a = int(rng.integers(0, n - m + 1))
         win = lambda x: x.view(-1)[a:a + m].cpu()
-        th, t0, gs, gt = win(t).numpy(), bits(win(inp.theta0[i])), bits(win(inp.grad_sim[i])), win(inp.grad_theta[i]).numpy()
-        start = time.perf_counter()
-        oracle.simulate(th, t0, t0_dt, out_dt, params[i], cfg.smat_seed, step, int(i), a)
-        oracle.backward_accum(gs, g_dt, gt, params[i], cfg.lam, cfg.smat_seed, step, int(i), a)
-        secs += time.perf_counter() - start
-        done += m
-        tensors += 1
-        if secs >= budget_s:
-            break
-    log(f"cpu oracle: {done} elements of {tensors} tensors in {secs:.1f} s")
-    return {"value": done / secs, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done} elements: windows of {100 * frac:.3f}% of {tensors} of the {cfg.count} tensors in "
-                      f"random order (simulate + backward, fp64 NumPy, one process), {secs:.1f} s of work"}
+        # windows above 2^20 elements are split so that the threads share the big tensors
+        for b in range(0, m, 1 << 20):
+            e = min(m, b + (1 << 20))
+            tasks.append((int(i), a + b, win(t)[b:e].numpy(), bits(win(inp.theta0[i])[b:e]),
+                          bits(win(inp.grad_sim[i])[b:e]), win(inp.grad_theta[i])[b:e].numpy()))
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    cores = max(1, min(cores, 16))
+    start = time.perf_counter()
+    deadline = start + budget_s
+
+    def run(task):
+        if time.perf_counter() >= deadline:
+            return 0
+        i, off, th, t0, gs, gt = task
+        oracle.simulate(th, t0, t0_dt, out_dt, params[i], cfg.smat_seed, step, i, off)
+        oracle.backward_accum(gs, g_dt, gt, params[i], cfg.lam, cfg.smat_seed, step, i, off)
+        return th.size
+
+    with cf.ThreadPoolExecutor(max_workers=cores) as pool:
+        done = sum(pool.map(run, tasks))
+    secs = time.perf_counter() - start
+    log(f"cpu oracle: {done} elements in {secs:.1f} s on {cores} threads")
+    return {"value": done / secs, "unit": "params/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} elements: windows of {100 * frac:.3f}% of the {cfg.count} tensors in random order "
+                      f"(simulate + backward, fp64 NumPy, {cores} threads), {secs:.1f} s wall"}
+
+
+def timed_copy(nbytes_step: int, torch, smat, reps: int = 5) -> dict:
+    """The library's plain streaming copy (smat_stream_copy) moving the same bytes as one step:
+    nbytes_step / 2 read and nbytes_step / 2 written, timed with HIP events."""
+    n = nbytes_step // 8 // 4 * 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    smat.smat_stream_copy(src, dst)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        smat.smat_stream_copy(src, dst)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    assert bool(dst[-1] == 1.0)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes": 8 * n, "ms": round(ms, 4), "gbps": round(8 * n / (ms * 1e6), 1)}
 
 
 # rocprofv3 passes behind profiles/.  Run from /tmp with TMPDIR=/tmp; $REPO is the repository root and
@@ -142,6 +180,16 @@ MERGE_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d $REPO/rocprof/mer
                    "python3 $REPO/bench.py --merge --steps 10 --warmup 2")
 MERGE_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d $REPO/rocprof/merge_{tag} -o c4 --kernel-include-regex "
                  "'k_merge_multi' -- python3 $REPO/bench.py --merge --steps 2 --warmup 1")
+VALU_CMDS = {  # VALU activity of every kernel of ours, one counter pass per benchmark mode
+    "valu_main": "rocprofv3 --pmc VALUBusy SQ_INSTS_VALU -f csv -d $REPO/rocprof/valu_main -o c4 "
+                 "--kernel-include-regex 'k_simulate_multi|k_backward_multi' -- "
+                 "python3 $REPO/bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+    "valu_opt": "rocprofv3 --pmc VALUBusy SQ_INSTS_VALU -f csv -d $REPO/rocprof/valu_opt -o c4 "
+                "--kernel-include-regex 'k_adamw_multi|k_sqnorm_multi' -- "
+                "python3 $REPO/bench.py --adamw --steps 2 --warmup 1 --no-cpu-baseline",
+    "valu_merge": "rocprofv3 --pmc VALUBusy SQ_INSTS_VALU -f csv -d $REPO/rocprof/valu_merge -o c4 "
+                  "--kernel-include-regex 'k_merge_multi' -- python3 $REPO/bench.py --merge --steps 2 --warmup 1",
+}
 COPY_GRID = 1 << 26   # threads of the calibration copy (2^28 fp32 values, 4 per thread)
 COPY_BYTES = 1 << 30  # read and written by one calibration dispatch
 
@@ -219,7 +267,52 @@ def summarize(root: str) -> int:
         summarize_optimizer(root, out_dir, fetch_factor, write_factor)
     if os.path.isdir(os.path.join(root, "merge_trace")):
         summarize_merge(root, out_dir, fetch_factor, write_factor)
+    if all(os.path.isdir(os.path.join(root, d)) for d in VALU_CMDS):
+        summarize_valu(root, out_dir)
     return 0
+
+
+def summarize_valu(root: str, out_dir: str) -> None:
+    """profiles/valu_c4_7b.md: VALU activity of each kernel (rocprofv3 VALUBusy and SQ_INSTS_VALU),
+    which tells the HBM-bound streams from the ones whose random draws bound them."""
+    import csv
+    import statistics
+
+    P = 7504924672
+    rows = {}
+    for d in VALU_CMDS:
+        recs = list(csv.DictReader(open(os.path.join(root, d, "c4_counter_collection.csv"))))
+        recs.sort(key=lambda r: int(r["Dispatch_Id"]))
+        for r in recs:
+            name = r["Kernel_Name"]
+            if "k_merge_multi" in name:
+                # launch order: 3 Task Arithmetic merges, then 3 DARE merges
+                k = "merge"
+            else:
+                k = next(x for x in ("k_simulate_multi", "k_backward_multi", "k_adamw_multi", "k_sqnorm_multi")
+                         if x in name)
+            rows.setdefault((k, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+    label = {"k_simulate_multi": "simulate (mask + Gaussian noise draws)", "k_backward_multi": "backward (mask draws)",
+             "k_adamw_multi": "fused AdamW (mask draws)", "k_sqnorm_multi": "gradient norm (mask draws, 2 B/param)"}
+    md = ["# VALU activity of the kernels on the 7B-shaped list (c4), rocprofv3 counters", "",
+          "Commands (run from /tmp with TMPDIR=/tmp; $REPO is the repository root):", ""]
+    md += [f"* `{c}`" for c in VALU_CMDS.values()]
+    md += ["", "VALUBusy = 100 * sum(SQ_ACTIVE_INST_VALU) / CU_NUM / GRBM_GUI_ACTIVE (rocprofv3's own expression); "
+           "SQ_INSTS_VALU counts wave-level VALU instructions, divided here by the parameters a launch covers.  "
+           "Medians over the dispatches of each kernel.", "",
+           "| kernel | dispatches | VALUBusy | VALU instructions per parameter (wave-level) |", "|---|---|---|---|"]
+    for k in ("k_simulate_multi", "k_backward_multi", "k_adamw_multi", "k_sqnorm_multi"):
+        vb, vi = rows.get((k, "VALUBusy"), []), rows.get((k, "SQ_INSTS_VALU"), [])
+        if vb:
+            md.append(f"| {label[k]} | {len(vb)} | {statistics.median(vb):.1f} | {statistics.median(vi) / P:.4f} |")
+    vb, vi = rows.get(("merge", "VALUBusy"), []), rows.get(("merge", "SQ_INSTS_VALU"), [])
+    for name, sl in (("merge, Task Arithmetic (7 experts, no draws)", slice(0, 3)),
+                     ("merge, DARE + Task Arithmetic (7 mask draws per quad)", slice(3, 6))):
+        if len(vb) >= 6:
+            md.append(f"| {name} | 3 | {statistics.median(vb[sl]):.1f} | {statistics.median(vi[sl]) / P:.4f} |")
+    with open(os.path.join(out_dir, "valu_c4_7b.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+    print("\n".join(md))
 
 
 def summarize_merge(root: str, out_dir: str, fetch_factor: float, write_factor: float) -> None:
@@ -675,6 +768,9 @@ def main() -> int:
     cfg = workloads.config(args.config)
     dt = {"bf16": torch.bfloat16, "f32": torch.float32}
     nbytes = {"bf16": 2, "f32": 4}
+    step_bytes = cfg.numel * (4 + nbytes[cfg.theta0_dtype] + nbytes[cfg.out_dtype] + nbytes[cfg.grad_dtype] + 8)
+    copy = timed_copy(step_bytes, torch, smat)   # before the inputs exist, so both fit in HBM
+    log(f"plain copy of {copy['bytes'] / 1e9:.1f} GB: {copy['ms']:.3f} ms = {copy['gbps']:.0f} GB/s")
     log(f"generating {cfg.name}: {cfg.count} tensors, {cfg.numel} params")
     t_gen = time.perf_counter()
     inp = workloads.make_inputs(cfg, device="cuda")
@@ -750,6 +846,7 @@ def main() -> int:
     sim_ms = [e[0].elapsed_time(e[1]) for e in evs]
     bwd_ms = [e[2].elapsed_time(e[3]) for e in evs]
     sim_avg, bwd_avg = sum(sim_ms) / K, sum(bwd_ms) / K
+    med = lambda v: sorted(v)[len(v) // 2]
     log(f"step {ms_step:.3f} ms  simulate {sim_avg:.3f} ms  backward {bwd_avg:.3f} ms")
 
     P = cfg.numel
@@ -796,8 +893,15 @@ def main() -> int:
                    "bytes_per_param_per_step": (sim_bytes + bwd_bytes) / P, "period": cfg.period},
         "hbm_gbps": round(step_gbps, 1),
         "hbm_frac_of_peak": round(step_gbps / PEAK_HBM_GBPS, 4),
-        "kernels": {"simulate": {"avg_ms": round(sim_avg, 4), "gbps": round(sim_gbps, 1)},
-                    "backward": {"avg_ms": round(bwd_avg, 4), "gbps": round(bwd_gbps, 1)}},
+        "kernels": {"simulate": {"avg_ms": round(sim_avg, 4), "median_ms": round(med(sim_ms), 4),
+                                 "min_ms": round(min(sim_ms), 4), "gbps": round(sim_gbps, 1),
+                                 "frac_of_copy": round(sim_gbps / copy["gbps"], 4)},
+                    "backward": {"avg_ms": round(bwd_avg, 4), "median_ms": round(med(bwd_ms), 4),
+                                 "min_ms": round(min(bwd_ms), 4), "gbps": round(bwd_gbps, 1),
+                                 "frac_of_copy": round(bwd_gbps / copy["gbps"], 4)}},
+        "copy": dict(copy, kernel="smat_stream_copy (plain nontemporal copy), same bytes as one step",
+                     frac_of_peak=round(copy["gbps"] / PEAK_HBM_GBPS, 4)),
+        "hbm_frac_of_copy": round(step_gbps / copy["gbps"], 4),
         "roofline": roofline,
         "cpu_baseline": None,
     }

@@ -379,6 +379,13 @@ smat_status smat_merge_multi(smat_merge_plan* plan, const smat_merge_term* terms
  * no-op. */
 smat_status smat_merge_plan_destroy(smat_merge_plan* plan);
 
+/* smat_stream_copy -- a plain device copy of `bytes` from src to dst, built like the library's
+ * kernels (one-wave blocks, 16-byte nontemporal accesses).  Not part of the method: the benchmark
+ * times it to state what fraction of the achievable HBM stream rate each kernel reaches.  Pointers
+ * and size must be multiples of 16 bytes and the ranges must not overlap.  Errors:
+ * SMAT_ERR_INVALID, SMAT_ERR_HIP. */
+smat_status smat_stream_copy(const void* src, void* dst, uint64_t bytes, hipStream_t stream);
+
 /* smat_last_error -- message of the last failure on the calling thread ("" if none). */
 const char* smat_last_error(void);
 

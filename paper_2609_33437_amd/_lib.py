@@ -28,6 +28,7 @@ EXPORTS = (
     "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi", "smat_grad_norm_multi",
     "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
     "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
+    "smat_stream_copy",
 )
 
 
@@ -103,6 +104,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_merge_multi": [P, POINTER(smat_merge_term), P],
         "smat_merge_plan_destroy": [P],
         "smat_plan_set_grads": [P, POINTER(P), POINTER(P), P],
+        "smat_stream_copy": [P, P, c_uint64, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -478,3 +480,11 @@ class MergePlan:
 
     def __exit__(self, *exc):
         self.close()
+
+
+def smat_stream_copy(src, dst, stream=None) -> None:
+    """Plain streaming copy src -> dst (same byte size, GPU tensors; the HBM reference)."""
+    nb = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nb:
+        raise SmatError(SMAT_ERR_INVALID, "src and dst differ in size")
+    _check(lib().smat_stream_copy(_dev_ptr(src, "src"), _dev_ptr(dst, "dst"), nb, _stream_handle(stream)))

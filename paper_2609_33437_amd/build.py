@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsmat.so")
-SOURCES = ["smat_kernels.hip", "smat_optim.hip", "smat_merge.hip", "smat_api.hip"]
+SOURCES = ["smat_kernels.hip", "smat_optim.hip", "smat_merge.hip", "smat_copy.hip", "smat_api.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -58,6 +58,9 @@ hipError_t launch_merge_multi(const TensorRec* recs, const void* const* experts,
                               const uint2* chunks, uint32_t nchunks, int nexp, int expert_dtype, int theta0_dtype,
                               int out_dtype, hipStream_t stream);
 
+// Plain streaming copy of n16 16-byte vectors (the measured HBM reference).
+hipError_t launch_stream_copy(const void* src, void* dst, uint64_t n16, hipStream_t stream);
+
 hipError_t launch_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t elem_offset,
                               int64_t n, const ParamRec& prm, uint32_t* mask_words, uint32_t* noise_words,
                               uint8_t* kept, float* z, hipStream_t stream);

@@ -258,3 +258,13 @@ def test_merge_plan_validation_without_gpu():
     shards = [D(P(1 * A), P(2 * A), 1000, 7, 0, 0), D(P(3 * A), P(4 * A), 10, 7, 0, 1000)]
     assert create(shards, ptrs) == _lib.SMAT_OK
     assert lib.smat_merge_plan_destroy(None) == 0
+
+
+def test_stream_copy_argument_errors_without_gpu():
+    lib = smat.lib()
+    P = ctypes.c_void_p
+    assert lib.smat_stream_copy(P(1 << 20), P(2 << 20), 0, None) == _lib.SMAT_OK               # nothing to copy
+    assert lib.smat_stream_copy(None, P(2 << 20), 16, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_stream_copy(P((1 << 20) + 8), P(2 << 20), 16, None) == _lib.SMAT_ERR_INVALID  # misaligned
+    assert lib.smat_stream_copy(P(1 << 20), P(2 << 20), 24, None) == _lib.SMAT_ERR_INVALID       # size
+    assert lib.smat_stream_copy(P(1 << 20), P((1 << 20) + 16), 64, None) == _lib.SMAT_ERR_INVALID  # overlap

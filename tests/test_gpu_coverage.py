@@ -57,3 +57,16 @@ def test_list_every_element_once():
         torch.cuda.synchronize()
         assert torch.equal(t[2].float(), kept), f"tensor {i}: theta~"
         assert torch.equal(t[4], kept), f"tensor {i}: grad"
+
+
+@pytest.mark.parametrize("nbytes", [48, 4096 + 16, (1 << 20) + 48, (1 << 27) + 4080])
+def test_stream_copy(nbytes):
+    g = torch.Generator(DEV).manual_seed(nbytes % 1000)
+    src = torch.randint(0, 255, (nbytes,), dtype=torch.uint8, device=DEV, generator=g)
+    dst = torch.zeros(nbytes + 64, dtype=torch.uint8, device=DEV)
+    smat.smat_stream_copy(src, dst[:nbytes])
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:nbytes], src)
+    assert int(dst[nbytes:].sum()) == 0          # nothing written past the end
+    with pytest.raises(smat.SmatError):
+        smat.smat_stream_copy(src[1:33], dst[1:33])   # not 16-byte aligned
