@@ -16,6 +16,11 @@ Each step computes one loss with one forward and one backward pass.  On a simula
    own moment tensors (smat_adamw_fused_multi).  No gradient tensor is written, and the caller
    skips `optimizer.step()` for that step.
 
+A gradient already in p.grad when `begin` runs (the expert loss's backward in the same step) is
+kept, and the simulated-loss gradient is added to it: the objective (1 - lam) L(theta) +
+lam L(theta~) of Eq. smat-objective with both losses every step, when the caller scales the expert
+loss by 1 - lam.  Periodic scheduling instead calls `begin` after zero_grad().
+
 Ordinary steps touch nothing.  In offload mode theta0 stays in pinned host memory.  The restore
 at the end of each simulated step starts the copy of theta0 into the buffers on the library's copy
 stream, and that copy runs during the following ordinary steps.  The arithmetic runs in libsmat.
@@ -161,6 +166,7 @@ class SimulatedMergeTraining:
         self._adam_key = None
         self._clip = None                       # GPU scalars (sumsq, clipping factor) of the fused update
         self._grads = None                      # gradients at theta~ the plan points at
+        self._expert_grads = None               # the expert loss's gradients of the open step, if any
         self.names = [f"param{i}" for i in range(n)]
 
     @classmethod
@@ -188,8 +194,9 @@ class SimulatedMergeTraining:
 
     # ------------------------------------------------------------------ simulated step
     def begin(self, step: int) -> bool:
-        """Call after zero_grad() and before the forward pass.  On a simulated step, point the
-        parameters at theta~ and at zeroed gradient buffers; returns whether the step is simulated."""
+        """Call before the forward pass of the simulated loss: after zero_grad() (periodic
+        scheduling), or after the expert loss's backward to add both gradients.  On a simulated step,
+        point the parameters at theta~; returns whether the step is simulated."""
         if self._step is not None:
             raise SmatError(SMAT_ERR_STATE, "begin() while a simulated step is open")
         if not self.is_simulated(step):
@@ -200,6 +207,11 @@ class SimulatedMergeTraining:
         self.plan.simulate(self.seed, step)
         self.plan.switch_storage(SMAT_SIMULATED)
         self._grads = None      # last step's gradients, no longer read by any queued kernel
+        self._expert_grads = None
+        if any(p.grad is not None for p in self.params):   # the expert loss's gradient of this step
+            self._expert_grads = [None if p.grad is None else
+                                  p.grad.to(dtype=torch.float32, memory_format=torch.contiguous_format)
+                                  for p in self.params]
         for p, b in zip(self.params, self.buffers):
             p.data = b
             p.grad = None       # autograd creates the gradient at theta~ and keeps it as p.grad
@@ -250,11 +262,14 @@ class SimulatedMergeTraining:
                 raise SmatError(SMAT_ERR_INVALID, "the optimizer holds parameters outside the wrapper that have "
                                                   "gradients; the fused update would skip them")
             self._restore()
-            self.plan.set_grads(grads, None)
+            acc = self._accumulator(zeros=False)
+            self.plan.set_grads(grads, acc)
             self._grads = grads     # kept alive until the kernels that read them have been queued
-            return self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step, max_norm)
-        # the expert gradient lands in fresh fp32 tensors, as an ordinary step's gradients do
-        expert = [torch.zeros_like(m) for m in self.master]
+            return self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step, max_norm,
+                                    accumulate=acc is not None)
+        # the expert gradient lands in fresh fp32 tensors, as an ordinary step's gradients do, or is
+        # added to the expert loss's gradient of this step
+        expert = self._accumulator(zeros=True)
         self.plan.set_grads(grads, expert)
         self._grads = grads
         self.plan.backward_accum(self.seed, step, self.lam)
@@ -263,13 +278,28 @@ class SimulatedMergeTraining:
             p.grad = g
         return None
 
+    def _accumulator(self, zeros: bool) -> Optional[List[torch.Tensor]]:
+        """fp32 gradients the simulated-loss gradient is added to: the expert loss's gradients kept
+        by begin() (zeros where a parameter had none), fresh zeros when `zeros`, else None."""
+        if self._expert_grads is None:
+            return [torch.zeros_like(m) for m in self.master] if zeros else None
+        acc = [torch.zeros_like(m) if g is None else g for g, m in zip(self._expert_grads, self.master)]
+        self._expert_grads = None
+        return acc
+
     def abort(self) -> None:
         """Leave an open simulated step without any update (e.g. after an exception or a skipped
-        step): the expert storage is restored and gradients are dropped.  No-op when none is open."""
+        step): the expert storage is restored, the gradients at theta~ are dropped and the expert
+        loss's gradients kept by begin() are put back.  No-op when no step is open."""
         if self._step is not None:
             self._restore()
+            if self._expert_grads is not None:
+                for p, g in zip(self.params, self._expert_grads):
+                    p.grad = g
+                self._expert_grads = None
 
-    def _fused_adam(self, optimizer, hp: dict, step: int, max_norm: Optional[float]) -> Optional[torch.Tensor]:
+    def _fused_adam(self, optimizer, hp: dict, step: int, max_norm: Optional[float],
+                    accumulate: bool = False) -> Optional[torch.Tensor]:
         exp_avg, exp_avg_sq, counts = [], [], []
         for p in self.params:
             st = optimizer.state[p]
@@ -293,9 +323,9 @@ class SimulatedMergeTraining:
                 dev = self.master[0].device
                 self._clip = (torch.zeros(1, dtype=torch.float64, device=dev), torch.ones(1, dtype=torch.float32, device=dev))
             sumsq, coef = self._clip
-            self.plan.grad_norm(self.seed, step, self.lam, False, float(max_norm), sumsq, coef)
+            self.plan.grad_norm(self.seed, step, self.lam, accumulate, float(max_norm), sumsq, coef)
             norm = sumsq.sqrt()
-        self.plan.adamw_fused(self.seed, step, self.lam, hp, grad_scale_dev=coef)
+        self.plan.adamw_fused(self.seed, step, self.lam, hp, accumulate=accumulate, grad_scale_dev=coef)
         for c in counts:        # the optimizer's own step counts (CPU or GPU scalars)
             c.add_(1)
         return norm

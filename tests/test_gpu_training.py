@@ -171,6 +171,48 @@ def test_fused_clipped_step_matches_oracle():
     w.close()
 
 
+@pytest.mark.parametrize("fused", [False, True])
+def test_mixed_objective_adds_both_gradients(fused):
+    """With the expert loss's backward before begin(), the simulated-loss gradient is added to it:
+    grad = g_expert + lam alpha m g~ (Eq. smat-objective with both losses in one step)."""
+    model = make_decoder(TINY, 43, DEV)
+    batches = token_batches(TINY, 2, 16, 2, 3, DEV)
+    lam = 0.25
+    w = wrap(model, lam=lam, period=1)
+    opt = torch.optim.AdamW(w.params, lr=1e-3, weight_decay=0.0)
+    ((1 - lam) * model.loss(batches[0])).backward()            # expert loss at theta
+    g_exp = [host(p.grad)[0] for p in w.params]
+    masters = [host(m)[0] for m in w.master]
+    assert w.begin(0)
+    model.loss(batches[1]).backward()                           # simulated loss at theta~
+    g_sim = [host(p.grad)[0] for p in w.params]
+    ops = [op(w, i) for i in range(len(w.params))]
+    w.end(opt, fused=fused)
+    torch.cuda.synchronize()
+    hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, grad_scale=1.0, step=1)
+    for i, p in enumerate(w.params):
+        if not fused:
+            want = oracle.backward_accum(g_sim[i], "f32", g_exp[i], ops[i], lam, SEED, 0, i)
+            incr = np.abs(oracle.simulated_gradient(g_sim[i], "f32", ops[i], lam, SEED, 0, i))
+            ok = check_grad(host(p.grad)[0], want, g_exp[i], incr)
+            assert ok.all(), f"{w.names[i]}: {np.count_nonzero(~ok)} gradient mismatches"
+        else:
+            old = (masters[i], np.zeros(p.numel(), np.float32), np.zeros(p.numel(), np.float32))
+            _, f64 = oracle.adamw_fused(g_sim[i], "f32", *old, ops[i], lam, hp, SEED, 0, i, grad_acc=g_exp[i])
+            gmag = np.abs(oracle.simulated_gradient(g_sim[i], "f32", ops[i], lam, SEED, 0, i)) + np.abs(g_exp[i])
+            st = opt.state[p]
+            got = (host(p.data)[0], host(st["exp_avg"])[0], host(st["exp_avg_sq"])[0])
+            for name, ok in zip(("theta", "exp_avg", "exp_avg_sq"), check_adam(got, old, f64, hp, gmag)):
+                assert ok.all(), f"{w.names[i]} {name}: {np.count_nonzero(~ok)} mismatches"
+    # abort() puts the expert loss's gradients back
+    ((1 - lam) * model.loss(batches[0])).backward()
+    before = [p.grad.clone() for p in w.params]
+    assert w.begin(1)
+    w.abort()
+    assert all(torch.equal(p.grad, b) for p, b in zip(w.params, before))
+    w.close()
+
+
 def test_fused_update_creates_missing_optimizer_state():
     model = make_decoder(TINY, 13, DEV)
     w = wrap(model, period=1)                       # every step simulated
