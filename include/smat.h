@@ -230,6 +230,17 @@ smat_status smat_plan_set_params(smat_plan* plan, const smat_op_params* per_tens
  * storage active), SMAT_ERR_HIP. */
 smat_status smat_simulate_multi(smat_plan* plan, uint64_t seed, uint32_t step, hipStream_t stream);
 
+/* smat_backward_multi -- the gradient through the simulation over every tensor of the plan in one
+ * launch (Sec. 4.2, Eq. smat-gradient, weighted by lambda).  accumulate = 1: grad_theta += lambda t m
+ * (.) grad_sim on kept coordinates, dropped ones bit-unchanged (smat_backward_accum_multi).
+ * accumulate = 0: grad_theta = lambda t m (.) grad_sim everywhere, +0 where dropped, without reading
+ * grad_theta: the bits of accumulating into +0, for a step whose simulated-loss gradient is the only
+ * gradient (periodic scheduling), at 6 B instead of 10 B per element for a bf16 grad_sim.
+ * Errors: SMAT_ERR_INVALID (lambda, step, accumulate), SMAT_ERR_STATE (no workspace or params,
+ * gradient arrays not set), SMAT_ERR_HIP. */
+smat_status smat_backward_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda, int32_t accumulate,
+                                hipStream_t stream);
+
 /* smat_backward_accum_multi -- smat_backward_accum over every tensor of the plan in one launch.
  * Errors: SMAT_ERR_INVALID (lambda, step), SMAT_ERR_STATE (no workspace or params, gradient arrays
  * not set), SMAT_ERR_HIP. */

@@ -28,7 +28,7 @@ EXPORTS = (
     "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi", "smat_grad_norm_multi",
     "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
     "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
-    "smat_stream_copy",
+    "smat_stream_copy", "smat_backward_multi",
 )
 
 
@@ -105,6 +105,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_merge_plan_destroy": [P],
         "smat_plan_set_grads": [P, POINTER(P), POINTER(P), P],
         "smat_stream_copy": [P, P, c_uint64, P],
+        "smat_backward_multi": [P, c_uint64, c_uint32, c_float, c_int32, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -299,6 +300,11 @@ class Plan:
 
     def backward_accum(self, seed: int, step: int, lam: float, stream=None) -> None:
         _check(lib().smat_backward_accum_multi(self._plan, int(seed), int(step), float(lam), _stream_handle(stream)))
+
+    def backward(self, seed: int, step: int, lam: float, accumulate: bool = True, stream=None) -> None:
+        """smat_backward_multi: accumulate into grad_theta, or overwrite it (zero where dropped)."""
+        _check(lib().smat_backward_multi(self._plan, int(seed), int(step), float(lam), 1 if accumulate else 0,
+                                         _stream_handle(stream)))
 
     def set_grads(self, grad_sims: Optional[Sequence] = None, grad_thetas: Optional[Sequence] = None,
                   stream=None) -> None:

@@ -556,21 +556,28 @@ extern "C" smat_status smat_simulate_multi(smat_plan* p, uint64_t seed, uint32_t
   return SMAT_OK;
 }
 
-extern "C" smat_status smat_backward_accum_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
-                                                 hipStream_t stream) {
-  if (!p) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: null plan");
-  if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: step must be < 2^30");
-  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_backward_accum_multi: lambda must be finite");
+extern "C" smat_status smat_backward_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
+                                           int32_t accumulate, hipStream_t stream) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_backward_multi: null plan");
+  if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_backward_multi: step must be < 2^30");
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_backward_multi: lambda must be finite");
+  if (accumulate != 0 && accumulate != 1) return fail(SMAT_ERR_INVALID, "smat_backward_multi: accumulate must be 0 or 1");
   if (!p->has_gs || !p->has_gt)
-    return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: gradient arrays not set (smat_plan_set_grads)");
-  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: no workspace bound");
-  if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_backward_accum_multi: parameters never set");
+    return fail(SMAT_ERR_STATE, "smat_backward_multi: gradient arrays not set (smat_plan_set_grads)");
+  if (!p->ws) return fail(SMAT_ERR_STATE, "smat_backward_multi: no workspace bound");
+  if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_backward_multi: parameters never set");
   if (!p->chunks.empty())
     SMAT_HIP(smat::launch_backward_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
                                          reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
                                          reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
-                                         (uint32_t)p->chunks.size(), p->g_dt, lambda, seed, step, stream));
+                                         (uint32_t)p->chunks.size(), p->g_dt, accumulate != 0, lambda, seed, step,
+                                         stream));
   return SMAT_OK;
+}
+
+extern "C" smat_status smat_backward_accum_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
+                                                 hipStream_t stream) {
+  return smat_backward_multi(p, seed, step, lambda, 1, stream);
 }
 
 extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_state* per_tensor, hipStream_t stream) {

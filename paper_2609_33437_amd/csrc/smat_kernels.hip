@@ -2,6 +2,7 @@
 //
 // simulate:  theta~ = theta0 + t m (theta - theta0) + sigma z      (Sec. 4.1, Eq. smat-state/smat-mask)
 // backward:  grad_theta += lambda t m g~ on kept coordinates       (Sec. 4.2, Eq. smat-gradient)
+//            (or grad_theta = lambda t m g~, zero where dropped, without reading grad_theta)
 //
 // Both are purely HBM-bound streams (no contraction, so no MFMA).  The unit of work is a quad
 // of 4 consecutive elements = one Philox group, so a thread draws one 128-bit Philox output per
@@ -126,16 +127,21 @@ __device__ __forceinline__ void simulate_tile(const Tile& T, const ParamRec& P, 
 }
 
 // ---------------------------------------------------------------- backward
-template <typename TG, int Q>
+// ACC: grad_theta += lambda t m g~ on kept coordinates, dropped ones left as they are (10 B per
+// element for bf16 g~).  !ACC: grad_theta = lambda t m g~ everywhere, zero where dropped, without
+// reading grad_theta (6 B per element): the same bits as accumulating into zeros, for a step whose
+// simulated-loss gradient is the only one.
+template <typename TG, int Q, bool ACC>
 __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step,
                                               float lambda) {
   const uint32_t flags = P.flags;
-  if (flags & kFlagDropAll) return;  // every coordinate dropped: the gradient is left as it is
+  if (ACC && (flags & kFlagDropAll)) return;  // every coordinate dropped: the gradient is left as it is
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
   const uint32_t tensor_id = T.tensor_id;
   const uint32_t len = T.len;
   const bool use_mask = (flags & kFlagMask) != 0;
+  const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
   const uint32_t thr = P.thr;
   const float c = lambda * P.t;
 
@@ -145,9 +151,13 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
 
   auto one = [&](uint32_t i) {
     const uint64_t e = e0 + i;
-    bool kept = true;
+    bool kept = all_kept;
     if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
-    if (kept) QuadIO<float>::store1(gt, i, __builtin_fmaf(c, QuadIO<TG>::load1(gs, i), QuadIO<float>::load1(gt, i)));
+    if (ACC) {
+      if (kept) QuadIO<float>::store1(gt, i, __builtin_fmaf(c, QuadIO<TG>::load1(gs, i), QuadIO<float>::load1(gt, i)));
+    } else {
+      QuadIO<float>::store1(gt, i, kept ? __builtin_fmaf(c, QuadIO<TG>::load1(gs, i), 0.0f) : 0.0f);
+    }
   };
 
   if (!(T.sflags & kVecBwd)) {
@@ -168,13 +178,13 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
       const uint32_t q = u * kBlock + threadIdx.x;
       const uint32_t qc = q < nq ? q : nq - 1;
       ra[u] = QuadIO<TG>::load_raw(gs, qc);
-      rb[u] = QuadIO<float>::load_raw(gt, qc);
+      if (ACC) rb[u] = QuadIO<float>::load_raw(gt, qc);
     }
     bool kept[Q][4];
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kept[u][j] = true;
+      for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
       if (use_mask) {
         const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, cmask, k0, k1);
         kept[u][0] = w.w0 < thr;
@@ -187,9 +197,9 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
     for (int u = 0; u < Q; ++u) {
       const uint32_t q = u * kBlock + threadIdx.x;
       if (q < nq) {
-        float a[4], b[4], o[4];
+        float a[4], b[4] = {0.f, 0.f, 0.f, 0.f}, o[4];
         QuadIO<TG>::unpack(ra[u], a);
-        QuadIO<float>::unpack(rb[u], b);
+        if (ACC) QuadIO<float>::unpack(rb[u], b);
 #pragma unroll
         for (int j = 0; j < 4; ++j) o[j] = kept[u][j] ? __builtin_fmaf(c, a[j], b[j]) : b[j];
         QuadIO<float>::store(gt, q, o);
@@ -216,7 +226,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_one(TensorRec R, ParamRec P
   Tile T = tensor_tile<float, float>(R, begin, tile);
   T.grad_sim = advance<TG>(R.grad_sim, begin);
   T.grad_theta = R.grad_theta + begin;
-  backward_tile<TG, kBwdQuads>(T, P, seed, step, lambda);
+  backward_tile<TG, kBwdQuads, true>(T, P, seed, step, lambda);
 }
 
 template <typename T0, typename TO>
@@ -232,7 +242,7 @@ __global__ __launch_bounds__(kBlock) void k_simulate_multi(const TensorRec* __re
   simulate_tile<T0, TO, kSimQuads>(T, prms[ch.x], seed, step);
 }
 
-template <typename TG>
+template <typename TG, bool ACC>
 __global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __restrict__ recs,
                                                            const ParamRec* __restrict__ prms,
                                                            const uint2* __restrict__ chunks, uint64_t seed,
@@ -242,7 +252,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __re
   const uint2 ch = chunks[blockIdx.x / tpc];
   const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;
-  backward_tile<TG, kBwdQuads>(T, prms[ch.x], seed, step, lambda);
+  backward_tile<TG, kBwdQuads, ACC>(T, prms[ch.x], seed, step, lambda);
 }
 
 constexpr int kDebugBlock = 256;
@@ -310,12 +320,17 @@ hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, co
 }
 
 hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
-                                 int grad_dtype, float lambda, uint64_t seed, uint32_t step, hipStream_t stream) {
+                                 int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
+                                 hipStream_t stream) {
   const dim3 grid(nchunks * tiles_per_chunk(kBwdQuads)), block(kBlock);
-  if (grad_dtype == 1)
-    k_backward_multi<Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+  if (grad_dtype == 1 && accumulate)
+    k_backward_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+  else if (grad_dtype == 1)
+    k_backward_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+  else if (accumulate)
+    k_backward_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
   else
-    k_backward_multi<float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+    k_backward_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
   return hipGetLastError();
 }
 

@@ -16,7 +16,8 @@ hipError_t launch_backward_one(const TensorRec& rec, const ParamRec& prm, int gr
 hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                  int theta0_dtype, int out_dtype, uint64_t seed, uint32_t step, hipStream_t stream);
 hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
-                                 int grad_dtype, float lambda, uint64_t seed, uint32_t step, hipStream_t stream);
+                                 int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
+                                 hipStream_t stream);
 hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const ParamRec& prm, const AdamConsts& A,
                             int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
                             const float* dev_scale, hipStream_t stream);

@@ -267,12 +267,13 @@ class SimulatedMergeTraining:
             self._grads = grads     # kept alive until the kernels that read them have been queued
             return self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step, max_norm,
                                     accumulate=acc is not None)
-        # the expert gradient lands in fresh fp32 tensors, as an ordinary step's gradients do, or is
-        # added to the expert loss's gradient of this step
-        expert = self._accumulator(zeros=True)
+        # the expert gradient is written into fresh fp32 tensors, as an ordinary step's gradients
+        # are, or added to the expert loss's gradient of this step
+        acc = self._accumulator(zeros=False)
+        expert = acc if acc is not None else [torch.empty_like(m) for m in self.master]
         self.plan.set_grads(grads, expert)
         self._grads = grads
-        self.plan.backward_accum(self.seed, step, self.lam)
+        self.plan.backward(self.seed, step, self.lam, accumulate=acc is not None)
         self._restore()
         for p, g in zip(self.params, expert):
             p.grad = g
@@ -280,7 +281,8 @@ class SimulatedMergeTraining:
 
     def _accumulator(self, zeros: bool) -> Optional[List[torch.Tensor]]:
         """fp32 gradients the simulated-loss gradient is added to: the expert loss's gradients kept
-        by begin() (zeros where a parameter had none), fresh zeros when `zeros`, else None."""
+        by begin() (zeros where a parameter had none); without them, fresh zeros when `zeros`, else
+        None."""
         if self._expert_grads is None:
             return [torch.zeros_like(m) for m in self.master] if zeros else None
         acc = [torch.zeros_like(m) if g is None else g for g, m in zip(self._expert_grads, self.master)]

@@ -70,3 +70,19 @@ def test_stream_copy(nbytes):
     assert int(dst[nbytes:].sum()) == 0          # nothing written past the end
     with pytest.raises(smat.SmatError):
         smat.smat_stream_copy(src[1:33], dst[1:33])   # not 16-byte aligned
+
+
+def test_backward_overwrite_writes_every_element():
+    sizes = [(1 << 23) + 3, 1, 3 * (1 << 20) + 17]
+    ts = [tensors(n) for n in sizes]
+    for t in ts:
+        t[4].fill_(float("nan"))                     # grad_theta is never read in overwrite mode
+    with smat.Plan([t[0] for t in ts], [t[2] for t in ts], [t[1] for t in ts], [t[3] for t in ts],
+                   [t[4] for t in ts]) as plan:
+        plan.set_params([P] * len(sizes))
+        plan.backward(17, 5, 1.0, accumulate=False)
+        torch.cuda.synchronize()
+    for i, (n, t) in enumerate(zip(sizes, ts)):
+        kept = kept_mask(n, i, 0).float()
+        torch.cuda.synchronize()
+        assert torch.equal(t[4], kept), f"tensor {i}"

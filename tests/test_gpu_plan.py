@@ -349,3 +349,34 @@ def test_set_grads_rebinds_the_gradient_arrays(mini):
             plan.set_grads([o for o in out])                      # overlaps the simulated buffer
         with pytest.raises(smat.SmatError):
             plan.set_grads(None, [x.view(-1) for x in th])          # the expert storage itself
+
+
+def test_backward_overwrite_equals_accumulate_into_zeros(mini):
+    """smat_backward_multi with accumulate = 0 writes lambda t m g~ (+0 where dropped) without
+    reading grad_theta: the bits of accumulating into zeros, on aligned and misaligned arrays, for
+    masked, unmasked and fully dropped tensors."""
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    step = 9
+    params = workloads.step_params(cfg, inp.settings, step)
+    params[0] = dict(params[0], keep=0.0)                  # every coordinate dropped
+    params[1] = dict(params[1], keep=1.0)                  # no mask
+    zeros = [torch.zeros(x.numel(), device=DEV) for x in th]
+    g = torch.Generator(DEV).manual_seed(4)
+    garbage = []
+    for i, x in enumerate(th):                             # NaN-filled, every other one misaligned
+        buf = torch.full((x.numel() + 4,), float("nan"), device=DEV)
+        garbage.append(buf[1:1 + x.numel()] if i % 2 else buf[:x.numel()])
+    with smat.Plan(th, out, t0, gs, zeros) as plan:
+        plan.set_params(params)
+        plan.backward(cfg.smat_seed, step, cfg.lam, accumulate=True)
+        plan.set_grads(None, garbage)
+        plan.backward(cfg.smat_seed, step, cfg.lam, accumulate=False)
+        torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(garbage, zeros)):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32)), f"tensor {i}"
+        gsn = host(inp.grad_sim[i])[0].ravel()
+        want = oracle.backward_accum(gsn, "bf16", np.zeros(gsn.size, np.float32), params[i], cfg.lam,
+                                     cfg.smat_seed, step, i)
+        incr = np.abs(oracle.simulated_gradient(gsn, "bf16", params[i], cfg.lam, cfg.smat_seed, step, i))
+        assert check_grad(host(a)[0], want, np.zeros(gsn.size, np.float32), incr).all(), f"tensor {i}"
