@@ -141,7 +141,8 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
   const uint32_t tensor_id = T.tensor_id;
   const uint32_t len = T.len;
   const bool use_mask = (flags & kFlagMask) != 0;
-  const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
+  // ACC has returned above on DropAll, so there a coordinate without a mask is always kept
+  const bool all_kept = ACC || (flags & (kFlagMask | kFlagDropAll)) == 0;
   const uint32_t thr = P.thr;
   const float c = lambda * P.t;
 
