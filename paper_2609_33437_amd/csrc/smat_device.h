@@ -103,20 +103,27 @@ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t key) {
   return __builtin_amdgcn_bitop3_b32(a, b, key, 0x96);
 }
 
+constexpr uint32_t kPhiloxM0 = 0xD2511F53u, kPhiloxM1 = 0xCD9E8D57u;  // round multipliers
+constexpr uint32_t kPhiloxW0 = 0x9E3779B9u, kPhiloxW1 = 0xBB67AE85u;  // key increments
+
+// One Philox4x32 round on counter words (c0, c1, c2, c3) under round key (k0, k1), with the product
+// p0 = c0 * M0 given (64 bits).
+__device__ __forceinline__ void philox_round(uint64_t p0, uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3,
+                                             uint32_t k0, uint32_t k1) {
+  const uint64_t p1 = (uint64_t)c2 * kPhiloxM1;
+  c0 = xor3((uint32_t)(p1 >> 32), c1, k0);
+  c2 = xor3((uint32_t)(p0 >> 32), c3, k1);
+  c1 = (uint32_t)p1;
+  c3 = (uint32_t)p0;
+}
+
 __device__ __forceinline__ Words philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                                uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    const uint64_t p0 = (uint64_t)c0 * 0xD2511F53u;
-    const uint64_t p1 = (uint64_t)c2 * 0xCD9E8D57u;
-    const uint32_t n0 = xor3((uint32_t)(p1 >> 32), c1, k0);
-    const uint32_t n2 = xor3((uint32_t)(p0 >> 32), c3, k1);
-    c0 = n0;
-    c1 = (uint32_t)p1;
-    c2 = n2;
-    c3 = (uint32_t)p0;
-    k0 += 0x9E3779B9u;
-    k1 += 0xBB67AE85u;
+    philox_round((uint64_t)c0 * kPhiloxM0, c0, c1, c2, c3, k0, k1);
+    k0 += kPhiloxW0;
+    k1 += kPhiloxW1;
   }
   return {c0, c1, c2, c3};
 }
@@ -125,6 +132,61 @@ __device__ __forceinline__ Words philox4x32_10(uint32_t c0, uint32_t c1, uint32_
 __device__ __forceinline__ Words group_words(uint64_t g, uint32_t tensor_id, uint32_t c3, uint32_t k0,
                                              uint32_t k1) {
   return philox4x32_10((uint32_t)g, (uint32_t)(g >> 32), tensor_id, c3, k0, k1);
+}
+
+// ---------------------------------------------------------------- Philox on a tile's groups
+// Thread x, slot u of a tile's vector path draws group g0 + u kBlock + x.  Unless the tile crosses a
+// multiple of 2^32 groups, these groups share the high counter word, and then counter words 1-3
+// and the key are wave-uniform: the first rounds mix one per-lane word with uniform ones, and their
+// uniform parts run on the scalar unit.  A crossing tile (possible only past element 2^34) takes the
+// element-by-element path instead.
+struct TileGroups {
+  uint32_t lo;  // low word of the tile's first group
+  uint32_t hi;  // high word of every group of the tile
+};
+__device__ __forceinline__ TileGroups tile_groups(uint64_t e0) { return {(uint32_t)(e0 >> 2), (uint32_t)(e0 >> 34)}; }
+// Whether the groups of a tile of `quads` quads starting at element e0 wrap the low counter word.
+__device__ __forceinline__ bool groups_wrap(uint64_t e0, uint32_t quads) {
+  return (uint32_t)(e0 >> 2) > 0xFFFFFFFFu - (quads - 1u);
+}
+
+// Round 1's product of the per-lane counter word.  Streams of one group, and masks of one group
+// under several keys, differ only in c3 or the key, so a caller drawing several forms it once.
+__device__ __forceinline__ uint64_t philox_p0(uint32_t glo) { return (uint64_t)glo * kPhiloxM0; }
+
+// Philox4x32-10 of counter (glo, hi, c2, c3) under key (k0, k1), given p0 = philox_p0(glo), for
+// wave-uniform hi, c2, c3, k0, k1.  The same rounds as philox4x32_10, with each xor grouped so
+// that its uniform operands combine first.
+__device__ __forceinline__ Words philox_tile(uint64_t p0, uint32_t hi, uint32_t c2, uint32_t c3, uint32_t k0,
+                                             uint32_t k1) {
+  // round 1: only the products' lane-dependent half (p0) is per lane
+  const uint64_t q1 = (uint64_t)c2 * kPhiloxM1;
+  const uint32_t a0 = (uint32_t)(q1 >> 32) ^ hi ^ k0, a1 = (uint32_t)q1;
+  const uint32_t a2 = (uint32_t)(p0 >> 32) ^ (c3 ^ k1), a3 = (uint32_t)p0;
+  // round 2: a0 and a1 are uniform
+  k0 += kPhiloxW0;
+  k1 += kPhiloxW1;
+  const uint64_t r0 = (uint64_t)a0 * kPhiloxM0, r1 = (uint64_t)a2 * kPhiloxM1;
+  uint32_t c0 = (uint32_t)(r1 >> 32) ^ (a1 ^ k0), w1 = (uint32_t)r1;
+  uint32_t w2 = a3 ^ ((uint32_t)(r0 >> 32) ^ k1), w3 = (uint32_t)r0;
+  // round 3: w3 is uniform
+  k0 += kPhiloxW0;
+  k1 += kPhiloxW1;
+  {
+    const uint64_t s0 = (uint64_t)c0 * kPhiloxM0, s1 = (uint64_t)w2 * kPhiloxM1;
+    c0 = xor3((uint32_t)(s1 >> 32), w1, k0);
+    w2 = (uint32_t)(s0 >> 32) ^ (w3 ^ k1);
+    w1 = (uint32_t)s1;
+    w3 = (uint32_t)s0;
+  }
+  // rounds 4-10
+#pragma unroll
+  for (int r = 3; r < 10; ++r) {
+    k0 += kPhiloxW0;
+    k1 += kPhiloxW1;
+    philox_round((uint64_t)c0 * kPhiloxM0, c0, w1, w2, w3, k0, k1);
+  }
+  return {c0, w1, w2, w3};
 }
 
 __device__ __forceinline__ uint32_t pick(const Words& w, uint32_t lane) {

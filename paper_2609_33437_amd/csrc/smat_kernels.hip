@@ -53,7 +53,7 @@ __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec
     QuadIO<TO>::store1(out, i, y);
   };
 
-  if (!(T.sflags & kVecSim)) {
+  if (!(T.sflags & kVecSim) || groups_wrap(e0, Q * kBlock)) {
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
       const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
@@ -61,7 +61,8 @@ __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec
     }
     return;
   }
-  // whole quads: each is one Philox group, since e0 is a multiple of 4 on this path.
+  // whole quads: each is one Philox group, since e0 is a multiple of 4 on this path.  The mask and
+  // noise streams of a group share round 1's product.
   // Phase 1 issues every load (indices clamped into the tile, so no branch guards them), phase 2
   // draws the mask and noise while the loads are in flight, phase 3 combines and stores.
   const uint32_t nq = len >> 2;
@@ -77,19 +78,20 @@ __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec
     }
     bool kept[Q][4];
     float z[Q][4];
+    const TileGroups G = tile_groups(e0);
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
-      const uint64_t g = (e0 >> 2) + u * kBlock + threadIdx.x;
+      const uint64_t p0 = philox_p0(G.lo + u * kBlock + threadIdx.x);
 #pragma unroll
       for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
       if (use_mask) {
-        const Words w = group_words(g, tensor_id, cmask, k0, k1);
+        const Words w = philox_tile(p0, G.hi, tensor_id, cmask, k0, k1);
         kept[u][0] = w.w0 < thr;
         kept[u][1] = w.w1 < thr;
         kept[u][2] = w.w2 < thr;
         kept[u][3] = w.w3 < thr;
       }
-      if (use_noise) quad_noise<KIND>(group_words(g, tensor_id, cnoise, k0, k1), z[u]);
+      if (use_noise) quad_noise<KIND>(philox_tile(p0, G.hi, tensor_id, cnoise, k0, k1), z[u]);
     }
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
@@ -161,7 +163,7 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
     }
   };
 
-  if (!(T.sflags & kVecBwd)) {
+  if (!(T.sflags & kVecBwd) || groups_wrap(e0, Q * kBlock)) {
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
       const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
@@ -181,13 +183,14 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
       ra[u] = QuadIO<TG>::load_raw(gs, qc);
       if (ACC) rb[u] = QuadIO<float>::load_raw(gt, qc);
     }
+    const TileGroups G = tile_groups(e0);
     bool kept[Q][4];
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
       if (use_mask) {
-        const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, cmask, k0, k1);
+        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, k0, k1);
         kept[u][0] = w.w0 < thr;
         kept[u][1] = w.w1 < thr;
         kept[u][2] = w.w2 < thr;

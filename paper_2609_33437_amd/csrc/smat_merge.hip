@@ -33,7 +33,7 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
     QuadIO<TO>::store1(outp, i, acc);
   };
 
-  if (!vec) {
+  if (!vec || groups_wrap(e0, kMergeQuads * kBlock)) {
 #pragma unroll
     for (int u = 0; u < kMergeQuads; ++u) {
       const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
@@ -44,6 +44,11 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
   const uint32_t nq = len >> 2;
   if (nq > 0) {
     float b[kMergeQuads][4], acc[kMergeQuads][4];
+    // the experts' masks of a group differ only in the key, so they share round 1's product
+    const TileGroups G = tile_groups(e0);
+    uint64_t p0[kMergeQuads];
+#pragma unroll
+    for (int u = 0; u < kMergeQuads; ++u) p0[u] = philox_p0(G.lo + u * kBlock + threadIdx.x);
     {
       typename QuadIO<T0>::Raw r0[kMergeQuads];
 #pragma unroll
@@ -74,8 +79,8 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
 #pragma unroll
         for (int j = 0; j < 4; ++j) kept[u][j] = true;
         if (R.flags & kFlagMask) {
-          const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, (R.step << 2) | kStreamMask,
-                                      (uint32_t)R.seed, (uint32_t)(R.seed >> 32));
+          const Words w = philox_tile(p0[u], G.hi, tensor_id, (R.step << 2) | kStreamMask, (uint32_t)R.seed,
+                                          (uint32_t)(R.seed >> 32));
           kept[u][0] = w.w0 < R.thr;
           kept[u][1] = w.w1 < R.thr;
           kept[u][2] = w.w2 < R.thr;

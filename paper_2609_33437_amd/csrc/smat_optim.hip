@@ -55,7 +55,7 @@ __device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p
   };
 
   const uint32_t vec = ACC ? kVecAdamAcc : kVecAdam;
-  if (!(T.sflags & vec)) {
+  if (!(T.sflags & vec) || groups_wrap(e0, Q * kBlock)) {
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
       const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
@@ -77,13 +77,14 @@ __device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p
       r1[u] = QuadIO<float>::load_raw(m1p, qc);
       r2[u] = QuadIO<float>::load_raw(m2p, qc);
     }
+    const TileGroups G = tile_groups(e0);
     bool kept[Q][4];
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
       if (use_mask) {
-        const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, cmask, k0, k1);
+        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, k0, k1);
         kept[u][0] = w.w0 < thr;
         kept[u][1] = w.w1 < thr;
         kept[u][2] = w.w2 < thr;
@@ -184,7 +185,7 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, u
     s = __builtin_fmaf(g, g, s);
   };
 
-  if (!(T.sflags & kVecBwd)) {
+  if (!(T.sflags & kVecBwd) || groups_wrap(e0, kNormQuads * kBlock)) {
 #pragma unroll
     for (int u = 0; u < kNormQuads; ++u) {
       const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
@@ -203,13 +204,14 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, u
       rg[u] = QuadIO<TG>::load_raw(gs, qc);
       if (ACC) ra[u] = QuadIO<float>::load_raw(ga, qc);
     }
+    const TileGroups G = tile_groups(e0);
     bool kept[kNormQuads][4];
 #pragma unroll
     for (int u = 0; u < kNormQuads; ++u) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
       if (use_mask) {
-        const Words w = group_words((e0 >> 2) + u * kBlock + threadIdx.x, tensor_id, cmask, k0, k1);
+        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, k0, k1);
         kept[u][0] = w.w0 < thr;
         kept[u][1] = w.w1 < thr;
         kept[u][2] = w.w2 < thr;

@@ -41,7 +41,7 @@ def _check(th, m1, m2, old, gsn, gs_dt, p, lam, hp, seed, step, tid, off, acc=No
 
 
 @pytest.mark.parametrize("n,shift,off", [(1, 0, 0), (5, 0, 0), (4096, 0, 0), (100003, 0, 0), (50001, 1, 3),
-                                          (70000, 0, 2 ** 34 + 8)])
+                                          (70000, 0, 2 ** 34 + 8), (5000, 0, 2 ** 34 - 1000)])
 @pytest.mark.parametrize("g_dtype", [torch.bfloat16, torch.float32])
 @pytest.mark.parametrize("accumulate", [False, True])
 def test_single_tensor(n, shift, off, g_dtype, accumulate):
@@ -133,3 +133,28 @@ def test_plan_matches_oracle_and_needs_expert_storage(accumulate):
         acc = host(inp.grad_theta[i])[0].ravel() if accumulate else None
         _check(th[i], m1[i], m2[i], old[i], host(inp.grad_sim[i])[0].ravel(), "bf16", params[i], cfg.lam, hp,
                cfg.smat_seed, step, i, 0, acc)
+
+
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_plan_tiles_across_a_high_counter_word_boundary(accumulate):
+    # global offsets just below multiples of 2^34 elements: one tile of each tensor crosses the
+    # change of the group index's high word
+    g = torch.Generator(DEV).manual_seed(35)
+    sizes, offs, ids = [5000, 20001], [2 ** 34 - 1000, 2 ** 35 - 8192], [6, 7]
+    states = [_state(n, g) for n in sizes]
+    th = [s[0] for s in states]
+    gs = [(torch.randn(n, device=DEV, generator=g) * 1e-2).to(torch.bfloat16) for n in sizes]
+    acc = [torch.randn(n, device=DEV, generator=g) * 1e-3 for n in sizes]
+    out = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    old = [tuple(host(x)[0] for x in s) for s in states]
+    params = [dict(s=0.6, keep=0.3, sigma=0.0, rescale=1), dict(s=0.8, keep=0.5, sigma=0.0, rescale=1)]
+    hp = dict(HP, step=4, grad_scale=0.5)
+    t0 = [x.to(torch.bfloat16) for x in th]
+    with smat.Plan(th, out, t0, gs, acc, tensor_ids=ids, elem_offsets=offs) as plan:
+        plan.set_params(params)
+        plan.bind_adam_state([s[1] for s in states], [s[2] for s in states])
+        plan.adamw_fused(21, 6, 0.5, hp, accumulate=accumulate)
+        torch.cuda.synchronize()
+    for i in range(len(sizes)):
+        _check(*states[i], old[i], host(gs[i])[0], "bf16", params[i], 0.5, hp, 21, 6, ids[i], offs[i],
+               host(acc[i])[0] if accumulate else None)

@@ -90,10 +90,10 @@ def test_misaligned_ragged_and_dropped_tensors(g_dtype):
     # sizes across several chunks with tails; tensors at odd element offsets within their buffers
     # (pointers off the quad alignment) and odd global offsets take the per-element path
     g = torch.Generator(DEV).manual_seed(3)
-    sizes = [1, 3, 4, 5, 16384, 16385, 40000 + 3, 70001]
-    shifts = [0, 1, 0, 3, 0, 0, 1, 0]
-    offs = [0, 0, 6, 0, 0, 2 ** 33 + 1, 4, 2 ** 34 + 8]
-    keeps = [0.5, 0.0, 1.0, 0.3, 0.25, 0.5, 0.0, 0.7]
+    sizes = [1, 3, 4, 5, 16384, 16385, 40000 + 3, 70001, 9001]
+    shifts = [0, 1, 0, 3, 0, 0, 1, 0, 0]
+    offs = [0, 0, 6, 0, 0, 2 ** 33 + 1, 4, 2 ** 34 + 8, 2 ** 34 - 4096]  # the last crosses 2^34 mid-tile
+    keeps = [0.5, 0.0, 1.0, 0.3, 0.25, 0.5, 0.0, 0.7, 0.4]
     bufs = [torch.randn(n + 8, device=DEV, generator=g) for n in sizes]
     gs = [(b * 1e-2).to(g_dtype)[s:s + n] for b, s, n in zip(bufs, shifts, sizes)]
     gt = [(torch.randn(n + 8, device=DEV, generator=g) * 1e-3)[s:s + n] for s, n in zip(shifts, sizes)]

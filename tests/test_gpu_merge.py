@@ -63,7 +63,7 @@ def oracle_check(out, ex, t0, terms, tid, off):
 
 
 @pytest.mark.parametrize("n,shift,off", [(1, 0, 0), (5, 0, 0), (4096, 0, 0), (100003, 0, 0), (50001, 1, 3),
-                                          (70000, 0, 2 ** 34 + 8)])
+                                          (70000, 0, 2 ** 34 + 8), (5000, 0, 2 ** 34 - 1000)])
 @pytest.mark.parametrize("t0_dt,out_dt", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32")])
 @pytest.mark.parametrize("keep", [0.5, 1.0, 0.0])
 def test_one_expert_is_the_simulated_state_bit_for_bit(n, shift, off, t0_dt, out_dt, keep):
@@ -79,7 +79,8 @@ def test_one_expert_is_the_simulated_state_bit_for_bit(n, shift, off, t0_dt, out
 @pytest.mark.parametrize("nexp", [1, 3, 7, 16])
 @pytest.mark.parametrize("e_dt,t0_dt,out_dt", [("bf16", "bf16", "bf16"), ("f32", "bf16", "f32"),
                                                ("bf16", "f32", "bf16"), ("f32", "f32", "f32")])
-@pytest.mark.parametrize("n,shift,off", [(7, 0, 0), (65539, 0, 0), (40001, 1, 2), (16384 * 3 + 1, 0, 2 ** 33)])
+@pytest.mark.parametrize("n,shift,off", [(7, 0, 0), (65539, 0, 0), (40001, 1, 2), (16384 * 3 + 1, 0, 2 ** 33),
+                                          (16384 + 5, 0, 2 ** 34 - 8192)])
 def test_single_tensor_matches_oracle(nexp, e_dt, t0_dt, out_dt, n, shift, off):
     t0, ex = make(n, nexp, e_dt, t0_dt, 1000 * nexp + n, shift)
     out = torch.empty(n, dtype=DT[out_dt], device=DEV)
@@ -189,3 +190,20 @@ def test_errors():
         plan.merge([dict(gamma=0.3)] * 2)
     with smat.MergePlan([], [], [[], []]) as plan:                             # empty list
         plan.merge([dict(gamma=0.3)] * 2)
+
+
+def test_plan_tiles_across_a_high_counter_word_boundary():
+    # global offsets just below multiples of 2^34 elements: one tile of each tensor crosses the
+    # change of the group index's high word, for every expert's mask
+    nexp = 5
+    parts = [make(n, nexp, "bf16", "bf16", 40 + n) for n in (5000, 20001)]
+    offs, ids = [2 ** 34 - 1000, 2 ** 35 - 8192], [8, 9]
+    t0 = [p[0] for p in parts]
+    ex = [[p[1][j] for p in parts] for j in range(nexp)]
+    outs = [torch.empty_like(x) for x in t0]
+    terms = [terms_for(nexp, keep=0.6), terms_for(nexp, keep=0.35, seed0=300)]
+    with smat.MergePlan(t0, outs, ex, tensor_ids=ids, elem_offsets=offs) as plan:
+        plan.merge(terms)
+        torch.cuda.synchronize()
+    for i in range(2):
+        oracle_check(outs[i], [e[i] for e in ex], t0[i], terms[i], ids[i], offs[i])

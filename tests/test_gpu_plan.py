@@ -380,3 +380,47 @@ def test_backward_overwrite_equals_accumulate_into_zeros(mini):
                                      cfg.smat_seed, step, i)
         incr = np.abs(oracle.simulated_gradient(gsn, "bf16", params[i], cfg.lam, cfg.smat_seed, step, i))
         assert check_grad(host(a)[0], want, np.zeros(gsn.size, np.float32), incr).all(), f"tensor {i}"
+
+
+def test_tiles_across_a_high_counter_word_boundary():
+    """Global offsets just below multiples of 2^34 elements: the high word of the Philox group index
+    changes inside one tile, which takes the element-by-element path while the tiles around it take
+    the vector path.  Simulate (each noise form), accumulate and overwrite backward against the
+    oracle."""
+    g = torch.Generator(DEV).manual_seed(34)
+    sizes = [5000, 40000, 3001]
+    offs = [2 ** 34 - 1000, 2 ** 35 - 16384 - 512, 3 * 2 ** 34 - 2048]
+    ids = [3, 4, 5]
+    th = [torch.randn(n, device=DEV, generator=g) * 0.02 for n in sizes]
+    t0 = [(x + torch.randn(n, device=DEV, generator=g) * 1e-3).to(torch.bfloat16) for x, n in zip(th, sizes)]
+    gs = [(torch.randn(n, device=DEV, generator=g) * 1e-2).to(torch.bfloat16) for n in sizes]
+    gt = [torch.randn(n, device=DEV, generator=g) * 1e-3 for n in sizes]
+    fresh = [torch.full((n,), float("nan"), device=DEV) for n in sizes]
+    out = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    params = [dict(s=0.7, keep=0.4, sigma=2e-3, rescale=1, noise_kind=k) for k in (0, 1, 2)]
+    seed, step, lam = 0x5EED, 11, 0.5
+    g_old = [host(x)[0] for x in gt]
+    with smat.Plan(th, out, t0, gs, gt, tensor_ids=ids, elem_offsets=offs) as plan:
+        plan.set_params(params)
+        plan.simulate(seed, step)
+        plan.backward(seed, step, lam, accumulate=True)
+        plan.set_grads(None, fresh)
+        plan.backward(seed, step, lam, accumulate=False)
+        torch.cuda.synchronize()
+    for i, p in enumerate(params):
+        thn, _ = host(th[i])
+        t0n, _ = host(t0[i])
+        y, kept, eps = oracle.simulate_f64(thn, t0n, "bf16", p, seed, step, ids[i], offs[i])
+        coef = np.where(kept, oracle.coefficient(p["s"], p["keep"], p["rescale"]), 0.0)
+        got, _ = host(out[i])
+        ok, strict = check_theta_tilde(got, "bf16", y, thn, oracle.as_f64(t0n, "bf16"), coef, eps, p["sigma"])
+        assert ok.all(), f"tensor {i}: {np.count_nonzero(~ok)} theta~ mismatches"
+        assert np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))[strict].max(initial=0) <= 1
+        gsn, _ = host(gs[i])
+        incr = np.abs(oracle.simulated_gradient(gsn, "bf16", p, lam, seed, step, ids[i], offs[i]))
+        want = oracle.backward_accum(gsn, "bf16", g_old[i], p, lam, seed, step, ids[i], offs[i])
+        assert check_grad(host(gt[i])[0], want, g_old[i], incr).all(), f"tensor {i}"
+        np.testing.assert_array_equal(host(gt[i])[0].view(np.uint32)[~kept], g_old[i].view(np.uint32)[~kept])
+        zero = np.zeros(sizes[i], np.float32)
+        want0 = oracle.backward_accum(gsn, "bf16", zero, p, lam, seed, step, ids[i], offs[i])
+        assert check_grad(host(fresh[i])[0], want0, zero, incr).all(), f"tensor {i} (overwrite)"

@@ -170,11 +170,13 @@ def test_closed_forms_exact():
     assert torch.equal(gt, want)
 
 
-# sizes around quads and chunks; element offsets and base misalignment that force the per-element path
+# sizes around quads and chunks; element offsets and base misalignment that force the per-element path;
+# offsets whose tiles cross a multiple of 2^34 elements, where the high counter word of the groups changes
 @pytest.mark.parametrize("n,shift,off", [(1, 0, 0), (3, 0, 0), (4, 0, 0), (5, 0, 0), (4095, 0, 0),
                                           (16384, 0, 0), (16384 + 7, 0, 0), (3 * 16384 + 1, 0, 4),
                                           (50000, 1, 0), (50000, 0, 2), (50001, 3, 5), (70000, 2, 2 ** 33 + 1),
-                                          (70000, 0, 2 ** 34 + 4096)])
+                                          (70000, 0, 2 ** 34 + 4096), (5000, 0, 2 ** 34 - 1000),
+                                          (70001, 0, 2 ** 35 - 30000)])
 @pytest.mark.parametrize("dts", [("bf16", "bf16", "bf16"), ("f32", "f32", "f32"), ("f32", "bf16", "bf16")])
 def test_ragged_and_misaligned(n, shift, off, dts):
     tmap = {"bf16": torch.bfloat16, "f32": torch.float32}
