@@ -214,8 +214,9 @@ smat_status smat_plan_workspace_bytes(const smat_plan* plan, size_t* bytes);
 
 /* smat_plan_bind_workspace -- hand the plan its device workspace and upload its static tables on
  * `stream` (in offload mode also the first theta0 prefetch).  The workspace stays owned by the
- * caller and must outlive the plan.  Errors: SMAT_ERR_INVALID (null, misaligned or too small),
- * SMAT_ERR_STATE (already bound), SMAT_ERR_HIP. */
+ * caller and must outlive the plan.  A call that failed with SMAT_ERR_HIP leaves the plan unbound
+ * and may be repeated.  Errors: SMAT_ERR_INVALID (null, misaligned or too small), SMAT_ERR_STATE
+ * (already bound), SMAT_ERR_HIP. */
 smat_status smat_plan_bind_workspace(smat_plan* plan, void* workspace, size_t bytes, hipStream_t stream);
 
 /* smat_plan_set_params -- per-tensor s, keep, sigma for the next operations (count entries, in
@@ -255,8 +256,9 @@ typedef struct smat_adam_state {
 
 /* smat_plan_bind_adam_state -- hand the plan the optimizer state of every tensor (count entries in
  * descriptor order) for smat_adamw_fused_multi; uploads a small table on `stream`.  May be called
- * again to rebind.  Errors: SMAT_ERR_INVALID (null or overlapping arrays), SMAT_ERR_STATE (no
- * workspace), SMAT_ERR_HIP. */
+ * again to rebind.  The two moments of a tensor must not overlap each other, theta, theta0, the
+ * simulated buffer or the gradient arrays.  Errors: SMAT_ERR_INVALID (null or overlapping arrays),
+ * SMAT_ERR_STATE (no workspace), SMAT_ERR_HIP. */
 smat_status smat_plan_bind_adam_state(smat_plan* plan, const smat_adam_state* per_tensor, hipStream_t stream);
 
 /* smat_plan_set_grads -- point the plan at new gradient arrays: grad_sims (count device pointers

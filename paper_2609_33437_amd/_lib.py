@@ -171,6 +171,18 @@ def _scalar_ptr(t, what: str, dtype: str):
     return _dev_ptr(t, what)
 
 
+def _expect(t, n: int, code: int, what: str) -> None:
+    """The C ABI sees only pointers and element counts, so the binding checks that each array holds
+    exactly n elements of the dtype the launch assumes (a shorter or narrower array would be
+    overrun by the kernel)."""
+    if t is None:
+        return
+    if t.numel() != n:
+        raise SmatError(SMAT_ERR_INVALID, f"{what} holds {t.numel()} elements, expected {n}")
+    if dtype_code(t) != code:
+        raise SmatError(SMAT_ERR_DTYPE, f"{what} has dtype {t.dtype}, expected {'float32' if code == SMAT_F32 else 'bfloat16'}")
+
+
 def op_params(p) -> smat_op_params:
     """dict(s, keep, sigma, rescale=1, noise_kind=0) or an smat_op_params -> smat_op_params."""
     if isinstance(p, smat_op_params):
@@ -198,6 +210,7 @@ def smat_simulate(theta, theta0, out, params, seed: int, step: int, tensor_id: i
     n = theta.numel()
     if theta0.numel() != n or out.numel() != n:
         raise SmatError(SMAT_ERR_INVALID, "theta, theta0 and out differ in size")
+    _expect(theta, n, SMAT_F32, "theta")
     _check(lib().smat_simulate(_dev_ptr(theta, "theta"), _dev_ptr(theta0, "theta0"), dtype_code(theta0),
                                _dev_ptr(out, "out"), dtype_code(out), n, op_params(params),
                                rng_key(seed, step, tensor_id, elem_offset), _stream_handle(stream)))
@@ -209,6 +222,7 @@ def smat_backward_accum(grad_sim, grad_theta, params, lam: float, seed: int, ste
     n = grad_theta.numel()
     if grad_sim.numel() != n:
         raise SmatError(SMAT_ERR_INVALID, "grad_sim and grad_theta differ in size")
+    _expect(grad_theta, n, SMAT_F32, "grad_theta")
     _check(lib().smat_backward_accum(_dev_ptr(grad_sim, "grad_sim"), dtype_code(grad_sim),
                                      _dev_ptr(grad_theta, "grad_theta"), n, op_params(params), float(lam),
                                      rng_key(seed, step, tensor_id, elem_offset), _stream_handle(stream)))
@@ -217,9 +231,13 @@ def smat_backward_accum(grad_sim, grad_theta, params, lam: float, seed: int, ste
 def smat_debug_draws(n: int, params, seed: int, step: int, tensor_id: int = 0, elem_offset: int = 0,
                      mask_words=None, noise_words=None, kept=None, z=None, stream=None) -> None:
     """Raw per-element draws into the given GPU tensors (uint32 viewed as int32, uint8, fp32)."""
-    for name, t in (("mask_words", mask_words), ("noise_words", noise_words), ("kept", kept), ("z", z)):
-        if t is not None and t.numel() != n:
-            raise SmatError(SMAT_ERR_INVALID, f"{name} must hold n elements")
+    torch = _torch()
+    for name, t, size in (("mask_words", mask_words, 4), ("noise_words", noise_words, 4), ("kept", kept, 1),
+                          ("z", z, 4)):
+        if t is not None and (t.numel() != n or t.element_size() != size):
+            raise SmatError(SMAT_ERR_INVALID, f"{name} must hold n elements of {size} byte(s)")
+    if z is not None and z.dtype != torch.float32:
+        raise SmatError(SMAT_ERR_DTYPE, "z must be float32")
     _check(lib().smat_debug_draws(rng_key(seed, step, tensor_id, elem_offset), int(n), op_params(params),
                                   _dev_ptr(mask_words, "mask_words"), _dev_ptr(noise_words, "noise_words"),
                                   _dev_ptr(kept, "kept"), _dev_ptr(z, "z"), _stream_handle(stream)))
@@ -234,6 +252,8 @@ def smat_adamw_fused(grad_sim, theta, exp_avg, exp_avg_sq, params, lam: float, h
     for name, t in (("grad_sim", grad_sim), ("exp_avg", exp_avg), ("exp_avg_sq", exp_avg_sq), ("grad_acc", grad_acc)):
         if t is not None and t.numel() != n:
             raise SmatError(SMAT_ERR_INVALID, f"{name} differs in size from theta")
+    for name, t in (("theta", theta), ("exp_avg", exp_avg), ("exp_avg_sq", exp_avg_sq), ("grad_acc", grad_acc)):
+        _expect(t, n, SMAT_F32, name)
     _check(lib().smat_adamw_fused(_dev_ptr(grad_sim, "grad_sim"), dtype_code(grad_sim), _dev_ptr(grad_acc, "grad_acc"),
                                   _dev_ptr(theta, "theta"), _dev_ptr(exp_avg, "exp_avg"),
                                   _dev_ptr(exp_avg_sq, "exp_avg_sq"), n, op_params(params), float(lam),
@@ -256,6 +276,27 @@ class Plan:
         self._refs = [thetas, outs, theta0s, grad_sims, grad_thetas, theta0_hosts]
         ids = list(tensor_ids) if tensor_ids is not None else list(range(count))
         offs = list(elem_offsets) if elem_offsets is not None else [0] * count
+        if len(outs) != count or any(x is not None and len(x) != count
+                                      for x in (theta0s, grad_sims, grad_thetas, theta0_hosts, tensor_ids, elem_offsets)):
+            raise SmatError(SMAT_ERR_INVALID, "every per-tensor list must have one entry per tensor")
+        if dtypes is None:
+            t0_dt = dtype_code(theta0s[0] if theta0s is not None else outs[0]) if count else SMAT_BF16
+            out_dt = dtype_code(outs[0]) if count else SMAT_BF16
+            g_dt = dtype_code(grad_sims[0]) if (count and grad_sims is not None) else SMAT_BF16
+        else:
+            t0_dt, out_dt, g_dt = dtypes
+        for i in range(count):
+            n = thetas[i].numel()
+            _expect(thetas[i], n, SMAT_F32, f"tensor {i}: theta")
+            _expect(outs[i], n, out_dt, f"tensor {i}: out")
+            if theta0s is not None:
+                _expect(theta0s[i], n, t0_dt, f"tensor {i}: theta0")
+            if grad_sims is not None:
+                _expect(grad_sims[i], n, g_dt, f"tensor {i}: grad_sim")
+            if grad_thetas is not None:
+                _expect(grad_thetas[i], n, SMAT_F32, f"tensor {i}: grad_theta")
+            if theta0_hosts is not None:
+                _expect(theta0_hosts[i], n, t0_dt, f"tensor {i}: theta0_host")
         descs = (smat_tensor_desc * max(count, 1))()
         for i in range(count):
             d = descs[i]
@@ -272,12 +313,6 @@ class Plan:
             d.n = thetas[i].numel()
             d.tensor_id = ids[i]
             d.elem_offset = offs[i]
-        if dtypes is None:
-            t0_dt = dtype_code(theta0s[0] if theta0s is not None else outs[0]) if count else SMAT_BF16
-            out_dt = dtype_code(outs[0]) if count else SMAT_BF16
-            g_dt = dtype_code(grad_sims[0]) if (count and grad_sims is not None) else SMAT_BF16
-        else:
-            t0_dt, out_dt, g_dt = dtypes
         self.dtypes = (t0_dt, out_dt, g_dt)
         plan = c_void_p()
         _check(lib().smat_plan_create(descs, count, t0_dt, out_dt, g_dt, 1 if offload else 0, ctypes.byref(plan)))
@@ -317,9 +352,8 @@ class Plan:
                 continue
             if len(ts) != self.count:
                 raise SmatError(SMAT_ERR_INVALID, f"one {what} per tensor")
-            for g, th in zip(ts, self._refs[0]):
-                if g.numel() != th.numel() or dtype_code(g) != dt:
-                    raise SmatError(SMAT_ERR_INVALID, f"{what} must match the plan's sizes and dtype")
+            for i, (g, th) in enumerate(zip(ts, self._refs[0])):
+                _expect(g, th.numel(), dt, f"tensor {i}: {what}")
             arrays.append((c_void_p * max(self.count, 1))(*[_dev_ptr(g, what) for g in ts]))
         _check(lib().smat_plan_set_grads(self._plan, arrays[0], arrays[1], _stream_handle(stream)))
         if grad_sims is not None:
@@ -330,6 +364,9 @@ class Plan:
     def bind_adam_state(self, exp_avgs: Sequence, exp_avg_sqs: Sequence, stream=None) -> None:
         if len(exp_avgs) != self.count or len(exp_avg_sqs) != self.count:
             raise SmatError(SMAT_ERR_INVALID, "one optimizer state per tensor")
+        for i, (a, b, th) in enumerate(zip(exp_avgs, exp_avg_sqs, self._refs[0])):
+            _expect(a, th.numel(), SMAT_F32, f"tensor {i}: exp_avg")
+            _expect(b, th.numel(), SMAT_F32, f"tensor {i}: exp_avg_sq")
         arr = (smat_adam_state * max(self.count, 1))(
             *[smat_adam_state(_dev_ptr(a, "exp_avg"), _dev_ptr(b, "exp_avg_sq")) for a, b in zip(exp_avgs, exp_avg_sqs)])
         self._refs.append((exp_avgs, exp_avg_sqs))
@@ -426,12 +463,23 @@ class MergePlan:
         self._refs = [theta0s, outs, experts]
         ids = list(tensor_ids) if tensor_ids is not None else list(range(count))
         offs = list(elem_offsets) if elem_offsets is not None else [0] * count
+        if count:
+            dts = {dtype_code(experts[j][i]) for j in range(nexp) for i in range(count)}
+            if len(dts) != 1:
+                raise SmatError(SMAT_ERR_DTYPE, "all experts must share one dtype")
+            e_dt, t0_dt, out_dt = dts.pop(), dtype_code(theta0s[0]), dtype_code(outs[0])
+        else:
+            e_dt = t0_dt = out_dt = SMAT_BF16
+        for i in range(count):
+            n = theta0s[i].numel()
+            _expect(theta0s[i], n, t0_dt, f"tensor {i}: theta0")
+            _expect(outs[i], n, out_dt, f"tensor {i}: out")
+            for j in range(nexp):
+                _expect(experts[j][i], n, e_dt, f"tensor {i}: expert {j}")
         descs = (smat_merge_desc * max(count, 1))()
         ptrs = (c_void_p * max(count * nexp, 1))()
         for i in range(count):
             n = theta0s[i].numel()
-            if outs[i].numel() != n or any(experts[j][i].numel() != n for j in range(nexp)):
-                raise SmatError(SMAT_ERR_INVALID, f"tensor {i}: experts, theta0 and out differ in size")
             d = descs[i]
             d.theta0 = _dev_ptr(theta0s[i], "theta0")
             d.out = _dev_ptr(outs[i], "out")
@@ -440,13 +488,6 @@ class MergePlan:
             d.elem_offset = offs[i]
             for j in range(nexp):
                 ptrs[i * nexp + j] = _dev_ptr(experts[j][i], "expert")
-        if count:
-            dts = {dtype_code(experts[j][i]) for j in range(nexp) for i in range(count)}
-            if len(dts) != 1:
-                raise SmatError(SMAT_ERR_DTYPE, "all experts must share one dtype")
-            e_dt, t0_dt, out_dt = dts.pop(), dtype_code(theta0s[0]), dtype_code(outs[0])
-        else:
-            e_dt = t0_dt = out_dt = SMAT_BF16
         plan = c_void_p()
         _check(lib().smat_merge_plan_create(descs, count, ptrs, nexp, e_dt, t0_dt, out_dt, ctypes.byref(plan)))
         self._plan = plan

@@ -492,27 +492,32 @@ extern "C" smat_status smat_plan_bind_workspace(smat_plan* p, void* workspace, s
     return fail(SMAT_ERR_INVALID, "smat_plan_bind_workspace: workspace of %zu bytes, need %zu", bytes, p->ws_bytes);
 
   const size_t static_bytes = p->off_params;
-  SMAT_HIP(hipHostMalloc((void**)&p->static_staging, std::max<size_t>(static_bytes, 256), hipHostMallocDefault));
+  // each resource is created once: a call that failed part-way can be retried without leaking
+  if (!p->static_staging)
+    SMAT_HIP(hipHostMalloc((void**)&p->static_staging, std::max<size_t>(static_bytes, 256), hipHostMallocDefault));
   for (ParamRec*& s : p->params_staging)
-    SMAT_HIP(hipHostMalloc((void**)&s, sizeof(ParamRec) * std::max(p->count, 1), hipHostMallocDefault));
+    if (!s) SMAT_HIP(hipHostMalloc((void**)&s, sizeof(ParamRec) * std::max(p->count, 1), hipHostMallocDefault));
   std::memset(p->static_staging, 0, static_bytes);
   std::memcpy(p->static_staging + p->off_recs, p->recs.data(), sizeof(TensorRec) * p->count);
   std::memcpy(p->static_staging + p->off_chunks, p->chunks.data(), sizeof(uint2) * p->chunks.size());
   std::memcpy(p->static_staging + p->off_expert, p->expert_ptrs.data(), sizeof(void*) * p->count);
   std::memcpy(p->static_staging + p->off_sim, p->sim_ptrs.data(), sizeof(void*) * p->count);
-  SMAT_HIP(hipEventCreateWithFlags(&p->ev_static, hipEventDisableTiming));
-  for (hipEvent_t& e : p->ev_params) SMAT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  if (!p->ev_static) SMAT_HIP(hipEventCreateWithFlags(&p->ev_static, hipEventDisableTiming));
+  for (hipEvent_t& e : p->ev_params)
+    if (!e) SMAT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  if (p->offload) {
+    if (!p->copy_stream) SMAT_HIP(hipStreamCreateWithFlags(&p->copy_stream, hipStreamNonBlocking));
+    if (!p->ev_release) SMAT_HIP(hipEventCreateWithFlags(&p->ev_release, hipEventDisableTiming));
+    if (!p->ev_prefetch) SMAT_HIP(hipEventCreateWithFlags(&p->ev_prefetch, hipEventDisableTiming));
+  }
   if (static_bytes > 0)
     SMAT_HIP(hipMemcpyAsync(workspace, p->static_staging, static_bytes, hipMemcpyHostToDevice, stream));
   SMAT_HIP(hipEventRecord(p->ev_static, stream));
-  p->ws = static_cast<char*>(workspace);
   if (p->offload) {
-    SMAT_HIP(hipStreamCreateWithFlags(&p->copy_stream, hipStreamNonBlocking));
-    SMAT_HIP(hipEventCreateWithFlags(&p->ev_release, hipEventDisableTiming));
-    SMAT_HIP(hipEventCreateWithFlags(&p->ev_prefetch, hipEventDisableTiming));
     smat_status st = enqueue_prefetch(p, stream);
     if (st != SMAT_OK) return st;
   }
+  p->ws = static_cast<char*>(workspace);
   return SMAT_OK;
 }
 
@@ -594,9 +599,10 @@ extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_s
     smat_status st = check_adam_ptrs(r.theta, adam[i].exp_avg, adam[i].exp_avg_sq, r.grad_sim, p->g_dt, r.grad_theta,
                                      r.n, where);
     if (st != SMAT_OK) return st;
-    if (overlap(adam[i].exp_avg, (size_t)r.n * 4, r.out, (size_t)r.n * dtype_bytes(p->out_dt)) ||
-        overlap(adam[i].exp_avg_sq, (size_t)r.n * 4, r.out, (size_t)r.n * dtype_bytes(p->out_dt)))
-      return fail(SMAT_ERR_INVALID, "%s: moments must not overlap the simulated buffer", where);
+    for (const float* m : {adam[i].exp_avg, adam[i].exp_avg_sq})
+      if (overlap(m, (size_t)r.n * 4, r.out, (size_t)r.n * dtype_bytes(p->out_dt)) ||
+          overlap(m, (size_t)r.n * 4, r.theta0, (size_t)r.n * dtype_bytes(p->t0_dt)))
+        return fail(SMAT_ERR_INVALID, "%s: moments must not overlap theta0 or the simulated buffer", where);
     recs[i].sflags = (r.sflags & ~(smat::kVecAdam | smat::kVecAdamAcc)) |
                      adam_flags(r.theta, adam[i].exp_avg, adam[i].exp_avg_sq, r.grad_sim, p->g_dt, r.grad_theta,
                                 r.elem_offset);
@@ -979,15 +985,18 @@ extern "C" smat_status smat_merge_plan_bind_workspace(smat_merge_plan* p, void* 
     return fail(SMAT_ERR_INVALID, "smat_merge_plan_bind_workspace: workspace of %zu bytes, need %zu", bytes, p->ws_bytes);
   const size_t static_bytes = p->off_terms;
   const size_t cells = (size_t)p->count * p->nexp;
-  SMAT_HIP(hipHostMalloc((void**)&p->static_staging, std::max<size_t>(static_bytes, 256), hipHostMallocDefault));
+  // each resource is created once: a call that failed part-way can be retried without leaking
+  if (!p->static_staging)
+    SMAT_HIP(hipHostMalloc((void**)&p->static_staging, std::max<size_t>(static_bytes, 256), hipHostMallocDefault));
   for (MergeRec*& s : p->terms_staging)
-    SMAT_HIP(hipHostMalloc((void**)&s, sizeof(MergeRec) * std::max<size_t>(cells, 1), hipHostMallocDefault));
+    if (!s) SMAT_HIP(hipHostMalloc((void**)&s, sizeof(MergeRec) * std::max<size_t>(cells, 1), hipHostMallocDefault));
   std::memset(p->static_staging, 0, static_bytes);
   std::memcpy(p->static_staging + p->off_recs, p->recs.data(), sizeof(TensorRec) * p->count);
   std::memcpy(p->static_staging + p->off_chunks, p->chunks.data(), sizeof(uint2) * p->chunks.size());
   std::memcpy(p->static_staging + p->off_experts, p->experts.data(), sizeof(void*) * cells);
-  SMAT_HIP(hipEventCreateWithFlags(&p->ev_static, hipEventDisableTiming));
-  for (hipEvent_t& e : p->ev_terms) SMAT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  if (!p->ev_static) SMAT_HIP(hipEventCreateWithFlags(&p->ev_static, hipEventDisableTiming));
+  for (hipEvent_t& e : p->ev_terms)
+    if (!e) SMAT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   if (static_bytes > 0)
     SMAT_HIP(hipMemcpyAsync(workspace, p->static_staging, static_bytes, hipMemcpyHostToDevice, stream));
   SMAT_HIP(hipEventRecord(p->ev_static, stream));

@@ -158,3 +158,20 @@ def test_plan_tiles_across_a_high_counter_word_boundary(accumulate):
     for i in range(len(sizes)):
         _check(*states[i], old[i], host(gs[i])[0], "bf16", params[i], 0.5, hp, 21, 6, ids[i], offs[i],
                host(acc[i])[0] if accumulate else None)
+
+
+def test_bind_adam_state_rejects_moments_over_theta0_or_buffer():
+    # the optimizer step writes the moments: they must not alias theta0 (resident mode) or the buffer
+    n = 4096
+    th = torch.zeros(n, device=DEV)
+    t0_store = torch.zeros(2 * n, dtype=torch.bfloat16, device=DEV)    # theta0 = its first n entries
+    out_store = torch.zeros(2 * n, dtype=torch.bfloat16, device=DEV)   # buffer = its first n entries
+    gs = torch.zeros(n, dtype=torch.bfloat16, device=DEV)
+    m2 = torch.zeros(n, device=DEV)
+    with smat.Plan([th], [out_store[:n]], [t0_store[:n]], [gs], None) as plan:
+        for bad in (t0_store.view(torch.float32), out_store.view(torch.float32)):   # n floats each
+            with pytest.raises(smat.SmatError, match="INVALID"):
+                plan.bind_adam_state([bad], [m2])
+            with pytest.raises(smat.SmatError, match="INVALID"):
+                plan.bind_adam_state([m2.clone()], [bad])
+        plan.bind_adam_state([torch.zeros(n, device=DEV)], [m2])      # disjoint arrays are accepted

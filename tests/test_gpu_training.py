@@ -278,7 +278,7 @@ def test_bf16_autocast_loop_runs():
         with torch.autocast("cuda", dtype=torch.bfloat16):
             loss = model.loss(batches[step])
         loss.backward()
-        losses.append(float(loss))
+        losses.append(float(loss.detach()))
         if sim:
             w.end(opt, fused=(step == 7))
             assert all(p.dtype == torch.float32 and p.data_ptr() == m.data_ptr() for p, m in zip(w.params, masters))
