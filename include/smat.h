@@ -273,6 +273,15 @@ smat_status smat_plan_bind_adam_state(smat_plan* plan, const smat_adam_state* pe
 smat_status smat_plan_set_grads(smat_plan* plan, const void* const* grad_sims, float* const* grad_thetas,
                                 hipStream_t stream);
 
+/* smat_plan_clear_grads -- forget the plan's gradient arrays: bit 0 of `which` drops grad_sim, bit 1
+ * grad_theta.  A caller whose gradient tensors live for one step clears them once the step's
+ * operations are queued, so that no pointer to a freed tensor is kept (set_grads with a NULL array
+ * keeps the current one, and would check new arrays for overlap against it).  Operations that read
+ * a cleared kind return SMAT_ERR_STATE until set_grads supplies it again.  Host-side only: enqueues
+ * nothing, and operations already queued keep the arrays they were given.
+ * Errors: SMAT_ERR_INVALID (null plan, `which` outside 1..3). */
+smat_status smat_plan_clear_grads(smat_plan* plan, int32_t which);
+
 /* smat_adamw_fused_multi -- smat_adamw_fused over every tensor of the plan in one launch: theta is
  * desc.theta (the expert storage, updated in place), grad_sim is desc.grad_sim and, when accumulate
  * is nonzero, grad_acc is desc.grad_theta (read, not written); grad_scale_dev as in

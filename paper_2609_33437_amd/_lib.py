@@ -28,7 +28,7 @@ EXPORTS = (
     "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi", "smat_grad_norm_multi",
     "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
     "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
-    "smat_stream_copy", "smat_backward_multi",
+    "smat_stream_copy", "smat_backward_multi", "smat_plan_clear_grads",
 )
 
 
@@ -106,6 +106,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_plan_set_grads": [P, POINTER(P), POINTER(P), P],
         "smat_stream_copy": [P, P, c_uint64, P],
         "smat_backward_multi": [P, c_uint64, c_uint32, c_float, c_int32, P],
+        "smat_plan_clear_grads": [P, c_int32],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -360,6 +361,17 @@ class Plan:
             self._refs[3] = list(grad_sims)
         if grad_thetas is not None:
             self._refs[4] = list(grad_thetas)
+
+    def clear_grads(self, grad_sims: bool = True, grad_thetas: bool = True) -> None:
+        """Forget the plan's gradient arrays of the chosen kinds (smat_plan_clear_grads) and drop
+        the references the plan object held to them."""
+        which = (1 if grad_sims else 0) | (2 if grad_thetas else 0)
+        if which:
+            _check(lib().smat_plan_clear_grads(self._plan, which))
+        if grad_sims:
+            self._refs[3] = None
+        if grad_thetas:
+            self._refs[4] = None
 
     def bind_adam_state(self, exp_avgs: Sequence, exp_avg_sqs: Sequence, stream=None) -> None:
         if len(exp_avgs) != self.count or len(exp_avg_sqs) != self.count:

@@ -673,6 +673,26 @@ extern "C" smat_status smat_plan_set_grads(smat_plan* p, const void* const* grad
   return SMAT_OK;
 }
 
+extern "C" smat_status smat_plan_clear_grads(smat_plan* p, int32_t which) {
+  if (!p) return fail(SMAT_ERR_INVALID, "smat_plan_clear_grads: null plan");
+  if (which < 1 || which > 3) return fail(SMAT_ERR_INVALID, "smat_plan_clear_grads: which must be 1, 2 or 3");
+  // the device records keep the old pointers, but no launch reads a kind whose has_* flag is false,
+  // and set_grads uploads fresh records before any launch that needs them
+  for (int32_t i = 0; i < p->count; ++i) {
+    if (which & 1) {
+      p->recs[i].grad_sim = nullptr;
+      p->descs[i].grad_sim = nullptr;
+    }
+    if (which & 2) {
+      p->recs[i].grad_theta = nullptr;
+      p->descs[i].grad_theta = nullptr;
+    }
+  }
+  if (which & 1) p->has_gs = false;
+  if (which & 2) p->has_gt = false;
+  return SMAT_OK;
+}
+
 extern "C" smat_status smat_adamw_fused_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
                                               smat_adamw_params hp, int32_t accumulate, const float* grad_scale_dev,
                                               hipStream_t stream) {

@@ -265,8 +265,10 @@ class SimulatedMergeTraining:
             acc = self._accumulator(zeros=False)
             self.plan.set_grads(grads, acc)
             self._grads = grads     # kept alive until the kernels that read them have been queued
-            return self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step, max_norm,
+            norm = self._fused_adam(optimizer, dict(hp, grad_scale=float(grad_scale)), step, max_norm,
                                     accumulate=acc is not None)
+            self.plan.clear_grads()  # this step's gradient tensors may be freed from here on
+            return norm
         # the expert gradient is written into fresh fp32 tensors, as an ordinary step's gradients
         # are, or added to the expert loss's gradient of this step
         acc = self._accumulator(zeros=False)
@@ -274,6 +276,7 @@ class SimulatedMergeTraining:
         self.plan.set_grads(grads, expert)
         self._grads = grads
         self.plan.backward(self.seed, step, self.lam, accumulate=acc is not None)
+        self.plan.clear_grads()      # the caller frees these tensors (zero_grad) after its optimizer step
         self._restore()
         for p, g in zip(self.params, expert):
             p.grad = g

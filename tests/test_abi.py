@@ -157,6 +157,30 @@ def test_plan_create_validation_without_gpu():
     assert lib.smat_plan_destroy(None) == 0
 
 
+def test_clear_grads_without_gpu():
+    """Clearing is host-side: it validates `which`, and afterwards the operations that read a cleared
+    kind are state errors whatever else is missing."""
+    lib = smat.lib()
+    A = 1 << 20
+    arr = (_lib.smat_tensor_desc * 1)(_desc(1 * A, 2 * A, 3 * A, 4 * A, 5 * A, 1000, 0))
+    p = ctypes.c_void_p()
+    assert lib.smat_plan_create(arr, 1, 1, 1, 1, 0, ctypes.byref(p)) == 0
+    assert lib.smat_plan_clear_grads(None, 3) == _lib.SMAT_ERR_INVALID
+    for bad in (0, 4, -1):
+        assert lib.smat_plan_clear_grads(p, bad) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_plan_clear_grads(p, 2) == _lib.SMAT_OK
+    lib.smat_last_error.restype = ctypes.c_char_p
+    assert lib.smat_backward_multi(p, 0, 0, 1.0, 0, None) == _lib.SMAT_ERR_STATE        # grad_theta gone
+    assert b"gradient arrays not set" in lib.smat_last_error()
+    assert lib.smat_grad_norm_multi(p, 0, 0, 1.0, 1, 1.0, ctypes.c_void_p(6 * A), None, None) == _lib.SMAT_ERR_STATE
+    assert b"gradient arrays not set" in lib.smat_last_error()
+    assert lib.smat_plan_clear_grads(p, 1) == _lib.SMAT_OK
+    assert lib.smat_grad_norm_multi(p, 0, 0, 1.0, 0, 1.0, ctypes.c_void_p(6 * A), None, None) == _lib.SMAT_ERR_STATE
+    assert b"gradient arrays not set" in lib.smat_last_error()
+    assert lib.smat_plan_clear_grads(p, 3) == _lib.SMAT_OK                               # clearing twice is fine
+    assert lib.smat_plan_destroy(p) == 0
+
+
 @pytest.mark.parametrize("bad", [dict(beta1=1.0), dict(beta2=-0.5), dict(eps=0.0), dict(lr=-1.0), dict(step=0),
                                  dict(weight_decay=float("nan")), dict(grad_scale=float("inf"))])
 def test_invalid_adamw_hyperparameters_rejected_before_launch(bad):

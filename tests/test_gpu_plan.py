@@ -424,3 +424,37 @@ def test_tiles_across_a_high_counter_word_boundary():
         zero = np.zeros(sizes[i], np.float32)
         want0 = oracle.backward_accum(gsn, "bf16", zero, p, lam, seed, step, ids[i], offs[i])
         assert check_grad(host(fresh[i])[0], want0, zero, incr).all(), f"tensor {i} (overwrite)"
+
+
+def test_clear_grads_lets_new_arrays_reuse_freed_memory(mini):
+    """A plan keeps its gradient pointers until they are replaced.  Once the tensors behind them are
+    freed, the caching allocator may place the next step's gradients in the same memory: setting
+    those with grad_thetas kept would be refused as an overlap, clearing first lets them in, and a
+    cleared kind is a state error until it is supplied again."""
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    step = 6
+    params = workloads.step_params(cfg, inp.settings, step)
+    with smat.Plan(th, out, t0) as plan:
+        plan.set_params(params)
+        old = [torch.zeros(x.numel(), device=DEV) for x in th]
+        plan.set_grads(gs, old)
+        reuse = [o.view(torch.bfloat16)[:x.numel()] for o, x in zip(old, th)]   # inside the old arrays
+        for r, g in zip(reuse, gs):
+            r.copy_(g.view(-1))
+        with pytest.raises(smat.SmatError, match="INVALID"):
+            plan.set_grads(reuse, None)
+        plan.clear_grads(grad_sims=False, grad_thetas=True)
+        plan.set_grads(reuse, None)
+        with pytest.raises(smat.SmatError, match="STATE"):
+            plan.backward(cfg.smat_seed, step, cfg.lam, accumulate=True)
+        fresh = [torch.empty(x.numel(), device=DEV) for x in th]
+        plan.set_grads(None, fresh)
+        plan.backward(cfg.smat_seed, step, cfg.lam, accumulate=False)
+        torch.cuda.synchronize()
+    for i in range(cfg.count):
+        gsn = host(inp.grad_sim[i])[0].ravel()
+        zero = np.zeros(gsn.size, np.float32)
+        want = oracle.backward_accum(gsn, "bf16", zero, params[i], cfg.lam, cfg.smat_seed, step, i)
+        incr = np.abs(oracle.simulated_gradient(gsn, "bf16", params[i], cfg.lam, cfg.smat_seed, step, i))
+        assert check_grad(host(fresh[i])[0], want, zero, incr).all(), f"tensor {i}"
