@@ -788,7 +788,8 @@ extern "C" smat_status smat_stream_copy(const void* src, void* dst, uint64_t byt
   if (!aligned(src, 16) || !aligned(dst, 16) || bytes % 16 != 0)
     return fail(SMAT_ERR_INVALID, "smat_stream_copy: pointers and size must be multiples of 16 bytes");
   if (overlap(src, (size_t)bytes, dst, (size_t)bytes)) return fail(SMAT_ERR_INVALID, "smat_stream_copy: overlap");
-  if (bytes / 16 / (smat::kBlock * 4) >= 0x7FFFFFFFull) return fail(SMAT_ERR_INVALID, "smat_stream_copy: too large");
+  if (bytes / 16 / (smat::kBlock * smat::kCopyVecs) >= 0x7FFFFFFFull)
+    return fail(SMAT_ERR_INVALID, "smat_stream_copy: too large");
   SMAT_HIP(smat::launch_stream_copy(src, dst, bytes / 16, stream));
   return SMAT_OK;
 }

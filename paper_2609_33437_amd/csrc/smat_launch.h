@@ -60,6 +60,7 @@ hipError_t launch_merge_multi(const TensorRec* recs, const void* const* experts,
                               int out_dtype, hipStream_t stream);
 
 // Plain streaming copy of n16 16-byte vectors (the measured HBM reference).
+constexpr int kCopyVecs = 1;  // 16-byte vectors per thread of the reference copy
 hipError_t launch_stream_copy(const void* src, void* dst, uint64_t n16, hipStream_t stream);
 
 hipError_t launch_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t elem_offset,
