@@ -1,0 +1,115 @@
+"""Seeded random sweep of the simulate/backward parity against the oracle, over combinations the
+hand-written cases do not enumerate: sizes from 1 to ~70K, buffer misalignment, element offsets
+anywhere below 2^40 (and tiles that cross a multiple of 2^34), all dtype mixes, keep at 0, tiny,
+just below 1 and 1, negative and zero scales, every noise form, rescale on and off, accumulate and
+overwrite.  Single tensors through smat_simulate / smat_backward_accum, ragged lists through a plan."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_33437_amd as smat
+from tolerances import check_grad, check_theta_tilde, ordered
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+DT = {"bf16": torch.bfloat16, "f32": torch.float32}
+KEEP_FP32_BELOW_1 = float(np.nextafter(np.float32(1.0), np.float32(0.0)))
+
+
+def host(t):
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16), "bf16"
+    return t.numpy().copy(), "f32"
+
+
+def draw_case(rng):
+    n = int(np.exp(rng.uniform(0.0, np.log(70000.0))))
+    off = int(rng.choice([0, 4 * int(rng.integers(0, 2 ** 38)), int(rng.integers(0, 2 ** 40)),
+                          2 ** 34 - 4 * int(rng.integers(1, 600)), 2 ** 35 - int(rng.integers(1, 3000))]))
+    keep = float(np.float32(rng.choice([0.0, 1.0, 0.5, rng.uniform(0.01, 0.99), 1e-9, KEEP_FP32_BELOW_1])))
+    s = float(np.float32(rng.choice([0.0, 1.0, rng.uniform(-1.0, 2.0)])))
+    sigma = float(np.float32(rng.choice([0.0, 10 ** rng.uniform(-4, -2)])))
+    p = dict(s=s, keep=keep, sigma=sigma, rescale=int(rng.integers(0, 2)), noise_kind=int(rng.integers(0, 3)))
+    return n, off, p, int(rng.integers(0, 4))
+
+
+def tensors(rng, n, shift, t0_dt, out_dt, g_dt, gen):
+    base = torch.randn(n + 8, device=DEV, generator=gen) * 0.02
+    th = base[shift:shift + n]
+    t0 = (base + torch.randn(n + 8, device=DEV, generator=gen) * 1e-3).to(DT[t0_dt])[shift:shift + n]
+    out = torch.empty(n + 8, dtype=DT[out_dt], device=DEV)[shift:shift + n]
+    gs = (torch.randn(n + 8, device=DEV, generator=gen) * 1e-2).to(DT[g_dt])[shift:shift + n]
+    gt = (torch.randn(n + 8, device=DEV, generator=gen) * 1e-3)[shift:shift + n]
+    return th, t0, out, gs, gt
+
+
+def check_sim(th, t0, out, p, seed, step, tid, off, what):
+    thn, _ = host(th)
+    t0n, t0_dt = host(t0)
+    got, out_dt = host(out)
+    y, kept, eps = oracle.simulate_f64(thn, t0n, t0_dt, p, seed, step, tid, off)
+    coef = np.where(kept, oracle.coefficient(p["s"], p["keep"], p["rescale"]), 0.0)
+    ok, strict = check_theta_tilde(got, out_dt, y, thn, oracle.as_f64(t0n, t0_dt), coef, eps, p["sigma"])
+    assert ok.all(), f"{what}: {np.count_nonzero(~ok)} theta~ mismatches, first {np.flatnonzero(~ok)[:5]}"
+    if out_dt == "bf16":
+        assert np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))[strict].max(initial=0) <= 1, what
+    return kept
+
+
+def check_bwd(got, gs, g_old, p, lam, seed, step, tid, off, kept, what):
+    gsn, gs_dt = host(gs)
+    want = oracle.backward_accum(gsn, gs_dt, g_old, p, lam, seed, step, tid, off)
+    incr = np.abs(oracle.simulated_gradient(gsn, gs_dt, p, lam, seed, step, tid, off))
+    assert check_grad(got, want, g_old, incr).all(), what
+    np.testing.assert_array_equal(got.view(np.uint32)[~kept], g_old.view(np.uint32)[~kept], err_msg=what)
+
+
+def test_random_single_tensors():
+    rng = np.random.default_rng(20260)
+    gen = torch.Generator(DEV).manual_seed(20260)
+    for case in range(120):
+        n, off, p, shift = draw_case(rng)
+        t0_dt, out_dt, g_dt = (str(rng.choice(["bf16", "f32"])) for _ in range(3))
+        seed, step, tid = int(rng.integers(0, 2 ** 63)), int(rng.integers(0, 2 ** 30)), int(rng.integers(0, 2 ** 32))
+        lam = float(np.float32(rng.uniform(-1.0, 2.0)))
+        what = f"case {case}: n={n} off={off} shift={shift} dtypes={t0_dt}/{out_dt}/{g_dt} p={p} lam={lam}"
+        th, t0, out, gs, gt = tensors(rng, n, shift, t0_dt, out_dt, g_dt, gen)
+        g_old = host(gt)[0]
+        smat.smat_simulate(th, t0, out, p, seed, step, tid, off)
+        smat.smat_backward_accum(gs, gt, p, lam, seed, step, tid, off)
+        torch.cuda.synchronize()
+        kept = check_sim(th, t0, out, p, seed, step, tid, off, what)
+        check_bwd(host(gt)[0], gs, g_old, p, lam, seed, step, tid, off, kept, what)
+
+
+def test_random_lists():
+    rng = np.random.default_rng(20261)
+    gen = torch.Generator(DEV).manual_seed(20261)
+    for case in range(50):
+        count = int(rng.integers(1, 7))
+        t0_dt, out_dt, g_dt = (str(rng.choice(["bf16", "f32"])) for _ in range(3))
+        seed, step = int(rng.integers(0, 2 ** 63)), int(rng.integers(0, 2 ** 30))
+        lam = float(np.float32(rng.uniform(-1.0, 2.0)))
+        items = [draw_case(rng) for _ in range(count)]
+        ids = [int(x) for x in rng.choice(2 ** 32, size=count, replace=False)]
+        ts = [tensors(rng, n, shift, t0_dt, out_dt, g_dt, gen) for n, _, _, shift in items]
+        th, t0, out, gs, gt = (list(x) for x in zip(*ts))
+        fresh = [torch.full_like(g, float("nan")) for g in gt]
+        offs, params = [it[1] for it in items], [it[2] for it in items]
+        g_old = [host(g)[0] for g in gt]
+        with smat.Plan(th, out, t0, gs, gt, tensor_ids=ids, elem_offsets=offs) as plan:
+            plan.set_params(params)
+            plan.simulate(seed, step)
+            plan.backward(seed, step, lam, accumulate=True)
+            plan.set_grads(None, fresh)
+            plan.backward(seed, step, lam, accumulate=False)
+            torch.cuda.synchronize()
+        for i in range(count):
+            n, off, p, shift = items[i]
+            what = f"list {case} tensor {i}: n={n} off={off} shift={shift} dtypes={t0_dt}/{out_dt}/{g_dt} p={p}"
+            kept = check_sim(th[i], t0[i], out[i], p, seed, step, ids[i], off, what)
+            check_bwd(host(gt[i])[0], gs[i], g_old[i], p, lam, seed, step, ids[i], off, kept, what)
+            zero = np.zeros(n, np.float32)
+            check_bwd(host(fresh[i])[0], gs[i], zero, p, lam, seed, step, ids[i], off, kept, what + " (overwrite)")
