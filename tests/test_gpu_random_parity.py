@@ -1,8 +1,9 @@
-"""Seeded random sweep of the simulate/backward parity against the oracle, over combinations the
-hand-written cases do not enumerate: sizes from 1 to ~70K, buffer misalignment, element offsets
-anywhere below 2^40 (and tiles that cross a multiple of 2^34), all dtype mixes, keep at 0, tiny,
-just below 1 and 1, negative and zero scales, every noise form, rescale on and off, accumulate and
-overwrite.  Single tensors through smat_simulate / smat_backward_accum, ragged lists through a plan."""
+"""Seeded random sweeps of the simulate/backward, the fused AdamW step and the merge against the
+oracle, over combinations the hand-written cases do not enumerate: sizes from 1 to ~70K, buffer
+misalignment, element offsets anywhere below 2^40 (and tiles that cross a multiple of 2^34), all
+dtype mixes, keep at 0, tiny, just below 1 and 1, negative and zero scales, every noise form,
+rescale on and off, accumulate and overwrite, random optimizer settings, 1-16 experts.  Single
+tensors through the single-tensor entry points, ragged lists through a plan."""
 import numpy as np
 import pytest
 import torch
@@ -113,3 +114,83 @@ def test_random_lists():
             check_bwd(host(gt[i])[0], gs[i], g_old[i], p, lam, seed, step, ids[i], off, kept, what)
             zero = np.zeros(n, np.float32)
             check_bwd(host(fresh[i])[0], gs[i], zero, p, lam, seed, step, ids[i], off, kept, what + " (overwrite)")
+
+
+def draw_adam(rng):
+    return dict(lr=float(10 ** rng.uniform(-6, -2)), beta1=float(rng.choice([0.0, 0.9, rng.uniform(0.5, 0.99)])),
+                beta2=float(rng.choice([0.999, rng.uniform(0.9, 0.9999)])), eps=float(10 ** rng.uniform(-10, -6)),
+                weight_decay=float(rng.choice([0.0, 1e-3, rng.uniform(0.0, 0.1)])),
+                grad_scale=float(rng.choice([1.0, rng.uniform(0.1, 2.0)])), step=int(rng.integers(1, 1000)))
+
+
+def check_adamw(th, m1, m2, old, gs, p, lam, hp, seed, step, tid, off, acc, what):
+    from tolerances import check_adam
+    gsn, gs_dt = host(gs)
+    _, f64 = oracle.adamw_fused(gsn, gs_dt, old[0], old[1], old[2], p, lam, hp, seed, step, tid, off, grad_acc=acc)
+    gmag = np.abs(oracle.simulated_gradient(gsn, gs_dt, p, lam, seed, step, tid, off, None, hp["grad_scale"]))
+    if acc is not None:
+        gmag = gmag + abs(float(np.float32(hp["grad_scale"]))) * np.abs(np.asarray(acc, dtype=np.float64))
+    ok = check_adam((host(th)[0], host(m1)[0], host(m2)[0]), old, f64, hp, gmag)
+    for name, o in zip(("theta", "exp_avg", "exp_avg_sq"), ok):
+        assert o.all(), f"{what}: {name} {np.count_nonzero(~o)} mismatches, first {np.flatnonzero(~o)[:5]}"
+
+
+def test_random_fused_adamw():
+    rng = np.random.default_rng(20262)
+    gen = torch.Generator(DEV).manual_seed(20262)
+    for case in range(40):
+        n, off, p, shift = draw_case(rng)
+        g_dt = str(rng.choice(["bf16", "f32"]))
+        accumulate = bool(rng.integers(0, 2))
+        seed, step, tid = int(rng.integers(0, 2 ** 63)), int(rng.integers(0, 2 ** 30)), int(rng.integers(0, 2 ** 32))
+        lam = float(np.float32(rng.uniform(-1.0, 2.0)))
+        hp = draw_adam(rng)
+        what = f"case {case}: n={n} off={off} shift={shift} g={g_dt} acc={accumulate} p={p} lam={lam} hp={hp}"
+        th = (torch.randn(n + 8, device=DEV, generator=gen) * 0.02)[shift:shift + n]
+        m1 = (torch.randn(n + 8, device=DEV, generator=gen) * 1e-3)[shift:shift + n]
+        m2 = (torch.rand(n + 8, device=DEV, generator=gen) * 1e-6)[shift:shift + n]
+        gs = (torch.randn(n + 8, device=DEV, generator=gen) * 1e-2).to(DT[g_dt])[shift:shift + n]
+        acc = (torch.randn(n + 8, device=DEV, generator=gen) * 1e-3)[shift:shift + n] if accumulate else None
+        old = (host(th)[0], host(m1)[0], host(m2)[0])
+        accn = host(acc)[0] if accumulate else None
+        smat.smat_adamw_fused(gs, th, m1, m2, p, lam, hp, seed, step, tid, off, grad_acc=acc)
+        torch.cuda.synchronize()
+        check_adamw(th, m1, m2, old, gs, p, lam, hp, seed, step, tid, off, accn, what)
+
+
+def test_random_merges():
+    from tolerances import check_merge
+    rng = np.random.default_rng(20263)
+    gen = torch.Generator(DEV).manual_seed(20263)
+    for case in range(40):
+        n, off, _, shift = draw_case(rng)
+        nexp = int(rng.integers(1, 17))
+        e_dt, t0_dt, out_dt = (str(rng.choice(["bf16", "f32"])) for _ in range(3))
+        tid = int(rng.integers(0, 2 ** 32))
+        terms = [dict(gamma=float(np.float32(rng.uniform(-1.0, 1.5))),
+                      keep=float(np.float32(rng.choice([0.0, 1.0, rng.uniform(0.05, 0.99), KEEP_FP32_BELOW_1]))),
+                      rescale=int(rng.integers(0, 2)), seed=int(rng.integers(0, 2 ** 63)),
+                      step=int(rng.integers(0, 2 ** 30))) for _ in range(nexp)]
+        what = f"case {case}: n={n} off={off} shift={shift} nexp={nexp} dtypes={e_dt}/{t0_dt}/{out_dt}"
+        base = torch.randn(n + 8, device=DEV, generator=gen) * 0.02
+        t0 = base.to(DT[t0_dt])[shift:shift + n]
+        ex = [(base + torch.randn(n + 8, device=DEV, generator=gen) * 1e-3).to(DT[e_dt])[shift:shift + n]
+              for _ in range(nexp)]
+        out = torch.empty(n + 8, dtype=DT[out_dt], device=DEV)[shift:shift + n]
+        smat.smat_merge(ex, t0, out, terms, tid, off)
+        torch.cuda.synchronize()
+        exn = [host(x) for x in ex]
+        t0n, t0dt = host(t0)
+        y = oracle.merge_f64([x for x, _ in exn], e_dt, t0n, t0dt, terms, tid, off)
+        b = oracle.as_f64(t0n, t0dt)
+        A, used = np.abs(b).copy(), 0
+        for (x, dt), t in zip(exn, terms):
+            kept = oracle.keep_mask(t["seed"], t["step"], tid, off, n, t["keep"])
+            tj = oracle.coefficient(t["gamma"], t["keep"], t["rescale"])
+            A += np.where(kept, abs(tj) * (np.abs(oracle.as_f64(x, dt)) + np.abs(b)), 0.0)
+            used += float(np.float32(t["keep"])) > 0
+        got, _ = host(out)
+        ok, strict = check_merge(got, out_dt, y, A, max(used, 1))
+        assert ok.all(), f"{what}: {np.count_nonzero(~ok)} mismatches, first {np.flatnonzero(~ok)[:5]}"
+        if out_dt == "bf16":
+            assert np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))[strict].max(initial=0) <= 1, what
