@@ -194,3 +194,42 @@ def test_random_merges():
         assert ok.all(), f"{what}: {np.count_nonzero(~ok)} mismatches, first {np.flatnonzero(~ok)[:5]}"
         if out_dt == "bf16":
             assert np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))[strict].max(initial=0) <= 1, what
+
+
+def test_random_list_norms():
+    from tolerances import SQNORM_ULPS, U, check_sqnorm
+    rng = np.random.default_rng(20264)
+    gen = torch.Generator(DEV).manual_seed(20264)
+    for case in range(30):
+        count = int(rng.integers(1, 7))
+        g_dt = str(rng.choice(["bf16", "f32"]))
+        accumulate = bool(rng.integers(0, 2))
+        seed, step = int(rng.integers(0, 2 ** 63)), int(rng.integers(0, 2 ** 30))
+        lam = float(np.float32(rng.uniform(-1.0, 2.0)))
+        items = [draw_case(rng) for _ in range(count)]
+        ids = [int(x) for x in rng.choice(2 ** 32, size=count, replace=False)]
+        ts = [tensors(rng, n, shift, "bf16", "bf16", g_dt, gen) for n, _, _, shift in items]
+        th, t0, out, gs, gt = (list(x) for x in zip(*ts))
+        offs, params = [it[1] for it in items], [it[2] for it in items]
+        what = f"list {case}: sizes={[it[0] for it in items]} offs={offs} g={g_dt} acc={accumulate} lam={lam}"
+        want, m2 = 0.0, 0.0
+        for i in range(count):
+            gsn, gs_dt = host(gs[i])
+            acc = host(gt[i])[0] if accumulate else None
+            want += oracle.grad_sqnorm(gsn, gs_dt, params[i], lam, seed, step, ids[i], offs[i], acc)
+            m = np.abs(oracle.simulated_gradient(gsn, gs_dt, params[i], lam, seed, step, ids[i], offs[i]))
+            if acc is not None:
+                m = m + np.abs(acc.astype(np.float64))
+            m2 += float(np.dot(m, m))
+        sumsq = torch.zeros(1, dtype=torch.float64, device=DEV)
+        coef = torch.zeros(1, dtype=torch.float32, device=DEV)
+        max_norm = float(rng.uniform(0.1, 2.0)) * max(want, 1e-30) ** 0.5
+        with smat.Plan(th, out, t0, gs, gt, tensor_ids=ids, elem_offsets=offs) as plan:
+            plan.set_params(params)
+            plan.grad_norm(seed, step, lam, accumulate, max_norm, sumsq, coef)
+            torch.cuda.synchronize()
+        assert check_sqnorm(sumsq.item(), want, m2), (what, sumsq.item(), want)
+        if want > 0:
+            want_coef = oracle.clip_coefficient(want ** 0.5, max_norm)
+            rel = 0.5 * SQNORM_ULPS * U * m2 / want + 2 * U
+            assert abs(coef.item() - want_coef) <= rel * want_coef + 2 * U, (what, coef.item(), want_coef)
