@@ -11,6 +11,8 @@ import os
 from ctypes import POINTER, c_char_p, c_float, c_int32, c_int64, c_size_t, c_uint8, c_uint32, c_uint64, c_void_p
 from typing import Optional, Sequence
 
+import numpy as np
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsmat.so")
 
@@ -34,6 +36,20 @@ EXPORTS = (
 
 class smat_op_params(ctypes.Structure):
     _fields_ = [("s", c_float), ("keep", c_float), ("sigma", c_float), ("rescale", c_int32), ("noise_kind", c_int32)]
+
+
+# smat_op_params as a NumPy record, for lists of per-tensor parameters filled column by column
+OP_PARAMS_DTYPE = np.dtype([("s", "<f4"), ("keep", "<f4"), ("sigma", "<f4"), ("rescale", "<i4"),
+                            ("noise_kind", "<i4")], align=True)
+assert OP_PARAMS_DTYPE.itemsize == ctypes.sizeof(smat_op_params)
+
+
+def op_params_array(count: int, s, keep, sigma, rescale=1, noise_kind=0) -> np.ndarray:
+    """`count` smat_op_params records in one array; each field is a scalar shared by all tensors or
+    a sequence of `count` values.  Plan.set_params takes it without a per-tensor Python loop."""
+    a = np.empty(count, dtype=OP_PARAMS_DTYPE)
+    a["s"], a["keep"], a["sigma"], a["rescale"], a["noise_kind"] = s, keep, sigma, rescale, noise_kind
+    return a
 
 
 class smat_rng_key(ctypes.Structure):
@@ -314,6 +330,7 @@ class Plan:
             d.n = thetas[i].numel()
             d.tensor_id = ids[i]
             d.elem_offset = offs[i]
+        self.offload = bool(offload)
         self.dtypes = (t0_dt, out_dt, g_dt)
         plan = c_void_p()
         _check(lib().smat_plan_create(descs, count, t0_dt, out_dt, g_dt, 1 if offload else 0, ctypes.byref(plan)))
@@ -325,11 +342,18 @@ class Plan:
         _check(lib().smat_plan_bind_workspace(plan, c_void_p(self.workspace.data_ptr()), nbytes.value,
                                               _stream_handle(stream)))
 
-    def set_params(self, params: Sequence, stream=None) -> None:
-        arr = (smat_op_params * max(self.count, 1))(*[op_params(p) for p in params])
+    def set_params(self, params, stream=None) -> None:
+        """Per-tensor parameters: a sequence of dicts / smat_op_params, or an op_params_array."""
         if len(params) != self.count:
             raise SmatError(SMAT_ERR_INVALID, "one parameter record per tensor")
-        _check(lib().smat_plan_set_params(self._plan, arr, _stream_handle(stream)))
+        if isinstance(params, np.ndarray):
+            if params.dtype != OP_PARAMS_DTYPE:
+                raise SmatError(SMAT_ERR_INVALID, "a parameter array must have OP_PARAMS_DTYPE records")
+            arr = np.ascontiguousarray(params)
+            ptr = arr.ctypes.data_as(POINTER(smat_op_params)) if self.count else None
+        else:
+            ptr = (smat_op_params * max(self.count, 1))(*[op_params(p) for p in params])
+        _check(lib().smat_plan_set_params(self._plan, ptr, _stream_handle(stream)))
 
     def simulate(self, seed: int, step: int, stream=None) -> None:
         _check(lib().smat_simulate_multi(self._plan, int(seed), int(step), _stream_handle(stream)))
@@ -400,7 +424,9 @@ class Plan:
                                           _scalar_ptr(clip_coef, "clip_coef", "float32"), _stream_handle(stream)))
 
     def switch_storage(self, to: int, stream=None) -> None:
-        _check(lib().smat_switch_storage(self._plan, int(to), _stream_handle(stream)))
+        # the stream orders only the offload prefetch; a resident plan's switch enqueues nothing
+        handle = _stream_handle(stream) if (self.offload or stream is not None) else None
+        _check(lib().smat_switch_storage(self._plan, int(to), handle))
 
     @property
     def state(self) -> int:

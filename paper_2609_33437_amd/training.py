@@ -202,8 +202,8 @@ class SimulatedMergeTraining:
         if not self.is_simulated(step):
             return False
         self.alpha = float(np.float32(self._rng.uniform(self.alpha_min, 1.0)))
-        self.plan.set_params([dict(s=self.alpha, keep=k, sigma=s, rescale=self.rescale, noise_kind=self.noise_kind)
-                              for k, s in zip(self.keep, self.sigma)])
+        self.plan.set_params(_lib.op_params_array(len(self.params), self.alpha, self.keep, self.sigma, self.rescale,
+                                                  self.noise_kind))
         self.plan.simulate(self.seed, step)
         self.plan.switch_storage(SMAT_SIMULATED)
         self._grads = None      # last step's gradients, no longer read by any queued kernel

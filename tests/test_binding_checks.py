@@ -77,3 +77,16 @@ def test_merge_lists():
         == SMAT_ERR_INVALID
     assert status_of(lambda: smat.MergePlan(t0, [x.clone() for x in t0], [[ex[0][0], ex[0][1].float()]])) \
         == SMAT_ERR_DTYPE
+
+
+def test_op_params_array_matches_the_c_records():
+    import ctypes
+    import numpy as np
+    from paper_2609_33437_amd import _lib
+    keeps, kinds = [0.1, 1.0, 0.0, 0.37], [0, 1, 2, 0]
+    a = smat.op_params_array(4, 0.5, keeps, [1e-3, 0.0, 2e-3, 5e-4], [1, 0, 1, 1], kinds)
+    recs = (_lib.smat_op_params * 4)(*[_lib.op_params(dict(s=0.5, keep=k, sigma=sg, rescale=r, noise_kind=nk))
+                                       for k, sg, r, nk in zip(keeps, [1e-3, 0.0, 2e-3, 5e-4], [1, 0, 1, 1], kinds)])
+    assert a.tobytes() == ctypes.string_at(recs, ctypes.sizeof(recs))
+    assert smat.OP_PARAMS_DTYPE.itemsize == ctypes.sizeof(_lib.smat_op_params)
+    assert np.all(a["keep"] == np.float32(keeps))

@@ -458,3 +458,27 @@ def test_clear_grads_lets_new_arrays_reuse_freed_memory(mini):
         want = oracle.backward_accum(gsn, "bf16", zero, params[i], cfg.lam, cfg.smat_seed, step, i)
         incr = np.abs(oracle.simulated_gradient(gsn, "bf16", params[i], cfg.lam, cfg.smat_seed, step, i))
         assert check_grad(host(fresh[i])[0], want, zero, incr).all(), f"tensor {i}"
+
+
+def test_set_params_array_form_equals_dict_form(mini):
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    step = 11
+    params = workloads.step_params(cfg, inp.settings, step)
+    arr = smat.op_params_array(cfg.count, [p["s"] for p in params], [p["keep"] for p in params],
+                               [p["sigma"] for p in params], [p.get("rescale", 1) for p in params],
+                               [p.get("noise_kind", 0) for p in params])
+    out2 = [torch.empty_like(o) for o in out]
+    gt2 = [g.clone() for g in gt]
+    with smat.Plan(th, out, t0, gs, gt) as a, smat.Plan(th, out2, t0, gs, gt2) as b:
+        a.set_params(params)
+        b.set_params(arr)
+        for plan in (a, b):
+            plan.simulate(cfg.smat_seed, step)
+            plan.backward_accum(cfg.smat_seed, step, 0.5)
+        with pytest.raises(smat.SmatError):
+            b.set_params(arr[:-1])                    # one record per tensor
+        torch.cuda.synchronize()
+    for i in range(cfg.count):
+        assert torch.equal(bits(out[i]), bits(out2[i]))
+        assert torch.equal(bits(gt[i]), bits(gt2[i]))
