@@ -24,6 +24,12 @@ if ROOT not in sys.path:
 
 METRIC = "fused simulate+backward params/s and achieved HBM GB/s (% of peak), 7B-shaped"
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
+# Peak Philox4x32-10 rate on MI355X, derived from the chip: the fp32 vector peak (157.3 TFLOP/s =
+# 78.6e12 FMA/s over 256 CUs x 4 SIMDs at 2.4 GHz) is 32 lanes per cycle per SIMD for single-rate
+# operations; v_mad_u64_u32 runs at a quarter of that (measured 1.9e13/s chip-wide).  One call as the
+# kernels form it costs 17 such products and 19 single-rate xors: 17 x 8 + 19 x 2 = 174 SIMD cycles
+# per 64 calls, i.e. 1024 x 2.4e9 x 64 / 174 calls/s.
+PEAK_PHILOX_CALLS = 1024 * 2.4e9 * 64 / 174
 KERNEL_SOURCES = ("paper_2609_33437_amd/csrc/smat_kernels.hip", "paper_2609_33437_amd/csrc/smat_device.h",
                   "paper_2609_33437_amd/csrc/smat_tile.h")
 MERGE_SOURCES = ("paper_2609_33437_amd/csrc/smat_merge.hip", "paper_2609_33437_amd/csrc/smat_device.h",
@@ -603,6 +609,21 @@ def bench_merge(args, torch, smat, workloads) -> int:
             log(f"{mode}: {ms:.3f} ms = {nbytes / (ms * 1e6):.0f} GB/s")
     dom = max(res, key=lambda m: res[m]["ms"])
     traffic = load_traffic("merge", cfg.name, MERGE_SOURCES) if N == 7 else None
+    # DARE draws one Philox call per quad of a masked tensor per expert (all tensors here are whole
+    # quads, aligned): its VALU work, not HBM, bounds it, so its roofline is the Philox rate
+    calls = {mode: sum(t.numel() // 4 * sum(1 for term in row if 0.0 < term["keep"] < 1.0)
+                       for t, row in zip(t0s, terms)) for mode, terms in modes.items()}
+    hbm_view = {"bound": "hbm", "achieved": res[dom]["gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": res[dom]["frac"], "traffic": traffic["bytes_per_launch"][dom] if traffic else None,
+                "algorithmic_bytes_per_launch": nbytes}
+    if calls[dom]:
+        rate = calls[dom] / (res[dom]["ms"] * 1e-3)
+        roofline = {"bound": "alu", "achieved": round(rate, 1), "peak": round(PEAK_PHILOX_CALLS, 1),
+                    "unit": "Philox4x32-10 calls/s", "frac": round(rate / PEAK_PHILOX_CALLS, 4),
+                    "traffic": None, "kernel": f"merge ({dom})", "calls_per_launch": calls[dom],
+                    "avg_launch_ms": res[dom]["ms"], "hbm": hbm_view}
+    else:
+        roofline = dict(hbm_view, kernel=f"merge ({dom})", avg_launch_ms=res[dom]["ms"])
     if args.calibrate_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -620,10 +641,7 @@ def bench_merge(args, torch, smat, workloads) -> int:
         "config": {"workload": f"{cfg.name}: {cfg.description}; {N} bf16 experts, bf16 theta0 and output",
                    "params": P, "tensors": cfg.count, "experts": N, "bytes_per_param": 2 * N + 4},
         "modes": res,
-        "roofline": {"bound": "hbm", "achieved": res[dom]["gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": res[dom]["frac"], "traffic": traffic["bytes_per_launch"][dom] if traffic else None,
-                     "kernel": f"merge ({dom})",
-                     "algorithmic_bytes_per_launch": nbytes, "avg_launch_ms": res[dom]["ms"]},
+        "roofline": roofline,
     }
     print(json.dumps(result))
     return 0

@@ -810,6 +810,11 @@ smat_status make_merge(const smat_merge_term& m, MergeRec* out, const char* wher
   MergeRec r{};
   r.seed = m.seed;
   r.step = m.step;
+  uint32_t a = (uint32_t)m.seed, b = (uint32_t)(m.seed >> 32);
+  for (int k = 0; k < 10; ++k, a += 0x9E3779B9u, b += 0xBB67AE85u) {
+    r.rk0[k] = a;
+    r.rk1[k] = b;
+  }
   if (m.keep >= 1.f) {
     r.t = m.gamma;
   } else if (m.keep <= 0.f) {

@@ -154,39 +154,40 @@ __device__ __forceinline__ bool groups_wrap(uint64_t e0, uint32_t quads) {
 // under several keys, differ only in c3 or the key, so a caller drawing several forms it once.
 __device__ __forceinline__ uint64_t philox_p0(uint32_t glo) { return (uint64_t)glo * kPhiloxM0; }
 
-// Philox4x32-10 of counter (glo, hi, c2, c3) under key (k0, k1), given p0 = philox_p0(glo), for
-// wave-uniform hi, c2, c3, k0, k1.  The same rounds as philox4x32_10, with each xor grouped so
-// that its uniform operands combine first.
-__device__ __forceinline__ Words philox_tile(uint64_t p0, uint32_t hi, uint32_t c2, uint32_t c3, uint32_t k0,
-                                             uint32_t k1) {
-  // round 1: only the products' lane-dependent half (p0) is per lane
+// Philox4x32-10 of counter (glo, hi, c2, c3) under the round keys (rk0[r], rk1[r]) of rounds
+// r = 0..9 (formed from the seed in advance), given p0 = philox_p0(glo), for wave-uniform hi, c2, c3.
+// The same rounds as philox_tile below.
+__device__ __forceinline__ Words philox_tile_rk(uint64_t p0, uint32_t hi, uint32_t c2, uint32_t c3,
+                                                const uint32_t* rk0, const uint32_t* rk1) {
   const uint64_t q1 = (uint64_t)c2 * kPhiloxM1;
-  const uint32_t a0 = (uint32_t)(q1 >> 32) ^ hi ^ k0, a1 = (uint32_t)q1;
-  const uint32_t a2 = (uint32_t)(p0 >> 32) ^ (c3 ^ k1), a3 = (uint32_t)p0;
-  // round 2: a0 and a1 are uniform
-  k0 += kPhiloxW0;
-  k1 += kPhiloxW1;
+  const uint32_t a0 = (uint32_t)(q1 >> 32) ^ hi ^ rk0[0], a1 = (uint32_t)q1;
+  const uint32_t a2 = (uint32_t)(p0 >> 32) ^ (c3 ^ rk1[0]), a3 = (uint32_t)p0;
   const uint64_t r0 = (uint64_t)a0 * kPhiloxM0, r1 = (uint64_t)a2 * kPhiloxM1;
-  uint32_t c0 = (uint32_t)(r1 >> 32) ^ (a1 ^ k0), w1 = (uint32_t)r1;
-  uint32_t w2 = a3 ^ ((uint32_t)(r0 >> 32) ^ k1), w3 = (uint32_t)r0;
-  // round 3: w3 is uniform
-  k0 += kPhiloxW0;
-  k1 += kPhiloxW1;
+  uint32_t c0 = (uint32_t)(r1 >> 32) ^ (a1 ^ rk0[1]), w1 = (uint32_t)r1;
+  uint32_t w2 = a3 ^ ((uint32_t)(r0 >> 32) ^ rk1[1]), w3 = (uint32_t)r0;
   {
     const uint64_t s0 = (uint64_t)c0 * kPhiloxM0, s1 = (uint64_t)w2 * kPhiloxM1;
-    c0 = xor3((uint32_t)(s1 >> 32), w1, k0);
-    w2 = (uint32_t)(s0 >> 32) ^ (w3 ^ k1);
+    c0 = xor3((uint32_t)(s1 >> 32), w1, rk0[2]);
+    w2 = (uint32_t)(s0 >> 32) ^ (w3 ^ rk1[2]);
     w1 = (uint32_t)s1;
     w3 = (uint32_t)s0;
   }
-  // rounds 4-10
 #pragma unroll
-  for (int r = 3; r < 10; ++r) {
-    k0 += kPhiloxW0;
-    k1 += kPhiloxW1;
-    philox_round((uint64_t)c0 * kPhiloxM0, c0, w1, w2, w3, k0, k1);
-  }
+  for (int r = 3; r < 10; ++r) philox_round((uint64_t)c0 * kPhiloxM0, c0, w1, w2, w3, rk0[r], rk1[r]);
   return {c0, w1, w2, w3};
+}
+
+// Philox4x32-10 of counter (glo, hi, c2, c3) under key (k0, k1), given p0 = philox_p0(glo), for
+// wave-uniform hi, c2, c3, k0, k1: philox_tile_rk with the round keys added up in place.
+__device__ __forceinline__ Words philox_tile(uint64_t p0, uint32_t hi, uint32_t c2, uint32_t c3, uint32_t k0,
+                                             uint32_t k1) {
+  uint32_t rk0[10], rk1[10];
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    rk0[r] = k0 + (uint32_t)r * 0x9E3779B9u;
+    rk1[r] = k1 + (uint32_t)r * 0xBB67AE85u;
+  }
+  return philox_tile_rk(p0, hi, c2, c3, rk0, rk1);
 }
 
 __device__ __forceinline__ uint32_t pick(const Words& w, uint32_t lane) {

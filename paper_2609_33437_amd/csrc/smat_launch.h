@@ -36,15 +36,18 @@ hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, cons
                                hipStream_t stream);
 // ---------------------------------------------------------------- N-expert merge
 // One expert's term on one tensor: its mask key (seed, step), threshold and coefficient
-// t = gamma/keep (rescaled) or gamma, and kFlagMask / kFlagDropAll.
+// t = gamma/keep (rescaled) or gamma, and kFlagMask / kFlagDropAll, plus the ten Philox round keys of
+// the seed, formed on the host so that no wave adds them up again for every expert.
 struct alignas(8) MergeRec {
   uint64_t seed;
   uint32_t step;
   uint32_t thr;
   float t;
   uint32_t flags;
+  uint32_t rk0[10];
+  uint32_t rk1[10];
 };
-static_assert(sizeof(MergeRec) == 24, "MergeRec layout");
+static_assert(sizeof(MergeRec) == 104, "MergeRec layout");
 constexpr int kMaxExperts = 16;
 constexpr int kMergeQuads = 2;
 constexpr uint32_t kVecMerge = 16u;  // TensorRec::sflags: theta0, out and every expert quad-aligned, offset % 4 == 0

@@ -65,8 +65,10 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
     }
     for (int x = 0; x < nexp; ++x) {
       const MergeRec R = rec_at(x);
-      if (R.flags & kFlagDropAll) continue;
       const void* xp = expert_at(x);
+      // the expert's pointer and its term's fields in one round of scalar loads, before any branch
+      asm volatile("" ::"s"(xp), "s"(R.t), "s"(R.flags), "s"(R.thr), "s"(R.step));
+      if (R.flags & kFlagDropAll) continue;
       typename QuadIO<TE>::Raw rx[kMergeQuads];
 #pragma unroll
       for (int u = 0; u < kMergeQuads; ++u) {
@@ -79,8 +81,7 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
 #pragma unroll
         for (int j = 0; j < 4; ++j) kept[u][j] = true;
         if (R.flags & kFlagMask) {
-          const Words w = philox_tile(p0[u], G.hi, tensor_id, (R.step << 2) | kStreamMask, (uint32_t)R.seed,
-                                          (uint32_t)(R.seed >> 32));
+          const Words w = philox_tile_rk(p0[u], G.hi, tensor_id, (R.step << 2) | kStreamMask, R.rk0, R.rk1);
           kept[u][0] = w.w0 < R.thr;
           kept[u][1] = w.w1 < R.thr;
           kept[u][2] = w.w2 < R.thr;
