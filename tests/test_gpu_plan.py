@@ -482,3 +482,48 @@ def test_set_params_array_form_equals_dict_form(mini):
     for i in range(cfg.count):
         assert torch.equal(bits(out[i]), bits(out2[i]))
         assert torch.equal(bits(gt[i]), bits(gt2[i]))
+
+
+def test_work_runs_on_the_given_stream(mini):
+    """Every upload and launch goes on the stream the call names (torch's current stream by
+    default): a plan driven on a side stream, as the current stream or passed explicitly, gives the
+    bits of the default-stream run once that stream has finished."""
+    cfg, inp = mini
+    step = 13
+    params = workloads.step_params(cfg, inp.settings, step)
+    runs = []
+    side = torch.cuda.Stream()                                 # default priority
+    for mode in ("default", "current", "explicit"):
+        th, t0, gs, gt, out = to_dev(inp)
+        torch.cuda.synchronize()
+        if mode == "current":
+            with torch.cuda.stream(side):
+                with smat.Plan(th, out, t0, gs, gt) as plan:
+                    plan.set_params(params)
+                    plan.simulate(cfg.smat_seed, step)
+                    plan.switch_storage(smat.SMAT_SIMULATED)
+                    plan.backward_accum(cfg.smat_seed, step, 0.5)
+                    plan.switch_storage(smat.SMAT_EXPERT)
+                    side.synchronize()
+        elif mode == "explicit":
+            with smat.Plan(th, out, t0, gs, gt, stream=side) as plan:
+                plan.set_params(params, stream=side)
+                plan.simulate(cfg.smat_seed, step, stream=side)
+                plan.switch_storage(smat.SMAT_SIMULATED, stream=side)
+                plan.backward_accum(cfg.smat_seed, step, 0.5, stream=side)
+                plan.switch_storage(smat.SMAT_EXPERT, stream=side)
+                side.synchronize()
+        else:
+            with smat.Plan(th, out, t0, gs, gt) as plan:
+                plan.set_params(params)
+                plan.simulate(cfg.smat_seed, step)
+                plan.switch_storage(smat.SMAT_SIMULATED)
+                plan.backward_accum(cfg.smat_seed, step, 0.5)
+                plan.switch_storage(smat.SMAT_EXPERT)
+                torch.cuda.synchronize()
+        runs.append(([bits(o).clone() for o in out], [bits(g).clone() for g in gt]))
+    for outs, grads in runs[1:]:
+        for a, b in zip(outs, runs[0][0]):
+            assert torch.equal(a, b)
+        for a, b in zip(grads, runs[0][1]):
+            assert torch.equal(a, b)
