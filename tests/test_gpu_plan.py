@@ -527,3 +527,39 @@ def test_work_runs_on_the_given_stream(mini):
             assert torch.equal(a, b)
         for a, b in zip(grads, runs[0][1]):
             assert torch.equal(a, b)
+
+
+def test_offload_prefetch_waits_for_the_readers_of_the_buffers(mini):
+    """In offload mode the restore starts the theta0 prefetch into the buffers on the plan's copy
+    stream, ordered after the point the caller's stream has reached.  Work queued before the restore
+    that still reads theta~ from the buffers (here a long chain of matmuls, then copies of the
+    buffers) must see theta~, however long it runs; afterwards the buffers hold theta0 again."""
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    hosts = [t.contiguous().pin_memory() for t in inp.theta0]
+    bufs = [torch.empty(t.numel(), dtype=torch.bfloat16, device=DEV) for t in th]
+    step = 3
+    params = workloads.step_params(cfg, inp.settings, step)
+    gen = torch.Generator(DEV).manual_seed(1)
+    a = torch.randn(4096, 4096, device=DEV, generator=gen) * (1.0 / 64)
+    with smat.Plan(th, out, t0) as res, smat.Plan(th, bufs, None, offload=True, theta0_hosts=hosts,
+                                                  dtypes=(smat.SMAT_BF16, smat.SMAT_BF16, smat.SMAT_BF16)) as off:
+        res.set_params(params)
+        res.simulate(cfg.smat_seed, step)
+        for rep in range(3):
+            off.set_params(params)
+            off.simulate(cfg.smat_seed, step)
+            off.switch_storage(smat.SMAT_SIMULATED)
+            x = a
+            for _ in range(24):                              # tens of milliseconds on the caller's stream
+                x = torch.mm(x, a)
+            snaps = [b.clone() for b in bufs]                # read theta~ after the delay
+            off.switch_storage(smat.SMAT_EXPERT)             # the prefetch may start only here
+            torch.cuda.synchronize()
+            assert torch.isfinite(x).all()
+            for s_, r in zip(snaps, out):
+                assert torch.equal(bits(s_), bits(r)), f"repeat {rep}: a buffer changed before its readers ran"
+        off.close()
+        torch.cuda.synchronize()
+    for b, h in zip(bufs, inp.theta0):
+        assert torch.equal(bits(b.cpu()), bits(h.view(-1)))
