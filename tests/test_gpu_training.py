@@ -312,3 +312,33 @@ def test_wrapper_errors():
         SimulatedMergeTraining([torch.nn.Parameter(torch.zeros(4, device=DEV, dtype=torch.bfloat16))],
                                [torch.zeros(4, device=DEV)], [1.0], 0.2, 1e-3)
     w.close()
+
+
+def test_micro_batches_accumulate_in_a_simulated_step():
+    """Gradient accumulation inside a simulated step: several forward/backward passes on theta~
+    accumulate into the gradient at theta~ (autograd adds into p.grad), and end() turns the sum into
+    the expert gradient lam alpha m (.) (sum of g~) for the optimizer."""
+    torch.manual_seed(0)
+    model = make_decoder(TINY, 5, DEV)
+    batches = token_batches(TINY, 2, 24, 3, 11, DEV)
+    w = wrap(model)
+    assert w.begin(3)
+    for tokens in batches:                              # three micro-batches
+        (model.loss(tokens) / len(batches)).backward()
+    g_sum = [host(p.grad)[0] for p in w.params]         # what autograd accumulated at theta~
+    # the same sum from a copy of the model holding theta~
+    ref = make_decoder(TINY, 5, DEV)
+    with torch.no_grad():
+        for q, p in zip(ref.parameters(), w.params):
+            q.copy_(p.data)
+    for tokens in batches:
+        (ref.loss(tokens) / len(batches)).backward()
+    for p, q in zip(w.params, ref.parameters()):
+        torch.testing.assert_close(p.grad, q.grad, rtol=1e-5, atol=1e-7)
+    w.end()
+    for i, p in enumerate(w.params):
+        zeros = np.zeros(p.numel(), np.float32)
+        want = oracle.backward_accum(g_sum[i], "f32", zeros, op(w, i), w.lam, SEED, 3, i)
+        incr = np.abs(oracle.simulated_gradient(g_sum[i], "f32", op(w, i), w.lam, SEED, 3, i))
+        assert check_grad(host(p.grad)[0], want, zeros, incr).all(), w.names[i]
+    w.close()
