@@ -811,7 +811,7 @@ smat_status make_merge(const smat_merge_term& m, MergeRec* out, const char* wher
   r.seed = m.seed;
   r.step = m.step;
   uint32_t a = (uint32_t)m.seed, b = (uint32_t)(m.seed >> 32);
-  for (int k = 0; k < 10; ++k, a += 0x9E3779B9u, b += 0xBB67AE85u) {
+  for (int k = 0; k < 10; ++k, a += smat::kPhiloxW0, b += smat::kPhiloxW1) {
     r.rk0[k] = a;
     r.rk1[k] = b;
   }

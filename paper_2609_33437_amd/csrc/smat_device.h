@@ -155,16 +155,20 @@ __device__ __forceinline__ bool groups_wrap(uint64_t e0, uint32_t quads) {
 __device__ __forceinline__ uint64_t philox_p0(uint32_t glo) { return (uint64_t)glo * kPhiloxM0; }
 
 // Philox4x32-10 of counter (glo, hi, c2, c3) under the round keys (rk0[r], rk1[r]) of rounds
-// r = 0..9 (formed from the seed in advance), given p0 = philox_p0(glo), for wave-uniform hi, c2, c3.
-// The same rounds as philox_tile below.
+// r = 0..9, given p0 = philox_p0(glo), for wave-uniform hi, c2, c3 and keys.  The same rounds as
+// philox4x32_10, with each xor of the first three rounds grouped so that its uniform operands
+// combine first.
 __device__ __forceinline__ Words philox_tile_rk(uint64_t p0, uint32_t hi, uint32_t c2, uint32_t c3,
                                                 const uint32_t* rk0, const uint32_t* rk1) {
+  // round 1: of the two products only p0 depends on the lane
   const uint64_t q1 = (uint64_t)c2 * kPhiloxM1;
   const uint32_t a0 = (uint32_t)(q1 >> 32) ^ hi ^ rk0[0], a1 = (uint32_t)q1;
   const uint32_t a2 = (uint32_t)(p0 >> 32) ^ (c3 ^ rk1[0]), a3 = (uint32_t)p0;
+  // round 2: a0 and a1 are uniform
   const uint64_t r0 = (uint64_t)a0 * kPhiloxM0, r1 = (uint64_t)a2 * kPhiloxM1;
   uint32_t c0 = (uint32_t)(r1 >> 32) ^ (a1 ^ rk0[1]), w1 = (uint32_t)r1;
   uint32_t w2 = a3 ^ ((uint32_t)(r0 >> 32) ^ rk1[1]), w3 = (uint32_t)r0;
+  // round 3: w3 is uniform; rounds 4-10 mix per-lane words only
   {
     const uint64_t s0 = (uint64_t)c0 * kPhiloxM0, s1 = (uint64_t)w2 * kPhiloxM1;
     c0 = xor3((uint32_t)(s1 >> 32), w1, rk0[2]);
@@ -184,8 +188,8 @@ __device__ __forceinline__ Words philox_tile(uint64_t p0, uint32_t hi, uint32_t 
   uint32_t rk0[10], rk1[10];
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    rk0[r] = k0 + (uint32_t)r * 0x9E3779B9u;
-    rk1[r] = k1 + (uint32_t)r * 0xBB67AE85u;
+    rk0[r] = k0 + (uint32_t)r * kPhiloxW0;
+    rk1[r] = k1 + (uint32_t)r * kPhiloxW1;
   }
   return philox_tile_rk(p0, hi, c2, c3, rk0, rk1);
 }
