@@ -7,18 +7,12 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 import workloads
+from helpers import host
 from tolerances import check_adam
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
 HP = dict(lr=2e-5, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-3, grad_scale=1.0, step=1)
-
-
-def host(t):
-    t = t.detach().cpu()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16), "bf16"
-    return t.numpy().copy(), "f32"
 
 
 def _state(n, g, shift=0):

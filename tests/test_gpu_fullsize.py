@@ -9,6 +9,7 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 import workloads
+from helpers import host
 from tolerances import check_grad, check_theta_tilde, ordered
 
 pytestmark = pytest.mark.gpu
@@ -21,13 +22,6 @@ def windows(n, rng):
         return [(0, n)]
     r = int(rng.integers(W, n - 2 * W))
     return [(0, W), (r, r + W), (n - W - 3, n)]
-
-
-def host(t):
-    t = t.detach().cpu()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16), "bf16"
-    return t.numpy().copy(), "f32"
 
 
 @pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])

@@ -15,6 +15,7 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 import workloads
+from helpers import host
 from tolerances import SQNORM_ULPS, U, check_adam, check_merge, ordered
 
 pytestmark = pytest.mark.gpu
@@ -28,13 +29,6 @@ def windows(n, rng):
         return [(0, n)]
     r = int(rng.integers(W, n - 2 * W))
     return [(0, W), (r, r + W), (n - W - 3, n)]
-
-
-def host(t):
-    t = t.detach().cpu().contiguous()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16).ravel(), "bf16"
-    return t.numpy().ravel().copy(), "f32"
 
 
 def test_fullsize_norm_and_clipped_fused_adamw_c4():

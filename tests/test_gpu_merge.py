@@ -9,22 +9,12 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 import workloads
+from helpers import bits, host
 from tolerances import check_merge, ordered
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
 DT = {"bf16": torch.bfloat16, "f32": torch.float32}
-
-
-def host(t):
-    t = t.detach().cpu().contiguous()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16).ravel(), "bf16"
-    return t.numpy().ravel().copy(), "f32"
-
-
-def bits(t):
-    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
 
 
 def make(n, nexp, e_dt, t0_dt, seed, shift=0, scale=1e-3):

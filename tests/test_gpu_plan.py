@@ -9,21 +9,11 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 import workloads
+from helpers import bits, host
 from tolerances import check_grad, check_theta_tilde, ordered
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
-
-
-def host(t):
-    t = t.detach().cpu()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16), "bf16"
-    return t.numpy().copy(), "f32"
-
-
-def bits(t):
-    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
 
 
 @pytest.fixture(scope="module")

@@ -10,19 +10,13 @@ import torch
 
 import oracle
 import paper_2609_33437_amd as smat
+from helpers import host
 from tolerances import check_grad, check_theta_tilde, ordered
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
 DT = {"bf16": torch.bfloat16, "f32": torch.float32}
 KEEP_FP32_BELOW_1 = float(np.nextafter(np.float32(1.0), np.float32(0.0)))
-
-
-def host(t):
-    t = t.detach().cpu()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16), "bf16"
-    return t.numpy().copy(), "f32"
 
 
 def draw_case(rng):

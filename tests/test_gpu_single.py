@@ -9,17 +9,11 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 import workloads
+from helpers import host
 from tolerances import GRAD_RTOL, Z_TOL, check_grad, check_theta_tilde, ordered
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
-
-
-def host(t):
-    t = t.detach().cpu()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16), "bf16"
-    return t.numpy().copy(), "f32"
 
 
 def run_simulate(theta, theta0, out, p, seed, step, tid, off=0):

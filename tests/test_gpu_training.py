@@ -15,19 +15,13 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 from paper_2609_33437_amd.training import SimulatedMergeTraining
+from helpers import host
 from tolerances import SQNORM_ULPS, U, check_adam, check_grad, check_sqnorm, check_theta_tilde, ordered
 from workloads.model import TINY, make_decoder, token_batches
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
 SEED = 0x51A7
-
-
-def host(t):
-    t = t.detach().cpu().contiguous()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16).ravel(), "bf16"
-    return t.numpy().ravel().copy(), "f32"
 
 
 def base_weights(model, seed=3, scale=0.01):
