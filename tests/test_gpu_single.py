@@ -10,7 +10,7 @@ import oracle
 import paper_2609_33437_amd as smat
 import workloads
 from helpers import host
-from tolerances import GRAD_RTOL, Z_TOL, check_grad, check_theta_tilde, ordered
+from tolerances import Z_TOL, check_grad, check_theta_tilde, ordered
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"

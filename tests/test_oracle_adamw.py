@@ -1,7 +1,6 @@
 """Pins of the oracle's fused optimizer step: the AdamW definition against PyTorch's own AdamW
 (CPU, float64) over several steps; Adam's first-step magnitude; zero gradient on dropped
 coordinates entering the update; argument errors."""
-import math
 
 import numpy as np
 import pytest
