@@ -66,7 +66,7 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
-    ap.add_argument("--cpu-sample", type=int, default=1 << 27, help="most elements the CPU oracle baseline visits")
+    ap.add_argument("--cpu-sample", type=int, default=3 << 27, help="most elements the CPU oracle baseline visits")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU work budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--adamw", action="store_true",
