@@ -173,7 +173,7 @@ def timed_copy(nbytes_step: int, torch, smat, reps: int = 5) -> dict:
 # $REPO/rocprof the output root that `bench.py --summarize $REPO/rocprof` reads.
 PROF_NOTE = "run from /tmp with TMPDIR=/tmp; $REPO is the repository root"
 TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d $REPO/rocprof/trace -o c4 -- "
-             "python3 $REPO/bench.py --steps 20 --warmup 5 --no-cpu-baseline --calibrate-copy")
+             "python3 $REPO/bench.py")  # the default run: the kernel times behind its JSON line
 PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d $REPO/rocprof/{tag} -o c4 --kernel-include-regex "
            "'k_simulate_multi|k_backward_multi|elementwise' -- "
            "python3 $REPO/bench.py --steps 2 --warmup 1 --no-cpu-baseline --calibrate-copy")
@@ -219,9 +219,12 @@ def summarize(root: str) -> int:
     stats = list(csv.DictReader(open(os.path.join(root, "trace", "c4_kernel_stats.csv"))))
     lines = ["# Kernel time on the 7B-shaped list (c4), rocprofv3 kernel trace", "",
              f"Command (on one MI355X; {PROF_NOTE}): `{TRACE_CMD}`", "",
-             "Each step launches one simulate and one backward over the 290-tensor list "
-             "(7,504,924,672 parameters); 5 warmup + 20 timed steps = 25 calls each.  The other kernels are "
-             "torch's input generation and the copy calibration.", "",
+             "The default `bench.py` run, whose JSON line quotes the same kernels' HIP-event times.  Each step "
+             "launches one simulate and one backward over the 290-tensor list (7,504,924,672 parameters); "
+             "5 warmup + 20 timed steps = 25 calls each.  It first runs `smat_stream_copy` over the step's "
+             "bytes, the plain-copy reference of the JSON line; the other kernels are torch's input "
+             "generation and the runtime's copies (`__amd_rocclr_copyBuffer`) of the CPU baseline's windows "
+             "to the host.", "",
              "| kernel | calls | average ms | min ms | max ms | share of GPU time |", "|---|---|---|---|---|---|"]
     for r in stats[:12]:
         name = r["Name"].replace("(anonymous namespace)", "{anon}").split("(")[0].replace("void ", "")
