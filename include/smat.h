@@ -17,9 +17,10 @@
  * (Sec. 4.3, "Parameter storage switching"; App. "Implementation details").
  *
  * Conventions for every entry point:
- *   - Every function returns an smat_status; SMAT_OK is 0.  On failure nothing
- *     is enqueued and smat_last_error() describes the cause.  No C++
- *     exception crosses this boundary.
+ *   - Every function returns an smat_status; SMAT_OK is 0.  An argument, dtype
+ *     or state error enqueues nothing; a HIP runtime failure (SMAT_ERR_HIP) may
+ *     leave work the call issued before it enqueued.  smat_last_error()
+ *     describes the cause.  No C++ exception crosses this boundary.
  *   - Tensor arguments are device pointers to contiguous memory owned by the
  *     caller (for example PyTorch tensors); the library never frees them.
  *     Element counts are int64_t; 0 elements is a valid no-op.
