@@ -249,6 +249,36 @@ smat_status smat_backward_multi(smat_plan* plan, uint64_t seed, uint32_t step, f
 smat_status smat_backward_accum_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda,
                                       hipStream_t stream);
 
+/* Per-step values that the device-driven list calls read from device memory when their kernels
+ * run, so that a call recorded once into a HIP graph (stream capture) serves every later step: the
+ * caller rewrites the 16 bytes between replays, or has kernels of its own graph advance them.
+ *   seed   Philox key
+ *   step   global step; the counter word uses it modulo 2^30 (steps 2^30 apart share draws)
+ *   scale  the step's sampled scale (Sec. 4.1, "Scale"): tensor i uses s' = fl32(scale * s_i) in
+ *          place of its s_i from smat_plan_set_params, so s_i = 1 gives every tensor the sampled
+ *          scale and other s_i give fixed per-tensor multiples of it.  The coefficient is then
+ *          s'/keep (rescale, 0 < keep < 1) or s', rounded exactly as smat_plan_set_params rounds
+ *          it: the results are the bits of the host-driven call given s'.  The value is not
+ *          checked; a non-finite scale makes every kept coordinate non-finite. */
+typedef struct smat_step_state {
+  uint64_t seed;
+  uint32_t step;
+  float scale;
+} smat_step_state;
+
+/* smat_simulate_multi_dev / smat_backward_multi_dev -- smat_simulate_multi and smat_backward_multi
+ * with seed, step and scale read from `state` (device-accessible, 16-byte aligned, caller-owned; it
+ * must hold its values when the kernels run).  keep, sigma, noise kind and rescale still come from
+ * smat_plan_set_params, and the backward of a step must read the state its simulate read.  The
+ * host does no synchronisation and waits on no event, so both calls may be recorded under stream
+ * capture.  Not for offload plans, whose theta0 prefetch runs on the plan's own copy stream.
+ * Errors: SMAT_ERR_INVALID (null or misaligned state; lambda, accumulate), SMAT_ERR_STATE (offload
+ * plan, no workspace or params, simulated storage active for the simulate, gradient arrays not set
+ * for the backward), SMAT_ERR_HIP. */
+smat_status smat_simulate_multi_dev(smat_plan* plan, const smat_step_state* state, hipStream_t stream);
+smat_status smat_backward_multi_dev(smat_plan* plan, const smat_step_state* state, float lambda,
+                                    int32_t accumulate, hipStream_t stream);
+
 /* Optimizer state of one tensor of a plan (device pointers, [n] fp32 each). */
 typedef struct smat_adam_state {
   float* exp_avg;

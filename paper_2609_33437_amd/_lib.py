@@ -30,7 +30,8 @@ EXPORTS = (
     "smat_adamw_fused", "smat_plan_bind_adam_state", "smat_adamw_fused_multi", "smat_grad_norm_multi",
     "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
     "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
-    "smat_stream_copy", "smat_backward_multi", "smat_plan_clear_grads",
+    "smat_stream_copy", "smat_backward_multi", "smat_plan_clear_grads", "smat_simulate_multi_dev",
+    "smat_backward_multi_dev",
 )
 
 
@@ -123,6 +124,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_stream_copy": [P, P, c_uint64, P],
         "smat_backward_multi": [P, c_uint64, c_uint32, c_float, c_int32, P],
         "smat_plan_clear_grads": [P, c_int32],
+        "smat_simulate_multi_dev": [P, P, P],
+        "smat_backward_multi_dev": [P, P, c_float, c_int32, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -186,6 +189,46 @@ def _scalar_ptr(t, what: str, dtype: str):
     if str(t.dtype) != f"torch.{dtype}" or t.numel() != 1:
         raise SmatError(SMAT_ERR_INVALID, f"{what} must be a one-element {dtype} tensor")
     return _dev_ptr(t, what)
+
+
+class StepState:
+    """The 16 bytes that the device-driven list calls read when their kernels run, in GPU memory:
+    seed (uint64), step (uint32), scale (float32), the layout of smat_step_state.
+
+    set() writes all three from the host (between graph replays); seed_view, step_view and
+    scale_view are one-element views of the same bytes that torch ops, captured into the same graph,
+    can update in place (for example step_view.add_(1), or scale_view.copy_ of a sampled scale)."""
+
+    def __init__(self, seed: int = 0, step: int = 0, scale: float = 1.0, device=None):
+        torch = _torch()
+        self.tensor = torch.zeros(4, dtype=torch.int32, device=device if device is not None else "cuda")
+        self.set(seed, step, scale)
+
+    def set(self, seed: int, step: int, scale: float) -> None:
+        import numpy as np
+        rec = np.zeros(1, dtype=[("seed", "<u8"), ("step", "<u4"), ("scale", "<f4")])
+        rec["seed"], rec["step"], rec["scale"] = int(seed), int(step), float(scale)
+        self.tensor.copy_(_torch().from_numpy(rec.view(np.int32).copy()))
+
+    @property
+    def seed_view(self):
+        return self.tensor[0:2].view(_torch().int64)
+
+    @property
+    def step_view(self):
+        return self.tensor[2:3]
+
+    @property
+    def scale_view(self):
+        return self.tensor[3:4].view(_torch().float32)
+
+
+def _state_ptr(state):
+    """Device pointer of a StepState, or of a contiguous 16-byte GPU tensor in its layout."""
+    t = state.tensor if isinstance(state, StepState) else state
+    if t is None or t.numel() * t.element_size() != 16:
+        raise SmatError(SMAT_ERR_INVALID, "step state must be a StepState or a 16-byte GPU tensor")
+    return _dev_ptr(t, "step state")
 
 
 def _expect(t, n: int, code: int, what: str) -> None:
@@ -360,6 +403,15 @@ class Plan:
 
     def backward_accum(self, seed: int, step: int, lam: float, stream=None) -> None:
         _check(lib().smat_backward_accum_multi(self._plan, int(seed), int(step), float(lam), _stream_handle(stream)))
+
+    def simulate_dev(self, state, stream=None) -> None:
+        """smat_simulate_multi_dev: seed, step and scale read from `state` when the kernels run."""
+        _check(lib().smat_simulate_multi_dev(self._plan, _state_ptr(state), _stream_handle(stream)))
+
+    def backward_dev(self, state, lam: float, accumulate: bool = True, stream=None) -> None:
+        """smat_backward_multi_dev: the backward of the step whose seed, step and scale `state` holds."""
+        _check(lib().smat_backward_multi_dev(self._plan, _state_ptr(state), float(lam), 1 if accumulate else 0,
+                                             _stream_handle(stream)))
 
     def backward(self, seed: int, step: int, lam: float, accumulate: bool = True, stream=None) -> None:
         """smat_backward_multi: accumulate into grad_theta, or overwrite it (zero where dropped)."""

@@ -15,6 +15,8 @@
 using smat::AdamConsts;
 using smat::AdamRec;
 using smat::ParamRec;
+using smat::ScaleRec;
+using smat::StepState;
 using smat::TensorRec;
 
 namespace {
@@ -77,6 +79,17 @@ smat_status make_param(const smat_op_params& p, ParamRec* out, const char* where
   }
   *out = r;
   return SMAT_OK;
+}
+
+// The inputs of the coefficient when the scale comes from device memory (checked by make_param):
+// t = fl32(scale * s) / keep under rescale with 0 < keep < 1, else fl32(scale * s); a tensor with
+// keep <= 0 keeps nothing and never reads t.
+ScaleRec make_scale(const smat_op_params& p) {
+  ScaleRec r{};
+  r.s = p.s;
+  r.keep = p.keep;
+  r.divide = (p.rescale && p.keep > 0.f && p.keep < 1.f) ? 1u : 0u;
+  return r;
 }
 
 uint32_t sim_flags(const float* theta, const void* theta0, int t0_dt, const void* out, int out_dt,
@@ -293,16 +306,17 @@ struct smat_plan {
   std::vector<uint2> chunks;  // (tensor index, chunk index within the tensor)
   std::vector<void*> expert_ptrs, sim_ptrs;
 
-  // workspace layout: [tensor records][chunk table][expert pointer table][simulated pointer table][params]
-  // [optimizer state table][gradient-norm partials: kNormPartialsPerChunk floats per chunk][their fp64 sums]
-  size_t off_recs = 0, off_chunks = 0, off_expert = 0, off_sim = 0, off_params = 0, ws_bytes = 0;
+  // workspace layout: [tensor records][chunk table][expert pointer table][simulated pointer table]
+  // [params, then the scale records of the device-driven launches][optimizer state table][gradient-norm partials: kNormPartialsPerChunk floats per chunk][their fp64 sums]
+  size_t off_recs = 0, off_chunks = 0, off_expert = 0, off_sim = 0, off_params = 0, off_scales = 0, ws_bytes = 0;
   size_t off_partials = 0, off_sums = 0;
   char* ws = nullptr;
 
-  // pinned staging for the asynchronous uploads: the static tables once, the params every step
-  // through two alternating slots, so a new upload only waits for the one before the last
+  // pinned staging for the asynchronous uploads: the static tables once, the params (with their
+  // scale records) every step through two alternating slots, so a new upload only waits for the one
+  // before the last
   char* static_staging = nullptr;
-  ParamRec* params_staging[2] = {nullptr, nullptr};
+  char* params_staging[2] = {nullptr, nullptr};
   hipEvent_t ev_static = nullptr;
   hipEvent_t ev_params[2] = {nullptr, nullptr};
   bool params_pending[2] = {false, false};
@@ -333,7 +347,7 @@ smat_status release(smat_plan* p) {
     if (e) (void)hipEventSynchronize(e);
   if (p->static_staging) (void)hipHostFree(p->static_staging);
   if (p->adam_staging) (void)hipHostFree(p->adam_staging);
-  for (ParamRec* s : p->params_staging)
+  for (char* s : p->params_staging)
     if (s) (void)hipHostFree(s);
   for (hipEvent_t e : {p->ev_static, p->ev_params[0], p->ev_params[1], p->ev_release, p->ev_prefetch, p->ev_adam})
     if (e) (void)hipEventDestroy(e);
@@ -466,7 +480,8 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
   p->off_sim = off;
   off = align256(off + sizeof(void*) * count);
   p->off_params = off;
-  off = align256(off + sizeof(ParamRec) * count);
+  p->off_scales = off + sizeof(ParamRec) * count;
+  off = align256(off + (sizeof(ParamRec) + sizeof(ScaleRec)) * count);
   p->off_adam = off;
   off = align256(off + sizeof(AdamRec) * count);
   p->off_partials = off;
@@ -495,8 +510,10 @@ extern "C" smat_status smat_plan_bind_workspace(smat_plan* p, void* workspace, s
   // each resource is created once: a call that failed part-way can be retried without leaking
   if (!p->static_staging)
     SMAT_HIP(hipHostMalloc((void**)&p->static_staging, std::max<size_t>(static_bytes, 256), hipHostMallocDefault));
-  for (ParamRec*& s : p->params_staging)
-    if (!s) SMAT_HIP(hipHostMalloc((void**)&s, sizeof(ParamRec) * std::max(p->count, 1), hipHostMallocDefault));
+  for (char*& s : p->params_staging)
+    if (!s)
+      SMAT_HIP(hipHostMalloc((void**)&s, (sizeof(ParamRec) + sizeof(ScaleRec)) * std::max(p->count, 1),
+                             hipHostMallocDefault));
   std::memset(p->static_staging, 0, static_bytes);
   std::memcpy(p->static_staging + p->off_recs, p->recs.data(), sizeof(TensorRec) * p->count);
   std::memcpy(p->static_staging + p->off_chunks, p->chunks.data(), sizeof(uint2) * p->chunks.size());
@@ -525,17 +542,22 @@ extern "C" smat_status smat_plan_set_params(smat_plan* p, const smat_op_params* 
   if (!p || (p->count > 0 && !per_tensor)) return fail(SMAT_ERR_INVALID, "smat_plan_set_params: null argument");
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_set_params: no workspace bound");
   std::vector<ParamRec> recs(p->count);
+  std::vector<ScaleRec> scales(p->count);
   for (int32_t i = 0; i < p->count; ++i) {
     char where[64];
     std::snprintf(where, sizeof(where), "smat_plan_set_params: tensor %d", i);
     smat_status st = make_param(per_tensor[i], &recs[i], where);
     if (st != SMAT_OK) return st;
+    scales[i] = make_scale(per_tensor[i]);
   }
   const int slot = p->params_slot;
   if (p->params_pending[slot]) SMAT_HIP(hipEventSynchronize(p->ev_params[slot]));  // slot still being read
-  std::memcpy(p->params_staging[slot], recs.data(), sizeof(ParamRec) * p->count);
+  // params and scale records are adjacent in the workspace: one upload carries both
+  const size_t prm_bytes = sizeof(ParamRec) * p->count;
+  std::memcpy(p->params_staging[slot], recs.data(), prm_bytes);
+  std::memcpy(p->params_staging[slot] + prm_bytes, scales.data(), sizeof(ScaleRec) * p->count);
   if (p->count > 0)
-    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_params, p->params_staging[slot], sizeof(ParamRec) * p->count,
+    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_params, p->params_staging[slot], prm_bytes + sizeof(ScaleRec) * p->count,
                             hipMemcpyHostToDevice, stream));
   SMAT_HIP(hipEventRecord(p->ev_params[slot], stream));
   p->params_pending[slot] = true;
@@ -583,6 +605,56 @@ extern "C" smat_status smat_backward_multi(smat_plan* p, uint64_t seed, uint32_t
 extern "C" smat_status smat_backward_accum_multi(smat_plan* p, uint64_t seed, uint32_t step, float lambda,
                                                  hipStream_t stream) {
   return smat_backward_multi(p, seed, step, lambda, 1, stream);
+}
+
+namespace {
+// Checks shared by the device-driven launches, which may run under stream capture: nothing here
+// synchronizes or waits on an event recorded outside the stream.
+smat_status check_dev_call(const smat_plan* p, const smat_step_state* state, const char* where) {
+  if (!p || !state) return fail(SMAT_ERR_INVALID, "%s: null argument", where);
+  if (!aligned(state, 16)) return fail(SMAT_ERR_INVALID, "%s: step state not 16-byte aligned", where);
+  if (p->offload)
+    return fail(SMAT_ERR_STATE, "%s: offload plans prefetch theta0 on their own copy stream; use the host-driven call",
+                where);
+  if (!p->ws) return fail(SMAT_ERR_STATE, "%s: no workspace bound", where);
+  if (!p->params_set) return fail(SMAT_ERR_STATE, "%s: parameters never set", where);
+  return SMAT_OK;
+}
+}  // namespace
+
+extern "C" smat_status smat_simulate_multi_dev(smat_plan* p, const smat_step_state* state, hipStream_t stream) {
+  smat_status st = check_dev_call(p, state, "smat_simulate_multi_dev");
+  if (st != SMAT_OK) return st;
+  if (p->state != SMAT_EXPERT)
+    return fail(SMAT_ERR_STATE, "smat_simulate_multi_dev: the simulated storage is active (restore the expert first)");
+  if (!p->chunks.empty())
+    SMAT_HIP(smat::launch_simulate_multi_dev(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                             reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                             reinterpret_cast<const ScaleRec*>(p->ws + p->off_scales),
+                                             reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
+                                             (uint32_t)p->chunks.size(), p->t0_dt, p->out_dt,
+                                             reinterpret_cast<const StepState*>(state), stream));
+  p->fresh = true;
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_backward_multi_dev(smat_plan* p, const smat_step_state* state, float lambda,
+                                               int32_t accumulate, hipStream_t stream) {
+  smat_status st = check_dev_call(p, state, "smat_backward_multi_dev");
+  if (st != SMAT_OK) return st;
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_backward_multi_dev: lambda must be finite");
+  if (accumulate != 0 && accumulate != 1)
+    return fail(SMAT_ERR_INVALID, "smat_backward_multi_dev: accumulate must be 0 or 1");
+  if (!p->has_gs || !p->has_gt)
+    return fail(SMAT_ERR_STATE, "smat_backward_multi_dev: gradient arrays not set (smat_plan_set_grads)");
+  if (!p->chunks.empty())
+    SMAT_HIP(smat::launch_backward_multi_dev(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                             reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                             reinterpret_cast<const ScaleRec*>(p->ws + p->off_scales),
+                                             reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
+                                             (uint32_t)p->chunks.size(), p->g_dt, accumulate != 0, lambda,
+                                             reinterpret_cast<const StepState*>(state), stream));
+  return SMAT_OK;
 }
 
 extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_state* per_tensor, hipStream_t stream) {

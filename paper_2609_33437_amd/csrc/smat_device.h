@@ -49,6 +49,33 @@ struct alignas(16) ParamRec {
 };
 static_assert(sizeof(ParamRec) == 16, "ParamRec layout");
 
+// Per-step values read from device memory by the graph-capturable launches (the layout of
+// smat_step_state): the Philox key, the global step (taken modulo 2^30 by the counter word) and a
+// scale multiplying every tensor's s.
+struct alignas(16) StepState {
+  uint64_t seed;
+  uint32_t step;
+  float scale;
+};
+static_assert(sizeof(StepState) == 16, "StepState layout");
+
+// What the coefficient of a tensor needs when the scale comes from device memory: the tensor's own
+// s and keep, and whether kept coordinates divide by keep (rescale with 0 < keep < 1).
+struct alignas(16) ScaleRec {
+  float s;
+  float keep;
+  uint32_t divide;
+  uint32_t pad;
+};
+static_assert(sizeof(ScaleRec) == 16, "ScaleRec layout");
+
+// t = s'/keep or s' for s' = fl32(scale * s): the same rounding as the host forms from s' (one fp64
+// division rounded once to fp32), so a device-driven step gives the bits of the host-driven one.
+__device__ __forceinline__ float device_coefficient(float scale, const ScaleRec& r) {
+  const float s = scale * r.s;
+  return r.divide ? (float)((double)s / (double)r.keep) : s;
+}
+
 // Optimizer state of one tensor for the fused optimizer step, and the per-call constants of that
 // step (all formed on the host in fp64 and rounded once to fp32).
 struct alignas(16) AdamRec {

@@ -259,6 +259,43 @@ __global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __re
   backward_tile<TG, kBwdQuads, ACC>(T, prms[ch.x], seed, step, lambda);
 }
 
+// The same list kernels with the step's seed, step and scale read from device memory, so that a
+// captured graph replays them with whatever the caller last wrote there.  Each block forms its
+// tensor's coefficient from that scale and the tensor's ScaleRec exactly as the host forms it.
+template <typename T0, typename TO>
+__global__ __launch_bounds__(kBlock) void k_simulate_multi_dev(const TensorRec* __restrict__ recs,
+                                                               const ParamRec* __restrict__ prms,
+                                                               const ScaleRec* __restrict__ scales,
+                                                               const uint2* __restrict__ chunks,
+                                                               const StepState* __restrict__ state) {
+  constexpr int64_t tile = tile_elems(kSimQuads);
+  constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
+  const uint2 ch = chunks[blockIdx.x / tpc];
+  const Tile T = list_tile<T0, TO, float>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  if (T.len == 0) return;
+  const StepState S = *state;
+  ParamRec P = prms[ch.x];
+  P.t = device_coefficient(S.scale, scales[ch.x]);
+  simulate_tile<T0, TO, kSimQuads>(T, P, S.seed, S.step);
+}
+
+template <typename TG, bool ACC>
+__global__ __launch_bounds__(kBlock) void k_backward_multi_dev(const TensorRec* __restrict__ recs,
+                                                               const ParamRec* __restrict__ prms,
+                                                               const ScaleRec* __restrict__ scales,
+                                                               const uint2* __restrict__ chunks,
+                                                               const StepState* __restrict__ state, float lambda) {
+  constexpr int64_t tile = tile_elems(kBwdQuads);
+  constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
+  const uint2 ch = chunks[blockIdx.x / tpc];
+  const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  if (T.len == 0) return;
+  const StepState S = *state;
+  ParamRec P = prms[ch.x];
+  P.t = device_coefficient(S.scale, scales[ch.x]);
+  backward_tile<TG, kBwdQuads, ACC>(T, P, S.seed, S.step, lambda);
+}
+
 constexpr int kDebugBlock = 256;
 
 __global__ __launch_bounds__(kDebugBlock) void k_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id,
@@ -335,6 +372,36 @@ hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, co
     k_backward_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
   else
     k_backward_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
+  return hipGetLastError();
+}
+
+hipError_t launch_simulate_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
+                                     const uint2* chunks, uint32_t nchunks, int theta0_dtype, int out_dtype,
+                                     const StepState* state, hipStream_t stream) {
+  const dim3 grid(nchunks * tiles_per_chunk(kSimQuads)), block(kBlock);
+  if (theta0_dtype == 1 && out_dtype == 1)
+    k_simulate_multi_dev<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state);
+  else if (theta0_dtype == 1 && out_dtype == 0)
+    k_simulate_multi_dev<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state);
+  else if (theta0_dtype == 0 && out_dtype == 1)
+    k_simulate_multi_dev<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state);
+  else
+    k_simulate_multi_dev<float, float><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state);
+  return hipGetLastError();
+}
+
+hipError_t launch_backward_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
+                                     const uint2* chunks, uint32_t nchunks, int grad_dtype, bool accumulate,
+                                     float lambda, const StepState* state, hipStream_t stream) {
+  const dim3 grid(nchunks * tiles_per_chunk(kBwdQuads)), block(kBlock);
+  if (grad_dtype == 1 && accumulate)
+    k_backward_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state, lambda);
+  else if (grad_dtype == 1)
+    k_backward_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state, lambda);
+  else if (accumulate)
+    k_backward_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state, lambda);
+  else
+    k_backward_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state, lambda);
   return hipGetLastError();
 }
 

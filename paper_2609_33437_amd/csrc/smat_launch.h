@@ -18,6 +18,14 @@ hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, co
 hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                  int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
                                  hipStream_t stream);
+// Graph-capturable forms: seed, step and scale read from `state` in device memory, each tensor's
+// coefficient formed from the scale and its ScaleRec.
+hipError_t launch_simulate_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
+                                     const uint2* chunks, uint32_t nchunks, int theta0_dtype, int out_dtype,
+                                     const StepState* state, hipStream_t stream);
+hipError_t launch_backward_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
+                                     const uint2* chunks, uint32_t nchunks, int grad_dtype, bool accumulate,
+                                     float lambda, const StepState* state, hipStream_t stream);
 hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const ParamRec& prm, const AdamConsts& A,
                             int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
                             const float* dev_scale, hipStream_t stream);

@@ -51,6 +51,7 @@ int main(void) {
          offsetof(smat_merge_desc, elem_offset));
   printf("%zu %zu %zu %zu\\n", offsetof(smat_tensor_desc, n), offsetof(smat_tensor_desc, tensor_id),
          offsetof(smat_tensor_desc, elem_offset), offsetof(smat_rng_key, elem_offset));
+  printf("%zu %zu %zu\\n", sizeof(smat_step_state), offsetof(smat_step_state, step), offsetof(smat_step_state, scale));
   return 0;
 }
 """)
@@ -64,6 +65,8 @@ int main(void) {
             _lib.smat_merge_term.seed.offset, _lib.smat_merge_desc.n.offset, _lib.smat_merge_desc.elem_offset.offset,
             _lib.smat_tensor_desc.n.offset, _lib.smat_tensor_desc.tensor_id.offset,
             _lib.smat_tensor_desc.elem_offset.offset, _lib.smat_rng_key.elem_offset.offset]
+    # smat_step_state as StepState packs it: seed, step, scale in 16 bytes
+    want += [16, 8, 12]
     assert [int(x) for x in out] == want
 
 
@@ -155,6 +158,32 @@ def test_plan_create_validation_without_gpu():
     assert lib.smat_switch_storage(p, 5, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_plan_destroy(p) == 0
     assert lib.smat_plan_destroy(None) == 0
+
+
+def test_device_driven_calls_without_gpu():
+    """The device-driven list calls check their arguments and the plan's state on the host and
+    return before any HIP call: null or misaligned state, offload plans, unbound plans."""
+    lib = smat.lib()
+    lib.smat_last_error.restype = ctypes.c_char_p
+    A = 1 << 20
+    state = ctypes.c_void_p(64 * A)
+    arr = (_lib.smat_tensor_desc * 1)(_desc(1 * A, 2 * A, 3 * A, 4 * A, 5 * A, 1000, 0))
+    p = ctypes.c_void_p()
+    assert lib.smat_plan_create(arr, 1, 1, 1, 1, 0, ctypes.byref(p)) == 0
+    assert lib.smat_simulate_multi_dev(None, state, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_simulate_multi_dev(p, None, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_simulate_multi_dev(p, ctypes.c_void_p(64 * A + 8), None) == _lib.SMAT_ERR_INVALID
+    assert b"16-byte aligned" in lib.smat_last_error()
+    assert lib.smat_simulate_multi_dev(p, state, None) == _lib.SMAT_ERR_STATE           # no workspace
+    assert lib.smat_backward_multi_dev(p, None, 1.0, 1, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_backward_multi_dev(p, state, 1.0, 1, None) == _lib.SMAT_ERR_STATE    # no workspace
+    assert lib.smat_plan_destroy(p) == 0
+    arr = (_lib.smat_tensor_desc * 1)(_desc(1 * A, 2 * A, None, 4 * A, 5 * A, 1000, 0, 0, 11 * A))
+    assert lib.smat_plan_create(arr, 1, 1, 1, 1, 1, ctypes.byref(p)) == 0
+    assert lib.smat_simulate_multi_dev(p, state, None) == _lib.SMAT_ERR_STATE
+    assert b"offload" in lib.smat_last_error()
+    assert lib.smat_backward_multi_dev(p, state, 1.0, 0, None) == _lib.SMAT_ERR_STATE
+    assert lib.smat_plan_destroy(p) == 0
 
 
 def test_clear_grads_without_gpu():

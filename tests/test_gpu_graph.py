@@ -1,0 +1,274 @@
+"""GPU tests of the device-driven list calls (smat_simulate_multi_dev, smat_backward_multi_dev),
+through the C ABI: they give the bits of the host-driven calls for s' = fl32(scale * s), agree with
+the oracle, and serve every step from one HIP graph (torch.cuda.CUDAGraph stream capture) whether
+the step state is rewritten from the host between replays or advanced by torch ops captured in the
+same graph; every replay is checked against the eager host-driven result of its step."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_33437_amd as smat
+import workloads
+from helpers import host
+from tolerances import check_grad, check_theta_tilde
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def mini():
+    cfg = workloads.config("mini")
+    inp = workloads.make_inputs(cfg, device="cpu")
+    return cfg, inp
+
+
+def base_params(cfg, inp, step):
+    """The mini list's per-tensor settings, with rescale off on one masked tensor, a tensor that keeps
+    nothing (and has no noise) and Laplace noise on another: every form of the coefficient."""
+    p = workloads.step_params(cfg, inp.settings, step)
+    p[2] = dict(p[2], rescale=0)
+    p[5] = dict(p[5], keep=0.0, sigma=0.0)
+    p[7] = dict(p[7], noise_kind=smat.SMAT_NOISE_LAPLACE, sigma=1e-4)
+    return p
+
+
+def scaled(params, scale):
+    """The host-driven parameters of a device step: s' = fl32(scale * s) per tensor."""
+    return [dict(p, s=float(np.float32(scale) * np.float32(p["s"]))) for p in params]
+
+
+def list_tensors(inp):
+    th = [t.to(DEV).view(-1) for t in inp.theta]
+    t0 = [t.to(DEV).view(-1) for t in inp.theta0]
+    gs = [t.to(DEV).view(-1) for t in inp.grad_sim]
+    return th, t0, gs
+
+
+def fresh(inp):
+    out = [torch.full((t.numel(),), float("nan"), dtype=torch.bfloat16, device=DEV) for t in inp.theta]
+    gt = [t.to(DEV).view(-1).clone() for t in inp.grad_theta]
+    return out, gt
+
+
+def same_bits(a, b):
+    return all(torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32),
+                           y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
+               for x, y in zip(a, b))
+
+
+@pytest.mark.parametrize("accumulate", [True, False])
+def test_device_step_is_host_step_with_scaled_s(mini, accumulate):
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out_d, gt_d = fresh(inp)
+    out_h, gt_h = fresh(inp)
+    step, scale = 5, 0.8125
+    base = base_params(cfg, inp, step)
+    state = smat.StepState(cfg.smat_seed, step, scale)
+    with smat.Plan(th, out_d, t0, gs, gt_d) as pd, smat.Plan(th, out_h, t0, gs, gt_h) as ph:
+        pd.set_params(base)
+        pd.simulate_dev(state)
+        pd.backward_dev(state, cfg.lam, accumulate)
+        ph.set_params(scaled(base, scale))
+        ph.simulate(cfg.smat_seed, step)
+        ph.backward(cfg.smat_seed, step, cfg.lam, accumulate)
+        torch.cuda.synchronize()
+    assert same_bits(out_d, out_h)
+    assert same_bits(gt_d, gt_h)
+
+
+def test_device_step_oracle_parity(mini):
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out, gt = fresh(inp)
+    step, scale = 9, 0.4375
+    base = base_params(cfg, inp, step)
+    params = scaled(base, scale)
+    state = smat.StepState(cfg.smat_seed, step, scale)
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        plan.set_params(base)
+        plan.simulate_dev(state)
+        plan.backward_dev(state, cfg.lam, True)
+        torch.cuda.synchronize()
+    for i in range(cfg.count):
+        p = params[i]
+        thn, _ = host(inp.theta[i])
+        t0n, t0_dt = host(inp.theta0[i])
+        y, kept, eps = oracle.simulate_f64(thn.ravel(), t0n.ravel(), t0_dt, p, cfg.smat_seed, step, i)
+        coef = np.where(kept, oracle.coefficient(p["s"], p["keep"], p["rescale"]), 0.0)
+        got, out_dt = host(out[i])
+        ok, _ = check_theta_tilde(got, out_dt, y, thn.ravel(), oracle.as_f64(t0n.ravel(), t0_dt), coef, eps,
+                                  p["sigma"])
+        assert ok.all(), f"tensor {i}: {np.count_nonzero(~ok)} theta~ mismatches"
+        gsn, gs_dt = host(inp.grad_sim[i])
+        g_old, _ = host(inp.grad_theta[i])
+        want = oracle.backward_accum(gsn.ravel(), gs_dt, g_old.ravel(), p, cfg.lam, cfg.smat_seed, step, i)
+        gotg, _ = host(gt[i])
+        incr = np.abs(cfg.lam * coef * oracle.as_f64(gsn.ravel(), gs_dt))
+        assert check_grad(gotg.ravel(), want, g_old.ravel(), incr).all(), f"tensor {i}"
+    assert (host(out[5])[0] == host(inp.theta0[5])[0].ravel()).all()    # keep = 0, no noise: theta0
+
+
+@pytest.mark.parametrize("g_dtype", [torch.bfloat16, torch.float32])
+def test_device_step_ragged_misaligned(g_dtype):
+    # per-element paths: pointers off the quad alignment, odd offsets, a tile that crosses 2^34
+    g = torch.Generator(DEV).manual_seed(4)
+    sizes = [1, 5, 16385, 70001, 9001, 40003]
+    shifts = [0, 3, 0, 1, 0, 2]
+    offs = [0, 0, 2 ** 33 + 1, 4, 2 ** 34 - 4096, 2 ** 34 + 8]
+    keeps = [0.5, 1.0, 0.25, 0.0, 0.4, 0.7]
+    th = [(torch.randn(n + 8, device=DEV, generator=g) * 0.02)[s:s + n] for n, s in zip(sizes, shifts)]
+    t0 = [(torch.randn(n + 8, device=DEV, generator=g) * 0.02)[s:s + n] for n, s in zip(sizes, shifts)]
+    gs = [(torch.randn(n + 8, device=DEV, generator=g) * 1e-2).to(g_dtype)[s:s + n] for n, s in zip(sizes, shifts)]
+    gt0 = [(torch.randn(n + 8, device=DEV, generator=g) * 1e-3)[s:s + n] for n, s in zip(sizes, shifts)]
+    ids = [20 + i for i in range(len(sizes))]
+    base = [dict(s=0.25 + 0.125 * i, keep=k, sigma=1e-3 * (i % 2), rescale=1, noise_kind=i % 3)
+            for i, k in enumerate(keeps)]
+    step, scale = 1 << 29, 0.6
+    res = {}
+    for mode in ("dev", "host"):
+        out = [torch.full((n,), float("nan"), device=DEV) for n in sizes]
+        gt = [x.clone() for x in gt0]
+        with smat.Plan(th, out, t0, gs, gt, tensor_ids=ids, elem_offsets=offs,
+                       dtypes=(smat.SMAT_F32, smat.SMAT_F32, smat.SMAT_BF16 if g_dtype == torch.bfloat16
+                               else smat.SMAT_F32)) as plan:
+            if mode == "dev":
+                state = smat.StepState(77, step, scale)
+                plan.set_params(base)
+                plan.simulate_dev(state)
+                plan.backward_dev(state, 0.5, True)
+            else:
+                plan.set_params(scaled(base, scale))
+                plan.simulate(77, step)
+                plan.backward(77, step, 0.5, True)
+            torch.cuda.synchronize()
+        res[mode] = (out, gt)
+    assert same_bits(res["dev"][0], res["host"][0])
+    assert same_bits(res["dev"][1], res["host"][1])
+
+
+def test_step_state_views():
+    st = smat.StepState((1 << 40) + 5, 123, 0.25)
+    assert st.seed_view.item() == (1 << 40) + 5
+    assert st.step_view.item() == 123
+    assert st.scale_view.item() == 0.25
+    st.step_view.add_(2)
+    st.scale_view.mul_(3.0)
+    assert st.step_view.item() == 125 and st.scale_view.item() == 0.75
+
+
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_graph_replays_with_host_written_state(mini, accumulate):
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out_d, gt_d = fresh(inp)
+    out_h, gt_h = fresh(inp)
+    base = base_params(cfg, inp, 0)
+    state = smat.StepState(cfg.smat_seed, 0, 1.0)
+    steps = [(cfg.smat_seed, 3, 0.5), (cfg.smat_seed + 1, 4, 0.9), (cfg.smat_seed, 1 << 20, 0.3125)]
+    gen = torch.Generator(DEV).manual_seed(6)
+    with smat.Plan(th, out_d, t0, gs, gt_d) as pd, smat.Plan(th, out_h, t0, gs, gt_h) as ph:
+        pd.set_params(base)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):                     # one eager call before capture
+            pd.simulate_dev(state)
+            pd.backward_dev(state, cfg.lam, accumulate)
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            pd.simulate_dev(state)
+            pd.backward_dev(state, cfg.lam, accumulate)
+        for seed, step, scale in steps:
+            # eager work between replays: fresh gradients in both lists, poisoned outputs
+            for a, b in zip(gt_d, gt_h):
+                a.copy_(torch.randn(a.numel(), device=DEV, generator=gen) * 1e-3)
+                b.copy_(a)
+            for o in out_d:
+                o.fill_(float("nan"))
+            state.set(seed, step, scale)
+            graph.replay()
+            ph.set_params(scaled(base, scale))
+            ph.simulate(seed, step)
+            ph.backward(seed, step, cfg.lam, accumulate)
+            torch.cuda.synchronize()
+            assert same_bits(out_d, out_h), (seed, step, scale)
+            assert same_bits(gt_d, gt_h), (seed, step, scale)
+        del graph
+
+
+def test_graph_advances_its_own_state(mini):
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out_d, gt_d = fresh(inp)
+    out_h, gt_h = fresh(inp)
+    base = base_params(cfg, inp, 0)
+    step0, scale0 = 40, 0.75
+    state = smat.StepState(cfg.smat_seed, step0, scale0)
+    with smat.Plan(th, out_d, t0, gs, gt_d) as pd, smat.Plan(th, out_h, t0, gs, gt_h) as ph:
+        pd.set_params(base)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):                     # warm the torch ops and the plan once
+            state.step_view.add_(1)
+            state.scale_view.mul_(0.5)
+            pd.simulate_dev(state)
+            pd.backward_dev(state, cfg.lam, False)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        state.set(cfg.smat_seed, step0, scale0)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            state.step_view.add_(1)
+            state.scale_view.mul_(0.5)
+            pd.simulate_dev(state)
+            pd.backward_dev(state, cfg.lam, False)
+        for k in range(1, 4):
+            for o in out_d:
+                o.fill_(float("nan"))
+            graph.replay()
+            step, scale = step0 + k, scale0 * 0.5 ** k
+            ph.set_params(scaled(base, scale))
+            ph.simulate(cfg.smat_seed, step)
+            ph.backward(cfg.smat_seed, step, cfg.lam, False)
+            torch.cuda.synchronize()
+            assert state.step_view.item() == step and state.scale_view.item() == scale
+            assert same_bits(out_d, out_h), k
+            assert same_bits(gt_d, gt_h), k
+        del graph
+
+
+def test_device_calls_errors(mini):
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out, gt = fresh(inp)
+    state = smat.StepState(1, 2, 0.5)
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        with pytest.raises(smat.SmatError):
+            plan.simulate_dev(state)                                   # parameters never set
+        plan.set_params(base_params(cfg, inp, 2))
+        with pytest.raises(smat.SmatError):
+            plan.simulate_dev(torch.zeros(3, dtype=torch.int32, device=DEV))   # 12 bytes
+        with pytest.raises(smat.SmatError):
+            plan.simulate_dev(torch.zeros(4, dtype=torch.int32))               # host tensor
+        with pytest.raises(smat.SmatError):
+            plan.simulate_dev(torch.zeros(8, dtype=torch.int32, device=DEV)[1:5])  # not 16-byte aligned
+        with pytest.raises(smat.SmatError):
+            plan.backward_dev(state, float("inf"))
+        plan.simulate_dev(state.tensor)                                # a plain 16-byte tensor works too
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        with pytest.raises(smat.SmatError):
+            plan.simulate_dev(state)                                   # simulated storage active
+        plan.backward_dev(state, cfg.lam)                              # the backward needs no switch
+        plan.switch_storage(smat.SMAT_EXPERT)
+        torch.cuda.synchronize()
+    hosts = [t.contiguous().view(-1).pin_memory() for t in inp.theta0]
+    bufs = [torch.zeros(t.numel(), dtype=torch.bfloat16, device=DEV) for t in th]
+    with smat.Plan(th, bufs, None, offload=True, theta0_hosts=hosts,
+                   dtypes=(smat.SMAT_BF16, smat.SMAT_BF16, smat.SMAT_BF16)) as off:
+        off.set_params(base_params(cfg, inp, 2))
+        with pytest.raises(smat.SmatError, match="offload"):
+            off.simulate_dev(state)
+        torch.cuda.synchronize()
