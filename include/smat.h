@@ -341,6 +341,35 @@ smat_status smat_adamw_fused_multi(smat_plan* plan, uint64_t seed, uint32_t step
 smat_status smat_grad_norm_multi(smat_plan* plan, uint64_t seed, uint32_t step, float lambda, int32_t accumulate,
                                  float max_norm, double* sumsq, float* clip_coef, hipStream_t stream);
 
+/* The optimizer's per-step values for smat_adamw_fused_multi_dev, read from device memory when the
+ * update runs (so a captured graph can advance them):
+ *   lr    learning rate of this step, finite and >= 0
+ *   step  the optimizer's step count k >= 1 of this update (bias corrections 1 - beta^k)
+ * Neither is checked on the device; step 0 or a non-finite lr makes the update non-finite. */
+typedef struct smat_adam_step_state {
+  float lr;
+  uint32_t step;
+} smat_adam_step_state;
+
+/* smat_adamw_fused_multi_dev / smat_grad_norm_multi_dev -- smat_adamw_fused_multi and
+ * smat_grad_norm_multi with seed, step and scale read from `state` (see smat_step_state; the
+ * coefficient of each tensor is formed as smat_simulate_multi_dev forms it).  The optimizer step
+ * also reads `adam_state` (device-accessible, 8-byte aligned, caller-owned); hp supplies beta1,
+ * beta2, eps, weight_decay and grad_scale, and its lr and step are ignored.  A one-thread launch
+ * first forms the step's constants into the plan's workspace with the same fp64 operations as
+ * the host-driven call: given the same values both calls give the same bits.  Optimizer calls on
+ * one plan share those constants, and norm calls the norm partials: calls that overlap (on
+ * different streams) race.  No host synchronisation and no wait on an outside event, so both may
+ * be recorded under stream capture; not for offload plans.  Errors: SMAT_ERR_INVALID (null or
+ * misaligned states, lambda, accumulate, hyperparameters, outputs as in smat_grad_norm_multi),
+ * SMAT_ERR_STATE (offload plan, no workspace, params or optimizer state, gradient arrays not set,
+ * simulated storage active for the optimizer step), SMAT_ERR_HIP. */
+smat_status smat_adamw_fused_multi_dev(smat_plan* plan, const smat_step_state* state,
+                                       const smat_adam_step_state* adam_state, smat_adamw_params hp, float lambda,
+                                       int32_t accumulate, const float* grad_scale_dev, hipStream_t stream);
+smat_status smat_grad_norm_multi_dev(smat_plan* plan, const smat_step_state* state, float lambda, int32_t accumulate,
+                                     float max_norm, double* sumsq, float* clip_coef, hipStream_t stream);
+
 /* smat_switch_storage -- point the model at the simulated buffer (SMAT_SIMULATED) or back at the
  * expert storage (SMAT_EXPERT) (Sec. 4.3, "Parameter storage switching").  The plan holds one
  * device table of per-tensor pointers for each storage; switching selects the active one (see

@@ -31,7 +31,7 @@ EXPORTS = (
     "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
     "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
     "smat_stream_copy", "smat_backward_multi", "smat_plan_clear_grads", "smat_simulate_multi_dev",
-    "smat_backward_multi_dev",
+    "smat_backward_multi_dev", "smat_adamw_fused_multi_dev", "smat_grad_norm_multi_dev",
 )
 
 
@@ -126,6 +126,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_plan_clear_grads": [P, c_int32],
         "smat_simulate_multi_dev": [P, P, P],
         "smat_backward_multi_dev": [P, P, c_float, c_int32, P],
+        "smat_adamw_fused_multi_dev": [P, P, P, smat_adamw_params, c_float, c_int32, P, P],
+        "smat_grad_norm_multi_dev": [P, P, c_float, c_int32, c_float, P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -223,12 +225,37 @@ class StepState:
         return self.tensor[3:4].view(_torch().float32)
 
 
-def _state_ptr(state):
-    """Device pointer of a StepState, or of a contiguous 16-byte GPU tensor in its layout."""
-    t = state.tensor if isinstance(state, StepState) else state
-    if t is None or t.numel() * t.element_size() != 16:
-        raise SmatError(SMAT_ERR_INVALID, "step state must be a StepState or a 16-byte GPU tensor")
-    return _dev_ptr(t, "step state")
+class AdamStepState:
+    """The optimizer's per-step values for the device-driven fused optimizer step, in GPU memory:
+    lr (float32) and the step count (uint32), the layout of smat_adam_step_state.  lr_view and
+    step_view are one-element views that captured torch ops can update in place."""
+
+    def __init__(self, lr: float = 0.0, step: int = 1, device=None):
+        torch = _torch()
+        self.tensor = torch.zeros(2, dtype=torch.int32, device=device if device is not None else "cuda")
+        self.set(lr, step)
+
+    def set(self, lr: float, step: int) -> None:
+        import numpy as np
+        rec = np.zeros(1, dtype=[("lr", "<f4"), ("step", "<u4")])
+        rec["lr"], rec["step"] = float(lr), int(step)
+        self.tensor.copy_(_torch().from_numpy(rec.view(np.int32).copy()))
+
+    @property
+    def lr_view(self):
+        return self.tensor[0:1].view(_torch().float32)
+
+    @property
+    def step_view(self):
+        return self.tensor[1:2]
+
+
+def _state_ptr(state, cls=StepState, nbytes: int = 16, what: str = "step state"):
+    """Device pointer of a StepState (AdamStepState), or of a contiguous GPU tensor of its size."""
+    t = state.tensor if isinstance(state, cls) else state
+    if t is None or t.numel() * t.element_size() != nbytes:
+        raise SmatError(SMAT_ERR_INVALID, f"{what} must be a {cls.__name__} or a {nbytes}-byte GPU tensor")
+    return _dev_ptr(t, what)
 
 
 def _expect(t, n: int, code: int, what: str) -> None:
@@ -474,6 +501,25 @@ class Plan:
         _check(lib().smat_grad_norm_multi(self._plan, int(seed), int(step), float(lam), 1 if accumulate else 0,
                                           float(max_norm), _scalar_ptr(sumsq, "sumsq", "float64"),
                                           _scalar_ptr(clip_coef, "clip_coef", "float32"), _stream_handle(stream)))
+
+    def adamw_fused_dev(self, state, adam_state, lam: float, hp, accumulate: bool = False, grad_scale_dev=None,
+                        stream=None) -> None:
+        """smat_adamw_fused_multi_dev: seed, step and scale from `state`, lr and the optimizer's step
+        count from `adam_state` (an AdamStepState); hp gives the other hyperparameters."""
+        if isinstance(hp, dict):
+            hp = dict(dict(lr=0.0, step=1), **hp)
+        _check(lib().smat_adamw_fused_multi_dev(self._plan, _state_ptr(state),
+                                                _state_ptr(adam_state, AdamStepState, 8, "optimizer step state"),
+                                                adamw_params(hp), float(lam), 1 if accumulate else 0,
+                                                _scalar_ptr(grad_scale_dev, "grad_scale_dev", "float32"),
+                                                _stream_handle(stream)))
+
+    def grad_norm_dev(self, state, lam: float, accumulate: bool = False, max_norm: float = 0.0, sumsq=None,
+                      clip_coef=None, stream=None) -> None:
+        """smat_grad_norm_multi_dev: grad_norm with seed, step and scale read from `state`."""
+        _check(lib().smat_grad_norm_multi_dev(self._plan, _state_ptr(state), float(lam), 1 if accumulate else 0,
+                                              float(max_norm), _scalar_ptr(sumsq, "sumsq", "float64"),
+                                              _scalar_ptr(clip_coef, "clip_coef", "float32"), _stream_handle(stream)))
 
     def switch_storage(self, to: int, stream=None) -> None:
         # the stream orders only the offload prefetch; a resident plan's switch enqueues nothing

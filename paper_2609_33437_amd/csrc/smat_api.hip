@@ -142,26 +142,29 @@ smat_status check_grad_ptrs(const float* theta, const void* theta0, int t0_dt, c
   return SMAT_OK;
 }
 
-// Per-call constants of the fused optimizer step, formed in fp64 and rounded once to fp32.
-smat_status make_adam(const smat_adamw_params& hp, AdamConsts* A, const char* where) {
-  if (!std::isfinite(hp.lr) || !std::isfinite(hp.beta1) || !std::isfinite(hp.beta2) || !std::isfinite(hp.eps) ||
+smat::AdamHyper adam_hyper(const smat_adamw_params& hp) {
+  return smat::AdamHyper{hp.beta1, hp.beta2, hp.eps, hp.weight_decay, hp.grad_scale};
+}
+
+// The step-independent hyperparameters (betas, eps, weight decay, gradient scale).
+smat_status check_adam_hyper(const smat_adamw_params& hp, const char* where) {
+  if (!std::isfinite(hp.beta1) || !std::isfinite(hp.beta2) || !std::isfinite(hp.eps) ||
       !std::isfinite(hp.weight_decay) || !std::isfinite(hp.grad_scale))
     return fail(SMAT_ERR_INVALID, "%s: optimizer hyperparameters must be finite", where);
   if (hp.beta1 < 0.f || hp.beta1 >= 1.f || hp.beta2 < 0.f || hp.beta2 >= 1.f)
     return fail(SMAT_ERR_INVALID, "%s: betas must lie in [0, 1)", where);
-  if (hp.eps <= 0.f || hp.lr < 0.f || hp.weight_decay < 0.f)
-    return fail(SMAT_ERR_INVALID, "%s: eps must be > 0, lr and weight_decay >= 0", where);
+  if (hp.eps <= 0.f || hp.weight_decay < 0.f)
+    return fail(SMAT_ERR_INVALID, "%s: eps must be > 0 and weight_decay >= 0", where);
+  return SMAT_OK;
+}
+
+// Per-call constants of the fused optimizer step, formed in fp64 and rounded once to fp32.
+smat_status make_adam(const smat_adamw_params& hp, AdamConsts* A, const char* where) {
+  smat_status st = check_adam_hyper(hp, where);
+  if (st != SMAT_OK) return st;
+  if (!std::isfinite(hp.lr) || hp.lr < 0.f) return fail(SMAT_ERR_INVALID, "%s: lr must be finite and >= 0", where);
   if (hp.step < 1) return fail(SMAT_ERR_INVALID, "%s: step must be >= 1", where);
-  const double b1 = hp.beta1, b2 = hp.beta2, lr = hp.lr;
-  const double bc1 = 1.0 - std::pow(b1, (double)hp.step), bc2 = 1.0 - std::pow(b2, (double)hp.step);
-  A->one_m_b1 = (float)(1.0 - b1);
-  A->b2 = hp.beta2;
-  A->one_m_b2 = (float)(1.0 - b2);
-  A->inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
-  A->step_size = (float)(lr / bc1);
-  A->decay = (float)(1.0 - lr * (double)hp.weight_decay);
-  A->eps = hp.eps;
-  A->grad_scale = hp.grad_scale;
+  *A = smat::adam_consts(adam_hyper(hp), hp.lr, (uint32_t)hp.step);
   return SMAT_OK;
 }
 
@@ -307,9 +310,11 @@ struct smat_plan {
   std::vector<void*> expert_ptrs, sim_ptrs;
 
   // workspace layout: [tensor records][chunk table][expert pointer table][simulated pointer table]
-  // [params, then the scale records of the device-driven launches][optimizer state table][gradient-norm partials: kNormPartialsPerChunk floats per chunk][their fp64 sums]
+  // [params, then the scale records of the device-driven launches][optimizer state table]
+  // [gradient-norm partials: kNormPartialsPerChunk floats per chunk][their fp64 sums]
+  // [the optimizer constants of a device-driven step]
   size_t off_recs = 0, off_chunks = 0, off_expert = 0, off_sim = 0, off_params = 0, off_scales = 0, ws_bytes = 0;
-  size_t off_partials = 0, off_sums = 0;
+  size_t off_partials = 0, off_sums = 0, off_aconsts = 0;
   char* ws = nullptr;
 
   // pinned staging for the asynchronous uploads: the static tables once, the params (with their
@@ -488,6 +493,8 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
   off = align256(off + sizeof(float) * smat::kNormPartialsPerChunk * p->chunks.size());
   p->off_sums = off;
   off = align256(off + sizeof(double) * smat::kNormSums);
+  p->off_aconsts = off;
+  off = align256(off + sizeof(AdamConsts));
   p->ws_bytes = std::max<size_t>(off, 256);
   *out_plan = p;
   return SMAT_OK;
@@ -810,6 +817,62 @@ extern "C" smat_status smat_grad_norm_multi(smat_plan* p, uint64_t seed, uint32_
                                      reinterpret_cast<float*>(p->ws + p->off_partials),
                                      reinterpret_cast<double*>(p->ws + p->off_sums), p->g_dt, accumulate != 0, lambda,
                                      seed, step, sumsq, clip_coef, max_norm, stream));
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_adamw_fused_multi_dev(smat_plan* p, const smat_step_state* state,
+                                                  const smat_adam_step_state* adam_state, smat_adamw_params hp,
+                                                  float lambda, int32_t accumulate, const float* grad_scale_dev,
+                                                  hipStream_t stream) {
+  smat_status st = check_dev_call(p, state, "smat_adamw_fused_multi_dev");
+  if (st != SMAT_OK) return st;
+  if (!adam_state) return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi_dev: null optimizer step state");
+  if (!aligned(adam_state, 8))
+    return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi_dev: optimizer step state not 8-byte aligned");
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi_dev: lambda must be finite");
+  if (accumulate != 0 && accumulate != 1)
+    return fail(SMAT_ERR_INVALID, "smat_adamw_fused_multi_dev: accumulate must be 0 or 1");
+  st = check_adam_hyper(hp, "smat_adamw_fused_multi_dev");
+  if (st != SMAT_OK) return st;
+  if (!p->adam_bound) return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi_dev: optimizer state never bound");
+  if (!p->has_gs || (accumulate && !p->has_gt))
+    return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi_dev: gradient arrays not set (smat_plan_set_grads)");
+  if (p->state != SMAT_EXPERT)
+    return fail(SMAT_ERR_STATE, "smat_adamw_fused_multi_dev: restore the expert storage before the optimizer step");
+  SMAT_HIP(smat::launch_adamw_multi_dev(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                        reinterpret_cast<const AdamRec*>(p->ws + p->off_adam),
+                                        reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                        reinterpret_cast<const ScaleRec*>(p->ws + p->off_scales),
+                                        reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
+                                        (uint32_t)p->chunks.size(), adam_hyper(hp),
+                                        reinterpret_cast<const smat::AdamStepState*>(adam_state),
+                                        reinterpret_cast<AdamConsts*>(p->ws + p->off_aconsts), p->g_dt,
+                                        accumulate != 0, lambda, reinterpret_cast<const StepState*>(state),
+                                        grad_scale_dev, stream));
+  return SMAT_OK;
+}
+
+extern "C" smat_status smat_grad_norm_multi_dev(smat_plan* p, const smat_step_state* state, float lambda,
+                                                int32_t accumulate, float max_norm, double* sumsq, float* clip_coef,
+                                                hipStream_t stream) {
+  smat_status st = check_dev_call(p, state, "smat_grad_norm_multi_dev");
+  if (st != SMAT_OK) return st;
+  if (!std::isfinite(lambda)) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi_dev: lambda must be finite");
+  if (accumulate != 0 && accumulate != 1)
+    return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi_dev: accumulate must be 0 or 1");
+  if (!sumsq && !clip_coef) return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi_dev: no output");
+  if (clip_coef && !(std::isfinite(max_norm) && max_norm > 0.f))
+    return fail(SMAT_ERR_INVALID, "smat_grad_norm_multi_dev: max_norm must be finite and > 0");
+  if (!p->has_gs || (accumulate && !p->has_gt))
+    return fail(SMAT_ERR_STATE, "smat_grad_norm_multi_dev: gradient arrays not set (smat_plan_set_grads)");
+  SMAT_HIP(smat::launch_sqnorm_multi_dev(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
+                                         reinterpret_cast<const ParamRec*>(p->ws + p->off_params),
+                                         reinterpret_cast<const ScaleRec*>(p->ws + p->off_scales),
+                                         reinterpret_cast<const uint2*>(p->ws + p->off_chunks),
+                                         (uint32_t)p->chunks.size(), reinterpret_cast<float*>(p->ws + p->off_partials),
+                                         reinterpret_cast<double*>(p->ws + p->off_sums), p->g_dt, accumulate != 0,
+                                         lambda, reinterpret_cast<const StepState*>(state), sumsq, clip_coef,
+                                         max_norm, stream));
   return SMAT_OK;
 }
 

@@ -77,7 +77,7 @@ __device__ __forceinline__ float device_coefficient(float scale, const ScaleRec&
 }
 
 // Optimizer state of one tensor for the fused optimizer step, and the per-call constants of that
-// step (all formed on the host in fp64 and rounded once to fp32).
+// step (formed in fp64 and rounded once to fp32, by adam_consts below).
 struct alignas(16) AdamRec {
   float* exp_avg;
   float* exp_avg_sq;
@@ -94,6 +94,46 @@ struct AdamConsts {
   float eps;
   float grad_scale;
 };
+
+// The hyperparameters that stay fixed across steps, and the per-step values that the
+// device-driven optimizer step reads from device memory (the layout of smat_adam_step_state).
+struct AdamHyper {
+  float beta1, beta2, eps, weight_decay, grad_scale;
+};
+struct alignas(8) AdamStepState {
+  float lr;
+  uint32_t step;
+};
+static_assert(sizeof(AdamStepState) == 8, "AdamStepState layout");
+
+// beta^k in fp64 by repeated squaring: a fixed sequence of IEEE multiplies.
+__host__ __device__ inline double pow_step(double b, uint32_t k) {
+  double r = 1.0;
+  while (k) {
+    if (k & 1u) r *= b;
+    b *= b;
+    k >>= 1;
+  }
+  return r;
+}
+
+// The constants of step k >= 1 in fp64, without fused multiply-adds, with correctly rounded
+// division and square root, each rounded once to fp32: the host and the device form the same bits.
+__host__ __device__ inline AdamConsts adam_consts(const AdamHyper& h, float lr, uint32_t k) {
+#pragma clang fp contract(off)
+  const double b1 = h.beta1, b2 = h.beta2, l = lr;
+  const double bc1 = 1.0 - pow_step(b1, k), bc2 = 1.0 - pow_step(b2, k);
+  AdamConsts A;
+  A.one_m_b1 = (float)(1.0 - b1);
+  A.b2 = h.beta2;
+  A.one_m_b2 = (float)(1.0 - b2);
+  A.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
+  A.step_size = (float)(l / bc1);
+  A.decay = (float)(1.0 - l * (double)h.weight_decay);
+  A.eps = h.eps;
+  A.grad_scale = h.grad_scale;
+  return A;
+}
 // Static flag: theta, the moments, grad_sim (and grad_theta when accumulating) aligned for quads.
 enum : uint32_t { kVecAdam = 4u, kVecAdamAcc = 8u };
 

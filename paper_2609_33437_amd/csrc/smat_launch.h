@@ -42,6 +42,18 @@ hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, cons
                                float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
                                uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
                                hipStream_t stream);
+// Graph-capturable forms of the list optimizer step and gradient norm: seed, step and scale from
+// `state`; the optimizer's learning rate and step count from `adam_state`, turned into the step's
+// constants in `consts` (device memory of the plan) by a one-thread launch ahead of the update.
+hipError_t launch_sqnorm_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
+                                   const uint2* chunks, uint32_t nchunks, float* partials, double* sums,
+                                   int grad_dtype, bool accumulate, float lambda, const StepState* state,
+                                   double* sumsq, float* clip_coef, float max_norm, hipStream_t stream);
+hipError_t launch_adamw_multi_dev(const TensorRec* recs, const AdamRec* states, const ParamRec* prms,
+                                  const ScaleRec* scales, const uint2* chunks, uint32_t nchunks, const AdamHyper& h,
+                                  const AdamStepState* adam_state, AdamConsts* consts, int grad_dtype,
+                                  bool accumulate, float lambda, const StepState* state, const float* dev_scale,
+                                  hipStream_t stream);
 // ---------------------------------------------------------------- N-expert merge
 // One expert's term on one tensor: its mask key (seed, step), threshold and coefficient
 // t = gamma/keep (rescaled) or gamma, and kFlagMask / kFlagDropAll, plus the ten Philox round keys of

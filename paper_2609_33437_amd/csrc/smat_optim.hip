@@ -144,6 +144,43 @@ __global__ __launch_bounds__(kBlock) void k_adamw_multi(const TensorRec* __restr
   adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, prms[ch.x], A, seed, step, lambda);
 }
 
+// The same list kernel with seed, step and scale read from device memory (each tensor's coefficient
+// formed as the simulate forms it) and the step's constants from `Ad`, which k_adam_consts writes
+// from the device-side learning rate and step count: a captured graph replays it for every step.
+template <typename TG, bool ACC>
+__global__ __launch_bounds__(kBlock) void k_adamw_multi_dev(const TensorRec* __restrict__ recs,
+                                                            const AdamRec* __restrict__ states,
+                                                            const ParamRec* __restrict__ prms,
+                                                            const ScaleRec* __restrict__ scales,
+                                                            const uint2* __restrict__ chunks,
+                                                            const AdamConsts* __restrict__ Ad,
+                                                            const StepState* __restrict__ state, float lambda,
+                                                            const float* dev_scale) {
+  constexpr int64_t tile = tile_elems(kAdamQuads);
+  constexpr uint32_t tpc = tiles_per_chunk(kAdamQuads);
+  const uint2 ch = chunks[blockIdx.x / tpc];
+  const TensorRec R = recs[ch.x];
+  const int64_t begin = (int64_t)ch.y * kChunk + (int64_t)(blockIdx.x % tpc) * tile;
+  const Tile T = list_tile<float, float, TG>(R, ch.y, blockIdx.x % tpc, tile);
+  if (T.len == 0) return;
+  AdamConsts A = *Ad;
+  if (dev_scale) A.grad_scale *= *dev_scale;
+  const StepState S = *state;
+  ParamRec P = prms[ch.x];
+  P.t = device_coefficient(S.scale, scales[ch.x]);
+  const AdamRec M = states[ch.x];
+  adamw_tile<TG, kAdamQuads, ACC>(T, M.exp_avg + begin, M.exp_avg_sq + begin, P, A, S.seed, S.step, lambda);
+}
+
+// One thread forms the step's constants from the learning rate and step count in device memory.
+__global__ __launch_bounds__(64) void k_adam_consts(const AdamStepState* __restrict__ st, AdamHyper h,
+                                                    AdamConsts* __restrict__ out) {
+  if (threadIdx.x == 0) {
+    const AdamStepState s = *st;
+    *out = adam_consts(h, s.lr, s.step);
+  }
+}
+
 // ---------------------------------------------------------------- gradient norm
 // Squared L2 norm of the expert gradient g = [grad_acc +] lambda t m g~ of a simulated step
 // (Eq. smat-gradient weighted by lambda): what norm clipping measures before the optimizer step.
@@ -273,6 +310,27 @@ __global__ __launch_bounds__(kBlock) void k_sqnorm_multi(const TensorRec* __rest
   if (threadIdx.x == 0) partials[blockIdx.x] = s;
 }
 
+template <typename TG, bool ACC>
+__global__ __launch_bounds__(kBlock) void k_sqnorm_multi_dev(const TensorRec* __restrict__ recs,
+                                                             const ParamRec* __restrict__ prms,
+                                                             const ScaleRec* __restrict__ scales,
+                                                             const uint2* __restrict__ chunks, float* partials,
+                                                             const StepState* __restrict__ state, float lambda) {
+  constexpr int64_t tile = tile_elems(kNormQuads);
+  constexpr uint32_t tpc = tiles_per_chunk(kNormQuads);
+  const uint2 ch = chunks[blockIdx.x / tpc];
+  const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  float s = 0.0f;
+  if (T.len > 0) {
+    const StepState S = *state;
+    ParamRec P = prms[ch.x];
+    P.t = device_coefficient(S.scale, scales[ch.x]);
+    s = tile_sqnorm<TG, ACC>(T, P, S.seed, S.step, lambda);
+  }
+  s = block_sum<float, kBlock>(s);
+  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+}
+
 // Block b adds partials [b per, (b + 1) per) in fp64.
 __global__ __launch_bounds__(kSumBlock) void k_sum_partials(const float* __restrict__ partials, uint32_t n,
                                                             uint32_t per, double* sums) {
@@ -330,6 +388,17 @@ hipError_t launch_adamw_multi(const TensorRec* recs, const AdamRec* states, cons
   return hipGetLastError();
 }
 
+// The partials' fp64 sums (m <= kNormSums blocks, each adding `per` consecutive partials), then the
+// outputs.
+static hipError_t launch_sqnorm_reduce(const float* partials, uint32_t npart, double* sums, double* sumsq,
+                                       float* clip_coef, float max_norm, hipStream_t stream) {
+  const uint32_t per = (npart + kNormSums - 1) / kNormSums;
+  const uint32_t m = per ? (npart + per - 1) / per : 0;
+  if (m > 0) k_sum_partials<<<dim3(m), dim3(kSumBlock), 0, stream>>>(partials, npart, per, sums);
+  k_sqnorm_finalize<<<dim3(1), dim3(kSumBlock), 0, stream>>>(sums, m, sumsq, clip_coef, max_norm);
+  return hipGetLastError();
+}
+
 hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
                                uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
@@ -346,11 +415,49 @@ hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, cons
     else
       k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
   }
-  // m <= kNormSums blocks, each adding `per` consecutive partials
-  const uint32_t per = (npart + kNormSums - 1) / kNormSums;
-  const uint32_t m = per ? (npart + per - 1) / per : 0;
-  if (m > 0) k_sum_partials<<<dim3(m), dim3(kSumBlock), 0, stream>>>(partials, npart, per, sums);
-  k_sqnorm_finalize<<<dim3(1), dim3(kSumBlock), 0, stream>>>(sums, m, sumsq, clip_coef, max_norm);
+  return launch_sqnorm_reduce(partials, npart, sums, sumsq, clip_coef, max_norm, stream);
+}
+
+hipError_t launch_sqnorm_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
+                                   const uint2* chunks, uint32_t nchunks, float* partials, double* sums,
+                                   int grad_dtype, bool accumulate, float lambda, const StepState* state,
+                                   double* sumsq, float* clip_coef, float max_norm, hipStream_t stream) {
+  const uint32_t npart = nchunks * kNormPartialsPerChunk;
+  if (npart > 0) {
+    const dim3 grid(npart), block(kBlock);
+    if (grad_dtype == 1 && accumulate)
+      k_sqnorm_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, partials, state, lambda);
+    else if (grad_dtype == 1)
+      k_sqnorm_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, partials, state, lambda);
+    else if (accumulate)
+      k_sqnorm_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, partials, state, lambda);
+    else
+      k_sqnorm_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, partials, state, lambda);
+  }
+  return launch_sqnorm_reduce(partials, npart, sums, sumsq, clip_coef, max_norm, stream);
+}
+
+hipError_t launch_adamw_multi_dev(const TensorRec* recs, const AdamRec* states, const ParamRec* prms,
+                                  const ScaleRec* scales, const uint2* chunks, uint32_t nchunks, const AdamHyper& h,
+                                  const AdamStepState* adam_state, AdamConsts* consts, int grad_dtype,
+                                  bool accumulate, float lambda, const StepState* state, const float* dev_scale,
+                                  hipStream_t stream) {
+  k_adam_consts<<<dim3(1), dim3(64), 0, stream>>>(adam_state, h, consts);
+  if (nchunks > 0) {
+    const dim3 grid(nchunks * tiles_per_chunk(kAdamQuads)), block(kBlock);
+    if (grad_dtype == 1 && accumulate)
+      k_adamw_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, scales, chunks, consts, state,
+                                                                lambda, dev_scale);
+    else if (grad_dtype == 1)
+      k_adamw_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, scales, chunks, consts, state,
+                                                                 lambda, dev_scale);
+    else if (accumulate)
+      k_adamw_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, states, prms, scales, chunks, consts, state,
+                                                                 lambda, dev_scale);
+    else
+      k_adamw_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, states, prms, scales, chunks, consts, state,
+                                                                  lambda, dev_scale);
+  }
   return hipGetLastError();
 }
 

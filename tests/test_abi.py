@@ -52,6 +52,7 @@ int main(void) {
   printf("%zu %zu %zu %zu\\n", offsetof(smat_tensor_desc, n), offsetof(smat_tensor_desc, tensor_id),
          offsetof(smat_tensor_desc, elem_offset), offsetof(smat_rng_key, elem_offset));
   printf("%zu %zu %zu\\n", sizeof(smat_step_state), offsetof(smat_step_state, step), offsetof(smat_step_state, scale));
+  printf("%zu %zu\\n", sizeof(smat_adam_step_state), offsetof(smat_adam_step_state, step));
   return 0;
 }
 """)
@@ -65,8 +66,8 @@ int main(void) {
             _lib.smat_merge_term.seed.offset, _lib.smat_merge_desc.n.offset, _lib.smat_merge_desc.elem_offset.offset,
             _lib.smat_tensor_desc.n.offset, _lib.smat_tensor_desc.tensor_id.offset,
             _lib.smat_tensor_desc.elem_offset.offset, _lib.smat_rng_key.elem_offset.offset]
-    # smat_step_state as StepState packs it: seed, step, scale in 16 bytes
-    want += [16, 8, 12]
+    # smat_step_state and smat_adam_step_state as StepState and AdamStepState pack them
+    want += [16, 8, 12, 8, 4]
     assert [int(x) for x in out] == want
 
 
@@ -177,6 +178,13 @@ def test_device_driven_calls_without_gpu():
     assert lib.smat_simulate_multi_dev(p, state, None) == _lib.SMAT_ERR_STATE           # no workspace
     assert lib.smat_backward_multi_dev(p, None, 1.0, 1, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_backward_multi_dev(p, state, 1.0, 1, None) == _lib.SMAT_ERR_STATE    # no workspace
+    hp = _lib.adamw_params(dict(lr=0.0, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1))
+    adam = ctypes.c_void_p(65 * A)
+    sq = ctypes.c_void_p(66 * A)
+    assert lib.smat_adamw_fused_multi_dev(p, None, adam, hp, 1.0, 0, None, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_adamw_fused_multi_dev(p, state, adam, hp, 1.0, 0, None, None) == _lib.SMAT_ERR_STATE
+    assert lib.smat_grad_norm_multi_dev(p, state, 1.0, 0, 1.0, sq, None, None) == _lib.SMAT_ERR_STATE
+    assert lib.smat_grad_norm_multi_dev(None, state, 1.0, 0, 1.0, sq, None, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_plan_destroy(p) == 0
     arr = (_lib.smat_tensor_desc * 1)(_desc(1 * A, 2 * A, None, 4 * A, 5 * A, 1000, 0, 0, 11 * A))
     assert lib.smat_plan_create(arr, 1, 1, 1, 1, 1, ctypes.byref(p)) == 0

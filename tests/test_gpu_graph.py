@@ -1,8 +1,9 @@
-"""GPU tests of the device-driven list calls (smat_simulate_multi_dev, smat_backward_multi_dev),
-through the C ABI: they give the bits of the host-driven calls for s' = fl32(scale * s), agree with
-the oracle, and serve every step from one HIP graph (torch.cuda.CUDAGraph stream capture) whether
-the step state is rewritten from the host between replays or advanced by torch ops captured in the
-same graph; every replay is checked against the eager host-driven result of its step."""
+"""GPU tests of the device-driven list calls (smat_simulate_multi_dev, smat_backward_multi_dev,
+smat_grad_norm_multi_dev, smat_adamw_fused_multi_dev), through the C ABI: they give the bits of the
+host-driven calls for s' = fl32(scale * s) (and the same learning rate and optimizer step), agree
+with the oracle, and serve every step from one HIP graph (torch.cuda.CUDAGraph stream capture)
+whether the step state is rewritten from the host between replays or advanced by torch ops captured
+in the same graph; every replay is checked against the eager host-driven result of its step."""
 import numpy as np
 import pytest
 import torch
@@ -11,7 +12,7 @@ import oracle
 import paper_2609_33437_amd as smat
 import workloads
 from helpers import host
-from tolerances import check_grad, check_theta_tilde
+from tolerances import check_adam, check_grad, check_theta_tilde
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -272,3 +273,172 @@ def test_device_calls_errors(mini):
         with pytest.raises(smat.SmatError, match="offload"):
             off.simulate_dev(state)
         torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- optimizer step and gradient norm
+HP = dict(beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-3, grad_scale=0.5)
+
+
+def adam_twin(inp, seed):
+    """theta and the two moments of every tensor, twice (one set per plan), equal bit for bit."""
+    gen = torch.Generator(DEV).manual_seed(seed)
+    th = [t.to(DEV).view(-1).clone() for t in inp.theta]
+    m1 = [torch.randn(t.numel(), device=DEV, generator=gen) * 1e-3 for t in th]
+    m2 = [torch.rand(t.numel(), device=DEV, generator=gen) * 1e-6 for t in th]
+    return (th, m1, m2), tuple([x.clone() for x in xs] for xs in (th, m1, m2))
+
+
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_device_norm_is_host_norm(mini, accumulate):
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out, gt = fresh(inp)
+    step, scale = 6, 0.6875
+    base = base_params(cfg, inp, step)
+    state = smat.StepState(cfg.smat_seed, step, scale)
+    sq_d, sq_h = (torch.zeros(1, dtype=torch.float64, device=DEV) for _ in range(2))
+    c_d, c_h = (torch.zeros(1, dtype=torch.float32, device=DEV) for _ in range(2))
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        plan.set_params(base)
+        plan.grad_norm_dev(state, cfg.lam, accumulate, 1e-3, sq_d, c_d)
+        plan.set_params(scaled(base, scale))
+        plan.grad_norm(cfg.smat_seed, step, cfg.lam, accumulate, 1e-3, sq_h, c_h)
+        torch.cuda.synchronize()
+    assert sq_d.item() > 0 and 0 < c_d.item() < 1
+    assert torch.equal(sq_d.view(torch.int64), sq_h.view(torch.int64))
+    assert torch.equal(c_d.view(torch.int32), c_h.view(torch.int32))
+
+
+@pytest.mark.parametrize("accumulate,clip", [(False, False), (True, False), (False, True), (True, True)])
+def test_device_adamw_is_host_adamw(mini, accumulate, clip):
+    cfg, inp = mini
+    _, t0, gs = list_tensors(inp)
+    (th_d, m1_d, m2_d), (th_h, m1_h, m2_h) = adam_twin(inp, 8)
+    out_d, gt = fresh(inp)
+    out_h, _ = fresh(inp)
+    step, scale, lr, k = 11, 0.8125, 2e-5, 7
+    base = base_params(cfg, inp, step)
+    state, adam = smat.StepState(cfg.smat_seed, step, scale), smat.AdamStepState(lr, k)
+    coef = torch.tensor([0.37], dtype=torch.float32, device=DEV) if clip else None
+    with smat.Plan(th_d, out_d, t0, gs, gt) as pd, smat.Plan(th_h, out_h, t0, gs, gt) as ph:
+        pd.set_params(base)
+        pd.bind_adam_state(m1_d, m2_d)
+        pd.adamw_fused_dev(state, adam, cfg.lam, HP, accumulate, coef)
+        ph.set_params(scaled(base, scale))
+        ph.bind_adam_state(m1_h, m2_h)
+        ph.adamw_fused(cfg.smat_seed, step, cfg.lam, dict(HP, lr=lr, step=k), accumulate, coef)
+        torch.cuda.synchronize()
+    for a, b in ((th_d, th_h), (m1_d, m1_h), (m2_d, m2_h)):
+        assert same_bits(a, b)
+
+
+def test_device_adamw_oracle_parity(mini):
+    cfg, inp = mini
+    _, t0, gs = list_tensors(inp)
+    (th, m1, m2), _ = adam_twin(inp, 9)
+    out, gt = fresh(inp)
+    old = [(host(a)[0], host(b)[0], host(c)[0]) for a, b, c in zip(th, m1, m2)]
+    step, scale, lr, k = 13, 0.5625, 3e-5, 4
+    base = base_params(cfg, inp, step)
+    params = scaled(base, scale)
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        plan.set_params(base)
+        plan.bind_adam_state(m1, m2)
+        plan.adamw_fused_dev(smat.StepState(cfg.smat_seed, step, scale), smat.AdamStepState(lr, k), cfg.lam, HP)
+        torch.cuda.synchronize()
+    hp = dict(HP, lr=lr, step=k)
+    for i in range(cfg.count):
+        gsn = host(inp.grad_sim[i])[0]
+        _, f64 = oracle.adamw_fused(gsn, "bf16", *old[i], params[i], cfg.lam, hp, cfg.smat_seed, step, i)
+        gmag = np.abs(oracle.simulated_gradient(gsn, "bf16", params[i], cfg.lam, cfg.smat_seed, step, i)) * hp["grad_scale"]
+        got = (host(th[i])[0], host(m1[i])[0], host(m2[i])[0])
+        for name, ok in zip(("theta", "exp_avg", "exp_avg_sq"), check_adam(got, old[i], f64, hp, gmag)):
+            assert ok.all(), f"tensor {i} {name}: {np.count_nonzero(~ok)} mismatches"
+
+
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_graph_of_a_clipped_fused_step(mini, accumulate):
+    """simulate, gradient norm and clipped fused update captured once; each replay advances the SMAT
+    step and the optimizer step on the device and matches the host-driven step on twin tensors."""
+    cfg, inp = mini
+    _, t0, gs = list_tensors(inp)
+    (th_d, m1_d, m2_d), (th_h, m1_h, m2_h) = adam_twin(inp, 10)
+    out_d, gt = fresh(inp)
+    out_h, _ = fresh(inp)
+    base = base_params(cfg, inp, 0)
+    step0, scale, lr, k0, max_norm = 20, 0.75, 1e-4, 3, 2e-3
+    state, adam = smat.StepState(cfg.smat_seed, step0, scale), smat.AdamStepState(lr, k0)
+    c_d, c_h = (torch.zeros(1, dtype=torch.float32, device=DEV) for _ in range(2))
+    with smat.Plan(th_d, out_d, t0, gs, gt) as pd, smat.Plan(th_h, out_h, t0, gs, gt) as ph:
+        pd.set_params(base)
+        pd.bind_adam_state(m1_d, m2_d)
+        ph.bind_adam_state(m1_h, m2_h)
+
+        def step_ops():
+            state.step_view.add_(1)
+            adam.step_view.add_(1)
+            pd.simulate_dev(state)
+            pd.grad_norm_dev(state, cfg.lam, accumulate, max_norm, clip_coef=c_d)
+            pd.adamw_fused_dev(state, adam, cfg.lam, HP, accumulate, c_d)
+
+        # warm the torch ops once on a side stream on scratch states, then capture
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            smat.StepState(0, 0, 1.0).step_view.add_(1)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step_ops()
+        torch.cuda.synchronize()
+        # capture ran nothing: the tensors and states are as they were
+        assert state.step_view.item() == step0 and adam.step_view.item() == k0
+        for r in range(1, 4):
+            for o in out_d:
+                o.fill_(float("nan"))
+            graph.replay()
+            step, k = step0 + r, k0 + r
+            ph.set_params(scaled(base, scale))
+            ph.simulate(cfg.smat_seed, step)
+            ph.grad_norm(cfg.smat_seed, step, cfg.lam, accumulate, max_norm, clip_coef=c_h)
+            ph.adamw_fused(cfg.smat_seed, step, cfg.lam, dict(HP, lr=lr, step=k), accumulate, c_h)
+            torch.cuda.synchronize()
+            assert 0 < c_d.item() < 1 and c_d.item() == c_h.item(), r
+            assert same_bits(out_d, out_h), r
+            for a, b in ((th_d, th_h), (m1_d, m1_h), (m2_d, m2_h)):
+                assert same_bits(a, b), r
+        del graph
+
+
+def test_device_optimizer_errors(mini):
+    cfg, inp = mini
+    _, t0, gs = list_tensors(inp)
+    (th, m1, m2), _ = adam_twin(inp, 11)
+    out, gt = fresh(inp)
+    state, adam = smat.StepState(1, 2, 0.5), smat.AdamStepState(1e-4, 1)
+    sq = torch.zeros(1, dtype=torch.float64, device=DEV)
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        plan.set_params(base_params(cfg, inp, 2))
+        with pytest.raises(smat.SmatError):
+            plan.adamw_fused_dev(state, adam, cfg.lam, HP)                      # optimizer state never bound
+        plan.bind_adam_state(m1, m2)
+        with pytest.raises(smat.SmatError):
+            plan.adamw_fused_dev(state, adam, cfg.lam, dict(HP, beta1=1.0))    # bad hyperparameter
+        with pytest.raises(smat.SmatError):
+            plan.adamw_fused_dev(state, torch.zeros(4, dtype=torch.int32, device=DEV), cfg.lam, HP)  # 16 bytes
+        with pytest.raises(smat.SmatError):
+            plan.adamw_fused_dev(state, torch.zeros(3, dtype=torch.int32, device=DEV)[1:3], cfg.lam, HP)  # misaligned
+        with pytest.raises(smat.SmatError):
+            plan.grad_norm_dev(state, cfg.lam)                                    # no output
+        with pytest.raises(smat.SmatError):
+            plan.grad_norm_dev(state, cfg.lam, max_norm=0.0, clip_coef=torch.zeros(1, device=DEV))
+        plan.grad_norm_dev(state, cfg.lam, sumsq=sq)
+        plan.simulate_dev(state)
+        plan.switch_storage(smat.SMAT_SIMULATED)
+        with pytest.raises(smat.SmatError):
+            plan.adamw_fused_dev(state, adam, cfg.lam, HP)                      # simulated storage active
+        plan.switch_storage(smat.SMAT_EXPERT)
+        plan.adamw_fused_dev(state, adam.tensor, cfg.lam, HP)                   # a plain 8-byte tensor
+        torch.cuda.synchronize()
+    assert sq.item() > 0
