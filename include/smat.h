@@ -203,7 +203,11 @@ typedef struct smat_tensor_desc {
  *               buffer `out` on a copy stream whenever the expert storage is restored, so each
  *               simulate runs in place over the buffer.  Requires theta0_dtype == out_dtype.
  * Each gradient pointer is given for every tensor or for none (smat_plan_set_grads can supply or
- * replace them later).  The caller owns *out_plan and must release it with smat_plan_destroy.
+ * replace them later).  Aliasing: within a tensor no two arrays overlap (the buffer may be exactly
+ * theta0, in place); across the list an array that an operation writes (theta, which the fused
+ * optimizer step updates, the buffer, grad_theta, bound moments) overlaps no other array, while
+ * theta0 and grad_sim of different tensors may share memory.  The caller owns *out_plan and must
+ * release it with smat_plan_destroy.
  * Errors: SMAT_ERR_INVALID (bad descriptor, duplicate tensor_id, aliasing, gradient pointers given
  * for some tensors only), SMAT_ERR_DTYPE. */
 smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t count, smat_dtype theta0_dtype,
@@ -288,7 +292,7 @@ typedef struct smat_adam_state {
 /* smat_plan_bind_adam_state -- hand the plan the optimizer state of every tensor (count entries in
  * descriptor order) for smat_adamw_fused_multi; uploads a small table on `stream`.  May be called
  * again to rebind.  The two moments of a tensor must not overlap each other, theta, theta0, the
- * simulated buffer or the gradient arrays.  Errors: SMAT_ERR_INVALID (null or overlapping arrays),
+ * simulated buffer, the gradient arrays or any array of another tensor.  Errors: SMAT_ERR_INVALID (null or overlapping arrays),
  * SMAT_ERR_STATE (no workspace), SMAT_ERR_HIP. */
 smat_status smat_plan_bind_adam_state(smat_plan* plan, const smat_adam_state* per_tensor, hipStream_t stream);
 
@@ -298,7 +302,8 @@ smat_status smat_plan_bind_adam_state(smat_plan* plan, const smat_adam_state* pe
  * fresh tensors every step instead of fixed buffers, and a plan created without gradient pointers
  * gain them.  Uploads the tensor records on `stream`; later operations on that stream use the new
  * arrays.  The arrays must not overlap theta, theta0, the simulated buffer, each other or bound
- * optimizer moments, and must stay valid until the operations that read them have run.
+ * optimizer moments, nor (grad_theta) any array of another tensor, and must stay valid until the
+ * operations that read them have run.
  * Errors: SMAT_ERR_INVALID (both NULL, a null entry, overlap), SMAT_ERR_STATE (no workspace),
  * SMAT_ERR_HIP. */
 smat_status smat_plan_set_grads(smat_plan* plan, const void* const* grad_sims, float* const* grad_thetas,
@@ -439,7 +444,9 @@ typedef struct smat_merge_desc {
 
 /* smat_merge_plan_create -- experts is a host array of count * n_experts device pointers, row i
  * holding tensor i's experts in expert order.  Checks as smat_merge for every tensor; a tensor id may
- * repeat only for disjoint element ranges.  Errors: SMAT_ERR_INVALID, SMAT_ERR_DTYPE. */
+ * repeat only for disjoint element ranges.  Across the list no output may overlap another tensor's
+ * output, theta0 or experts (inputs, which are only read, may share memory).
+ * Errors: SMAT_ERR_INVALID, SMAT_ERR_DTYPE. */
 smat_status smat_merge_plan_create(const smat_merge_desc* descs, int32_t count, const void* const* experts,
                                    int32_t n_experts, smat_dtype expert_dtype, smat_dtype theta0_dtype,
                                    smat_dtype out_dtype, smat_merge_plan** out_plan);

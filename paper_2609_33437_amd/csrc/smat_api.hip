@@ -346,6 +346,64 @@ struct smat_plan {
 
 namespace {
 
+// One array of a plan: bytes [lo, hi), whether an operation of the plan writes it, and whose it is.
+struct Span {
+  uintptr_t lo, hi;
+  bool written;
+  int32_t tensor;
+  const char* what;
+};
+
+void add_span(std::vector<Span>& s, const void* ptr, size_t bytes, bool written, int32_t i, const char* what) {
+  if (ptr) s.push_back({reinterpret_cast<uintptr_t>(ptr), reinterpret_cast<uintptr_t>(ptr) + bytes, written, i, what});
+}
+
+// No array that an operation writes may overlap any other array of the list, in the same tensor or
+// another; read-only arrays may share memory.  Sorted by start, an array overlaps an earlier one
+// exactly when it starts before the furthest end seen so far (among written arrays, for a read-only
+// one), so one sweep finds any conflict.
+smat_status check_spans(std::vector<Span>& s, const char* where) {
+  std::sort(s.begin(), s.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
+  uintptr_t end_any = 0, end_written = 0;
+  size_t i_any = 0, i_written = 0;
+  for (size_t k = 0; k < s.size(); ++k) {
+    const Span& x = s[k];
+    const bool hit = x.written ? end_any > x.lo : end_written > x.lo;
+    if (hit) {
+      const Span& y = s[x.written ? i_any : i_written];
+      return fail(SMAT_ERR_INVALID, "%s: %s of tensor %d overlaps %s of tensor %d", where, x.what, x.tensor, y.what,
+                  y.tensor);
+    }
+    if (x.hi > end_any) end_any = x.hi, i_any = k;
+    if (x.written && x.hi > end_written) end_written = x.hi, i_written = k;
+  }
+  return SMAT_OK;
+}
+
+// A plan's arrays: written are theta (the fused optimizer step updates it), the buffer, grad_theta
+// and the moments; read-only are theta0 and grad_sim.  The buffer of an in-place tensor holds its
+// theta0, which is not counted twice.
+smat_status check_plan_spans(const smat_plan* p, const std::vector<TensorRec>& recs, const std::vector<AdamRec>* adam,
+                             const char* where) {
+  std::vector<Span> s;
+  s.reserve(7 * recs.size());
+  for (int32_t i = 0; i < (int32_t)recs.size(); ++i) {
+    const TensorRec& r = recs[i];
+    if (r.n <= 0) continue;
+    const size_t n = (size_t)r.n;
+    add_span(s, r.theta, n * 4, true, i, "theta");
+    add_span(s, r.out, n * dtype_bytes(p->out_dt), true, i, "the buffer");
+    if (r.theta0 != r.out) add_span(s, r.theta0, n * dtype_bytes(p->t0_dt), false, i, "theta0");
+    add_span(s, r.grad_sim, n * dtype_bytes(p->g_dt), false, i, "grad_sim");
+    add_span(s, r.grad_theta, n * 4, true, i, "grad_theta");
+    if (adam) {
+      add_span(s, (*adam)[i].exp_avg, n * 4, true, i, "exp_avg");
+      add_span(s, (*adam)[i].exp_avg_sq, n * 4, true, i, "exp_avg_sq");
+    }
+  }
+  return check_spans(s, where);
+}
+
 smat_status release(smat_plan* p) {
   // wait for the plan's own work that still reads its pinned staging or owns its events
   for (hipEvent_t e : {p->ev_static, p->ev_params[0], p->ev_params[1], p->ev_prefetch, p->ev_adam})
@@ -464,6 +522,10 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
     p->expert_ptrs[i] = const_cast<float*>(d.theta);
     p->sim_ptrs[i] = d.out;
     nchunks += (uint64_t)((d.n + smat::kChunk - 1) / smat::kChunk);
+  }
+  if (smat_status st = check_plan_spans(p, p->recs, nullptr, "smat_plan_create"); st != SMAT_OK) {
+    delete p;
+    return st;
   }
   if (nchunks * smat::tiles_per_chunk(1) > 0x7FFFFFFFull) {  // one block per tile must fit in one grid
     delete p;
@@ -686,6 +748,7 @@ extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_s
                      adam_flags(r.theta, adam[i].exp_avg, adam[i].exp_avg_sq, r.grad_sim, p->g_dt, r.grad_theta,
                                 r.elem_offset);
   }
+  if (smat_status st = check_plan_spans(p, recs, &adam, "smat_plan_bind_adam_state"); st != SMAT_OK) return st;
   const size_t rec_bytes = sizeof(TensorRec) * p->count, adam_bytes = sizeof(AdamRec) * p->count;
   if (!p->adam_staging) {
     SMAT_HIP(hipHostMalloc((void**)&p->adam_staging, std::max<size_t>(rec_bytes + adam_bytes, 256), hipHostMallocDefault));
@@ -731,6 +794,9 @@ extern "C" smat_status smat_plan_set_grads(smat_plan* p, const void* const* grad
     if (p->adam_bound)
       r.sflags |= adam_flags(r.theta, p->adam[i].exp_avg, p->adam[i].exp_avg_sq, gs, p->g_dt, gt, r.elem_offset);
   }
+  if (smat_status st = check_plan_spans(p, recs, p->adam_bound ? &p->adam : nullptr, "smat_plan_set_grads");
+      st != SMAT_OK)
+    return st;
   const size_t rec_bytes = sizeof(TensorRec) * p->count, adam_bytes = sizeof(AdamRec) * p->count;
   if (!p->adam_staging) {
     SMAT_HIP(hipHostMalloc((void**)&p->adam_staging, std::max<size_t>(rec_bytes + adam_bytes, 256), hipHostMallocDefault));
@@ -1091,6 +1157,19 @@ extern "C" smat_status smat_merge_plan_create(const smat_merge_desc* descs, int3
                   ranges[i].first);
   if (nchunks * smat::tiles_per_chunk(1) > 0x7FFFFFFFull)
     return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: tensor list too large for one launch");
+  // across the list, no output may overlap another output, a theta0 or an expert (except the in-place
+  // theta0 of its own tensor); theta0 and the experts are only read
+  std::vector<Span> spans;
+  for (int32_t i = 0; i < count; ++i) {
+    const smat_merge_desc& d = descs[i];
+    if (d.n == 0) continue;
+    const size_t n = (size_t)d.n;
+    add_span(spans, d.out, n * dtype_bytes(out_dtype), true, i, "out");
+    if (d.theta0 != d.out) add_span(spans, d.theta0, n * dtype_bytes(theta0_dtype), false, i, "theta0");
+    for (int j = 0; j < n_experts; ++j)
+      add_span(spans, experts[(size_t)i * n_experts + j], n * dtype_bytes(expert_dtype), false, i, "an expert");
+  }
+  if (smat_status st = check_spans(spans, "smat_merge_plan_create"); st != SMAT_OK) return st;
 
   smat_merge_plan* p = new smat_merge_plan();
   p->count = count;
