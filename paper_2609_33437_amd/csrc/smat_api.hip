@@ -527,9 +527,9 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
     delete p;
     return st;
   }
-  if (nchunks * smat::tiles_per_chunk(1) > 0x7FFFFFFFull) {  // one block per tile must fit in one grid
+  if (nchunks * smat::tiles_per_chunk(1) > 0x7FFFFFFFull) {  // block and chunk counts stay within 31 bits
     delete p;
-    return fail(SMAT_ERR_INVALID, "smat_plan_create: tensor list too large for one launch");
+    return fail(SMAT_ERR_INVALID, "smat_plan_create: tensor list too large");
   }
   p->chunks.reserve(nchunks);
   for (int32_t i = 0; i < count; ++i) {
@@ -1156,7 +1156,7 @@ extern "C" smat_status smat_merge_plan_create(const smat_merge_desc* descs, int3
       return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: tensor_id %u given twice for overlapping elements",
                   ranges[i].first);
   if (nchunks * smat::tiles_per_chunk(1) > 0x7FFFFFFFull)
-    return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: tensor list too large for one launch");
+    return fail(SMAT_ERR_INVALID, "smat_merge_plan_create: tensor list too large");
   // across the list, no output may overlap another output, a theta0 or an expert (except the in-place
   // theta0 of its own tensor); theta0 and the experts are only read
   std::vector<Span> spans;

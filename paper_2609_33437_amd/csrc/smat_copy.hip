@@ -23,11 +23,14 @@ __global__ __launch_bounds__(kBlock) void k_stream_copy(const f32x4* __restrict_
   }
 }
 
+// Copies past max_grid_blocks blocks run as several launches over consecutive ranges.
 hipError_t launch_stream_copy(const void* src, void* dst, uint64_t n16, hipStream_t stream) {
   const uint64_t per_block = (uint64_t)kBlock * kCopyVecs;
-  const dim3 grid((uint32_t)((n16 + per_block - 1) / per_block)), block(kBlock);
-  k_stream_copy<<<grid, block, 0, stream>>>(static_cast<const f32x4*>(src), static_cast<f32x4*>(dst), n16);
-  return hipGetLastError();
+  return for_pieces(n16, (uint64_t)max_grid_blocks(kBlock) * per_block, [&](uint64_t first, uint64_t count) {
+    const dim3 grid((uint32_t)((count + per_block - 1) / per_block)), block(kBlock);
+    k_stream_copy<<<grid, block, 0, stream>>>(static_cast<const f32x4*>(src) + first, static_cast<f32x4*>(dst) + first,
+                                              count);
+  });
 }
 
 }  // namespace smat

@@ -320,98 +320,121 @@ __global__ __launch_bounds__(kDebugBlock) void k_debug_draws(uint64_t seed, uint
 }
 
 // ---------------------------------------------------------------- launchers
+// Every launcher splits a job whose grid would pass max_grid_blocks into several launches: a
+// one-tensor job into element ranges, a list job into ranges of its chunk table.
 static inline uint32_t blocks_for(int64_t n, int64_t per_block) { return (uint32_t)((n + per_block - 1) / per_block); }
 
 hipError_t launch_simulate_one(const TensorRec& rec, const ParamRec& prm, int theta0_dtype, int out_dtype,
                                uint64_t seed, uint32_t step, hipStream_t stream) {
-  const dim3 grid(blocks_for(rec.n, tile_elems(kSimQuads))), block(kBlock);
-  if (theta0_dtype == 1 && out_dtype == 1)
-    k_simulate_one<Bf16, Bf16><<<grid, block, 0, stream>>>(rec, prm, seed, step);
-  else if (theta0_dtype == 1 && out_dtype == 0)
-    k_simulate_one<Bf16, float><<<grid, block, 0, stream>>>(rec, prm, seed, step);
-  else if (theta0_dtype == 0 && out_dtype == 1)
-    k_simulate_one<float, Bf16><<<grid, block, 0, stream>>>(rec, prm, seed, step);
-  else
-    k_simulate_one<float, float><<<grid, block, 0, stream>>>(rec, prm, seed, step);
-  return hipGetLastError();
+  constexpr int64_t tile = tile_elems(kSimQuads);
+  return for_pieces((uint64_t)rec.n, (uint64_t)max_grid_blocks(kBlock) * tile, [&](uint64_t off, uint64_t len) {
+    const TensorRec r = rec_piece(rec, off, len, theta0_dtype, out_dtype, 0);
+    const dim3 grid(blocks_for((int64_t)len, tile)), block(kBlock);
+    if (theta0_dtype == 1 && out_dtype == 1)
+      k_simulate_one<Bf16, Bf16><<<grid, block, 0, stream>>>(r, prm, seed, step);
+    else if (theta0_dtype == 1 && out_dtype == 0)
+      k_simulate_one<Bf16, float><<<grid, block, 0, stream>>>(r, prm, seed, step);
+    else if (theta0_dtype == 0 && out_dtype == 1)
+      k_simulate_one<float, Bf16><<<grid, block, 0, stream>>>(r, prm, seed, step);
+    else
+      k_simulate_one<float, float><<<grid, block, 0, stream>>>(r, prm, seed, step);
+  });
 }
 
 hipError_t launch_backward_one(const TensorRec& rec, const ParamRec& prm, int grad_dtype, float lambda,
                                uint64_t seed, uint32_t step, hipStream_t stream) {
-  const dim3 grid(blocks_for(rec.n, tile_elems(kBwdQuads))), block(kBlock);
-  if (grad_dtype == 1)
-    k_backward_one<Bf16><<<grid, block, 0, stream>>>(rec, prm, seed, step, lambda);
-  else
-    k_backward_one<float><<<grid, block, 0, stream>>>(rec, prm, seed, step, lambda);
-  return hipGetLastError();
+  constexpr int64_t tile = tile_elems(kBwdQuads);
+  return for_pieces((uint64_t)rec.n, (uint64_t)max_grid_blocks(kBlock) * tile, [&](uint64_t off, uint64_t len) {
+    const TensorRec r = rec_piece(rec, off, len, 0, 0, grad_dtype);
+    const dim3 grid(blocks_for((int64_t)len, tile)), block(kBlock);
+    if (grad_dtype == 1)
+      k_backward_one<Bf16><<<grid, block, 0, stream>>>(r, prm, seed, step, lambda);
+    else
+      k_backward_one<float><<<grid, block, 0, stream>>>(r, prm, seed, step, lambda);
+  });
 }
 
 hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                  int theta0_dtype, int out_dtype, uint64_t seed, uint32_t step, hipStream_t stream) {
-  const dim3 grid(nchunks * tiles_per_chunk(kSimQuads)), block(kBlock);
-  if (theta0_dtype == 1 && out_dtype == 1)
-    k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
-  else if (theta0_dtype == 1 && out_dtype == 0)
-    k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
-  else if (theta0_dtype == 0 && out_dtype == 1)
-    k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
-  else
-    k_simulate_multi<float, float><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step);
-  return hipGetLastError();
+  constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
+  return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const uint2* ch = chunks + first;
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
+    if (theta0_dtype == 1 && out_dtype == 1)
+      k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step);
+    else if (theta0_dtype == 1 && out_dtype == 0)
+      k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step);
+    else if (theta0_dtype == 0 && out_dtype == 1)
+      k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step);
+    else
+      k_simulate_multi<float, float><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step);
+  });
 }
 
 hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                  int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
                                  hipStream_t stream) {
-  const dim3 grid(nchunks * tiles_per_chunk(kBwdQuads)), block(kBlock);
-  if (grad_dtype == 1 && accumulate)
-    k_backward_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
-  else if (grad_dtype == 1)
-    k_backward_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
-  else if (accumulate)
-    k_backward_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
-  else
-    k_backward_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, chunks, seed, step, lambda);
-  return hipGetLastError();
+  constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
+  return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const uint2* ch = chunks + first;
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
+    if (grad_dtype == 1 && accumulate)
+      k_backward_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step, lambda);
+    else if (grad_dtype == 1)
+      k_backward_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step, lambda);
+    else if (accumulate)
+      k_backward_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step, lambda);
+    else
+      k_backward_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step, lambda);
+  });
 }
 
 hipError_t launch_simulate_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
                                      const uint2* chunks, uint32_t nchunks, int theta0_dtype, int out_dtype,
                                      const StepState* state, hipStream_t stream) {
-  const dim3 grid(nchunks * tiles_per_chunk(kSimQuads)), block(kBlock);
-  if (theta0_dtype == 1 && out_dtype == 1)
-    k_simulate_multi_dev<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state);
-  else if (theta0_dtype == 1 && out_dtype == 0)
-    k_simulate_multi_dev<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state);
-  else if (theta0_dtype == 0 && out_dtype == 1)
-    k_simulate_multi_dev<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state);
-  else
-    k_simulate_multi_dev<float, float><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state);
-  return hipGetLastError();
+  constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
+  return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const uint2* ch = chunks + first;
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
+    if (theta0_dtype == 1 && out_dtype == 1)
+      k_simulate_multi_dev<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state);
+    else if (theta0_dtype == 1 && out_dtype == 0)
+      k_simulate_multi_dev<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state);
+    else if (theta0_dtype == 0 && out_dtype == 1)
+      k_simulate_multi_dev<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state);
+    else
+      k_simulate_multi_dev<float, float><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state);
+  });
 }
 
 hipError_t launch_backward_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
                                      const uint2* chunks, uint32_t nchunks, int grad_dtype, bool accumulate,
                                      float lambda, const StepState* state, hipStream_t stream) {
-  const dim3 grid(nchunks * tiles_per_chunk(kBwdQuads)), block(kBlock);
-  if (grad_dtype == 1 && accumulate)
-    k_backward_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state, lambda);
-  else if (grad_dtype == 1)
-    k_backward_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state, lambda);
-  else if (accumulate)
-    k_backward_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state, lambda);
-  else
-    k_backward_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, state, lambda);
-  return hipGetLastError();
+  constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
+  return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const uint2* ch = chunks + first;
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
+    if (grad_dtype == 1 && accumulate)
+      k_backward_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state, lambda);
+    else if (grad_dtype == 1)
+      k_backward_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state, lambda);
+    else if (accumulate)
+      k_backward_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state, lambda);
+    else
+      k_backward_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state, lambda);
+  });
 }
 
 hipError_t launch_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t elem_offset,
                               int64_t n, const ParamRec& prm, uint32_t* mask_words, uint32_t* noise_words,
                               uint8_t* kept, float* z, hipStream_t stream) {
-  const dim3 grid(blocks_for(n, kDebugBlock)), block(kDebugBlock);
-  k_debug_draws<<<grid, block, 0, stream>>>(seed, step, tensor_id, elem_offset, n, prm, mask_words, noise_words,
-                                            kept, z);
-  return hipGetLastError();
+  const uint64_t per = (uint64_t)max_grid_blocks(kDebugBlock) * kDebugBlock;
+  return for_pieces((uint64_t)n, per, [&](uint64_t off, uint64_t len) {
+    const dim3 grid(blocks_for((int64_t)len, kDebugBlock)), block(kDebugBlock);
+    k_debug_draws<<<grid, block, 0, stream>>>(seed, step, tensor_id, elem_offset + off, (int64_t)len, prm,
+                                              step_ptr(mask_words, off, 4), step_ptr(noise_words, off, 4),
+                                              step_ptr(kept, off, 1), step_ptr(z, off, 4));
+  });
 }
 
 }  // namespace smat

@@ -8,6 +8,49 @@
 
 namespace smat {
 
+// ---------------------------------------------------------------- launch size
+// A dispatch packet holds the grid's total work-items (blocks x threads per block) in 32 bits, and a
+// grid past that wraps without an error.  The launchers split larger jobs into several launches of
+// at most this many blocks each (for one-wave blocks 2^26 - 1, i.e. 17.2e9 elements at one quad per
+// thread).
+constexpr uint32_t max_grid_blocks(int threads) { return 0xFFFFFFFFu / (uint32_t)threads; }
+
+// fn(first, count) over consecutive pieces [first, first + count) of `total` units, count <= per,
+// stopping at the first launch error.
+template <typename F>
+hipError_t for_pieces(uint64_t total, uint64_t per, F&& fn) {
+  for (uint64_t first = 0; first < total; first += per) {
+    fn(first, total - first < per ? total - first : per);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipGetLastError();
+}
+
+// Storage bytes of a dtype code (0 = fp32, 1 = bf16).
+inline size_t storage_bytes(int dtype) { return dtype == 1 ? 2 : 4; }
+
+// p advanced by `elems` elements of `bytes` each (a null pointer stays null).
+template <typename P>
+inline P* step_ptr(P* p, uint64_t elems, size_t bytes) {
+  return p ? reinterpret_cast<P*>(reinterpret_cast<uintptr_t>(p) + elems * bytes) : p;
+}
+
+// Elements [off, off + len) of a one-tensor record as a record of its own.  off is a multiple of the
+// tile, hence of 4 elements, so every pointer keeps its alignment and the quad flags still hold.
+inline TensorRec rec_piece(const TensorRec& R, uint64_t off, uint64_t len, int t0_dtype, int out_dtype,
+                           int g_dtype) {
+  TensorRec r = R;
+  r.theta = step_ptr(R.theta, off, 4);
+  r.theta0 = step_ptr(R.theta0, off, storage_bytes(t0_dtype));
+  r.out = step_ptr(R.out, off, storage_bytes(out_dtype));
+  r.grad_sim = step_ptr(R.grad_sim, off, storage_bytes(g_dtype));
+  r.grad_theta = step_ptr(R.grad_theta, off, 4);
+  r.n = (int64_t)len;
+  r.elem_offset = R.elem_offset + off;
+  return r;
+}
+
 // Storage codes match smat_dtype: 0 = fp32, 1 = bf16.
 hipError_t launch_simulate_one(const TensorRec& rec, const ParamRec& prm, int theta0_dtype, int out_dtype,
                                uint64_t seed, uint32_t step, hipStream_t stream);

@@ -137,19 +137,30 @@ __global__ __launch_bounds__(kBlock) void k_merge_multi(const TensorRec* __restr
 }
 
 // ---------------------------------------------------------------- launchers
+// Jobs whose grid would pass max_grid_blocks run as several launches (element ranges of one tensor,
+// ranges of a list's chunk table).
 template <typename TE, typename T0, typename TO>
 static hipError_t merge_one(const TensorRec& rec, const MergeArgs& args, int nexp, hipStream_t stream) {
-  const dim3 grid((uint32_t)((rec.n + tile_elems(kMergeQuads) - 1) / tile_elems(kMergeQuads))), block(kBlock);
-  k_merge_one<TE, T0, TO><<<grid, block, 0, stream>>>(rec, args, nexp);
-  return hipGetLastError();
+  constexpr int64_t tile = tile_elems(kMergeQuads);
+  constexpr int e_dt = std::is_same<TE, Bf16>::value ? 1 : 0, t0_dt = std::is_same<T0, Bf16>::value ? 1 : 0,
+                o_dt = std::is_same<TO, Bf16>::value ? 1 : 0;
+  return for_pieces((uint64_t)rec.n, (uint64_t)max_grid_blocks(kBlock) * tile, [&](uint64_t off, uint64_t len) {
+    const TensorRec r = rec_piece(rec, off, len, t0_dt, o_dt, 0);
+    MergeArgs a = args;
+    for (int j = 0; j < nexp; ++j) a.x[j] = step_ptr(args.x[j], off, storage_bytes(e_dt));
+    const dim3 grid((uint32_t)((len + tile - 1) / tile)), block(kBlock);
+    k_merge_one<TE, T0, TO><<<grid, block, 0, stream>>>(r, a, nexp);
+  });
 }
 
 template <typename TE, typename T0, typename TO>
 static hipError_t merge_multi(const TensorRec* recs, const void* const* experts, const MergeRec* terms,
                               const uint2* chunks, uint32_t nchunks, int nexp, hipStream_t stream) {
-  const dim3 grid(nchunks * tiles_per_chunk(kMergeQuads)), block(kBlock);
-  k_merge_multi<TE, T0, TO><<<grid, block, 0, stream>>>(recs, experts, terms, chunks, nexp);
-  return hipGetLastError();
+  constexpr uint32_t tpc = tiles_per_chunk(kMergeQuads);
+  return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
+    k_merge_multi<TE, T0, TO><<<grid, block, 0, stream>>>(recs, experts, terms, chunks + first, nexp);
+  });
 }
 
 // Storage codes: 0 = fp32, 1 = bf16, for (expert, theta0, out).

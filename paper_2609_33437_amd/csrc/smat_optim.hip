@@ -356,36 +356,45 @@ __global__ __launch_bounds__(kSumBlock) void k_sqnorm_finalize(const double* __r
 }
 
 // ---------------------------------------------------------------- launchers
+// Jobs whose grid would pass max_grid_blocks run as several launches (element ranges of one tensor,
+// ranges of a list's chunk table).
 static inline uint32_t blocks_for(int64_t n, int64_t per_block) { return (uint32_t)((n + per_block - 1) / per_block); }
 
 hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const ParamRec& prm, const AdamConsts& A,
                             int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
                             const float* dev_scale, hipStream_t stream) {
-  const dim3 grid(blocks_for(rec.n, tile_elems(kAdamQuads))), block(kBlock);
-  if (grad_dtype == 1 && accumulate)
-    k_adamw_one<Bf16, true><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda, dev_scale);
-  else if (grad_dtype == 1)
-    k_adamw_one<Bf16, false><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda, dev_scale);
-  else if (accumulate)
-    k_adamw_one<float, true><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda, dev_scale);
-  else
-    k_adamw_one<float, false><<<grid, block, 0, stream>>>(rec, st, prm, A, seed, step, lambda, dev_scale);
-  return hipGetLastError();
+  constexpr int64_t tile = tile_elems(kAdamQuads);
+  return for_pieces((uint64_t)rec.n, (uint64_t)max_grid_blocks(kBlock) * tile, [&](uint64_t off, uint64_t len) {
+    const TensorRec r = rec_piece(rec, off, len, 0, 0, grad_dtype);
+    const AdamRec m{step_ptr(st.exp_avg, off, 4), step_ptr(st.exp_avg_sq, off, 4)};
+    const dim3 grid(blocks_for((int64_t)len, tile)), block(kBlock);
+    if (grad_dtype == 1 && accumulate)
+      k_adamw_one<Bf16, true><<<grid, block, 0, stream>>>(r, m, prm, A, seed, step, lambda, dev_scale);
+    else if (grad_dtype == 1)
+      k_adamw_one<Bf16, false><<<grid, block, 0, stream>>>(r, m, prm, A, seed, step, lambda, dev_scale);
+    else if (accumulate)
+      k_adamw_one<float, true><<<grid, block, 0, stream>>>(r, m, prm, A, seed, step, lambda, dev_scale);
+    else
+      k_adamw_one<float, false><<<grid, block, 0, stream>>>(r, m, prm, A, seed, step, lambda, dev_scale);
+  });
 }
 
 hipError_t launch_adamw_multi(const TensorRec* recs, const AdamRec* states, const ParamRec* prms, const uint2* chunks,
                               uint32_t nchunks, const AdamConsts& A, int grad_dtype, bool accumulate, float lambda,
                               uint64_t seed, uint32_t step, const float* dev_scale, hipStream_t stream) {
-  const dim3 grid(nchunks * tiles_per_chunk(kAdamQuads)), block(kBlock);
-  if (grad_dtype == 1 && accumulate)
-    k_adamw_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda, dev_scale);
-  else if (grad_dtype == 1)
-    k_adamw_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda, dev_scale);
-  else if (accumulate)
-    k_adamw_multi<float, true><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda, dev_scale);
-  else
-    k_adamw_multi<float, false><<<grid, block, 0, stream>>>(recs, states, prms, chunks, A, seed, step, lambda, dev_scale);
-  return hipGetLastError();
+  constexpr uint32_t tpc = tiles_per_chunk(kAdamQuads);
+  return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const uint2* ch = chunks + first;
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
+    if (grad_dtype == 1 && accumulate)
+      k_adamw_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, seed, step, lambda, dev_scale);
+    else if (grad_dtype == 1)
+      k_adamw_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, seed, step, lambda, dev_scale);
+    else if (accumulate)
+      k_adamw_multi<float, true><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, seed, step, lambda, dev_scale);
+    else
+      k_adamw_multi<float, false><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, seed, step, lambda, dev_scale);
+  });
 }
 
 // The partials' fp64 sums (m <= kNormSums blocks, each adding `per` consecutive partials), then the
@@ -399,42 +408,49 @@ static hipError_t launch_sqnorm_reduce(const float* partials, uint32_t npart, do
   return hipGetLastError();
 }
 
+// One partial per block: a piece starting at chunk `first` writes partials from first * kNormPartialsPerChunk.
 hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
                                uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
                                hipStream_t stream) {
-  const uint32_t npart = nchunks * kNormPartialsPerChunk;
-  if (npart > 0) {
-    const dim3 grid(npart), block(kBlock);
+  constexpr uint32_t tpc = kNormPartialsPerChunk;
+  const hipError_t e = for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const uint2* ch = chunks + first;
+    float* part = partials + first * tpc;
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
     if (grad_dtype == 1 && accumulate)
-      k_sqnorm_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
+      k_sqnorm_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
     else if (grad_dtype == 1)
-      k_sqnorm_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
+      k_sqnorm_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
     else if (accumulate)
-      k_sqnorm_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
+      k_sqnorm_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
     else
-      k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, chunks, partials, seed, step, lambda);
-  }
-  return launch_sqnorm_reduce(partials, npart, sums, sumsq, clip_coef, max_norm, stream);
+      k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
+  });
+  if (e != hipSuccess) return e;
+  return launch_sqnorm_reduce(partials, nchunks * tpc, sums, sumsq, clip_coef, max_norm, stream);
 }
 
 hipError_t launch_sqnorm_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
                                    const uint2* chunks, uint32_t nchunks, float* partials, double* sums,
                                    int grad_dtype, bool accumulate, float lambda, const StepState* state,
                                    double* sumsq, float* clip_coef, float max_norm, hipStream_t stream) {
-  const uint32_t npart = nchunks * kNormPartialsPerChunk;
-  if (npart > 0) {
-    const dim3 grid(npart), block(kBlock);
+  constexpr uint32_t tpc = kNormPartialsPerChunk;
+  const hipError_t e = for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const uint2* ch = chunks + first;
+    float* part = partials + first * tpc;
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
     if (grad_dtype == 1 && accumulate)
-      k_sqnorm_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, partials, state, lambda);
+      k_sqnorm_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, scales, ch, part, state, lambda);
     else if (grad_dtype == 1)
-      k_sqnorm_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, partials, state, lambda);
+      k_sqnorm_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, scales, ch, part, state, lambda);
     else if (accumulate)
-      k_sqnorm_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, partials, state, lambda);
+      k_sqnorm_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, prms, scales, ch, part, state, lambda);
     else
-      k_sqnorm_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, prms, scales, chunks, partials, state, lambda);
-  }
-  return launch_sqnorm_reduce(partials, npart, sums, sumsq, clip_coef, max_norm, stream);
+      k_sqnorm_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, prms, scales, ch, part, state, lambda);
+  });
+  if (e != hipSuccess) return e;
+  return launch_sqnorm_reduce(partials, nchunks * tpc, sums, sumsq, clip_coef, max_norm, stream);
 }
 
 hipError_t launch_adamw_multi_dev(const TensorRec* recs, const AdamRec* states, const ParamRec* prms,
@@ -443,22 +459,25 @@ hipError_t launch_adamw_multi_dev(const TensorRec* recs, const AdamRec* states, 
                                   bool accumulate, float lambda, const StepState* state, const float* dev_scale,
                                   hipStream_t stream) {
   k_adam_consts<<<dim3(1), dim3(64), 0, stream>>>(adam_state, h, consts);
-  if (nchunks > 0) {
-    const dim3 grid(nchunks * tiles_per_chunk(kAdamQuads)), block(kBlock);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  constexpr uint32_t tpc = tiles_per_chunk(kAdamQuads);
+  return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
+    const uint2* ch = chunks + first;
+    const dim3 grid((uint32_t)count * tpc), block(kBlock);
     if (grad_dtype == 1 && accumulate)
-      k_adamw_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, scales, chunks, consts, state,
-                                                                lambda, dev_scale);
+      k_adamw_multi_dev<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, scales, ch, consts, state, lambda,
+                                                                dev_scale);
     else if (grad_dtype == 1)
-      k_adamw_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, scales, chunks, consts, state,
+      k_adamw_multi_dev<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, scales, ch, consts, state,
                                                                  lambda, dev_scale);
     else if (accumulate)
-      k_adamw_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, states, prms, scales, chunks, consts, state,
+      k_adamw_multi_dev<float, true><<<grid, block, 0, stream>>>(recs, states, prms, scales, ch, consts, state,
                                                                  lambda, dev_scale);
     else
-      k_adamw_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, states, prms, scales, chunks, consts, state,
+      k_adamw_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, states, prms, scales, ch, consts, state,
                                                                   lambda, dev_scale);
-  }
-  return hipGetLastError();
+  });
 }
 
 }  // namespace smat
