@@ -84,6 +84,10 @@ def parse_args():
     ap.add_argument("--merge", action="store_true",
                     help="time the N-expert merge (Task Arithmetic and DARE + Task Arithmetic) of seven bf16 "
                          "experts shaped like the chosen list, print that as the JSON line and exit")
+    ap.add_argument("--graph", action="store_true",
+                    help="time one simulated step (simulate + backward-accumulate, a new sampled scale per step) "
+                         "issued from the host against the same step replayed from one captured HIP graph of "
+                         "the device-driven calls, on the chosen list; print that as the JSON line and exit")
     ap.add_argument("--experts", type=int, default=7)
     ap.add_argument("--train-batch", type=int, default=8)
     ap.add_argument("--train-seq", type=int, default=512)
@@ -650,6 +654,90 @@ def bench_merge(args, torch, smat, workloads) -> int:
     return 0
 
 
+def bench_graph(args, torch, smat, workloads) -> int:
+    """Per-step cost of a simulated step on the chosen list when each step samples one scale
+    alpha ~ U[alpha_min, 1] shared by every tensor (Sec. 4.1, "Scale"): issued from the host (new
+    per-tensor records uploaded, then smat_simulate_multi and smat_backward_multi) against one
+    captured HIP graph of the device-driven calls, whose replays advance the step and sample the
+    scale on the device.  Both time K back-to-back steps after W warmup steps."""
+    import numpy as np
+    cfg = workloads.config(args.config)
+    inp = workloads.make_inputs(cfg, device="cuda")
+    dt = {"bf16": torch.bfloat16, "f32": torch.float32}
+    outs = [torch.empty(t.numel(), dtype=dt[cfg.out_dtype], device="cuda") for t in inp.theta]
+    K, W = args.steps, args.warmup
+    amin = cfg.s_range[0]
+    base = workloads.step_params(cfg, inp.settings, 0)
+    arr = smat.op_params_array(cfg.count, 1.0, [p["keep"] for p in base], [p["sigma"] for p in base],
+                               [p["rescale"] for p in base], [p["noise_kind"] for p in base])
+    rng = np.random.default_rng(cfg.index)
+    seed, lam = cfg.smat_seed, cfg.lam
+
+    def timed(fn, n):
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t = time.perf_counter()
+        a.record()
+        for k in range(n):
+            fn(k)
+        b.record()
+        host_us = (time.perf_counter() - t) / n * 1e6
+        torch.cuda.synchronize()
+        return {"gpu_us": round(a.elapsed_time(b) / n * 1e3, 2), "host_issue_us": round(host_us, 2)}
+
+    res = {}
+    with smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta) as plan:
+        def host_step(k):
+            arr["s"] = np.float32(rng.uniform(amin, 1.0))
+            plan.set_params(arr)
+            plan.simulate(seed, k)
+            plan.backward(seed, k, lam, True)
+
+        for k in range(W):
+            host_step(k)
+        res["host_driven"] = timed(host_step, K)
+
+        arr["s"] = 1.0
+        plan.set_params(arr)
+        state = smat.StepState(seed, 0, 1.0)
+        torch.cuda.manual_seed(cfg.index)   # the default generator: graph replays advance its offset
+
+        def dev_step():
+            state.step_view.add_(1)
+            state.scale_view.copy_(torch.rand(1, device="cuda") * (1.0 - amin) + amin)
+            plan.simulate_dev(state)
+            plan.backward_dev(state, lam, True)
+
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            dev_step()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            dev_step()
+        for _ in range(W):
+            graph.replay()
+        res["graph_replay"] = timed(lambda k: graph.replay(), K)
+        torch.cuda.synchronize()
+        del graph
+    for mode, r in res.items():
+        log(f"{mode}: GPU {r['gpu_us']:.1f} us/step, host issue {r['host_issue_us']:.1f} us/step")
+    g = res["graph_replay"]["gpu_us"]
+    result = {
+        "metric": f"simulated-step time issued from the host vs replayed from a captured HIP graph, {cfg.name}",
+        "value": cfg.numel / (g * 1e-6),
+        "unit": "params/s",
+        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": round(g / 1e3, 5), "higher_is_better": True,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.description}; one sampled scale per step shared by all tensors",
+                   "params": cfg.numel, "tensors": cfg.count},
+        "modes": res,
+    }
+    print(json.dumps(result))
+    return 0
+
+
 def bench_train(args, torch, smat) -> int:
     """SMAT in a training loop against plain fine-tuning (FT), the measurement behind the method's
     training-time table (App. "Implementation and Measurement Details"): same model, data and AdamW
@@ -786,6 +874,8 @@ def main() -> int:
         return bench_train(args, torch, smat)
     if args.merge:
         return bench_merge(args, torch, smat, workloads)
+    if args.graph:
+        return bench_graph(args, torch, smat, workloads)
     cfg = workloads.config(args.config)
     dt = {"bf16": torch.bfloat16, "f32": torch.float32}
     nbytes = {"bf16": 2, "f32": 4}
