@@ -25,7 +25,11 @@
  *     caller (for example PyTorch tensors); the library never frees them.
  *     Element counts are int64_t; 0 elements is a valid no-op.
  *   - Work is enqueued on the caller's HIP stream (NULL = the default
- *     stream) without synchronising the host.
+ *     stream) without synchronising the host.  Calls that upload host tables
+ *     (smat_plan_bind_workspace, smat_plan_set_params, smat_plan_set_grads,
+ *     smat_plan_bind_adam_state, smat_merge_plan_bind_workspace, smat_merge_multi)
+ *     return SMAT_ERR_STATE while `stream` is being captured into a graph; the
+ *     *_dev calls are the ones meant for capture.
  *   - Random draws are never stored.  They are regenerated from Philox4x32-10
  *     (Salmon et al., SC'11) with key = seed and counter
  *     (g_lo, g_hi, tensor_id, 4*step + stream), where g = e >> 2 for the
@@ -381,8 +385,10 @@ smat_status smat_grad_norm_multi_dev(smat_plan* plan, const smat_step_state* sta
  * smat_plan_active_ptrs) and moves no data.  SMAT_SIMULATED requires a simulate since the last
  * restore and is an error when already active; SMAT_EXPERT is idempotent.  In offload mode,
  * restoring the expert storage also starts the theta0 prefetch into the buffers on the plan's copy
- * stream once `stream` has reached this point; the next simulate waits for it.  Expert storage is
- * never written.  Errors: SMAT_ERR_INVALID (bad `to`), SMAT_ERR_STATE, SMAT_ERR_HIP. */
+ * stream once `stream` has reached this point; the next simulate waits for it.  A restore whose
+ * prefetch fails with SMAT_ERR_HIP leaves the simulated storage active, so repeating it enqueues
+ * the whole prefetch again.  Expert storage is never written.  Errors: SMAT_ERR_INVALID (bad `to`),
+ * SMAT_ERR_STATE, SMAT_ERR_HIP. */
 smat_status smat_switch_storage(smat_plan* plan, int32_t to, hipStream_t stream);
 
 /* smat_plan_state -- the active storage (an smat_storage value) in *state. */

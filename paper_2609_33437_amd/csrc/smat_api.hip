@@ -121,6 +121,17 @@ smat_status check_simulate_ptrs(const float* theta, const void* theta0, int t0_d
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Calls that upload host tables through pinned staging (reused by the next call) and wait on their
+// own events cannot be recorded into a graph: a replay would copy whatever the staging holds then.
+smat_status refuse_capture(hipStream_t stream, const char* where) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  SMAT_HIP(hipStreamIsCapturing(stream, &cs));
+  if (cs != hipStreamCaptureStatusNone)
+    return fail(SMAT_ERR_STATE, "%s: uploads host tables and cannot be captured; call it before capture "
+                "(the *_dev calls read per-step values from device memory)", where);
+  return SMAT_OK;
+}
+
 // Gradient arrays of one plan tensor (either may be absent) must not overlap each other, theta,
 // theta0, the simulated buffer or the optimizer moments.
 smat_status check_grad_ptrs(const float* theta, const void* theta0, int t0_dt, const void* out, int out_dt,
@@ -574,6 +585,7 @@ extern "C" smat_status smat_plan_bind_workspace(smat_plan* p, void* workspace, s
   if (!aligned(workspace, 256)) return fail(SMAT_ERR_INVALID, "smat_plan_bind_workspace: workspace not 256-byte aligned");
   if (bytes < p->ws_bytes)
     return fail(SMAT_ERR_INVALID, "smat_plan_bind_workspace: workspace of %zu bytes, need %zu", bytes, p->ws_bytes);
+  if (smat_status st = refuse_capture(stream, "smat_plan_bind_workspace"); st != SMAT_OK) return st;
 
   const size_t static_bytes = p->off_params;
   // each resource is created once: a call that failed part-way can be retried without leaking
@@ -610,6 +622,7 @@ extern "C" smat_status smat_plan_bind_workspace(smat_plan* p, void* workspace, s
 extern "C" smat_status smat_plan_set_params(smat_plan* p, const smat_op_params* per_tensor, hipStream_t stream) {
   if (!p || (p->count > 0 && !per_tensor)) return fail(SMAT_ERR_INVALID, "smat_plan_set_params: null argument");
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_set_params: no workspace bound");
+  if (smat_status st = refuse_capture(stream, "smat_plan_set_params"); st != SMAT_OK) return st;
   std::vector<ParamRec> recs(p->count);
   std::vector<ScaleRec> scales(p->count);
   for (int32_t i = 0; i < p->count; ++i) {
@@ -729,6 +742,7 @@ extern "C" smat_status smat_backward_multi_dev(smat_plan* p, const smat_step_sta
 extern "C" smat_status smat_plan_bind_adam_state(smat_plan* p, const smat_adam_state* per_tensor, hipStream_t stream) {
   if (!p || (p->count > 0 && !per_tensor)) return fail(SMAT_ERR_INVALID, "smat_plan_bind_adam_state: null argument");
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_bind_adam_state: no workspace bound");
+  if (smat_status st = refuse_capture(stream, "smat_plan_bind_adam_state"); st != SMAT_OK) return st;
   std::vector<AdamRec> adam(p->count);
   std::vector<TensorRec> recs = p->recs;
   for (int32_t i = 0; i < p->count; ++i) {
@@ -774,6 +788,7 @@ extern "C" smat_status smat_plan_set_grads(smat_plan* p, const void* const* grad
   if (!p) return fail(SMAT_ERR_INVALID, "smat_plan_set_grads: null plan");
   if (!grad_sims && !grad_thetas) return fail(SMAT_ERR_INVALID, "smat_plan_set_grads: nothing to set");
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_plan_set_grads: no workspace bound");
+  if (smat_status st = refuse_capture(stream, "smat_plan_set_grads"); st != SMAT_OK) return st;
   std::vector<TensorRec> recs = p->recs;
   for (int32_t i = 0; i < p->count; ++i) {
     TensorRec& r = recs[i];
@@ -955,9 +970,14 @@ extern "C" smat_status smat_switch_storage(smat_plan* p, int32_t to, hipStream_t
     return SMAT_OK;
   }
   if (p->state == SMAT_EXPERT) return SMAT_OK;  // restoring is idempotent
+  if (p->offload) {
+    // a failed prefetch leaves the simulated storage active, so that a retry enqueues all of it again
+    // rather than a simulate running over partly refilled buffers
+    smat_status st = enqueue_prefetch(p, stream);
+    if (st != SMAT_OK) return st;
+  }
   p->state = SMAT_EXPERT;
   p->fresh = false;
-  if (p->offload) return enqueue_prefetch(p, stream);
   return SMAT_OK;
 }
 
@@ -1223,6 +1243,7 @@ extern "C" smat_status smat_merge_plan_bind_workspace(smat_merge_plan* p, void* 
     return fail(SMAT_ERR_INVALID, "smat_merge_plan_bind_workspace: workspace not 256-byte aligned");
   if (bytes < p->ws_bytes)
     return fail(SMAT_ERR_INVALID, "smat_merge_plan_bind_workspace: workspace of %zu bytes, need %zu", bytes, p->ws_bytes);
+  if (smat_status st = refuse_capture(stream, "smat_merge_plan_bind_workspace"); st != SMAT_OK) return st;
   const size_t static_bytes = p->off_terms;
   const size_t cells = (size_t)p->count * p->nexp;
   // each resource is created once: a call that failed part-way can be retried without leaking
@@ -1249,6 +1270,7 @@ extern "C" smat_status smat_merge_multi(smat_merge_plan* p, const smat_merge_ter
   const size_t cells = (size_t)p->count * p->nexp;
   if (cells > 0 && !terms) return fail(SMAT_ERR_INVALID, "smat_merge_multi: null terms");
   if (!p->ws) return fail(SMAT_ERR_STATE, "smat_merge_multi: no workspace bound");
+  if (smat_status st = refuse_capture(stream, "smat_merge_multi"); st != SMAT_OK) return st;
   std::vector<MergeRec> recs(cells);
   for (size_t c = 0; c < cells; ++c) {
     char where[80];

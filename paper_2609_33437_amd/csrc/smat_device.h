@@ -154,7 +154,6 @@ constexpr int tiles_per_chunk(int quads) { return (int)(kChunk / tile_elems(quad
 static_assert(kChunk % tile_elems(kSimQuads) == 0 && kChunk % tile_elems(kBwdQuads) == 0 &&
                   kChunk % tile_elems(kAdamQuads) == 0,
               "tiles split chunks");
-constexpr int64_t kMaxTile = tile_elems(kSimQuads > kBwdQuads ? kSimQuads : kBwdQuads);
 
 constexpr uint32_t kStreamMask = 0u;
 constexpr uint32_t kStreamNoise = 1u;

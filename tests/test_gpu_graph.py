@@ -442,3 +442,34 @@ def test_device_optimizer_errors(mini):
         plan.adamw_fused_dev(state, adam.tensor, cfg.lam, HP)                   # a plain 8-byte tensor
         torch.cuda.synchronize()
     assert sq.item() > 0
+
+
+def test_uploads_refused_under_capture(mini):
+    """Calls that upload host tables through staging refuse to be captured; the capture itself stays
+    usable and replays the device-driven call recorded before the refusal."""
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out_d, gt = fresh(inp)
+    out_e, _ = fresh(inp)
+    base = base_params(cfg, inp, 4)
+    state = smat.StepState(cfg.smat_seed, 4, 0.625)
+    refused = []
+    with smat.Plan(th, out_d, t0, gs, gt) as pd, smat.Plan(th, out_e, t0, gs, gt) as pe:
+        pd.set_params(base)
+        pe.set_params(base)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            pd.simulate_dev(state)
+            for call in (lambda: pd.set_params(base), lambda: pd.set_grads(grad_sims=gs),
+                         lambda: pd.bind_adam_state([torch.empty_like(x) for x in th], [torch.empty_like(x) for x in th])):
+                try:
+                    call()
+                except smat.SmatError as e:
+                    refused.append(str(e))
+        graph.replay()
+        pe.simulate_dev(state)
+        torch.cuda.synchronize()
+        del graph
+    assert len(refused) == 3 and all("cannot be captured" in m for m in refused), refused
+    assert same_bits(out_d, out_e)
