@@ -1,8 +1,8 @@
 """GPU tests of jobs whose one-launch grid would hold more than 2^32 work-items, which a dispatch
 cannot express (the count would wrap without an error): the launchers split them into several
-launches.  A copy of 68.7 GB, a one-tensor backward of 17.2e9 elements and lists of 2.2 million
-tensors (2.2 million chunks) are checked against the oracle at the piece boundaries and at the end,
-and for having written every element."""
+launches.  A copy of 68.7 GB, a one-tensor backward of 17.2e9 elements, 4.3e9 raw Philox words and
+a list of 2.2 million tensors (2.2 million chunks) are checked against the oracle at the piece
+boundaries and at the end, and for having written every element."""
 import ctypes
 
 import numpy as np
@@ -66,6 +66,23 @@ def test_backward_one_past_the_grid_limit():
         assert check_grad(got, want, g_old, np.abs(lam * coef * oracle.as_f64(gsn, gs_dt))).all(), lo
         assert (got != 0.25).any(), lo                  # the range was reached
     del gs, gt
+    torch.cuda.empty_cache()
+
+
+def test_debug_draws_past_the_grid_limit():
+    boundary = (0xFFFFFFFF // 256) * 256               # 256-thread blocks: first element of the second launch
+    n = boundary + 1029
+    if free_gib() < n * 4 / GIB + 8:
+        pytest.skip("needs about 25 GB of free device memory")
+    words = torch.zeros(n, dtype=torch.int32, device=DEV)
+    seed, step, tid, off = 12345, 6, 3, 1 << 33
+    smat.smat_debug_draws(n, dict(s=1.0, keep=1.0, sigma=0.0), seed, step, tid, off, mask_words=words)
+    torch.cuda.synchronize()
+    for lo, hi in ((0, 1024), (boundary - 2048, boundary + 1029), (n - 1029, n)):
+        want = oracle.element_words(seed, step, tid, off + lo, hi - lo, 0)
+        got = words[lo:hi].cpu().numpy().view(np.uint32)
+        np.testing.assert_array_equal(got, want, err_msg=str(lo))
+    del words
     torch.cuda.empty_cache()
 
 
