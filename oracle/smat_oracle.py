@@ -29,6 +29,9 @@ and noise in-kernel but gives no generator):
   counter = (g_lo, g_hi, tensor_id, step*4 + stream) where g = e >> 2 for the
   global element index e = elem_offset + i; element e takes word e & 3.
   Stream 0 draws the mask, stream 1 the noise;
+* the step's shared scale alpha ~ U[alpha_min, 1], when drawn from the same
+  generator: word 0 of counter (0, 0, 0, step*4 + 2) (stream 2, group 0 of
+  tensor id 0), u = (w0 >> 8) 2^-24, alpha = alpha_min + (1 - alpha_min) u;
 * mask: kept iff word < floor(keep * 2^32); keep >= 1 keeps everything and
   keep <= 0 drops everything without drawing;
 * Gaussian noise: lanes (0, 1) of a group pair words (w0, w1), lanes (2, 3)
@@ -59,6 +62,7 @@ MASK32 = 0xFFFFFFFF
 
 STREAM_MASK = 0
 STREAM_NOISE = 1
+STREAM_SCALE = 2
 
 NOISE_GAUSSIAN = 0
 NOISE_UNIFORM = 1
@@ -110,6 +114,19 @@ def group_words(seed: int, step: int, tensor_id: int, groups, stream: int):
     c2 = np.uint64(tensor_id)
     c3 = np.uint64(((step << 2) | stream) & MASK32)
     return philox4x32(c0, c1, c2, c3, seed & MASK32, seed >> 32)
+
+
+def scale_draw(seed: int, step: int, alpha_min: float) -> float:
+    """The scale shared by every coordinate in one simulated update, alpha ~ U[alpha_min, 1]
+    (Sec. 4.1, "Scale"), as a function of (seed, step): word 0 of the counter (0, 0, 0, 4 step + 2)
+    gives u = (w0 >> 8) 2^-24 in [0, 1); alpha = alpha_min + (1 - alpha_min) u, with alpha_min taken
+    as fp32, formed in fp64 and rounded once to fp32 (nearest even)."""
+    a = float(np.float32(alpha_min))
+    if not (0.0 <= a <= 1.0):
+        raise ValueError("alpha_min must lie in [0, 1]")
+    w0 = int(group_words(seed, step, 0, [0], STREAM_SCALE)[0][0])
+    u = float(w0 >> 8) * 2.0 ** -24
+    return float(np.float32(a + (1.0 - a) * u))
 
 
 def element_words(seed: int, step: int, tensor_id: int, elem_offset: int, n: int, stream: int) -> np.ndarray:
