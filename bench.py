@@ -658,8 +658,9 @@ def bench_graph(args, torch, smat, workloads) -> int:
     """Per-step cost of a simulated step on the chosen list when each step samples one scale
     alpha ~ U[alpha_min, 1] shared by every tensor (Sec. 4.1, "Scale"): issued from the host (new
     per-tensor records uploaded, then smat_simulate_multi and smat_backward_multi) against one
-    captured HIP graph of the device-driven calls, whose replays advance the step and sample the
-    scale on the device.  Both time K back-to-back steps after W warmup steps."""
+    captured HIP graph of smat_step_state_advance and the device-driven calls, whose replays advance
+    the step and draw its scale on the device.  Both time K back-to-back steps after W warmup
+    steps."""
     import numpy as np
     cfg = workloads.config(args.config)
     inp = workloads.make_inputs(cfg, device="cuda")
@@ -700,11 +701,9 @@ def bench_graph(args, torch, smat, workloads) -> int:
         arr["s"] = 1.0
         plan.set_params(arr)
         state = smat.StepState(seed, 0, 1.0)
-        torch.cuda.manual_seed(cfg.index)   # the default generator: graph replays advance its offset
 
         def dev_step():
-            state.step_view.add_(1)
-            state.scale_view.copy_(torch.rand(1, device="cuda") * (1.0 - amin) + amin)
+            state.advance(amin)             # step + 1 and its scale, drawn from (seed, step) on the GPU
             plan.simulate_dev(state)
             plan.backward_dev(state, lam, True)
 

@@ -274,6 +274,17 @@ typedef struct smat_step_state {
   float scale;
 } smat_step_state;
 
+/* smat_step_state_advance -- step += increment (modulo 2^32), then scale = the step's shared scale
+ * alpha ~ U[alpha_min, 1] (Sec. 4.1, "Scale": one coefficient per simulated update, shared by every
+ * coordinate), written in place by one thread on `stream`.  alpha comes from word 0 of the Philox
+ * counter (0, 0, 0, 4 step + 2) under key seed (stream 2, which no tensor uses):
+ * u = (w0 >> 8) 2^-24 and alpha = fl32(alpha_min + (1 - alpha_min) u), the sum formed in fp64.  It
+ * is a function of (seed, step) only, so a run resumed at a step draws the same scales; increment 0
+ * only sets the scale of the current step.  One kernel node under stream capture.  state as for
+ * smat_simulate_multi_dev.  Errors: SMAT_ERR_INVALID (null or misaligned state, alpha_min outside
+ * [0, 1]), SMAT_ERR_HIP. */
+smat_status smat_step_state_advance(smat_step_state* state, uint32_t increment, float alpha_min, hipStream_t stream);
+
 /* smat_simulate_multi_dev / smat_backward_multi_dev -- smat_simulate_multi and smat_backward_multi
  * with seed, step and scale read from `state` (device-accessible, 16-byte aligned, caller-owned; it
  * must hold its values when the kernels run).  keep, sigma, noise kind and rescale still come from

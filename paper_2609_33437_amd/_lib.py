@@ -31,7 +31,7 @@ EXPORTS = (
     "smat_merge", "smat_merge_plan_create", "smat_merge_plan_workspace_bytes", "smat_merge_plan_bind_workspace",
     "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
     "smat_stream_copy", "smat_backward_multi", "smat_plan_clear_grads", "smat_simulate_multi_dev",
-    "smat_backward_multi_dev", "smat_adamw_fused_multi_dev", "smat_grad_norm_multi_dev",
+    "smat_backward_multi_dev", "smat_adamw_fused_multi_dev", "smat_grad_norm_multi_dev", "smat_step_state_advance",
 )
 
 
@@ -128,6 +128,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_backward_multi_dev": [P, P, c_float, c_int32, P],
         "smat_adamw_fused_multi_dev": [P, P, P, smat_adamw_params, c_float, c_int32, P, P],
         "smat_grad_norm_multi_dev": [P, P, c_float, c_int32, c_float, P, P, P],
+        "smat_step_state_advance": [P, c_uint32, c_float, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -211,6 +212,12 @@ class StepState:
         rec = np.zeros(1, dtype=[("seed", "<u8"), ("step", "<u4"), ("scale", "<f4")])
         rec["seed"], rec["step"], rec["scale"] = int(seed), int(step), float(scale)
         self.tensor.copy_(_torch().from_numpy(rec.view(np.int32).copy()))
+
+    def advance(self, alpha_min: float, increment: int = 1, stream=None) -> None:
+        """smat_step_state_advance on the GPU: step += increment, then the scale of that step
+        drawn from (seed, step) as alpha ~ U[alpha_min, 1].  Capturable."""
+        _check(lib().smat_step_state_advance(_dev_ptr(self.tensor, "step state"), int(increment) & 0xFFFFFFFF,
+                                             float(alpha_min), _stream_handle(stream)))
 
     @property
     def seed_view(self):

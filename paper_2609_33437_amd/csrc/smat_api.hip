@@ -704,6 +704,16 @@ smat_status check_dev_call(const smat_plan* p, const smat_step_state* state, con
 }
 }  // namespace
 
+extern "C" smat_status smat_step_state_advance(smat_step_state* state, uint32_t increment, float alpha_min,
+                                               hipStream_t stream) {
+  if (!state) return fail(SMAT_ERR_INVALID, "smat_step_state_advance: null state");
+  if (!aligned(state, 16)) return fail(SMAT_ERR_INVALID, "smat_step_state_advance: state not 16-byte aligned");
+  if (!(alpha_min >= 0.f && alpha_min <= 1.f))
+    return fail(SMAT_ERR_INVALID, "smat_step_state_advance: alpha_min must lie in [0, 1]");
+  SMAT_HIP(smat::launch_step_advance(reinterpret_cast<StepState*>(state), increment, alpha_min, stream));
+  return SMAT_OK;
+}
+
 extern "C" smat_status smat_simulate_multi_dev(smat_plan* p, const smat_step_state* state, hipStream_t stream) {
   smat_status st = check_dev_call(p, state, "smat_simulate_multi_dev");
   if (st != SMAT_OK) return st;

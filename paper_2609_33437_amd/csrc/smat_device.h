@@ -59,6 +59,14 @@ struct alignas(16) StepState {
 };
 static_assert(sizeof(StepState) == 16, "StepState layout");
 
+// The step's shared scale alpha ~ U[alpha_min, 1] from one Philox word: u = (w >> 8) 2^-24 and
+// alpha = alpha_min + (1 - alpha_min) u formed in fp64 (exact up to the one sum) and rounded once.
+__device__ __forceinline__ float scale_from_word(uint32_t w, float alpha_min) {
+#pragma clang fp contract(off)
+  const double a = alpha_min, u = (double)(w >> 8) * 0x1p-24;
+  return (float)(a + (1.0 - a) * u);
+}
+
 // What the coefficient of a tensor needs when the scale comes from device memory: the tensor's own
 // s and keep, and whether kept coordinates divide by keep (rescale with 0 < keep < 1).
 struct alignas(16) ScaleRec {
@@ -157,6 +165,7 @@ static_assert(kChunk % tile_elems(kSimQuads) == 0 && kChunk % tile_elems(kBwdQua
 
 constexpr uint32_t kStreamMask = 0u;
 constexpr uint32_t kStreamNoise = 1u;
+constexpr uint32_t kStreamScale = 2u;  // the step's shared scale: group 0 of tensor id 0
 
 // ---------------------------------------------------------------- Philox4x32-10
 struct Words {

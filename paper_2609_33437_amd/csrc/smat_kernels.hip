@@ -296,6 +296,18 @@ __global__ __launch_bounds__(kBlock) void k_backward_multi_dev(const TensorRec* 
   backward_tile<TG, kBwdQuads, ACC>(T, P, S.seed, S.step, lambda);
 }
 
+// One thread advances the step state: step += increment, then the scale of that step drawn from the
+// scale stream, so that it depends on (seed, step) only.
+__global__ __launch_bounds__(64) void k_step_advance(StepState* __restrict__ state, uint32_t increment,
+                                                     float alpha_min) {
+  if (threadIdx.x != 0) return;
+  StepState S = *state;
+  S.step += increment;
+  const Words w = group_words(0, 0, (S.step << 2) | kStreamScale, (uint32_t)S.seed, (uint32_t)(S.seed >> 32));
+  S.scale = scale_from_word(w.w0, alpha_min);
+  *state = S;
+}
+
 constexpr int kDebugBlock = 256;
 
 __global__ __launch_bounds__(kDebugBlock) void k_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id,
@@ -423,6 +435,11 @@ hipError_t launch_backward_multi_dev(const TensorRec* recs, const ParamRec* prms
     else
       k_backward_multi_dev<float, false><<<grid, block, 0, stream>>>(recs, prms, scales, ch, state, lambda);
   });
+}
+
+hipError_t launch_step_advance(StepState* state, uint32_t increment, float alpha_min, hipStream_t stream) {
+  k_step_advance<<<dim3(1), dim3(64), 0, stream>>>(state, increment, alpha_min);
+  return hipGetLastError();
 }
 
 hipError_t launch_debug_draws(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t elem_offset,

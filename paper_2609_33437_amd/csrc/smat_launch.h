@@ -69,6 +69,8 @@ hipError_t launch_simulate_multi_dev(const TensorRec* recs, const ParamRec* prms
 hipError_t launch_backward_multi_dev(const TensorRec* recs, const ParamRec* prms, const ScaleRec* scales,
                                      const uint2* chunks, uint32_t nchunks, int grad_dtype, bool accumulate,
                                      float lambda, const StepState* state, hipStream_t stream);
+// step += increment and the scale of that step, in place (one thread).
+hipError_t launch_step_advance(StepState* state, uint32_t increment, float alpha_min, hipStream_t stream);
 hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const ParamRec& prm, const AdamConsts& A,
                             int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
                             const float* dev_scale, hipStream_t stream);

@@ -186,6 +186,10 @@ def test_device_driven_calls_without_gpu():
     assert lib.smat_grad_norm_multi_dev(p, state, 1.0, 0, 1.0, sq, None, None) == _lib.SMAT_ERR_STATE
     assert lib.smat_grad_norm_multi_dev(None, state, 1.0, 0, 1.0, sq, None, None) == _lib.SMAT_ERR_INVALID
     assert lib.smat_plan_destroy(p) == 0
+    assert lib.smat_step_state_advance(None, 1, 0.2, None) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_step_state_advance(ctypes.c_void_p(64 * A + 8), 1, 0.2, None) == _lib.SMAT_ERR_INVALID
+    for bad in (-0.1, 1.5, float("nan")):
+        assert lib.smat_step_state_advance(state, 1, bad, None) == _lib.SMAT_ERR_INVALID
     arr = (_lib.smat_tensor_desc * 1)(_desc(1 * A, 2 * A, None, 4 * A, 5 * A, 1000, 0, 0, 11 * A))
     assert lib.smat_plan_create(arr, 1, 1, 1, 1, 1, ctypes.byref(p)) == 0
     assert lib.smat_simulate_multi_dev(p, state, None) == _lib.SMAT_ERR_STATE

@@ -473,3 +473,56 @@ def test_uploads_refused_under_capture(mini):
         del graph
     assert len(refused) == 3 and all("cannot be captured" in m for m in refused), refused
     assert same_bits(out_d, out_e)
+
+
+# ---------------------------------------------------------------- the step's scale drawn on the device
+@pytest.mark.parametrize("seed,step0,alpha_min", [(0, 0, 0.2), (2 ** 64 - 1, 41, 0.1), (12345, 2 ** 30 - 5, 0.75),
+                                                  (7, 100, 0.0), (7, 100, 1.0)])
+def test_step_advance_matches_oracle(seed, step0, alpha_min):
+    st = smat.StepState(seed, step0, -1.0)
+    st.advance(alpha_min, 0)                     # the scale of the current step
+    torch.cuda.synchronize()
+    assert st.step_view.item() == step0
+    assert st.scale_view.item() == oracle.scale_draw(seed, step0, alpha_min)
+    for k in range(1, 4):
+        st.advance(alpha_min)
+        torch.cuda.synchronize()
+        assert st.step_view.item() == step0 + k
+        assert st.scale_view.item() == oracle.scale_draw(seed, step0 + k, alpha_min)
+    assert st.seed_view.item() == (seed if seed < 2 ** 63 else seed - 2 ** 64)
+    with pytest.raises(smat.SmatError):
+        st.advance(1.5)
+
+
+def test_graph_with_scale_drawn_on_the_device(mini):
+    """One graph: advance (step + 1, scale of that step), simulate, backward; each replay equals the
+    host-driven step with the oracle's scale for that step."""
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out_d, gt_d = fresh(inp)
+    out_h, gt_h = fresh(inp)
+    base = base_params(cfg, inp, 0)
+    step0, amin = 60, 0.2
+    state = smat.StepState(cfg.smat_seed, step0, 1.0)
+    with smat.Plan(th, out_d, t0, gs, gt_d) as pd, smat.Plan(th, out_h, t0, gs, gt_h) as ph:
+        pd.set_params(base)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            state.advance(amin)
+            pd.simulate_dev(state)
+            pd.backward_dev(state, cfg.lam, False)
+        for k in range(1, 4):
+            for o in out_d:
+                o.fill_(float("nan"))
+            graph.replay()
+            step = step0 + k
+            scale = oracle.scale_draw(cfg.smat_seed, step, amin)
+            ph.set_params(scaled(base, scale))
+            ph.simulate(cfg.smat_seed, step)
+            ph.backward(cfg.smat_seed, step, cfg.lam, False)
+            torch.cuda.synchronize()
+            assert state.step_view.item() == step and state.scale_view.item() == scale
+            assert same_bits(out_d, out_h), k
+            assert same_bits(gt_d, gt_h), k
+        del graph
