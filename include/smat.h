@@ -285,6 +285,11 @@ typedef struct smat_step_state {
  * [0, 1]), SMAT_ERR_HIP. */
 smat_status smat_step_state_advance(smat_step_state* state, uint32_t increment, float alpha_min, hipStream_t stream);
 
+/* smat_scale_draw -- the same scale on the host, for the host-driven calls: *alpha = the scale that
+ * smat_step_state_advance draws for (seed, step, alpha_min), bit for bit.  Host only (no GPU, no
+ * stream).  Errors: SMAT_ERR_INVALID (null alpha, alpha_min outside [0, 1]). */
+smat_status smat_scale_draw(uint64_t seed, uint32_t step, float alpha_min, float* alpha);
+
 /* smat_simulate_multi_dev / smat_backward_multi_dev -- smat_simulate_multi and smat_backward_multi
  * with seed, step and scale read from `state` (device-accessible, 16-byte aligned, caller-owned; it
  * must hold its values when the kernels run).  keep, sigma, noise kind and rescale still come from

@@ -32,6 +32,7 @@ EXPORTS = (
     "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
     "smat_stream_copy", "smat_backward_multi", "smat_plan_clear_grads", "smat_simulate_multi_dev",
     "smat_backward_multi_dev", "smat_adamw_fused_multi_dev", "smat_grad_norm_multi_dev", "smat_step_state_advance",
+    "smat_scale_draw",
 )
 
 
@@ -129,6 +130,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_adamw_fused_multi_dev": [P, P, P, smat_adamw_params, c_float, c_int32, P, P],
         "smat_grad_norm_multi_dev": [P, P, c_float, c_int32, c_float, P, P, P],
         "smat_step_state_advance": [P, c_uint32, c_float, P],
+        "smat_scale_draw": [c_uint64, c_uint32, c_float, POINTER(c_float)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -192,6 +194,15 @@ def _scalar_ptr(t, what: str, dtype: str):
     if str(t.dtype) != f"torch.{dtype}" or t.numel() != 1:
         raise SmatError(SMAT_ERR_INVALID, f"{what} must be a one-element {dtype} tensor")
     return _dev_ptr(t, what)
+
+
+def scale_draw(seed: int, step: int, alpha_min: float) -> float:
+    """The step's shared scale alpha ~ U[alpha_min, 1] as a function of (seed, step): the value
+    smat_step_state_advance writes on the GPU, computed on the host (smat_scale_draw)."""
+    out = c_float()
+    _check(lib().smat_scale_draw(int(seed) & 0xFFFFFFFFFFFFFFFF, int(step) & 0xFFFFFFFF, float(alpha_min),
+                                 ctypes.byref(out)))
+    return out.value
 
 
 class StepState:

@@ -704,6 +704,37 @@ smat_status check_dev_call(const smat_plan* p, const smat_step_state* state, con
 }
 }  // namespace
 
+namespace {
+// The step's scale on the host, the same bits as k_step_advance draws on the device: word 0 of
+// Philox4x32-10 at counter (0, 0, 0, 4 step + 2) under key seed, then u = (w0 >> 8) 2^-24 and
+// alpha_min + (1 - alpha_min) u in fp64, rounded once to fp32.
+float host_scale(uint64_t seed, uint32_t step, float alpha_min) {
+#pragma clang fp contract(off)
+  uint32_t c0 = 0, c1 = 0, c2 = 0, c3 = (step << 2) | smat::kStreamScale;
+  uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)c0 * smat::kPhiloxM0, p1 = (uint64_t)c2 * smat::kPhiloxM1;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0, n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += smat::kPhiloxW0;
+    k1 += smat::kPhiloxW1;
+  }
+  const double a = alpha_min, u = (double)(c0 >> 8) * 0x1p-24;
+  return (float)(a + (1.0 - a) * u);
+}
+}  // namespace
+
+extern "C" smat_status smat_scale_draw(uint64_t seed, uint32_t step, float alpha_min, float* alpha) {
+  if (!alpha) return fail(SMAT_ERR_INVALID, "smat_scale_draw: null output");
+  if (!(alpha_min >= 0.f && alpha_min <= 1.f))
+    return fail(SMAT_ERR_INVALID, "smat_scale_draw: alpha_min must lie in [0, 1]");
+  *alpha = host_scale(seed, step, alpha_min);
+  return SMAT_OK;
+}
+
 extern "C" smat_status smat_step_state_advance(smat_step_state* state, uint32_t increment, float alpha_min,
                                                hipStream_t stream) {
   if (!state) return fail(SMAT_ERR_INVALID, "smat_step_state_advance: null state");

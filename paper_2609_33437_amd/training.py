@@ -3,7 +3,8 @@
 Each cycle of t steps has t - 1 ordinary steps and one simulated step (step mod t == t - 1).
 Each step computes one loss with one forward and one backward pass.  On a simulated step:
 
-1. `begin(step)` draws one scale alpha ~ U[alpha_min, 1] for all tensors (Sec. 4.1, Scale),
+1. `begin(step)` draws one scale alpha ~ U[alpha_min, 1] for all tensors (Sec. 4.1, Scale) from
+   (seed, step) (smat_scale_draw, the generator's scale stream),
    writes theta~ = theta0 + alpha m (.) (theta - theta0) + eps into one reusable buffer per
    parameter (smat_simulate_multi), and rebinds each parameter's `.data` to its buffer.  The
    model's forward and backward then run on theta~; autograd's gradient tensors at theta~ are
@@ -160,7 +161,6 @@ class SimulatedMergeTraining:
         else:
             self.theta0 = [t.detach().to(device=dev, dtype=buffer_dtype).contiguous() for t in theta0]
             self.plan = Plan(self.master, self.buffers, self.theta0, dtypes=(dt, dt, dt))
-        self._rng = np.random.default_rng(self.seed)
         self.alpha: Optional[float] = None      # the scale of the current (or last) simulated step
         self._step: Optional[int] = None        # set between begin() and end()
         self._adam_key = None
@@ -201,7 +201,8 @@ class SimulatedMergeTraining:
             raise SmatError(SMAT_ERR_STATE, "begin() while a simulated step is open")
         if not self.is_simulated(step):
             return False
-        self.alpha = float(np.float32(self._rng.uniform(self.alpha_min, 1.0)))
+        # alpha is a function of (seed, step), like the masks and the noise: a resumed run draws the same
+        self.alpha = _lib.scale_draw(self.seed, step, self.alpha_min)
         self.plan.set_params(_lib.op_params_array(len(self.params), self.alpha, self.keep, self.sigma, self.rescale,
                                                   self.noise_kind))
         self.plan.simulate(self.seed, step)

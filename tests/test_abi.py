@@ -333,3 +333,19 @@ def test_stream_copy_argument_errors_without_gpu():
     assert lib.smat_stream_copy(P((1 << 20) + 8), P(2 << 20), 16, None) == _lib.SMAT_ERR_INVALID  # misaligned
     assert lib.smat_stream_copy(P(1 << 20), P(2 << 20), 24, None) == _lib.SMAT_ERR_INVALID       # size
     assert lib.smat_stream_copy(P(1 << 20), P((1 << 20) + 16), 64, None) == _lib.SMAT_ERR_INVALID  # overlap
+
+
+def test_scale_draw_matches_oracle_without_gpu():
+    """smat_scale_draw is host code: the step's scale, bit for bit the oracle's draw, for many keys."""
+    import numpy as np
+    import oracle
+    rng = np.random.default_rng(3)
+    for _ in range(300):
+        seed = int(rng.integers(0, 2 ** 63)) * 2 + int(rng.integers(0, 2))
+        step = int(rng.integers(0, 2 ** 30))
+        amin = float(rng.choice([0.0, 0.1, 0.2, float(rng.random()), 1.0]))
+        assert smat.scale_draw(seed, step, amin) == oracle.scale_draw(seed, step, amin), (seed, step, amin)
+    lib = smat.lib()
+    out = ctypes.c_float()
+    assert lib.smat_scale_draw(1, 2, 1.5, ctypes.byref(out)) == _lib.SMAT_ERR_INVALID
+    assert lib.smat_scale_draw(1, 2, 0.5, None) == _lib.SMAT_ERR_INVALID

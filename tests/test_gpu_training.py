@@ -66,6 +66,7 @@ def test_simulated_step_matches_oracle():
         assert [p.data_ptr() for p in w.params] == ids
     assert w.begin(3) and w.active
     assert 0.2 <= w.alpha <= 1.0
+    assert w.alpha == oracle.scale_draw(SEED, 3, 0.2)    # a function of (seed, step): resumable
     assert all(p.data_ptr() == b.data_ptr() for p, b in zip(w.params, w.buffers))
     check_simulated(w, masters, 3)
     # the forward and backward run on theta~: compare with a copy of the model holding theta~
