@@ -349,3 +349,31 @@ def test_scale_draw_matches_oracle_without_gpu():
     out = ctypes.c_float()
     assert lib.smat_scale_draw(1, 2, 1.5, ctypes.byref(out)) == _lib.SMAT_ERR_INVALID
     assert lib.smat_scale_draw(1, 2, 0.5, None) == _lib.SMAT_ERR_INVALID
+
+
+def test_every_entry_point_survives_zero_arguments():
+    """Every exported call, given null pointers, zero counts and zeroed records, returns a status
+    (a no-op or an argument error) without touching memory or needing a GPU."""
+    lib = smat.lib()
+    statuses = {}
+    for name in _lib.EXPORTS:
+        if name == "smat_last_error":
+            continue
+        fn = getattr(lib, name)
+        args = []
+        for t in fn.argtypes:
+            if isinstance(t, type) and issubclass(t, ctypes.Structure):
+                args.append(t())
+            elif t in (ctypes.c_float, ctypes.c_double):
+                args.append(0.0)
+            elif t in (ctypes.c_int32, ctypes.c_uint32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t):
+                args.append(0)
+            else:
+                args.append(None)
+        statuses[name] = fn(*args)
+    allowed = (_lib.SMAT_OK, _lib.SMAT_ERR_INVALID, _lib.SMAT_ERR_DTYPE, _lib.SMAT_ERR_STATE)
+    assert all(st in allowed for st in statuses.values()), statuses
+    # calls that take a plan or an output pointer refuse a null one
+    for name, st in statuses.items():
+        if "plan" in name and name not in ("smat_plan_destroy", "smat_merge_plan_destroy"):
+            assert st == _lib.SMAT_ERR_INVALID, name
