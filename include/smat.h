@@ -35,8 +35,9 @@
  *     (g_lo, g_hi, tensor_id, 4*step + stream), where g = e >> 2 for the
  *     global element index e = elem_offset + i and element e takes word e & 3.
  *     Stream 0 draws the mask (kept iff word < floor(keep * 2^32)), stream 1
- *     the noise.  Gaussian noise pairs words (w0, w1) for lanes 0/1 and
- *     (w2, w3) for lanes 2/3 by Box-Muller on 24-bit uniforms
+ *     the noise, stream 2 (group 0 of tensor id 0) the step's shared scale
+ *     (smat_step_state_advance, smat_scale_draw).  Gaussian noise pairs words
+ *     (w0, w1) for lanes 0/1 and (w2, w3) for lanes 2/3 by Box-Muller on 24-bit uniforms
  *     u1 = ((a >> 8) + 1) 2^-24, u2 = (b >> 8) 2^-24 (cosine on the even lane).
  *     step must be below 2^30.
  *   - A tensor split into shards (elem_offset = index of its first element
