@@ -526,3 +526,102 @@ def test_graph_with_scale_drawn_on_the_device(mini):
             assert same_bits(out_d, out_h), k
             assert same_bits(gt_d, gt_h), k
         del graph
+
+
+# ---------------------------------------------------------------- a whole captured training step
+def _mlp(seed):
+    g = torch.Generator().manual_seed(seed)
+    model = torch.nn.Sequential(torch.nn.Linear(32, 96), torch.nn.GELU(), torch.nn.Linear(96, 24))
+    with torch.no_grad():
+        for p in model.parameters():
+            p.copy_(torch.randn(p.shape, generator=g) * 0.1)
+    return model.to(DEV)
+
+
+def test_captured_training_step_with_a_model():
+    """A simulated training step captured once with the model inside: advance (step + 1, its
+    scale), simulate into the buffers the model reads, forward and backward into static gradient
+    tensors, gradient norm and clipped fused AdamW on the expert storage, the optimizer's step count
+    advanced on the device.  Three replays against the same steps run eagerly through the
+    host-driven calls on a twin model."""
+    x = torch.randn(64, 32, generator=torch.Generator().manual_seed(1)).to(DEV)
+    y = torch.randn(64, 24, generator=torch.Generator().manual_seed(2)).to(DEV)
+    seed, step0, amin, lam, lr, k0, max_norm = 99, 10, 0.2, 1.0, 1e-3, 0, 0.05
+    hp = dict(beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, grad_scale=1.0)
+    keeps = [0.5, 1.0, 0.5, 1.0]                        # weights masked, biases not
+    twins = []
+    for _ in range(2):
+        model = _mlp(7)
+        params = list(model.parameters())
+        master = [p.data for p in params]
+        theta0 = [(p.data + 0.01 * torch.randn(p.shape, generator=torch.Generator().manual_seed(3)).to(DEV))
+                  for p in params]
+        buffers = [torch.empty_like(p) for p in params]
+        for p, b in zip(params, buffers):
+            p.data = b                                  # the model reads theta~ from here on
+            p.grad = torch.zeros_like(b)                # static gradient tensors at theta~
+        m1 = [torch.zeros_like(m) for m in master]
+        m2 = [torch.zeros_like(m) for m in master]
+        plan = smat.Plan(master, buffers, theta0, [p.grad for p in params])
+        plan.set_params(smat.op_params_array(len(params), 1.0, keeps, 1e-3, 1, smat.SMAT_NOISE_UNIFORM))
+        plan.bind_adam_state(m1, m2)
+        twins.append((model, params, master, plan, m1, m2))
+
+    def loss_backward(model, params):
+        for p in params:
+            p.grad.zero_()
+        torch.nn.functional.mse_loss(model(x), y).backward()
+
+    # A: device-driven, then captured
+    model_a, params_a, master_a, plan_a, m1_a, m2_a = twins[0]
+    state, adam = smat.StepState(seed, step0, 1.0), smat.AdamStepState(lr, k0)
+    coef_a = torch.zeros(1, device=DEV)
+
+    def step_a():
+        state.advance(amin)
+        adam.step_view.add_(1)
+        plan_a.simulate_dev(state)
+        loss_backward(model_a, params_a)
+        plan_a.grad_norm_dev(state, lam, False, max_norm, clip_coef=coef_a)
+        plan_a.adamw_fused_dev(state, adam, lam, hp, False, coef_a)
+
+    # B: the same steps issued from the host
+    model_b, params_b, master_b, plan_b, m1_b, m2_b = twins[1]
+    coef_b = torch.zeros(1, device=DEV)
+    base = smat.op_params_array(len(params_b), 1.0, keeps, 1e-3, 1, smat.SMAT_NOISE_UNIFORM)
+
+    def step_b(step, k):
+        arr = base.copy()
+        arr["s"] = smat.scale_draw(seed, step, amin)
+        plan_b.set_params(arr)
+        plan_b.simulate(seed, step)
+        loss_backward(model_b, params_b)
+        plan_b.grad_norm(seed, step, lam, False, max_norm, clip_coef=coef_b)
+        plan_b.adamw_fused(seed, step, lam, dict(hp, lr=lr, step=k), False, coef_b)
+
+    def same_state():
+        torch.cuda.synchronize()
+        for a, b in zip(master_a + m1_a + m2_a, master_b + m1_b + m2_b):
+            torch.testing.assert_close(a, b, rtol=1e-6, atol=1e-9)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):                       # eager warmup steps before the capture
+        for _ in range(2):
+            step_a()
+    torch.cuda.current_stream().wait_stream(side)
+    for r in (1, 2):
+        step_b(step0 + r, k0 + r)
+    same_state()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step_a()
+    for r in range(3, 6):
+        graph.replay()
+        step_b(step0 + r, k0 + r)
+        same_state()
+        assert 0 < coef_a.item() <= 1 and state.step_view.item() == step0 + r
+    assert coef_a.item() < 1                            # the clipping is active
+    del graph
+    for t in twins:
+        t[3].close()
