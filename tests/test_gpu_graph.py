@@ -625,3 +625,42 @@ def test_captured_training_step_with_a_model():
     del graph
     for t in twins:
         t[3].close()
+
+
+def test_device_calls_on_empty_lists_and_tensors():
+    """An empty plan and zero-size tensors in a list: the device-driven calls launch nothing for them
+    and leave every other tensor as the host-driven calls do."""
+    state, adam = smat.StepState(3, 4, 0.5), smat.AdamStepState(1e-3, 2)
+    sq = torch.full((1,), 7.0, dtype=torch.float64, device=DEV)
+    with smat.Plan([], [], [], [], []) as plan:
+        plan.set_params([])
+        plan.bind_adam_state([], [])
+        plan.simulate_dev(state)
+        plan.backward_dev(state, 1.0)
+        plan.grad_norm_dev(state, 1.0, sumsq=sq)
+        plan.adamw_fused_dev(state, adam, 1.0, dict(beta1=0.9, beta2=0.99, eps=1e-8, weight_decay=0.0))
+        torch.cuda.synchronize()
+    assert sq.item() == 0.0
+    g = torch.Generator(DEV).manual_seed(9)
+    sizes = [0, 37, 0, 4100]
+    res = {}
+    for mode in ("dev", "host"):
+        th = [torch.randn(n, device=DEV, generator=torch.Generator(DEV).manual_seed(n + 1)) for n in sizes]
+        t0 = [x.to(torch.bfloat16) for x in th]
+        gs = [(torch.randn(n, device=DEV, generator=g) * 0.0 + 0.01 * (i + 1)).to(torch.bfloat16)
+              for i, n in enumerate(sizes)]
+        gt = [torch.zeros(n, device=DEV) for n in sizes]
+        out = [torch.full((n,), float("nan"), device=DEV, dtype=torch.bfloat16) for n in sizes]
+        base = [dict(s=0.5 + 0.1 * i, keep=0.6, sigma=1e-3, rescale=1) for i in range(len(sizes))]
+        with smat.Plan(th, out, t0, gs, gt) as plan:
+            if mode == "dev":
+                plan.set_params(base)
+                plan.simulate_dev(state)
+                plan.backward_dev(state, 0.5, True)
+            else:
+                plan.set_params(scaled(base, 0.5))
+                plan.simulate(3, 4)
+                plan.backward(3, 4, 0.5, True)
+            torch.cuda.synchronize()
+        res[mode] = (out, gt)
+    assert same_bits(res["dev"][0], res["host"][0]) and same_bits(res["dev"][1], res["host"][1])
