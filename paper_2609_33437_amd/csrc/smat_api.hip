@@ -626,10 +626,13 @@ extern "C" smat_status smat_plan_set_params(smat_plan* p, const smat_op_params* 
   std::vector<ParamRec> recs(p->count);
   std::vector<ScaleRec> scales(p->count);
   for (int32_t i = 0; i < p->count; ++i) {
-    char where[64];
-    std::snprintf(where, sizeof(where), "smat_plan_set_params: tensor %d", i);
-    smat_status st = make_param(per_tensor[i], &recs[i], where);
-    if (st != SMAT_OK) return st;
+    // a per-step call over the whole list: the tensor's name for the message is formed only when
+    // its record is rejected, by checking it again
+    if (make_param(per_tensor[i], &recs[i], "") != SMAT_OK) {
+      char where[64];
+      std::snprintf(where, sizeof(where), "smat_plan_set_params: tensor %d", i);
+      return make_param(per_tensor[i], &recs[i], where);
+    }
     scales[i] = make_scale(per_tensor[i]);
   }
   const int slot = p->params_slot;
@@ -834,15 +837,20 @@ extern "C" smat_status smat_plan_set_grads(smat_plan* p, const void* const* grad
   for (int32_t i = 0; i < p->count; ++i) {
     TensorRec& r = recs[i];
     if (r.n == 0) continue;
-    char where[64];
-    std::snprintf(where, sizeof(where), "smat_plan_set_grads: tensor %d", i);
     const void* gs = grad_sims ? grad_sims[i] : r.grad_sim;
     float* gt = grad_thetas ? grad_thetas[i] : r.grad_theta;
-    if ((grad_sims && !gs) || (grad_thetas && !gt)) return fail(SMAT_ERR_INVALID, "%s: null gradient pointer", where);
-    smat_status st = check_grad_ptrs(r.theta, r.theta0, p->t0_dt, r.out, p->out_dt, gs, p->g_dt, gt,
-                                     p->adam_bound ? p->adam[i].exp_avg : nullptr,
-                                     p->adam_bound ? p->adam[i].exp_avg_sq : nullptr, r.n, where);
-    if (st != SMAT_OK) return st;
+    if ((grad_sims && !gs) || (grad_thetas && !gt))
+      return fail(SMAT_ERR_INVALID, "smat_plan_set_grads: tensor %d: null gradient pointer", i);
+    auto check = [&](const char* where) {
+      return check_grad_ptrs(r.theta, r.theta0, p->t0_dt, r.out, p->out_dt, gs, p->g_dt, gt,
+                             p->adam_bound ? p->adam[i].exp_avg : nullptr,
+                             p->adam_bound ? p->adam[i].exp_avg_sq : nullptr, r.n, where);
+    };
+    if (check("") != SMAT_OK) {  // the message names the tensor, formed only on failure
+      char where[64];
+      std::snprintf(where, sizeof(where), "smat_plan_set_grads: tensor %d", i);
+      return check(where);
+    }
     r.grad_sim = gs;
     r.grad_theta = gt;
     r.sflags &= ~(smat::kVecBwd | smat::kVecAdam | smat::kVecAdamAcc);
@@ -1314,10 +1322,11 @@ extern "C" smat_status smat_merge_multi(smat_merge_plan* p, const smat_merge_ter
   if (smat_status st = refuse_capture(stream, "smat_merge_multi"); st != SMAT_OK) return st;
   std::vector<MergeRec> recs(cells);
   for (size_t c = 0; c < cells; ++c) {
-    char where[80];
-    std::snprintf(where, sizeof(where), "smat_merge_multi: tensor %zu, expert %zu", c / p->nexp, c % p->nexp);
-    smat_status st = make_merge(terms[c], &recs[c], where);
-    if (st != SMAT_OK) return st;
+    if (make_merge(terms[c], &recs[c], "") != SMAT_OK) {  // the message names the cell, formed only on failure
+      char where[80];
+      std::snprintf(where, sizeof(where), "smat_merge_multi: tensor %zu, expert %zu", c / p->nexp, c % p->nexp);
+      return make_merge(terms[c], &recs[c], where);
+    }
   }
   const int slot = p->slot;
   if (p->terms_pending[slot]) SMAT_HIP(hipEventSynchronize(p->ev_terms[slot]));  // slot still being read

@@ -664,3 +664,25 @@ def test_device_calls_on_empty_lists_and_tensors():
             torch.cuda.synchronize()
         res[mode] = (out, gt)
     assert same_bits(res["dev"][0], res["host"][0]) and same_bits(res["dev"][1], res["host"][1])
+
+
+def test_rejected_records_name_their_tensor(mini):
+    cfg, inp = mini
+    th, t0, gs = list_tensors(inp)
+    out, gt = fresh(inp)
+    bad = base_params(cfg, inp, 1)
+    bad[4] = dict(bad[4], keep=1.5)
+    with smat.Plan(th, out, t0, gs, gt) as plan:
+        with pytest.raises(smat.SmatError, match="smat_plan_set_params: tensor 4: keep"):
+            plan.set_params(bad)
+        with pytest.raises(smat.SmatError, match="smat_plan_set_grads: tensor 2"):
+            plan.set_grads(grad_thetas=[x if i != 2 else th[2] for i, x in enumerate(gt)])   # over theta
+    t0s = [t.to(torch.bfloat16) for t in th[:3]]
+    outs = [torch.empty_like(t) for t in t0s]
+    experts = [[t.clone() for t in t0s] for _ in range(3)]
+    with smat.MergePlan(t0s, outs, experts) as m:
+        terms = [[dict(gamma=0.3, keep=1.0, seed=j) for j in range(3)] for _ in range(3)]
+        terms[1][2] = dict(gamma=0.3, keep=-1.0, seed=2)
+        with pytest.raises(smat.SmatError, match="smat_merge_multi: tensor 1, expert 2"):
+            m.merge(terms)
+    torch.cuda.synchronize()
