@@ -150,10 +150,11 @@ enum : uint32_t { kVecAdam = 4u, kVecAdamAcc = 8u };
 // so every load/store instruction of the wave covers one contiguous span and consecutive blocks
 // stream consecutive memory.  A tensor list is cut into chunks of kChunk elements; block b of a
 // list launch takes tile (b mod tiles-per-chunk) of chunk (b / tiles-per-chunk), which keeps
-// the chunk table small.  The simulate carries two Philox calls and Box-Muller per quad and
-// takes two quads per thread to overlap that work with its loads; the backward takes one.
+// the chunk table small.  The simulate, the backward and the fused optimizer step take one quad
+// per thread: each wave then keeps one 64-lane piece of every array in flight, the access shape
+// that streams fastest on MI355X.
 constexpr int kBlock = 64;
-constexpr int kSimQuads = 2;
+constexpr int kSimQuads = 1;
 constexpr int kBwdQuads = 1;
 constexpr int kAdamQuads = 1;
 constexpr int64_t kChunk = 16384;
@@ -166,6 +167,14 @@ static_assert(kChunk % tile_elems(kSimQuads) == 0 && kChunk % tile_elems(kBwdQua
 constexpr uint32_t kStreamMask = 0u;
 constexpr uint32_t kStreamNoise = 1u;
 constexpr uint32_t kStreamScale = 2u;  // the step's shared scale: group 0 of tensor id 0
+
+// Wave priority while a wave issues its loads.  The simulate's waves spend most of their issue
+// slots on random draws; a wave that has just started is raised above them until its loads are
+// issued, so the memory system receives each wave's requests as early as possible, and then drops
+// back to the normal level for its draws.  (s_setprio orders waves of one SIMD when several are
+// ready to issue; it does not change the stream's or the queue's priority.)
+__device__ __forceinline__ void raise_priority() { __builtin_amdgcn_s_setprio(2); }
+__device__ __forceinline__ void normal_priority() { __builtin_amdgcn_s_setprio(0); }
 
 // ---------------------------------------------------------------- Philox4x32-10
 struct Words {
@@ -267,6 +276,46 @@ __device__ __forceinline__ Words philox_tile(uint64_t p0, uint32_t hi, uint32_t 
     rk1[r] = k1 + (uint32_t)r * kPhiloxW1;
   }
   return philox_tile_rk(p0, hi, c2, c3, rk0, rk1);
+}
+
+// The mask and noise words of one group: counter words 0-2 are equal in the two streams and c3
+// differs (ca, cb).  The streams share round 1's per-lane product p0; round 2's first product
+// operand is wave-uniform as in philox_tile_rk, and its result word 2 depends on counter words
+// 0-2 only, so round 3's second product is also common to both streams.  Rounds 3-10 of the two
+// streams run interleaved, which gives the wave two independent chains of products to issue.
+__device__ __forceinline__ void philox_tile_pair(uint64_t p0, uint32_t hi, uint32_t c2, uint32_t ca, uint32_t cb,
+                                                 uint32_t k0, uint32_t k1, Words& A, Words& B) {
+  uint32_t rk0[10], rk1[10];
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    rk0[r] = k0 + (uint32_t)r * kPhiloxW0;
+    rk1[r] = k1 + (uint32_t)r * kPhiloxW1;
+  }
+  // round 1: only p0 depends on the lane; the streams differ in word 2 (through c3)
+  const uint64_t q1 = (uint64_t)c2 * kPhiloxM1;
+  const uint32_t a0 = (uint32_t)(q1 >> 32) ^ hi ^ rk0[0], a1 = (uint32_t)q1;
+  const uint32_t a2a = (uint32_t)(p0 >> 32) ^ (ca ^ rk1[0]), a2b = (uint32_t)(p0 >> 32) ^ (cb ^ rk1[0]);
+  const uint32_t a3 = (uint32_t)p0;
+  // round 2: a0 and a1 are uniform; words 2 and 3 of the result are common to the streams
+  const uint64_t r0 = (uint64_t)a0 * kPhiloxM0;
+  const uint64_t r1a = (uint64_t)a2a * kPhiloxM1, r1b = (uint64_t)a2b * kPhiloxM1;
+  const uint32_t xa = (uint32_t)(r1a >> 32) ^ (a1 ^ rk0[1]), xb = (uint32_t)(r1b >> 32) ^ (a1 ^ rk0[1]);
+  const uint32_t w2 = a3 ^ ((uint32_t)(r0 >> 32) ^ rk1[1]), w3 = (uint32_t)r0;
+  // round 3: the product of the common word 2 is formed once
+  const uint64_t s1 = (uint64_t)w2 * kPhiloxM1;
+  const uint64_t s0a = (uint64_t)xa * kPhiloxM0, s0b = (uint64_t)xb * kPhiloxM0;
+  uint32_t c0a = xor3((uint32_t)(s1 >> 32), (uint32_t)r1a, rk0[2]);
+  uint32_t c0b = xor3((uint32_t)(s1 >> 32), (uint32_t)r1b, rk0[2]);
+  uint32_t c2a = (uint32_t)(s0a >> 32) ^ (w3 ^ rk1[2]), c2b = (uint32_t)(s0b >> 32) ^ (w3 ^ rk1[2]);
+  uint32_t c1a = (uint32_t)s1, c1b = (uint32_t)s1;
+  uint32_t c3a = (uint32_t)s0a, c3b = (uint32_t)s0b;
+#pragma unroll
+  for (int r = 3; r < 10; ++r) {
+    philox_round((uint64_t)c0a * kPhiloxM0, c0a, c1a, c2a, c3a, rk0[r], rk1[r]);
+    philox_round((uint64_t)c0b * kPhiloxM0, c0b, c1b, c2b, c3b, rk0[r], rk1[r]);
+  }
+  A = {c0a, c1a, c2a, c3a};
+  B = {c0b, c1b, c2b, c3b};
 }
 
 __device__ __forceinline__ uint32_t pick(const Words& w, uint32_t lane) {

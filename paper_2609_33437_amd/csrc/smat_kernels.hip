@@ -9,9 +9,10 @@
 // stream per quad and never stores a draw.  Consecutive lanes take consecutive quads, so every
 // load/store instruction of a wave covers one contiguous span (16 B per lane for fp32, 8 B per
 // lane for bf16), issued as nontemporal streaming accesses.  Each one-wave block handles one
-// tile of one or two quads per thread, and consecutive blocks take consecutive tiles, so the blocks in
+// tile of one quad per thread, and consecutive blocks take consecutive tiles, so the blocks in
 // flight stream one contiguous window of each array (measured on MI355X: looping blocks over
-// strided chunks or persistent grid-stride loops lose 10-30 % of the bandwidth).  The
+// strided chunks or persistent grid-stride loops lose 10-30 % of the bandwidth, and two quads per
+// thread keep more of each array in flight than the memory system serves best).  The
 // ragged-list kernels find a block's (tensor, chunk) pair in a table built once per tensor
 // list, so huge matrices and tiny vectors share one launch.
 #include "smat_launch.h"
@@ -20,19 +21,20 @@
 namespace smat {
 
 // ---------------------------------------------------------------- simulate
-// One tile of `len` (<= 4 kBlock Q) elements starting at element `begin` of a tensor.  Thread x
-// owns quads x + u kBlock (u < Q) of the tile.
-template <typename T0, typename TO, int Q, int KIND>
-__device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
+// One tile of `len` (<= 4 kBlock) elements starting at element `begin` of a tensor; thread x owns
+// quad x of the tile.  MASK and NOISE say whether the tile draws the mask and the noise; they and
+// the noise form KIND are fixed per tensor and step, and each combination is its own
+// instantiation, so a block runs only the code of its tensor's case.  The calling kernel raises
+// the wave's priority at entry; the tile drops it as soon as its loads are issued.
+template <typename T0, typename TO, int KIND, bool MASK, bool NOISE>
+__device__ __forceinline__ void simulate_tile_case(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
   const uint32_t cnoise = (step << 2) | kStreamNoise;
   const uint32_t tensor_id = T.tensor_id;
   const uint32_t len = T.len;
-  const uint32_t flags = P.flags;
-  const bool use_mask = (flags & kFlagMask) != 0;
-  const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
-  const bool use_noise = (flags & kFlagNoise) != 0;
+  // without a mask draw every coordinate is kept, or (keep = 0) every one dropped
+  const bool all_kept = (P.flags & kFlagDropAll) == 0;
   const float t = P.t, sigma = P.sigma;
   const uint32_t thr = P.thr;
 
@@ -41,91 +43,95 @@ __device__ __forceinline__ void simulate_tile_kind(const Tile& T, const ParamRec
   void* out = T.out;
   const uint64_t e0 = T.e0;
 
-  // element by element: ragged tails and tensors whose pointers or offset break quad alignment
-  auto one = [&](uint32_t i) {
-    const uint64_t e = e0 + i;
-    const uint64_t g = e >> 2;
-    const uint32_t lane = (uint32_t)e & 3u;
-    bool kept = all_kept;
-    if (use_mask) kept = pick(group_words(g, tensor_id, cmask, k0, k1), lane) < thr;
-    float y = sim_value(QuadIO<float>::load1(th, i), QuadIO<T0>::load1(t0, i), kept, t);
-    if (use_noise) y = __builtin_fmaf(sigma, lane_noise<KIND>(group_words(g, tensor_id, cnoise, k0, k1), lane), y);
-    QuadIO<TO>::store1(out, i, y);
-  };
-
-  if (!(T.sflags & kVecSim) || groups_wrap(e0, Q * kBlock)) {
-#pragma unroll
-    for (int u = 0; u < Q; ++u) {
-      const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
-      for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) one(i);
+  // element by element: tensors whose pointers or offset break quad alignment, and the tile that
+  // holds a tensor's last 1-3 elements
+  if (!(T.sflags & kVecSim) || (len & 3u) || groups_wrap(e0, kBlock)) {
+    normal_priority();
+    const uint32_t i0 = threadIdx.x * 4u;
+    for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) {
+      const uint64_t e = e0 + i;
+      const uint64_t g = e >> 2;
+      const uint32_t lane = (uint32_t)e & 3u;
+      bool kept = all_kept;
+      if (MASK) kept = pick(group_words(g, tensor_id, cmask, k0, k1), lane) < thr;
+      float y = sim_value(QuadIO<float>::load1(th, i), QuadIO<T0>::load1(t0, i), kept, t);
+      if (NOISE) y = __builtin_fmaf(sigma, lane_noise<KIND>(group_words(g, tensor_id, cnoise, k0, k1), lane), y);
+      QuadIO<TO>::store1(out, i, y);
     }
     return;
   }
-  // whole quads: each is one Philox group, since e0 is a multiple of 4 on this path.  The mask and
-  // noise streams of a group share round 1's product.
-  // Phase 1 issues every load (indices clamped into the tile, so no branch guards them), phase 2
-  // draws the mask and noise while the loads are in flight, phase 3 combines and stores.
+  // whole quads: each is one Philox group, since e0 is a multiple of 4 on this path.  The loads
+  // are issued first, the draws run while they are in flight, and a scheduling barrier keeps the
+  // first use of the loaded data after the draws.  A lane past the end of the tile works on the
+  // tile's last quad (loads, draws and all), so it stores the very bytes that quad's own lane
+  // stores, to the same place, and no branch splits the phases.
   const uint32_t nq = len >> 2;
-  if (nq > 0) {
-    typename QuadIO<float>::Raw ra[Q];
-    typename QuadIO<T0>::Raw rb[Q];
-#pragma unroll
-    for (int u = 0; u < Q; ++u) {
-      const uint32_t q = u * kBlock + threadIdx.x;
-      const uint32_t qc = q < nq ? q : nq - 1;
-      ra[u] = QuadIO<float>::load_raw(th, qc);
-      rb[u] = QuadIO<T0>::load_raw(t0, qc);
-    }
-    bool kept[Q][4];
-    float z[Q][4];
-    const TileGroups G = tile_groups(e0);
-#pragma unroll
-    for (int u = 0; u < Q; ++u) {
-      const uint64_t p0 = philox_p0(G.lo + u * kBlock + threadIdx.x);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
-      if (use_mask) {
-        const Words w = philox_tile(p0, G.hi, tensor_id, cmask, k0, k1);
-        kept[u][0] = w.w0 < thr;
-        kept[u][1] = w.w1 < thr;
-        kept[u][2] = w.w2 < thr;
-        kept[u][3] = w.w3 < thr;
-      }
-      if (use_noise) quad_noise<KIND>(philox_tile(p0, G.hi, tensor_id, cnoise, k0, k1), z[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < Q; ++u) {
-      const uint32_t q = u * kBlock + threadIdx.x;
-      if (q < nq) {
-        float a[4], b[4], y[4];
-        QuadIO<float>::unpack(ra[u], a);
-        QuadIO<T0>::unpack(rb[u], b);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) y[j] = sim_value(a[j], b[j], kept[u][j], t);
-        if (use_noise) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) y[j] = __builtin_fmaf(sigma, z[u][j], y[j]);
-        }
-        QuadIO<TO>::store(out, q, y);
-      }
-    }
+  const uint32_t q = threadIdx.x < nq ? threadIdx.x : nq - 1;
+  const typename QuadIO<float>::Raw ra = QuadIO<float>::load_raw(th, q);
+  const typename QuadIO<T0>::Raw rb = QuadIO<T0>::load_raw(t0, q);
+  normal_priority();
+  const TileGroups G = tile_groups(e0);
+  const uint64_t p0 = philox_p0(G.lo + q);
+  bool kept[4] = {all_kept, all_kept, all_kept, all_kept};
+  float z[4];
+  if (MASK && NOISE) {
+    Words wm, wn;
+    philox_tile_pair(p0, G.hi, tensor_id, cmask, cnoise, k0, k1, wm, wn);
+    kept[0] = wm.w0 < thr;
+    kept[1] = wm.w1 < thr;
+    kept[2] = wm.w2 < thr;
+    kept[3] = wm.w3 < thr;
+    quad_noise<KIND>(wn, z);
+  } else if (MASK) {
+    const Words w = philox_tile(p0, G.hi, tensor_id, cmask, k0, k1);
+    kept[0] = w.w0 < thr;
+    kept[1] = w.w1 < thr;
+    kept[2] = w.w2 < thr;
+    kept[3] = w.w3 < thr;
+  } else if (NOISE) {
+    quad_noise<KIND>(philox_tile(p0, G.hi, tensor_id, cnoise, k0, k1), z);
   }
-  // the last 1-3 elements of a tensor whose size is not a multiple of 4
-  if ((len & 3u) && threadIdx.x == (nq & (kBlock - 1))) {
-    for (uint32_t i = nq * 4u; i < len; ++i) one(i);
+  __builtin_amdgcn_sched_barrier(0);
+  float a[4], b[4], y[4];
+  QuadIO<float>::unpack(ra, a);
+  QuadIO<T0>::unpack(rb, b);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) y[j] = sim_value(a[j], b[j], kept[j], t);
+  if (NOISE) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) y[j] = __builtin_fmaf(sigma, z[j], y[j]);
   }
+  QuadIO<TO>::store(out, q, y);
 }
 
-// The noise kind is fixed per tensor and step; dispatching on it once per block keeps the
-// compiler from computing both noise forms and selecting between them.
-template <typename T0, typename TO, int Q>
+// Dispatch on the tensor's flags once per block: mask or not, and no noise or one of the three noise
+// forms (eight instantiations), so that no block computes a draw it discards or selects between
+// noise forms per element.
+template <typename T0, typename TO>
 __device__ __forceinline__ void simulate_tile(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
-  if (P.flags & kFlagUniform)
-    simulate_tile_kind<T0, TO, Q, kUniform>(T, P, seed, step);
-  else if (P.flags & kFlagLaplace)
-    simulate_tile_kind<T0, TO, Q, kLaplace>(T, P, seed, step);
-  else
-    simulate_tile_kind<T0, TO, Q, kGaussian>(T, P, seed, step);
+  const uint32_t f = P.flags;
+  const bool mask = (f & kFlagMask) != 0;
+  if (!(f & kFlagNoise)) {
+    if (mask)
+      simulate_tile_case<T0, TO, kGaussian, true, false>(T, P, seed, step);
+    else
+      simulate_tile_case<T0, TO, kGaussian, false, false>(T, P, seed, step);
+  } else if (f & kFlagUniform) {
+    if (mask)
+      simulate_tile_case<T0, TO, kUniform, true, true>(T, P, seed, step);
+    else
+      simulate_tile_case<T0, TO, kUniform, false, true>(T, P, seed, step);
+  } else if (f & kFlagLaplace) {
+    if (mask)
+      simulate_tile_case<T0, TO, kLaplace, true, true>(T, P, seed, step);
+    else
+      simulate_tile_case<T0, TO, kLaplace, false, true>(T, P, seed, step);
+  } else {
+    if (mask)
+      simulate_tile_case<T0, TO, kGaussian, true, true>(T, P, seed, step);
+    else
+      simulate_tile_case<T0, TO, kGaussian, false, true>(T, P, seed, step);
+  }
 }
 
 // ---------------------------------------------------------------- backward
@@ -218,8 +224,9 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
 // ---------------------------------------------------------------- kernels
 template <typename T0, typename TO>
 __global__ __launch_bounds__(kBlock) void k_simulate_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step) {
+  raise_priority();
   constexpr int64_t tile = tile_elems(kSimQuads);
-  simulate_tile<T0, TO, kSimQuads>(tensor_tile<T0, TO>(R, (int64_t)blockIdx.x * tile, tile), P, seed, step);
+  simulate_tile<T0, TO>(tensor_tile<T0, TO>(R, (int64_t)blockIdx.x * tile, tile), P, seed, step);
 }
 
 template <typename TG>
@@ -238,12 +245,13 @@ __global__ __launch_bounds__(kBlock) void k_simulate_multi(const TensorRec* __re
                                                            const ParamRec* __restrict__ prms,
                                                            const uint2* __restrict__ chunks, uint64_t seed,
                                                            uint32_t step) {
+  raise_priority();
   constexpr int64_t tile = tile_elems(kSimQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
   const Tile T = list_tile<T0, TO, float>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;  // unused tile of a tensor's last chunk
-  simulate_tile<T0, TO, kSimQuads>(T, prms[ch.x], seed, step);
+  simulate_tile<T0, TO>(T, prms[ch.x], seed, step);
 }
 
 template <typename TG, bool ACC>
@@ -268,6 +276,7 @@ __global__ __launch_bounds__(kBlock) void k_simulate_multi_dev(const TensorRec* 
                                                                const ScaleRec* __restrict__ scales,
                                                                const uint2* __restrict__ chunks,
                                                                const StepState* __restrict__ state) {
+  raise_priority();
   constexpr int64_t tile = tile_elems(kSimQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
@@ -276,7 +285,7 @@ __global__ __launch_bounds__(kBlock) void k_simulate_multi_dev(const TensorRec* 
   const StepState S = *state;
   ParamRec P = prms[ch.x];
   P.t = device_coefficient(S.scale, scales[ch.x]);
-  simulate_tile<T0, TO, kSimQuads>(T, P, S.seed, S.step);
+  simulate_tile<T0, TO>(T, P, S.seed, S.step);
 }
 
 template <typename TG, bool ACC>

@@ -115,7 +115,7 @@ def _list_plan(count, bufs):
 
 
 def test_list_of_two_million_tensors():
-    count = 2_200_000                                   # 2.2M chunks: 2 simulate, 3 backward launches
+    count = 2_200_000                                   # 2.2M chunks: 3 simulate and 3 backward launches
     gen = torch.Generator(DEV).manual_seed(6)
     n = 4 * count
     th = torch.randn(n, device=DEV, generator=gen) * 0.02
@@ -142,7 +142,7 @@ def test_list_of_two_million_tensors():
     ref = float((gt.double() ** 2).sum())
     assert abs(sumsq.item() - ref) <= 1e-5 * ref
     p = dict(s=float(np.float32(0.7)), keep=float(np.float32(0.4)), sigma=float(np.float32(1e-4)), rescale=1)
-    sim_cut, bwd_cut = MAX_BLOCKS // 32, MAX_BLOCKS // 64      # chunks per simulate / backward launch
+    sim_cut, bwd_cut = MAX_BLOCKS // 64, MAX_BLOCKS // 64      # chunks per simulate / backward launch
     picks = sorted(set(list(range(0, 40)) + list(range(sim_cut - 40, sim_cut + 40)) +
                        list(range(bwd_cut - 40, bwd_cut + 40)) + list(range(2 * bwd_cut - 40, 2 * bwd_cut + 40)) +
                        list(range(count - 40, count))))
