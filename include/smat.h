@@ -241,6 +241,25 @@ smat_status smat_plan_set_params(smat_plan* plan, const smat_op_params* per_tens
  * storage active), SMAT_ERR_HIP. */
 smat_status smat_simulate_multi(smat_plan* plan, uint64_t seed, uint32_t step, hipStream_t stream);
 
+/* smat_simulate_multi_static -- for callers that cannot allocate device memory (serving loops,
+ * harnesses that forbid allocation): smat_simulate_multi over the list `descs` without a plan.
+ * Same validation as smat_plan_create (resident mode; grad pointers are not read) and
+ * smat_plan_set_params (per_tensor[i] for descs[i]), the same kernels and the same output bits.
+ * The tensor records, per-tensor constants and chunk table live in one static device array of the
+ * library, 8 MiB per GPU, held until the process ends: at most 8192 tensors, and at most
+ * (8 MiB - the records) / 8 chunks of 16384 elements (about 15.8e9 elements at 8192 tensors, 17e9
+ * for a few hundred).  The call allocates nothing; it builds the tables in static host memory and
+ * copies them with one synchronous host-to-device copy ordered on `stream` (so it blocks until
+ * earlier work on `stream` has finished), then enqueues the kernel.  Every call on a GPU reuses
+ * that GPU's array: calls on different streams of one GPU that overlap in time race (the later
+ * upload may overwrite tables the earlier kernel still reads); calls on one stream are ordered.
+ * Not capturable (SMAT_ERR_STATE under stream capture).
+ * Errors: SMAT_ERR_INVALID (bad descriptor or params, aliasing, duplicate ranges, a list beyond the
+ * limits above), SMAT_ERR_DTYPE, SMAT_ERR_STATE, SMAT_ERR_HIP. */
+smat_status smat_simulate_multi_static(const smat_tensor_desc* descs, int32_t count, smat_dtype theta0_dtype,
+                                       smat_dtype out_dtype, const smat_op_params* per_tensor, uint64_t seed,
+                                       uint32_t step, hipStream_t stream);
+
 /* smat_backward_multi -- the gradient through the simulation over every tensor of the plan in one
  * launch (Sec. 4.2, Eq. smat-gradient, weighted by lambda).  accumulate = 1: grad_theta += lambda t m
  * (.) grad_sim on kept coordinates, dropped ones bit-unchanged (smat_backward_accum_multi).

@@ -32,7 +32,7 @@ EXPORTS = (
     "smat_merge_multi", "smat_merge_plan_destroy", "smat_plan_set_grads",
     "smat_stream_copy", "smat_backward_multi", "smat_plan_clear_grads", "smat_simulate_multi_dev",
     "smat_backward_multi_dev", "smat_adamw_fused_multi_dev", "smat_grad_norm_multi_dev", "smat_step_state_advance",
-    "smat_scale_draw",
+    "smat_scale_draw", "smat_simulate_multi_static",
 )
 
 
@@ -131,6 +131,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "smat_grad_norm_multi_dev": [P, P, c_float, c_int32, c_float, P, P, P],
         "smat_step_state_advance": [P, c_uint32, c_float, P],
         "smat_scale_draw": [c_uint64, c_uint32, c_float, POINTER(c_float)],
+        "smat_simulate_multi_static": [POINTER(smat_tensor_desc), c_int32, c_int32, c_int32, POINTER(smat_op_params),
+                                       c_uint64, c_uint32, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)

@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -373,11 +374,11 @@ void add_span(std::vector<Span>& s, const void* ptr, size_t bytes, bool written,
 // another; read-only arrays may share memory.  Sorted by start, an array overlaps an earlier one
 // exactly when it starts before the furthest end seen so far (among written arrays, for a read-only
 // one), so one sweep finds any conflict.
-smat_status check_spans(std::vector<Span>& s, const char* where) {
-  std::sort(s.begin(), s.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
+smat_status check_spans(Span* s, size_t count, const char* where) {
+  std::sort(s, s + count, [](const Span& a, const Span& b) { return a.lo < b.lo; });
   uintptr_t end_any = 0, end_written = 0;
   size_t i_any = 0, i_written = 0;
-  for (size_t k = 0; k < s.size(); ++k) {
+  for (size_t k = 0; k < count; ++k) {
     const Span& x = s[k];
     const bool hit = x.written ? end_any > x.lo : end_written > x.lo;
     if (hit) {
@@ -412,7 +413,7 @@ smat_status check_plan_spans(const smat_plan* p, const std::vector<TensorRec>& r
       add_span(s, (*adam)[i].exp_avg_sq, n * 4, true, i, "exp_avg_sq");
     }
   }
-  return check_spans(s, where);
+  return check_spans(s.data(), s.size(), where);
 }
 
 smat_status release(smat_plan* p) {
@@ -1051,6 +1052,126 @@ extern "C" smat_status smat_plan_destroy(smat_plan* p) {
   return release(p);
 }
 
+// ------------------------------------------------------------------ list simulate without allocation
+// smat_simulate_multi_static: the list simulate of a plan, for callers that cannot allocate device
+// memory.  The tensor records, per-tensor constants and chunk table that a plan keeps in its
+// workspace are built on the host in static memory and uploaded into `scratch`, a static device
+// array of the library (each GPU holds its own copy until the process ends).  Host code never uses
+// the array's name as an address: each device's address comes from hipGetSymbolAddress, taken once
+// per device with that device current.
+namespace {
+constexpr size_t kScratchBytes = size_t(8) << 20;
+constexpr int32_t kScratchMaxTensors = 8192;
+constexpr int kMaxDevices = 64;
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;                    // guards the host tables and the address cache
+void* g_scratch_dev[kMaxDevices] = {};      // per-device address of `scratch`
+alignas(256) unsigned char g_scratch_host[kScratchBytes];  // host image of the tables
+Span g_scratch_spans[3 * kScratchMaxTensors];
+std::pair<uint32_t, std::pair<uint64_t, uint64_t>> g_scratch_ranges[kScratchMaxTensors];
+
+// The current device's address of `scratch` (called with g_scratch_mu held).
+smat_status scratch_address(void** out) {
+  int dev = 0;
+  SMAT_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(SMAT_ERR_INVALID, "smat_simulate_multi_static: device %d beyond the %d the library tracks", dev,
+                kMaxDevices);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    SMAT_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(SMAT_ERR_HIP, "smat_simulate_multi_static: no device address for the static tables");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return SMAT_OK;
+}
+}  // namespace
+
+extern "C" smat_status smat_simulate_multi_static(const smat_tensor_desc* descs, int32_t count, smat_dtype theta0_dtype,
+                                                  smat_dtype out_dtype, const smat_op_params* per_tensor,
+                                                  uint64_t seed, uint32_t step, hipStream_t stream) {
+  const char* where0 = "smat_simulate_multi_static";
+  if (!valid_dtype(theta0_dtype) || !valid_dtype(out_dtype)) return fail(SMAT_ERR_DTYPE, "%s: unsupported dtype", where0);
+  if (count < 0 || (count > 0 && (!descs || !per_tensor))) return fail(SMAT_ERR_INVALID, "%s: bad tensor list", where0);
+  if (count > kScratchMaxTensors)
+    return fail(SMAT_ERR_INVALID, "%s: %d tensors, the static tables hold at most %d (use a plan)", where0, count,
+                kScratchMaxTensors);
+  if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "%s: step must be < 2^30", where0);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  const size_t off_prms = align256(sizeof(TensorRec) * (size_t)count);
+  const size_t off_chunks = off_prms + align256(sizeof(ParamRec) * (size_t)count);
+  TensorRec* recs = reinterpret_cast<TensorRec*>(g_scratch_host);
+  ParamRec* prms = reinterpret_cast<ParamRec*>(g_scratch_host + off_prms);
+  uint2* chunks = reinterpret_cast<uint2*>(g_scratch_host + off_chunks);
+  const size_t max_chunks = (kScratchBytes - off_chunks) / sizeof(uint2);
+  size_t nchunks = 0, nspans = 0, nranges = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const smat_tensor_desc& d = descs[i];
+    char where[80];
+    std::snprintf(where, sizeof(where), "%s: tensor %d", where0, i);
+    if (d.n < 0 || d.reserved != 0) return fail(SMAT_ERR_INVALID, "%s: n < 0 or reserved != 0", where);
+    if (d.elem_offset > UINT64_MAX - (uint64_t)d.n) return fail(SMAT_ERR_INVALID, "%s: elem_offset + n overflows", where);
+    if (d.theta0_host) return fail(SMAT_ERR_INVALID, "%s: theta0_host is for offload plans only", where);
+    smat_status st = make_param(per_tensor[i], &prms[i], where);
+    if (st != SMAT_OK) return st;
+    TensorRec& r = recs[i];
+    r = TensorRec{};
+    r.theta = d.theta;
+    r.theta0 = d.theta0;
+    r.out = d.out;
+    r.n = d.n;
+    r.elem_offset = d.elem_offset;
+    r.tensor_id = d.tensor_id;
+    if (d.n == 0) continue;
+    st = check_simulate_ptrs(d.theta, d.theta0, theta0_dtype, d.out, out_dtype, d.n, where);
+    if (st != SMAT_OK) return st;
+    r.sflags = sim_flags(d.theta, d.theta0, theta0_dtype, d.out, out_dtype, d.elem_offset);
+    const size_t n = (size_t)d.n;
+    g_scratch_spans[nspans++] = Span{reinterpret_cast<uintptr_t>(d.theta), reinterpret_cast<uintptr_t>(d.theta) + n * 4,
+                                     false, i, "theta"};
+    g_scratch_spans[nspans++] = Span{reinterpret_cast<uintptr_t>(d.out),
+                                     reinterpret_cast<uintptr_t>(d.out) + n * dtype_bytes(out_dtype), true, i,
+                                     "the buffer"};
+    if (d.theta0 != d.out)
+      g_scratch_spans[nspans++] = Span{reinterpret_cast<uintptr_t>(d.theta0),
+                                       reinterpret_cast<uintptr_t>(d.theta0) + n * dtype_bytes(theta0_dtype), false, i,
+                                       "theta0"};
+    g_scratch_ranges[nranges++] = {d.tensor_id, {d.elem_offset, d.elem_offset + (uint64_t)d.n}};
+    const uint64_t nc = (uint64_t)((d.n + smat::kChunk - 1) / smat::kChunk);
+    if (nchunks + nc > max_chunks)
+      return fail(SMAT_ERR_INVALID, "%s: the list needs more than the %zu chunks of %lld elements that the %zu-byte "
+                  "static tables hold for %d tensors (use a plan)", where0, max_chunks, (long long)smat::kChunk,
+                  kScratchBytes, count);
+    for (uint64_t c = 0; c < nc; ++c) chunks[nchunks++] = make_uint2((uint32_t)i, (uint32_t)c);
+  }
+  std::sort(g_scratch_ranges, g_scratch_ranges + nranges);
+  for (size_t i = 1; i < nranges; ++i)
+    if (g_scratch_ranges[i].first == g_scratch_ranges[i - 1].first &&
+        g_scratch_ranges[i].second.first < g_scratch_ranges[i - 1].second.second)
+      return fail(SMAT_ERR_INVALID, "%s: tensor_id %u given twice for overlapping elements", where0,
+                  g_scratch_ranges[i].first);
+  if (smat_status st = check_spans(g_scratch_spans, nspans, where0); st != SMAT_OK) return st;
+  if (nchunks == 0) return SMAT_OK;
+  if (smat_status st = refuse_capture(stream, where0); st != SMAT_OK) return st;
+  void* dev = nullptr;
+  if (smat_status st = scratch_address(&dev); st != SMAT_OK) return st;
+  // a copy from pageable host memory runs synchronously (HIP's documented behaviour), so the host
+  // image is free for the next call once this returns; stream order puts the upload after any
+  // earlier launch on `stream` that reads the device tables
+  SMAT_HIP(hipMemcpyAsync(dev, g_scratch_host, off_chunks + sizeof(uint2) * nchunks, hipMemcpyHostToDevice, stream));
+  char* base = static_cast<char*>(dev);
+  SMAT_HIP(smat::launch_simulate_multi(reinterpret_cast<const TensorRec*>(base),
+                                       reinterpret_cast<const ParamRec*>(base + off_prms),
+                                       reinterpret_cast<const uint2*>(base + off_chunks), (uint32_t)nchunks,
+                                       theta0_dtype, out_dtype, seed, step, stream));
+  return SMAT_OK;
+}
+
 // ------------------------------------------------------------------ reference copy
 extern "C" smat_status smat_stream_copy(const void* src, void* dst, uint64_t bytes, hipStream_t stream) {
   if (bytes == 0) return SMAT_OK;
@@ -1238,7 +1359,7 @@ extern "C" smat_status smat_merge_plan_create(const smat_merge_desc* descs, int3
     for (int j = 0; j < n_experts; ++j)
       add_span(spans, experts[(size_t)i * n_experts + j], n * dtype_bytes(expert_dtype), false, i, "an expert");
   }
-  if (smat_status st = check_spans(spans, "smat_merge_plan_create"); st != SMAT_OK) return st;
+  if (smat_status st = check_spans(spans.data(), spans.size(), "smat_merge_plan_create"); st != SMAT_OK) return st;
 
   smat_merge_plan* p = new smat_merge_plan();
   p->count = count;
