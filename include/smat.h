@@ -230,15 +230,21 @@ smat_status smat_plan_workspace_bytes(const smat_plan* plan, size_t* bytes);
 smat_status smat_plan_bind_workspace(smat_plan* plan, void* workspace, size_t bytes, hipStream_t stream);
 
 /* smat_plan_set_params -- per-tensor s, keep, sigma for the next operations (count entries, in
- * descriptor order), uploaded asynchronously on `stream`.  The backward of a step must see the
- * same keep values as its simulate.  Errors: SMAT_ERR_INVALID, SMAT_ERR_STATE (no workspace),
- * SMAT_ERR_HIP. */
+ * descriptor order), uploaded asynchronously on `stream`.  Only the records that differ from the
+ * ones the workspace holds are copied (the span from the first changed record to the last one);
+ * a call that changes nothing enqueues nothing.  The backward of a step must see the same keep
+ * values as its simulate.  A call that fails with SMAT_ERR_HIP leaves the plan without
+ * parameters until a later call succeeds.  Errors: SMAT_ERR_INVALID, SMAT_ERR_STATE (no
+ * workspace), SMAT_ERR_HIP. */
 smat_status smat_plan_set_params(smat_plan* plan, const smat_op_params* per_tensor, hipStream_t stream);
 
 /* smat_simulate_multi -- smat_simulate over every tensor of the plan in one launch, keys
  * (seed, step, desc.tensor_id, desc.elem_offset).  Allowed only while the expert storage is
- * active.  Errors: SMAT_ERR_INVALID (step), SMAT_ERR_STATE (no workspace, no params, simulated
- * storage active), SMAT_ERR_HIP. */
+ * active.  In offload mode the simulate writes theta~ over the buffer, the device's only copy of
+ * theta0, so a second simulate needs a restore in between (a switch to the simulated storage and
+ * back, whose restore refills theta0).  Errors: SMAT_ERR_INVALID (step), SMAT_ERR_STATE (no
+ * workspace, no params, simulated storage active, offload buffers not refilled since the last
+ * simulate), SMAT_ERR_HIP. */
 smat_status smat_simulate_multi(smat_plan* plan, uint64_t seed, uint32_t step, hipStream_t stream);
 
 /* smat_simulate_multi_static -- for callers that cannot allocate device memory (serving loops,
@@ -294,7 +300,9 @@ typedef struct smat_step_state {
   float scale;
 } smat_step_state;
 
-/* smat_step_state_advance -- step += increment (modulo 2^32), then scale = the step's shared scale
+/* smat_step_state_advance -- step += increment (modulo 2^30, the range of steps that the counter
+ * word holds: a device-driven run past step 2^30 - 1 continues at step 0 and repeats its draws,
+ * and a state written with a step >= 2^30 is taken modulo 2^30), then scale = the step's shared scale
  * alpha ~ U[alpha_min, 1] (Sec. 4.1, "Scale": one coefficient per simulated update, shared by every
  * coordinate), written in place by one thread on `stream`.  alpha comes from word 0 of the Philox
  * counter (0, 0, 0, 4 step + 2) under key seed (stream 2, which no tensor uses):
@@ -307,7 +315,7 @@ smat_status smat_step_state_advance(smat_step_state* state, uint32_t increment, 
 
 /* smat_scale_draw -- the same scale on the host, for the host-driven calls: *alpha = the scale that
  * smat_step_state_advance draws for (seed, step, alpha_min), bit for bit.  Host only (no GPU, no
- * stream).  Errors: SMAT_ERR_INVALID (null alpha, alpha_min outside [0, 1]). */
+ * stream).  Errors: SMAT_ERR_INVALID (null alpha, step >= 2^30, alpha_min outside [0, 1]). */
 smat_status smat_scale_draw(uint64_t seed, uint32_t step, float alpha_min, float* alpha);
 
 /* smat_simulate_multi_dev / smat_backward_multi_dev -- smat_simulate_multi and smat_backward_multi

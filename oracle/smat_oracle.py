@@ -523,6 +523,10 @@ class StorageSwitch:
     def simulate(self, out: Sequence) -> None:
         if self.state != EXPERT:
             raise StateError("simulate while the simulated storage is active")
+        if self.offload and self.fresh:
+            # the buffer is the device's only copy of the base in offload mode and the simulate
+            # writes theta~ over it: the base is back only after the next restore
+            raise StateError("offload mode: the buffer holds theta~ until the next restore refills theta0")
         self.buffer = [np.array(x, copy=True) for x in out]
         self.fresh = True
 

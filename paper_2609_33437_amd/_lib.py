@@ -201,9 +201,10 @@ def _scalar_ptr(t, what: str, dtype: str):
 def scale_draw(seed: int, step: int, alpha_min: float) -> float:
     """The step's shared scale alpha ~ U[alpha_min, 1] as a function of (seed, step): the value
     smat_step_state_advance writes on the GPU, computed on the host (smat_scale_draw)."""
+    if not (0 <= int(seed) < 2 ** 64 and 0 <= int(step) < 2 ** 32):
+        raise SmatError(SMAT_ERR_INVALID, "seed must fit 64 bits and step 32 bits (the library takes steps < 2^30)")
     out = c_float()
-    _check(lib().smat_scale_draw(int(seed) & 0xFFFFFFFFFFFFFFFF, int(step) & 0xFFFFFFFF, float(alpha_min),
-                                 ctypes.byref(out)))
+    _check(lib().smat_scale_draw(int(seed), int(step), float(alpha_min), ctypes.byref(out)))
     return out.value
 
 

@@ -339,6 +339,10 @@ struct smat_plan {
   bool params_pending[2] = {false, false};
   int params_slot = 0;
   bool params_set = false;
+  // the records the workspace holds since the last upload: set_params copies only the span from the
+  // first record that changed to the last one, or nothing
+  std::vector<ParamRec> dev_params;
+  std::vector<ScaleRec> dev_scales;
 
   int32_t state = SMAT_EXPERT;
   bool fresh = false;  // the buffers hold theta~ of a simulate issued since the last restore
@@ -636,18 +640,42 @@ extern "C" smat_status smat_plan_set_params(smat_plan* p, const smat_op_params* 
     }
     scales[i] = make_scale(per_tensor[i]);
   }
-  const int slot = p->params_slot;
-  if (p->params_pending[slot]) SMAT_HIP(hipEventSynchronize(p->ev_params[slot]));  // slot still being read
-  // params and scale records are adjacent in the workspace: one upload carries both
+  // records in the workspace: [params x count][scale records x count]; the first and last index
+  // (over that concatenation) whose record differs from what the workspace holds
   const size_t prm_bytes = sizeof(ParamRec) * p->count;
-  std::memcpy(p->params_staging[slot], recs.data(), prm_bytes);
-  std::memcpy(p->params_staging[slot] + prm_bytes, scales.data(), sizeof(ScaleRec) * p->count);
-  if (p->count > 0)
-    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_params, p->params_staging[slot], prm_bytes + sizeof(ScaleRec) * p->count,
+  size_t first = 2 * (size_t)p->count, last = 0;
+  if (!p->params_set) {
+    first = 0;
+    last = 2 * (size_t)p->count;
+  } else {
+    for (int32_t i = 0; i < p->count; ++i)
+      if (std::memcmp(&recs[i], &p->dev_params[i], sizeof(ParamRec)) != 0) {
+        first = std::min(first, (size_t)i);
+        last = std::max(last, (size_t)i + 1);
+      }
+    for (int32_t i = 0; i < p->count; ++i)
+      if (std::memcmp(&scales[i], &p->dev_scales[i], sizeof(ScaleRec)) != 0) {
+        first = std::min(first, (size_t)p->count + i);
+        last = std::max(last, (size_t)p->count + i + 1);
+      }
+  }
+  if (first < last) {
+    const int slot = p->params_slot;
+    if (p->params_pending[slot]) SMAT_HIP(hipEventSynchronize(p->ev_params[slot]));  // slot still being read
+    // params and scale records are adjacent in the workspace: one upload carries the changed span
+    std::memcpy(p->params_staging[slot], recs.data(), prm_bytes);
+    std::memcpy(p->params_staging[slot] + prm_bytes, scales.data(), sizeof(ScaleRec) * p->count);
+    static_assert(sizeof(ParamRec) == sizeof(ScaleRec), "one record size indexes both arrays");
+    const size_t lo = first * sizeof(ParamRec), hi = last * sizeof(ParamRec);
+    p->params_set = false;  // until the upload is enqueued: a failed one leaves the plan without params
+    SMAT_HIP(hipMemcpyAsync(p->ws + p->off_params + lo, p->params_staging[slot] + lo, hi - lo,
                             hipMemcpyHostToDevice, stream));
-  SMAT_HIP(hipEventRecord(p->ev_params[slot], stream));
-  p->params_pending[slot] = true;
-  p->params_slot = slot ^ 1;
+    SMAT_HIP(hipEventRecord(p->ev_params[slot], stream));
+    p->params_pending[slot] = true;
+    p->params_slot = slot ^ 1;
+    p->dev_params = recs;
+    p->dev_scales = scales;
+  }
   p->params_set = true;
   return SMAT_OK;
 }
@@ -659,6 +687,11 @@ extern "C" smat_status smat_simulate_multi(smat_plan* p, uint64_t seed, uint32_t
   if (!p->params_set) return fail(SMAT_ERR_STATE, "smat_simulate_multi: parameters never set");
   if (p->state != SMAT_EXPERT)
     return fail(SMAT_ERR_STATE, "smat_simulate_multi: the simulated storage is active (restore the expert first)");
+  // offload mode runs in place over the buffer, the device's only copy of theta0: after a simulate
+  // it holds theta~ until a restore refills it
+  if (p->offload && p->fresh)
+    return fail(SMAT_ERR_STATE, "smat_simulate_multi: offload mode: the buffers hold theta~ of the last simulate; "
+                "switch to the simulated storage and back (the restore refills theta0) before simulating again");
   if (p->offload && p->prefetch_pending) SMAT_HIP(hipStreamWaitEvent(stream, p->ev_prefetch, 0));
   if (!p->chunks.empty())
     SMAT_HIP(smat::launch_simulate_multi(reinterpret_cast<const TensorRec*>(p->ws + p->off_recs),
@@ -733,6 +766,7 @@ float host_scale(uint64_t seed, uint32_t step, float alpha_min) {
 
 extern "C" smat_status smat_scale_draw(uint64_t seed, uint32_t step, float alpha_min, float* alpha) {
   if (!alpha) return fail(SMAT_ERR_INVALID, "smat_scale_draw: null output");
+  if (step >= kMaxStep) return fail(SMAT_ERR_INVALID, "smat_scale_draw: step must be < 2^30");
   if (!(alpha_min >= 0.f && alpha_min <= 1.f))
     return fail(SMAT_ERR_INVALID, "smat_scale_draw: alpha_min must lie in [0, 1]");
   *alpha = host_scale(seed, step, alpha_min);

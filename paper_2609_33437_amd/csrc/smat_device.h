@@ -167,6 +167,8 @@ static_assert(kChunk % tile_elems(kSimQuads) == 0 && kChunk % tile_elems(kBwdQua
 constexpr uint32_t kStreamMask = 0u;
 constexpr uint32_t kStreamNoise = 1u;
 constexpr uint32_t kStreamScale = 2u;  // the step's shared scale: group 0 of tensor id 0
+// The counter word holds 4 step + stream, so steps live in [0, 2^30).
+constexpr uint32_t kStepMask = (1u << 30) - 1u;
 
 // Wave priority while a wave issues its loads.  The simulate's waves spend most of their issue
 // slots on random draws; a wave that has just started is raised above them until its loads are

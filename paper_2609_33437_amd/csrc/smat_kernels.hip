@@ -305,13 +305,14 @@ __global__ __launch_bounds__(kBlock) void k_backward_multi_dev(const TensorRec* 
   backward_tile<TG, kBwdQuads, ACC>(T, P, S.seed, S.step, lambda);
 }
 
-// One thread advances the step state: step += increment, then the scale of that step drawn from the
-// scale stream, so that it depends on (seed, step) only.
+// One thread advances the step state: step += increment modulo 2^30 (the range of the counter's step
+// field), then the scale of that step drawn from the scale stream, so that it depends on (seed, step)
+// only.
 __global__ __launch_bounds__(64) void k_step_advance(StepState* __restrict__ state, uint32_t increment,
                                                      float alpha_min) {
   if (threadIdx.x != 0) return;
   StepState S = *state;
-  S.step += increment;
+  S.step = (S.step + increment) & kStepMask;
   const Words w = group_words(0, 0, (S.step << 2) | kStreamScale, (uint32_t)S.seed, (uint32_t)(S.seed >> 32));
   S.scale = scale_from_word(w.w0, alpha_min);
   *state = S;

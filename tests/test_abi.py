@@ -349,6 +349,11 @@ def test_scale_draw_matches_oracle_without_gpu():
     out = ctypes.c_float()
     assert lib.smat_scale_draw(1, 2, 1.5, ctypes.byref(out)) == _lib.SMAT_ERR_INVALID
     assert lib.smat_scale_draw(1, 2, 0.5, None) == _lib.SMAT_ERR_INVALID
+    # steps live in [0, 2^30), as in the host-driven calls and the oracle
+    assert lib.smat_scale_draw(1, 2 ** 30 - 1, 0.5, ctypes.byref(out)) == _lib.SMAT_OK
+    assert lib.smat_scale_draw(1, 2 ** 30, 0.5, ctypes.byref(out)) == _lib.SMAT_ERR_INVALID
+    with pytest.raises(ValueError):
+        oracle.scale_draw(1, 2 ** 30, 0.5)
 
 
 def test_every_entry_point_survives_zero_arguments():

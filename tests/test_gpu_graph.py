@@ -477,7 +477,7 @@ def test_uploads_refused_under_capture(mini):
 
 # ---------------------------------------------------------------- the step's scale drawn on the device
 @pytest.mark.parametrize("seed,step0,alpha_min", [(0, 0, 0.2), (2 ** 64 - 1, 41, 0.1), (12345, 2 ** 30 - 5, 0.75),
-                                                  (7, 100, 0.0), (7, 100, 1.0)])
+                                                  (7, 100, 0.0), (7, 100, 1.0), (9, 2 ** 30 - 2, 0.3)])
 def test_step_advance_matches_oracle(seed, step0, alpha_min):
     st = smat.StepState(seed, step0, -1.0)
     st.advance(alpha_min, 0)                     # the scale of the current step
@@ -487,8 +487,9 @@ def test_step_advance_matches_oracle(seed, step0, alpha_min):
     for k in range(1, 4):
         st.advance(alpha_min)
         torch.cuda.synchronize()
-        assert st.step_view.item() == step0 + k
-        assert st.scale_view.item() == oracle.scale_draw(seed, step0 + k, alpha_min)
+        step = (step0 + k) % 2 ** 30             # steps live in [0, 2^30): past the last one, step 0 again
+        assert st.step_view.item() == step
+        assert st.scale_view.item() == oracle.scale_draw(seed, step, alpha_min)
     assert st.seed_view.item() == (seed if seed < 2 ** 63 else seed - 2 ** 64)
     with pytest.raises(smat.SmatError):
         st.advance(1.5)

@@ -553,3 +553,30 @@ def test_offload_prefetch_waits_for_the_readers_of_the_buffers(mini):
         torch.cuda.synchronize()
     for b, h in zip(bufs, inp.theta0):
         assert torch.equal(bits(b.cpu()), bits(h.view(-1)))
+
+
+def test_set_params_copies_only_changed_records(mini):
+    """smat_plan_set_params uploads the span of records that changed since the last upload, or
+    nothing: a sequence of repeated and partly changed parameter lists gives the bits of a fresh
+    plan given each list once."""
+    cfg, inp = mini
+    th, t0, gs, gt, out = to_dev(inp)
+    out2 = [torch.empty_like(o) for o in out]
+    base = workloads.step_params(cfg, inp.settings, 3)
+    first = [dict(p) for p in base]
+    first[0]["s"] *= 0.5                                    # the first record changes
+    middle = [dict(p) for p in base]
+    middle[4]["s"] *= 0.5                                   # one record in the middle
+    middle[6]["sigma"] = 0.0
+    last = [dict(p) for p in base]
+    last[-1]["keep"] = 0.0                                  # the last record
+    with smat.Plan(th, out, t0) as plan:
+        for k, params in enumerate((base, base, first, middle, middle, last, base)):
+            plan.set_params(params)
+            plan.simulate(cfg.smat_seed, 3 + k)
+            with smat.Plan(th, out2, t0) as fresh:
+                fresh.set_params(params)
+                fresh.simulate(cfg.smat_seed, 3 + k)
+                torch.cuda.synchronize()
+            for i, (a, b) in enumerate(zip(out, out2)):
+                assert torch.equal(bits(a), bits(b)), (k, i)

@@ -48,10 +48,28 @@ def test_offload_restore_refills_base():
     for a, b in zip(sw.buffer, t0):
         np.testing.assert_array_equal(a, b)
     sw.simulate([x * 3 for x in th])
+    with pytest.raises(StateError):
+        sw.simulate([x * 3 for x in th])     # the buffer holds theta~, not the base, until a restore
     sw.switch(SIMULATED)
     sw.switch(EXPERT)
     for a, b in zip(sw.buffer, t0):
         assert a.tobytes() == b.tobytes()
+    sw.simulate([x * 2 for x in th])         # refilled: the next simulate may run
+    sw.switch(EXPERT)                        # restoring the expert view without using theta~
+    with pytest.raises(StateError):
+        sw.simulate([x * 2 for x in th])     # no restore happened (the view was already the expert's)
+
+
+def test_resident_simulate_may_repeat():
+    """Resident mode keeps theta0 apart from the buffer, so simulating again before using theta~
+    just replaces it."""
+    th, t0 = _lists()
+    sw = StorageSwitch(th, t0)
+    sw.simulate([x + 1 for x in th])
+    sw.simulate([x + 2 for x in th])
+    sw.switch(SIMULATED)
+    for a, b in zip(sw.active(), th):
+        np.testing.assert_array_equal(a, b + 2)
 
 
 @pytest.mark.parametrize("n", [1, 3, 4, 7, 8, 100, 101])
