@@ -98,58 +98,127 @@ def parse_args():
     return ap.parse_args()
 
 
-def cpu_baseline(cfg, inp, params, step, max_elems, budget_s, torch, np):
-    """The CPU oracle on a bounded sample of the same workload: a window of every tensor with size
-    proportional to the tensor, simulate (with its rounding) then backward, on a pool of threads
-    (one per host core; the oracle is vectorized NumPy, whose array loops run without the GIL).
-    Windows are visited in random order; no new window starts after `budget_s` seconds."""
-    import concurrent.futures as cf
+# Worker threads of the CPU baseline: one per host core the process may run on, at most 16, the host
+# share that goes with one GPU on the MI355X boxes this runs on.
+CPU_WORKER_CAP = 16
 
-    import oracle
 
+def sample_windows(cfg, max_elems: int, seed: int = 1234):
+    """Windows (tensor, first element, length) of every tensor, each a fraction of its tensor,
+    together at most about max_elems elements, in random tensor order."""
+    import numpy as np
     frac = min(1.0, max_elems / cfg.numel)
-    rng = np.random.default_rng(1234)
-    order = rng.permutation(cfg.count)
-    t0_dt, g_dt, out_dt = cfg.theta0_dtype, cfg.grad_dtype, cfg.out_dtype
+    rng = np.random.default_rng(seed)
+    wins = []
+    for i in rng.permutation(cfg.count):
+        n = cfg.specs[i].numel
+        m = max(1, int(round(n * frac)))
+        wins.append((int(i), int(rng.integers(0, n - m + 1)), m))
+    return frac, wins
 
+
+def window_tasks(wins, inp, g_pre, torch, np, piece: int = 1 << 20):
+    """Host copies of the windows' inputs, split into pieces of at most `piece` elements so that the
+    threads share the big tensors: (tensor, global offset, theta, theta0, grad_sim, grad_theta before
+    the step).  bf16 arrays as their uint16 bits, as the oracle takes them."""
     def bits(x):
         return x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
 
     tasks = []
-    for i in order:
-        t = inp.theta[i]
-        n = t.numel()
-        m = max(1, int(round(n * frac)))
-        a = int(rng.integers(0, n - m + 1))
-        win = lambda x: x.view(-1)[a:a + m].cpu()
-        # windows above 2^20 elements are split so that the threads share the big tensors
-        for b in range(0, m, 1 << 20):
-            e = min(m, b + (1 << 20))
-            tasks.append((int(i), a + b, win(t)[b:e].numpy(), bits(win(inp.theta0[i])[b:e]),
-                          bits(win(inp.grad_sim[i])[b:e]), win(inp.grad_theta[i])[b:e].numpy()))
+    for (i, a, m), gp in zip(wins, g_pre):
+        th = inp.theta[i].view(-1)[a:a + m].cpu().numpy()
+        t0 = bits(inp.theta0[i].view(-1)[a:a + m].cpu())
+        gs = bits(inp.grad_sim[i].view(-1)[a:a + m].cpu())
+        for b in range(0, m, piece):
+            e = min(m, b + piece)
+            tasks.append((i, a + b, th[b:e], t0[b:e], gs[b:e], gp[b:e]))
+    return tasks
+
+
+def cpu_baseline(cfg, tasks, params, step, budget_s):
+    """The CPU oracle on a bounded sample of the same workload (the windows of `tasks`): simulate with
+    its rounding, then backward-accumulate, in fp64 NumPy on a pool of threads (NumPy's array loops
+    run without the GIL).  No new window starts after `budget_s` seconds.  Returns the baseline
+    record and the oracle outputs of every window it finished, for the parity check."""
+    import concurrent.futures as cf
+
+    import oracle
+
+    t0_dt, g_dt, out_dt = cfg.theta0_dtype, cfg.grad_dtype, cfg.out_dtype
     try:
-        cores = len(os.sched_getaffinity(0))
+        affinity = len(os.sched_getaffinity(0))
     except AttributeError:
-        cores = os.cpu_count() or 1
-    cores = max(1, min(cores, 16))
+        affinity = os.cpu_count() or 1
+    workers = max(1, min(affinity, CPU_WORKER_CAP))
     start = time.perf_counter()
     deadline = start + budget_s
 
-    def run(task):
+    def run(k):
         if time.perf_counter() >= deadline:
-            return 0
-        i, off, th, t0, gs, gt = task
-        oracle.simulate(th, t0, t0_dt, out_dt, params[i], cfg.smat_seed, step, i, off)
-        oracle.backward_accum(gs, g_dt, gt, params[i], cfg.lam, cfg.smat_seed, step, i, off)
-        return th.size
+            return None
+        i, off, th, t0, gs, gp = tasks[k]
+        y, kept, eps = oracle.simulate_f64(th, t0, t0_dt, params[i], cfg.smat_seed, step, i, off)
+        oracle.round_to(y, out_dt)
+        want = oracle.backward_accum(gs, g_dt, gp, params[i], cfg.lam, cfg.smat_seed, step, i, off)
+        return k, y, kept, eps, want
 
-    with cf.ThreadPoolExecutor(max_workers=cores) as pool:
-        done = sum(pool.map(run, tasks))
+    with cf.ThreadPoolExecutor(max_workers=workers) as pool:
+        outs = [r for r in pool.map(run, range(len(tasks))) if r is not None]
     secs = time.perf_counter() - start
-    log(f"cpu oracle: {done} elements in {secs:.1f} s on {cores} threads")
-    return {"value": done / secs, "unit": "params/s", "cores": cores, "kind": "oracle",
-            "sample": f"{done} elements: windows of {100 * frac:.3f}% of the {cfg.count} tensors in random order "
-                      f"(simulate + backward, fp64 NumPy, {cores} threads), {secs:.1f} s wall"}
+    done = sum(tasks[r[0]][2].size for r in outs)
+    log(f"cpu oracle: {done} elements in {secs:.1f} s on {workers} threads")
+    rec = {"value": done / secs, "unit": "params/s", "cores": workers, "kind": "oracle",
+           "affinity_cores": affinity, "worker_cap": CPU_WORKER_CAP,
+           "sample": f"{done} elements: windows of {100 * min(1.0, done / cfg.numel):.3f}% of the {cfg.count} "
+                     f"tensors in random order (simulate + backward, fp64 NumPy, {workers} threads), {secs:.1f} s wall"}
+    return rec, outs
+
+
+def parity_stats(cfg, tasks, oracle_outs, gpu_tt, gpu_g, params, np):
+    """The verification step's GPU outputs against the oracle's, window by window, under the test
+    suite's bars (tests/tolerances.py): theta~ within half an output ulp plus the fp32 error bound of
+    the kernel's arithmetic (within 1 bf16 ulp of the oracle's rounding wherever that bound is below
+    half an ulp, the "strict" elements), grad_theta within 1e-6 relative, dropped coordinates of
+    grad_theta bit-unchanged."""
+    import concurrent.futures as cf
+
+    import oracle
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import tolerances
+
+    t0_dt, g_dt, out_dt = cfg.theta0_dtype, cfg.grad_dtype, cfg.out_dtype
+
+    def one(r):
+        k, y, kept, eps, want = r
+        i, off, th, t0, gs, gp = tasks[k]
+        p = params[i]
+        got, gg = gpu_tt[k], gpu_g[k]
+        coef = np.where(kept, oracle.coefficient(p["s"], p["keep"], p.get("rescale", 1)), 0.0)
+        ok, strict = tolerances.check_theta_tilde(got, out_dt, y, th, oracle.as_f64(t0, t0_dt), coef, eps, p["sigma"])
+        if out_dt == "bf16":
+            ulp = np.abs(tolerances.ordered(got) - tolerances.ordered(oracle.round_to_bf16_bits(y)))
+        else:
+            ulp = np.abs(got.view(np.int32).astype(np.int64) - oracle.round_to(y, "f32").view(np.int32).astype(np.int64))
+        incr = np.abs(cfg.lam * coef * oracle.as_f64(gs, g_dt))
+        gok = tolerances.check_grad(gg, want, gp, incr)
+        scale = np.maximum(np.abs(want.astype(np.float64)), np.abs(gp.astype(np.float64)) + incr)
+        rel = np.abs(gg.astype(np.float64) - want.astype(np.float64)) / np.where(scale > 0, scale, 1.0)
+        dropped_changed = int(np.count_nonzero(gg.view(np.uint32)[~kept] != gp.view(np.uint32)[~kept]))
+        return (th.size, int(np.count_nonzero(~ok)), int(ulp.max(initial=0)), int(ulp[strict].max(initial=0)),
+                int(np.count_nonzero(~strict)), int(ulp[~strict].max(initial=0)), int(np.count_nonzero(~gok)),
+                float(rel.max(initial=0.0)), dropped_changed, int(np.count_nonzero(kept)))
+
+    with cf.ThreadPoolExecutor(max_workers=CPU_WORKER_CAP) as pool:
+        rows = list(pool.map(one, oracle_outs))
+    col = list(zip(*rows)) if rows else [[0]] * 10
+    n = sum(col[0])
+    return {"elements": n, "windows": len(rows),
+            "theta_tilde": {"mismatches": sum(col[1]), "max_ulp": max(col[2]), "max_ulp_strict": max(col[3]),
+                            "nonstrict": sum(col[4]), "nonstrict_max_ulp": max(col[5])},
+            "grad_theta": {"mismatches": sum(col[6]), "max_rel_err": max(col[7]),
+                           "dropped_changed": sum(col[8]), "kept": sum(col[9])},
+            "bars": "theta~ within 1/2 ulp + the fp32 error bound of the kernel's arithmetic (strict elements: "
+                    "1 bf16 ulp); grad_theta 1e-6 relative; dropped grad_theta bit-unchanged"}
 
 
 def timed_copy(nbytes_step: int, torch, smat, reps: int = 5) -> dict:
@@ -918,8 +987,9 @@ def main() -> int:
     else:
         plan = smat.Plan(inp.theta, outs, inp.theta0, inp.grad_sim, inp.grad_theta)
     K, W = args.steps, args.warmup
-    # the hot path runs on simulated steps only: every step, or steps = 3 mod 4 for the periodic list
-    step_ids = [k * cfg.period + cfg.period - 1 for k in range(W + K)]
+    # the hot path runs on simulated steps only: every step, or steps = 3 mod 4 for the periodic list.
+    # W warmup steps, K timed steps, K steps of the kernel-timing pass, one verification step.
+    step_ids = [k * cfg.period + cfg.period - 1 for k in range(W + 2 * K + 1)]
     params = [workloads.step_params(cfg, inp.settings, s) for s in step_ids]
     seed = cfg.smat_seed
 
@@ -942,22 +1012,54 @@ def main() -> int:
     for k in range(W):
         one(k)
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # the timed region: K whole steps with nothing but the steps' own calls between the two events
     log(f"timing {K} steps")
     torch.cuda.synchronize()
     start.record()
     for k in range(K):
-        one(W + k, evs[k])
+        one(W + k)
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms_step = total_ms / K
+    # kernel pass: K more steps with HIP events around each kernel on the launch stream (the events
+    # cost host issue time, which shows on small lists, so they stay out of the timed region)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    start.record()
+    for k in range(K):
+        one(W + K + k, evs[k])
+    end.record()
+    torch.cuda.synchronize()
+    ms_step_events = start.elapsed_time(end) / K
     sim_ms = [e[0].elapsed_time(e[1]) for e in evs]
     bwd_ms = [e[2].elapsed_time(e[3]) for e in evs]
     sim_avg, bwd_avg = sum(sim_ms) / K, sum(bwd_ms) / K
     med = lambda v: sorted(v)[len(v) // 2]
-    log(f"step {ms_step:.3f} ms  simulate {sim_avg:.3f} ms  backward {bwd_avg:.3f} ms")
+    log(f"step {ms_step:.3f} ms (kernel pass {ms_step_events:.3f} ms)  simulate {sim_avg:.3f} ms  "
+        f"backward {bwd_avg:.3f} ms")
+
+    # verification step (untimed, the launch configuration timed above): windows of grad_theta before
+    # it, then the windows of its outputs, for the oracle to check in the CPU baseline leg
+    verify = None
+    if not args.no_cpu_baseline:
+        kv = W + 2 * K
+        frac, wins = sample_windows(cfg, args.cpu_sample)
+        g_pre = [inp.grad_theta[i].view(-1)[a:a + m].cpu().numpy() for i, a, m in wins]
+        one(kv)
+        torch.cuda.synchronize()
+        tasks = window_tasks(wins, inp, g_pre, torch, np)
+        piece = 1 << 20
+        gpu_tt, gpu_g = [], []
+        for i, a, m in wins:
+            o = outs[i].view(-1)[a:a + m].cpu()
+            o = o.view(torch.int16).numpy().view(np.uint16) if o.dtype == torch.bfloat16 else o.numpy()
+            g = inp.grad_theta[i].view(-1)[a:a + m].cpu().numpy()
+            for b in range(0, m, piece):
+                gpu_tt.append(o[b:b + piece])
+                gpu_g.append(g[b:b + piece])
+        verify = (kv, tasks, gpu_tt, gpu_g)
+        del g_pre
 
     P = cfg.numel
     sim_bytes = P * (4 + nbytes[cfg.theta0_dtype] + nbytes[cfg.out_dtype])
@@ -1008,12 +1110,15 @@ def main() -> int:
                                  "frac_of_copy": round(sim_gbps / copy["gbps"], 4)},
                     "backward": {"avg_ms": round(bwd_avg, 4), "median_ms": round(med(bwd_ms), 4),
                                  "min_ms": round(min(bwd_ms), 4), "gbps": round(bwd_gbps, 1),
-                                 "frac_of_copy": round(bwd_gbps / copy["gbps"], 4)}},
+                                 "frac_of_copy": round(bwd_gbps / copy["gbps"], 4)},
+                    "timing": f"HIP events around each kernel in a second pass of {K} steps "
+                              f"({round(ms_step_events, 4)} ms per step with the events)"},
         "copy": dict(copy, kernel="smat_stream_copy (plain nontemporal copy), same bytes as one step",
                      frac_of_peak=round(copy["gbps"] / PEAK_HBM_GBPS, 4)),
         "hbm_frac_of_copy": round(step_gbps / copy["gbps"], 4),
         "roofline": roofline,
         "cpu_baseline": None,
+        "parity": None,
     }
     if cfg.period > 1:
         result["config"]["ms_per_training_step_avg"] = round(ms_step / cfg.period, 4)
@@ -1023,10 +1128,14 @@ def main() -> int:
     if args.adamw:
         plan.close()
         result["adamw_step"] = bench_adamw(cfg, inp, outs, params, step_ids, seed, K, W, torch, smat)
-    if not args.no_cpu_baseline:
-        last = W + K - 1
-        result["cpu_baseline"] = cpu_baseline(cfg, inp, params[last], step_ids[last], args.cpu_sample,
-                                              args.cpu_seconds, torch, np)
+    if verify is not None:
+        kv, tasks, gpu_tt, gpu_g = verify
+        result["cpu_baseline"], oracle_outs = cpu_baseline(cfg, tasks, params[kv], step_ids[kv], args.cpu_seconds)
+        result["parity"] = dict(parity_stats(cfg, tasks, oracle_outs, gpu_tt, gpu_g, params[kv], np),
+                                step=step_ids[kv])
+        log(f"parity: {result['parity']['elements']} elements, theta~ mismatches "
+            f"{result['parity']['theta_tilde']['mismatches']} (max {result['parity']['theta_tilde']['max_ulp']} ulp), "
+            f"grad mismatches {result['parity']['grad_theta']['mismatches']}")
     plan.close()
     print(json.dumps(result))
     return 0
