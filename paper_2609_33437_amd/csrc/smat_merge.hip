@@ -7,7 +7,8 @@
 // simulate's exact-endpoint lerp for one expert, so a one-expert merge reproduces the simulated
 // state without noise bit for bit.  A pure HBM stream (N + 2 arrays), built like the other
 // kernels: one-wave blocks over tiles of kMergeQuads quads per thread, loads issued before the
-// mask draws, the list form mapping blocks to (tensor, chunk) through the chunk table.
+// mask draws and at raised wave priority, the list form mapping blocks to (tensor, chunk) through
+// the chunk table.
 #include "smat_launch.h"
 #include "smat_tile.h"
 
@@ -34,6 +35,7 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
   };
 
   if (!vec || groups_wrap(e0, kMergeQuads * kBlock)) {
+    normal_priority();
 #pragma unroll
     for (int u = 0; u < kMergeQuads; ++u) {
       const uint32_t i0 = (u * kBlock + threadIdx.x) * 4u;
@@ -56,6 +58,7 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
         const uint32_t q = u * kBlock + threadIdx.x;
         r0[u] = QuadIO<T0>::load_raw(t0p, q < nq ? q : nq - 1);
       }
+      normal_priority();
 #pragma unroll
       for (int u = 0; u < kMergeQuads; ++u) {
         QuadIO<T0>::unpack(r0[u], b[u]);
@@ -69,12 +72,15 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
       // the expert's pointer and its term's fields in one round of scalar loads, before any branch
       asm volatile("" ::"s"(xp), "s"(R.t), "s"(R.flags), "s"(R.thr), "s"(R.step));
       if (R.flags & kFlagDropAll) continue;
+      // each expert's loads go out at raised priority, ahead of other waves' draws (as in the simulate)
       typename QuadIO<TE>::Raw rx[kMergeQuads];
+      raise_priority();
 #pragma unroll
       for (int u = 0; u < kMergeQuads; ++u) {
         const uint32_t q = u * kBlock + threadIdx.x;
         rx[u] = QuadIO<TE>::load_raw(xp, q < nq ? q : nq - 1);
       }
+      normal_priority();
       bool kept[kMergeQuads][4];
 #pragma unroll
       for (int u = 0; u < kMergeQuads; ++u) {
@@ -110,6 +116,7 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
 
 template <typename TE, typename T0, typename TO>
 __global__ __launch_bounds__(kBlock) void k_merge_one(TensorRec R, MergeArgs A, int nexp) {
+  raise_priority();
   constexpr int64_t tile = tile_elems(kMergeQuads);
   const int64_t begin = (int64_t)blockIdx.x * tile;
   merge_tile<TE, T0, TO>(
@@ -123,6 +130,7 @@ __global__ __launch_bounds__(kBlock) void k_merge_multi(const TensorRec* __restr
                                                         const void* const* __restrict__ experts,
                                                         const MergeRec* __restrict__ terms,
                                                         const uint2* __restrict__ chunks, int nexp) {
+  raise_priority();
   constexpr int64_t tile = tile_elems(kMergeQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kMergeQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];

@@ -241,18 +241,18 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, u
       rg[u] = QuadIO<TG>::load_raw(gs, qc);
       if (ACC) ra[u] = QuadIO<float>::load_raw(ga, qc);
     }
+    // the raw mask words wait in vector registers and are compared when the data is consumed: held
+    // as lane masks across the loads, the 4 kNormQuads decisions would not fit the scalar registers
     const TileGroups G = tile_groups(e0);
-    bool kept[kNormQuads][4];
+    uint32_t mw[kNormQuads][4];
+    if (use_mask) {
 #pragma unroll
-    for (int u = 0; u < kNormQuads; ++u) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
-      if (use_mask) {
+      for (int u = 0; u < kNormQuads; ++u) {
         const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, k0, k1);
-        kept[u][0] = w.w0 < thr;
-        kept[u][1] = w.w1 < thr;
-        kept[u][2] = w.w2 < thr;
-        kept[u][3] = w.w3 < thr;
+        mw[u][0] = w.w0;
+        mw[u][1] = w.w1;
+        mw[u][2] = w.w2;
+        mw[u][3] = w.w3;
       }
     }
 #pragma unroll
@@ -264,7 +264,8 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, u
         if (ACC) QuadIO<float>::unpack(ra[u], b);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float g = gval(kept[u][j], a[j], b[j]);
+          const bool kept = use_mask ? mw[u][j] < thr : all_kept;
+          const float g = gval(kept, a[j], b[j]);
           s = __builtin_fmaf(g, g, s);
         }
       }
