@@ -10,7 +10,7 @@ import oracle
 import paper_2609_33437_amd as smat
 import workloads
 from helpers import host
-from tolerances import check_grad, check_theta_tilde, ordered
+from tolerances import NONSTRICT_MAX_FRACTION, check_grad, check_theta_tilde, ordered, theta_tilde_report
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -50,6 +50,7 @@ def test_fullsize_sampled(name):
         torch.cuda.synchronize()
     print(f"[{name}] kernels done, checking {sum(len(w) for w in wins)} windows", flush=True)
     worst = 0
+    n_all = loose_all = worst_all = 0
     for i, ws in enumerate(samples):
         p = params[i]
         for a, b, th, t0, gs, g_old in ws:
@@ -58,13 +59,17 @@ def test_fullsize_sampled(name):
             got = host(outs[i][a:b])[0]
             ok, strict = check_theta_tilde(got, "bf16", y, th, oracle.as_f64(t0, "bf16"), coef, eps, p["sigma"])
             assert ok.all(), f"{name} tensor {i} [{a},{b}): theta~ mismatch"
-            dist = np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))
-            worst = max(worst, int(dist[strict].max(initial=0)))
+            n, loose, w_all, w_strict = theta_tilde_report(got, oracle.round_to_bf16_bits(y), strict)
+            worst = max(worst, w_strict)
+            n_all, loose_all, worst_all = n_all + n, loose_all + loose, max(worst_all, w_all)
             want = oracle.backward_accum(gs, "bf16", g_old, p, cfg.lam, cfg.smat_seed, step, i, a)
             gotg = host(inp.grad_theta[i].view(-1)[a:b])[0]
             assert check_grad(gotg, want, g_old, np.abs(cfg.lam * coef * oracle.as_f64(gs, "bf16"))).all(), \
                 f"{name} tensor {i} [{a},{b}): grad mismatch"
             np.testing.assert_array_equal(gotg.view(np.uint32)[~kept], g_old.view(np.uint32)[~kept])
+    print(f"[{name}] theta~ {n_all} elements: {loose_all} under the absolute clause, max {worst_all} ulp "
+          f"(strict {worst})", flush=True)
     assert worst <= 1
+    assert loose_all <= NONSTRICT_MAX_FRACTION * n_all, (loose_all, n_all)
     del inp, outs
     torch.cuda.empty_cache()

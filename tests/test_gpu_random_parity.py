@@ -11,7 +11,7 @@ import torch
 import oracle
 import paper_2609_33437_amd as smat
 from helpers import host
-from tolerances import check_grad, check_theta_tilde, ordered
+from tolerances import NONSTRICT_MAX_FRACTION, check_grad, check_theta_tilde, ordered, theta_tilde_report
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -49,7 +49,10 @@ def check_sim(th, t0, out, p, seed, step, tid, off, what):
     ok, strict = check_theta_tilde(got, out_dt, y, thn, oracle.as_f64(t0n, t0_dt), coef, eps, p["sigma"])
     assert ok.all(), f"{what}: {np.count_nonzero(~ok)} theta~ mismatches, first {np.flatnonzero(~ok)[:5]}"
     if out_dt == "bf16":
-        assert np.abs(ordered(got) - ordered(oracle.round_to_bf16_bits(y)))[strict].max(initial=0) <= 1, what
+        n, loose, _, worst_strict = theta_tilde_report(got, oracle.round_to_bf16_bits(y), strict)
+        assert worst_strict <= 1, what
+        if n >= 1000:
+            assert loose <= NONSTRICT_MAX_FRACTION * n, (what, loose, n)
     return kept
 
 

@@ -1,11 +1,16 @@
 """Comparison rules of the GPU path against the oracle, derived from the kernels' fp32 arithmetic.
 
-theta~: the kernel forms t = fl(s/keep), fma(t, theta, fma(-t, theta0, theta0)), fma(sigma, z, .)
-in fp32 and rounds once to the output type.  Each fp32 step adds at most u = 2^-24 relative to its
-operands, so the fp32 value is within E = 3u (|theta0| + |t| (|theta| + |theta0|) + |eps|)
-+ sigma * |z_gpu - z| of the exact value, and the final rounding adds half an ulp of the output
-type.  Away from cancellation this is "within 1 ulp of the oracle's correctly rounded value";
-near zero results the absolute bound E governs.
+theta~: the kernel forms t = fl(s/keep) (relative error u = 2^-24 against the oracle's s/keep), then
+a = fl(theta0 - t theta0) and b = fl(t theta + a) (the exact-endpoint lerp, two fmas) and
+c = fl(sigma z' + b) (z' the hardware Box-Muller value, |z' - z| <= Z_TOL), and rounds c once to the
+output type.  With D = theta - theta0 and y the exact value, the three roundings and t's give
+|c - y| <= E = u (|t| |D| + |theta0| |1 - t| + 2 |theta0 + t D| + |eps|) + sigma Z_TOL (to first
+order; a factor 1 + 8u covers the rest).  The inner fma's term |theta0| |1 - t| is what the
+two-fma lerp pays for being exact at t = 0 and t = 1; for t > 5 (rescaled keep below 1/5) it
+exceeds 4u |theta0|, so no bound of the form 2^-22 (|theta0| + |t D| + |eps|) holds for every
+element.  The output rounding adds half an ulp of the output type.  Where E is below half an ulp of
+y (the "strict" elements, all but a few per million on the benchmark lists) this means "within 1
+ulp of the oracle's correctly rounded value"; near zero results the absolute bound E governs.
 
 grad: one fma in fp32 with c = fl(lambda * fl(s/keep)): |err| <= 3u (|g_old| + |lambda t g~|),
 well inside the 1e-6 relative bar, which is the bound the tests use.
@@ -40,6 +45,14 @@ def ordered(bits16):
     return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
 
 
+def theta_tilde_bound(theta, theta0, t, eps, sigma):
+    """E above: the kernel's fp32 error before the output rounding (fp64 arrays; t = 0 where dropped)."""
+    d = theta - theta0
+    lin = np.abs(theta0 + t * d)
+    return (U * (np.abs(t) * np.abs(d) + np.abs(theta0) * np.abs(1.0 - t) + 2.0 * lin + np.abs(eps)) * (1 + 8 * U)
+            + Z_TOL * sigma * (1 + 2 * U))
+
+
 def check_theta_tilde(gpu, out_dtype, y, theta, theta0, t, eps, sigma):
     """Returns (ok, strict).  gpu: uint16 bits (bf16) or float32 values; y: the oracle's
     unrounded fp64 value; theta, theta0: fp64 inputs; t: fp64 coefficient (0 for dropped
@@ -48,7 +61,8 @@ def check_theta_tilde(gpu, out_dtype, y, theta, theta0, t, eps, sigma):
     half an output ulp of y; there the GPU value is within 1 ulp of the oracle's rounding of y."""
     theta = np.asarray(theta, dtype=np.float64)
     theta0 = np.asarray(theta0, dtype=np.float64)
-    E = 3 * U * (np.abs(theta0) + np.abs(t) * (np.abs(theta) + np.abs(theta0)) + np.abs(eps)) + Z_TOL * sigma
+    t = np.asarray(t, dtype=np.float64)
+    E = theta_tilde_bound(theta, theta0, t, eps, sigma)
     if out_dtype == "bf16":
         g = bf16_bits_to_f64(gpu)
         uy = _ulp_bf16(y)
@@ -60,6 +74,16 @@ def check_theta_tilde(gpu, out_dtype, y, theta, theta0, t, eps, sigma):
     ok = np.abs(g - y) <= half * (1 + 1e-12) + E
     strict = E < 0.5 * uy
     return ok, strict
+
+
+NONSTRICT_MAX_FRACTION = 1e-3   # elements under the absolute clause, out of a tensor or list of >= 1000
+
+
+def theta_tilde_report(gpu_bits, want_bits, strict):
+    """bf16 outputs against the oracle's rounding: (elements, elements under the absolute clause,
+    max ulp distance over all elements, max ulp distance over the strict ones)."""
+    d = np.abs(ordered(gpu_bits) - ordered(want_bits))
+    return d.size, int(np.count_nonzero(~strict)), int(d.max(initial=0)), int(d[strict].max(initial=0))
 
 
 def check_grad(gpu, oracle, g_old, incr):
