@@ -63,8 +63,10 @@ def load_traffic(kernel: str, workload: str, sources=KERNEL_SOURCES):
 def parse_args():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 20 on the 7B-shaped list; smaller lists take proportionally more, "
+                         "at most 2000, so that every list times about the same amount of work)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps first (default: 5, or steps / 4)")
     ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-sample", type=int, default=3 << 27, help="most elements the CPU oracle baseline visits")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="CPU work budget of the oracle baseline")
@@ -101,6 +103,16 @@ def parse_args():
 # Worker threads of the CPU baseline: one per host core the process may run on, at most 16, the host
 # share that goes with one GPU on the MI355X boxes this runs on.
 CPU_WORKER_CAP = 16
+
+
+def default_steps(args, cfg):
+    """(steps, warmup): as given, else 20 and 5 on the 7B-shaped list and, on a smaller list, as many
+    more as it takes to time about the same work (at most 2000 steps): a few hundred microseconds per
+    step are too short to time after the clock has settled with only 20 steps."""
+    ref = 7_504_924_672
+    k = args.steps if args.steps is not None else int(min(2000, max(20, -(-20 * ref // cfg.numel))))
+    w = args.warmup if args.warmup is not None else (5 if k <= 20 else max(5, k // 4))
+    return k, w
 
 
 def sample_windows(cfg, max_elems: int, seed: int = 1234):
@@ -259,16 +271,22 @@ MERGE_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d $REPO/rocprof/mer
                    "python3 $REPO/bench.py --merge --steps 10 --warmup 2")
 MERGE_PMC_CMD = ("rocprofv3 --pmc {ctr} -f csv -d $REPO/rocprof/merge_{tag} -o c4 --kernel-include-regex "
                  "'k_merge_multi' -- python3 $REPO/bench.py --merge --steps 2 --warmup 1")
-VALU_CMDS = {  # VALU activity of every kernel of ours, one counter pass per benchmark mode
-    "valu_main": "rocprofv3 --pmc VALUBusy SQ_INSTS_VALU -f csv -d $REPO/rocprof/valu_main -o c4 "
+VALU_CTRS = "VALUBusy SQ_INSTS_VALU SQ_INSTS_SALU SQ_WAVES"
+VALU_CMDS = {  # VALU activity and instructions per wave of every kernel of ours, one pass per benchmark mode
+    "valu_main": f"rocprofv3 --pmc {VALU_CTRS} -f csv -d $REPO/rocprof/valu_main -o c4 "
                  "--kernel-include-regex 'k_simulate_multi|k_backward_multi' -- "
                  "python3 $REPO/bench.py --steps 2 --warmup 1 --no-cpu-baseline",
-    "valu_opt": "rocprofv3 --pmc VALUBusy SQ_INSTS_VALU -f csv -d $REPO/rocprof/valu_opt -o c4 "
+    "valu_opt": f"rocprofv3 --pmc {VALU_CTRS} -f csv -d $REPO/rocprof/valu_opt -o c4 "
                 "--kernel-include-regex 'k_adamw_multi|k_sqnorm_multi' -- "
                 "python3 $REPO/bench.py --adamw --steps 2 --warmup 1 --no-cpu-baseline",
-    "valu_merge": "rocprofv3 --pmc VALUBusy SQ_INSTS_VALU -f csv -d $REPO/rocprof/valu_merge -o c4 "
+    "valu_merge": f"rocprofv3 --pmc {VALU_CTRS} -f csv -d $REPO/rocprof/valu_merge -o c4 "
                   "--kernel-include-regex 'k_merge_multi' -- python3 $REPO/bench.py --merge --steps 2 --warmup 1",
 }
+# the other lists: the bench line of `bench.py --config NAME` and its kernel trace, per list
+CONFIG_NAMES = {"c1": "c1_flat1m", "c2": "c2_125m", "c3": "c3_1p5b", "c5": "c5_vlm8b"}
+CONFIG_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d $REPO/rocprof/trace_{cfg} -o {cfg} -- "
+                    "python3 $REPO/bench.py --config {cfg}")
+CONFIG_BENCH_CMD = "python3 $REPO/bench.py --config {cfg} > $REPO/rocprof/bench_{cfg}.json"
 COPY_GRID = 1 << 26   # threads of the calibration copy (2^28 fp32 values, 4 per thread)
 COPY_BYTES = 1 << 30  # read and written by one calibration dispatch
 
@@ -294,7 +312,8 @@ def summarize(root: str) -> int:
              f"Command (on one MI355X; {PROF_NOTE}): `{TRACE_CMD}`", "",
              "The default `bench.py` run, whose JSON line quotes the same kernels' HIP-event times.  Each step "
              "launches one simulate and one backward over the 290-tensor list (7,504,924,672 parameters); "
-             "5 warmup + 20 timed steps = 25 calls each.  It first runs `smat_stream_copy` over the step's "
+             "5 warmup + 20 timed steps + 20 steps of the kernel-timing pass + 1 verification step = 46 calls "
+             "each.  It first runs `smat_stream_copy` over the step's "
              "bytes, the plain-copy reference of the JSON line; the other kernels are torch's input "
              "generation and the runtime's copies (`__amd_rocclr_copyBuffer`) of the CPU baseline's windows "
              "to the host.", "",
@@ -351,7 +370,44 @@ def summarize(root: str) -> int:
         summarize_merge(root, out_dir, fetch_factor, write_factor)
     if all(os.path.isdir(os.path.join(root, d)) for d in VALU_CMDS):
         summarize_valu(root, out_dir)
+    summarize_configs(root, out_dir)
     return 0
+
+
+def summarize_configs(root: str, out_dir: str) -> None:
+    """profiles/step_<list>.json (the bench line of `bench.py --config NAME`, with its command and the
+    kernel sources' hash) and profiles/kernels_<list>_trace.md (its rocprofv3 kernel trace), for the
+    lists other than the headline one."""
+    import csv
+
+    for cfg, label in CONFIG_NAMES.items():
+        line = os.path.join(root, f"bench_{cfg}.json")
+        if os.path.exists(line):
+            with open(line) as f:
+                rec = json.loads(f.read().strip().splitlines()[-1])
+            rec = {"command": CONFIG_BENCH_CMD.format(cfg=cfg), "run_from": PROF_NOTE, "kernel_sha": kernel_hash(),
+                   "result": rec}
+            with open(os.path.join(out_dir, f"step_{label}.json"), "w") as f:
+                json.dump(rec, f, indent=1)
+                f.write("\n")
+        stats_path = os.path.join(root, f"trace_{cfg}", f"{cfg}_kernel_stats.csv")
+        if not os.path.exists(stats_path):
+            continue
+        stats = list(csv.DictReader(open(stats_path)))
+        lines = [f"# Kernel time on the {label} list ({cfg}), rocprofv3 kernel trace", "",
+                 f"Command (on one MI355X; {PROF_NOTE}): `{CONFIG_TRACE_CMD.format(cfg=cfg)}`", "",
+                 f"`bench.py --config {cfg}` with the defaults: 5 warmup + 20 timed steps + 20 steps of the "
+                 "kernel-timing pass + 1 verification step, one simulate and one backward each; first the "
+                 "plain-copy reference (`smat_stream_copy`); the other kernels generate the inputs and copy the "
+                 f"CPU baseline's windows to the host.  Kernel sources hash {kernel_hash()}.", "",
+                 "| kernel | calls | average ms | min ms | max ms | share of GPU time |", "|---|---|---|---|---|---|"]
+        for r in stats[:12]:
+            name = r["Name"].replace("(anonymous namespace)", "{anon}").split("(")[0].replace("void ", "")
+            lines.append(f"| `{name[:80]}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.4f} | "
+                         f"{float(r['MinNs']) / 1e6:.4f} | {float(r['MaxNs']) / 1e6:.4f} | "
+                         f"{float(r['Percentage']):.2f}% |")
+        with open(os.path.join(out_dir, f"kernels_{label}_trace.md"), "w") as f:
+            f.write("\n".join(lines) + "\n")
 
 
 def summarize_valu(root: str, out_dir: str) -> None:
@@ -376,22 +432,30 @@ def summarize_valu(root: str, out_dir: str) -> None:
             rows.setdefault((k, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
     label = {"k_simulate_multi": "simulate (mask + Gaussian noise draws)", "k_backward_multi": "backward (mask draws)",
              "k_adamw_multi": "fused AdamW (mask draws)", "k_sqnorm_multi": "gradient norm (mask draws, 2 B/param)"}
-    md = ["# VALU activity of the kernels on the 7B-shaped list (c4), rocprofv3 counters", "",
-          "Commands (run from /tmp with TMPDIR=/tmp; $REPO is the repository root):", ""]
+    md = ["# VALU activity and instructions per wave of the kernels on the 7B-shaped list (c4), rocprofv3 counters",
+          "", "Commands (run from /tmp with TMPDIR=/tmp; $REPO is the repository root):", ""]
     md += [f"* `{c}`" for c in VALU_CMDS.values()]
     md += ["", "VALUBusy = 100 * sum(SQ_ACTIVE_INST_VALU) / CU_NUM / GRBM_GUI_ACTIVE (rocprofv3's own expression); "
-           "SQ_INSTS_VALU counts wave-level VALU instructions, divided here by the parameters a launch covers.  "
-           "Medians over the dispatches of each kernel.", "",
-           "| kernel | dispatches | VALUBusy | VALU instructions per parameter (wave-level) |", "|---|---|---|---|"]
+           "SQ_INSTS_VALU and SQ_INSTS_SALU count wave-level vector and scalar instructions, SQ_WAVES the waves "
+           "a launch ran; instructions are given per wave and per parameter of the launch.  Medians over the "
+           f"dispatches of each kernel.  Kernel sources hash {kernel_hash()} (merge: {kernel_hash(MERGE_SOURCES)}).",
+           "", "| kernel | dispatches | VALUBusy | waves | VALU / wave | SALU / wave | VALU / parameter |",
+           "|---|---|---|---|---|---|---|"]
+
+    def row(name, sel):
+        vb = rows.get((sel[0], "VALUBusy"), [])[sel[1]]
+        if not vb:
+            return
+        med = {c: statistics.median(rows[(sel[0], c)][sel[1]]) for c in ("SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_WAVES")}
+        md.append(f"| {name} | {len(vb)} | {statistics.median(vb):.1f} | {med['SQ_WAVES']:.0f} | "
+                  f"{med['SQ_INSTS_VALU'] / med['SQ_WAVES']:.1f} | {med['SQ_INSTS_SALU'] / med['SQ_WAVES']:.1f} | "
+                  f"{med['SQ_INSTS_VALU'] / P:.4f} |")
+
     for k in ("k_simulate_multi", "k_backward_multi", "k_adamw_multi", "k_sqnorm_multi"):
-        vb, vi = rows.get((k, "VALUBusy"), []), rows.get((k, "SQ_INSTS_VALU"), [])
-        if vb:
-            md.append(f"| {label[k]} | {len(vb)} | {statistics.median(vb):.1f} | {statistics.median(vi) / P:.4f} |")
-    vb, vi = rows.get(("merge", "VALUBusy"), []), rows.get(("merge", "SQ_INSTS_VALU"), [])
-    for name, sl in (("merge, Task Arithmetic (7 experts, no draws)", slice(0, 3)),
-                     ("merge, DARE + Task Arithmetic (7 mask draws per quad)", slice(3, 6))):
-        if len(vb) >= 6:
-            md.append(f"| {name} | 3 | {statistics.median(vb[sl]):.1f} | {statistics.median(vi[sl]) / P:.4f} |")
+        row(label[k], (k, slice(None)))
+    if len(rows.get(("merge", "VALUBusy"), [])) >= 6:
+        row("merge, Task Arithmetic (7 experts, no draws)", ("merge", slice(0, 3)))
+        row("merge, DARE + Task Arithmetic (7 mask draws per quad)", ("merge", slice(3, 6)))
     with open(os.path.join(out_dir, "valu_c4_7b.md"), "w") as f:
         f.write("\n".join(md) + "\n")
     print("\n".join(md))
@@ -938,6 +1002,9 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     smat.lib()  # fail loudly if the HIP library is missing
+    if args.train or args.merge or args.graph:
+        args.steps = 20 if args.steps is None else args.steps
+        args.warmup = 5 if args.warmup is None else args.warmup
     if args.train:
         return bench_train(args, torch, smat)
     if args.merge:
@@ -945,6 +1012,7 @@ def main() -> int:
     if args.graph:
         return bench_graph(args, torch, smat, workloads)
     cfg = workloads.config(args.config)
+    args.steps, args.warmup = default_steps(args, cfg)
     dt = {"bf16": torch.bfloat16, "f32": torch.float32}
     nbytes = {"bf16": 2, "f32": 4}
     step_bytes = cfg.numel * (4 + nbytes[cfg.theta0_dtype] + nbytes[cfg.out_dtype] + nbytes[cfg.grad_dtype] + 8)
@@ -991,10 +1059,15 @@ def main() -> int:
     # W warmup steps, K timed steps, K steps of the kernel-timing pass, one verification step.
     step_ids = [k * cfg.period + cfg.period - 1 for k in range(W + 2 * K + 1)]
     params = [workloads.step_params(cfg, inp.settings, s) for s in step_ids]
+    # each step's per-tensor records as one array of smat_op_params, built before any timing (the
+    # caller's own preparation); the timed step hands it to smat_plan_set_params
+    param_arrays = [smat.op_params_array(cfg.count, *[[p[f] for p in ps] for f in ("s", "keep", "sigma", "rescale",
+                                                                                  "noise_kind")])
+                    for ps in params]
     seed = cfg.smat_seed
 
     def one(k, ev=None):
-        plan.set_params(params[k])
+        plan.set_params(param_arrays[k])
         if ev:
             ev[0].record()
         plan.simulate(seed, step_ids[k])
