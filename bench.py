@@ -371,7 +371,48 @@ def summarize(root: str) -> int:
     if all(os.path.isdir(os.path.join(root, d)) for d in VALU_CMDS):
         summarize_valu(root, out_dir)
     summarize_configs(root, out_dir)
+    summarize_train(root, out_dir)
     return 0
+
+
+TRAIN_CMDS = {"resident": "python3 $REPO/bench.py --train > $REPO/rocprof/train_resident.json",
+              "offload": "python3 $REPO/bench.py --train --offload > $REPO/rocprof/train_offload.json"}
+TRAIN_TRACE_CMD = ("rocprofv3 --kernel-trace --stats -f csv -d $REPO/rocprof/train_trace -o train -- "
+                   "python3 $REPO/bench.py --train --train-reps 1")
+
+
+def summarize_train(root: str, out_dir: str) -> None:
+    """profiles/train_llama1b_<mode>.json (the `bench.py --train` lines: SMAT in a training loop
+    against plain fine-tuning) and profiles/kernels_train_llama1b_trace.md (the kernels of one
+    such run)."""
+    import csv
+
+    for mode, cmd in TRAIN_CMDS.items():
+        line = os.path.join(root, f"train_{mode}.json")
+        if os.path.exists(line):
+            with open(line) as f:
+                rec = json.loads(f.read().strip().splitlines()[-1])
+            with open(os.path.join(out_dir, f"train_llama1b_{mode}.json"), "w") as f:
+                json.dump({"command": cmd, "run_from": PROF_NOTE, "kernel_sha": kernel_hash(), "result": rec}, f,
+                          indent=1)
+                f.write("\n")
+    stats_path = os.path.join(root, "train_trace", "train_kernel_stats.csv")
+    if not os.path.exists(stats_path):
+        return
+    stats = list(csv.DictReader(open(stats_path)))
+    ours = [r for r in stats if "smat::" in r["Name"]]
+    lines = ["# Kernels of the training-loop benchmark (Llama-1B-shaped synthetic decoder), rocprofv3 kernel trace",
+             "", f"Command (on one MI355X; {PROF_NOTE}): `{TRAIN_TRACE_CMD}`", "",
+             "One repetition of the FT / SMAT / SMAT-fused blocks (each warm-up plus timed steps of batch 8 x 512, "
+             "t = 4).  The model's GEMMs (hipBLASLt `Cijk_*`), torch's fused AdamW and elementwise kernels take "
+             f"the time; the library's kernels are listed after the top ones.  Kernel sources hash {kernel_hash()}.",
+             "", "| kernel | calls | average ms | min ms | max ms | share of GPU time |", "|---|---|---|---|---|---|"]
+    for r in stats[:10] + [r for r in ours if r not in stats[:10]]:
+        name = r["Name"].replace("(anonymous namespace)", "{anon}").split("(")[0].replace("void ", "")
+        lines.append(f"| `{name[:80]}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.4f} | "
+                     f"{float(r['MinNs']) / 1e6:.4f} | {float(r['MaxNs']) / 1e6:.4f} | {float(r['Percentage']):.2f}% |")
+    with open(os.path.join(out_dir, "kernels_train_llama1b_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def summarize_configs(root: str, out_dir: str) -> None:
