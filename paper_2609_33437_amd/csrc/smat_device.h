@@ -331,7 +331,8 @@ __device__ __forceinline__ uint32_t pick(const Words& w, uint32_t lane) {
 // r = sqrt(-2 ln u1) with the hardware log2; cos/sin take revolutions (v_cos_f32/v_sin_f32 compute
 // cos/sin of 2*pi*x), so 2*pi*u2 never has to be formed.
 __device__ __forceinline__ void box_muller(uint32_t a, uint32_t b, float& zc, float& zs) {
-  const float u1 = (float)((a >> 8) + 1u) * 0x1p-24f;
+  // (k + 1) 2^-24 for k = a >> 8 < 2^24 as one fma: k 2^-24 and the sum are exact in fp32
+  const float u1 = __builtin_fmaf((float)(a >> 8), 0x1p-24f, 0x1p-24f);
   const float u2 = (float)(b >> 8) * 0x1p-24f;
   const float r = __builtin_amdgcn_sqrtf(-1.38629436111989061883f * __builtin_amdgcn_logf(u1));
   zc = r * __builtin_amdgcn_cosf(u2);
@@ -339,10 +340,11 @@ __device__ __forceinline__ void box_muller(uint32_t a, uint32_t b, float& zc, fl
 }
 
 // Unit-variance uniform value sqrt(3) (2u - 1), u = ((w >> 8) + 1/2) 2^-24.  The odd integer
-// 2 (w >> 8) + 1 - 2^24 is exact in fp32, so 2u - 1 is formed without rounding.
+// 2 (w >> 8) + 1 - 2^24 is exact in fp32, so 2u - 1 is formed without rounding, and scaling by 2^-24
+// is exact, so one product with fl(sqrt(3)) 2^-24 rounds like fl(sqrt(3)) times 2u - 1.
 __device__ __forceinline__ float uniform_unit(uint32_t w) {
   const int32_t k = (int32_t)((w >> 8) << 1) + 1 - (1 << 24);
-  return 1.73205080756887729353f * ((float)k * 0x1p-24f);
+  return (float)k * (1.73205080756887729353f * 0x1p-24f);
 }
 
 // Unit-variance Laplace value by inverting its CDF at u = ((w >> 8) + 1/2) 2^-24:
