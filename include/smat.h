@@ -213,8 +213,10 @@ typedef struct smat_tensor_desc {
  * optimizer step updates, the buffer, grad_theta, bound moments) overlaps no other array, while
  * theta0 and grad_sim of different tensors may share memory.  The caller owns *out_plan and must
  * release it with smat_plan_destroy.
+ * Limits: at most 2^26 tensors, and fewer than 2^31 256-element tiles over the whole list
+ * (about 5.5e11 elements).
  * Errors: SMAT_ERR_INVALID (bad descriptor, duplicate tensor_id, aliasing, gradient pointers given
- * for some tensors only), SMAT_ERR_DTYPE. */
+ * for some tensors only, a list beyond the limits), SMAT_ERR_DTYPE. */
 smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t count, smat_dtype theta0_dtype,
                              smat_dtype out_dtype, smat_dtype grad_dtype, int32_t offload,
                              smat_plan** out_plan);

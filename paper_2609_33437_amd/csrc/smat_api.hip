@@ -94,11 +94,12 @@ ScaleRec make_scale(const smat_op_params& p) {
 }
 
 uint32_t sim_flags(const float* theta, const void* theta0, int t0_dt, const void* out, int out_dt,
-                   uint64_t elem_offset) {
-  return (elem_offset % 4 == 0 && aligned(theta, 16) && aligned(theta0, quad_align(t0_dt)) &&
-          aligned(out, quad_align(out_dt)))
-             ? smat::kVecSim
-             : 0u;
+                   uint64_t elem_offset, int64_t n) {
+  if (!(elem_offset % 4 == 0 && aligned(theta, 16) && aligned(theta0, quad_align(t0_dt)) &&
+        aligned(out, quad_align(out_dt))))
+    return 0u;
+  const bool whole = n % 4 == 0 && elem_offset % (uint64_t)smat::tile_elems(smat::kSimQuads) == 0;
+  return smat::kVecSim | (whole ? smat::kSimWhole : 0u);
 }
 
 uint32_t bwd_flags(const void* grad_sim, int g_dt, const float* grad_theta, uint64_t elem_offset) {
@@ -228,7 +229,7 @@ extern "C" smat_status smat_simulate(const float* theta, const void* theta0, sma
   rec.n = n;
   rec.elem_offset = key.elem_offset;
   rec.tensor_id = key.tensor_id;
-  rec.sflags = sim_flags(theta, theta0, theta0_dtype, out, out_dtype, key.elem_offset);
+  rec.sflags = sim_flags(theta, theta0, theta0_dtype, out, out_dtype, key.elem_offset, n);
   SMAT_HIP(smat::launch_simulate_one(rec, prm, theta0_dtype, out_dtype, key.seed, key.step, stream));
   return SMAT_OK;
 }
@@ -460,6 +461,8 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
   if (!valid_dtype(theta0_dtype) || !valid_dtype(out_dtype) || !valid_dtype(grad_dtype))
     return fail(SMAT_ERR_DTYPE, "smat_plan_create: unsupported dtype");
   if (count < 0 || (count > 0 && !descs)) return fail(SMAT_ERR_INVALID, "smat_plan_create: bad tensor list");
+  if (count > smat::kMaxListTensors)
+    return fail(SMAT_ERR_INVALID, "smat_plan_create: %d tensors, at most %d", count, smat::kMaxListTensors);
   if (offload != 0 && offload != 1) return fail(SMAT_ERR_INVALID, "smat_plan_create: offload must be 0 or 1");
   if (offload && theta0_dtype != out_dtype)
     return fail(SMAT_ERR_INVALID, "smat_plan_create: offload mode keeps theta0 in the buffer, dtypes must match");
@@ -532,7 +535,7 @@ extern "C" smat_status smat_plan_create(const smat_tensor_desc* descs, int32_t c
     r.elem_offset = d.elem_offset;
     r.tensor_id = d.tensor_id;
     if (d.n > 0) {
-      r.sflags = sim_flags(r.theta, r.theta0, theta0_dtype, r.out, out_dtype, d.elem_offset);
+      r.sflags = sim_flags(r.theta, r.theta0, theta0_dtype, r.out, out_dtype, d.elem_offset, d.n);
       if (d.grad_sim) r.sflags |= bwd_flags(d.grad_sim, grad_dtype, d.grad_theta, d.elem_offset);
     }
     p->expert_ptrs[i] = const_cast<float*>(d.theta);
@@ -1164,7 +1167,7 @@ extern "C" smat_status smat_simulate_multi_static(const smat_tensor_desc* descs,
     if (d.n == 0) continue;
     st = check_simulate_ptrs(d.theta, d.theta0, theta0_dtype, d.out, out_dtype, d.n, where);
     if (st != SMAT_OK) return st;
-    r.sflags = sim_flags(d.theta, d.theta0, theta0_dtype, d.out, out_dtype, d.elem_offset);
+    r.sflags = sim_flags(d.theta, d.theta0, theta0_dtype, d.out, out_dtype, d.elem_offset, d.n);
     const size_t n = (size_t)d.n;
     g_scratch_spans[nspans++] = Span{reinterpret_cast<uintptr_t>(d.theta), reinterpret_cast<uintptr_t>(d.theta) + n * 4,
                                      false, i, "theta"};

@@ -25,8 +25,11 @@ enum : uint32_t {
 // Noise forms (smat_noise_kind).
 enum NoiseKind : int { kGaussian = 0, kUniform = 1, kLaplace = 2 };
 // Static flags of a tensor (TensorRec::sflags): pointers aligned for quad vectors and
-// elem_offset a multiple of 4, so quads line up with Philox groups.
-enum : uint32_t { kVecSim = 1u, kVecBwd = 2u };
+// elem_offset a multiple of 4, so quads line up with Philox groups.  kSimWhole adds that every
+// simulate tile of the tensor takes the vector path: n is a multiple of 4 (no ragged last tile) and
+// elem_offset a multiple of the 256-element tile (no tile's groups cross a multiple of 2^32), so a
+// block tests one bit instead of the three conditions.
+enum : uint32_t { kVecSim = 1u, kVecBwd = 2u, kSimWhole = 32u };
 
 struct alignas(16) TensorRec {
   const float* theta;
@@ -40,6 +43,8 @@ struct alignas(16) TensorRec {
   uint32_t sflags;
 };
 static_assert(sizeof(TensorRec) == 64, "TensorRec layout");
+// Most tensors a plan holds: the kernels address its per-tensor tables with 32-bit byte offsets.
+constexpr int32_t kMaxListTensors = 1 << 26;
 
 struct alignas(16) ParamRec {
   uint32_t thr;   // floor(keep * 2^32) when kFlagMask
@@ -192,6 +197,26 @@ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t key) {
 constexpr uint32_t kPhiloxM0 = 0xD2511F53u, kPhiloxM1 = 0xCD9E8D57u;  // round multipliers
 constexpr uint32_t kPhiloxW0 = 0x9E3779B9u, kPhiloxW1 = 0xBB67AE85u;  // key increments
 
+// The round keys of Philox4x32-10 under a 64-bit key (k0, k1): round r uses (k0 + r W0, k1 + r W1)
+// mod 2^32.  A launch whose seed the host knows forms them once and passes them as a kernel
+// argument, so each wave loads them with two scalar loads instead of forming them with 18 scalar
+// adds.
+struct PhiloxKeys {
+  uint32_t k0[10];
+  uint32_t k1[10];
+};
+
+__host__ __device__ __forceinline__ PhiloxKeys philox_keys(uint64_t seed) {
+  PhiloxKeys K;
+  const uint32_t a = (uint32_t)seed, b = (uint32_t)(seed >> 32);
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    K.k0[r] = a + (uint32_t)r * kPhiloxW0;
+    K.k1[r] = b + (uint32_t)r * kPhiloxW1;
+  }
+  return K;
+}
+
 // One Philox4x32 round on counter words (c0, c1, c2, c3) under round key (k0, k1), with the product
 // p0 = c0 * M0 given (64 bits).
 __device__ __forceinline__ void philox_round(uint64_t p0, uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3,
@@ -220,6 +245,14 @@ __device__ __forceinline__ Words group_words(uint64_t g, uint32_t tensor_id, uin
   return philox4x32_10((uint32_t)g, (uint32_t)(g >> 32), tensor_id, c3, k0, k1);
 }
 
+// The same under round keys formed beforehand.
+__device__ __forceinline__ Words group_words(uint64_t g, uint32_t tensor_id, uint32_t c3, const PhiloxKeys& K) {
+  uint32_t c0 = (uint32_t)g, c1 = (uint32_t)(g >> 32), c2 = tensor_id;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) philox_round((uint64_t)c0 * kPhiloxM0, c0, c1, c2, c3, K.k0[r], K.k1[r]);
+  return {c0, c1, c2, c3};
+}
+
 // ---------------------------------------------------------------- Philox on a tile's groups
 // Thread x, slot u of a tile's vector path draws group g0 + u kBlock + x.  Unless the tile crosses a
 // multiple of 2^32 groups, these groups share the high counter word, and then counter words 1-3
@@ -234,6 +267,10 @@ __device__ __forceinline__ TileGroups tile_groups(uint64_t e0) { return {(uint32
 // Whether the groups of a tile of `quads` quads starting at element e0 wrap the low counter word.
 __device__ __forceinline__ bool groups_wrap(uint64_t e0, uint32_t quads) {
   return (uint32_t)(e0 >> 2) > 0xFFFFFFFFu - (quads - 1u);
+}
+// The same as 0 or 1, formed as the carry of a 64-bit add so that it stays in scalar registers.
+__device__ __forceinline__ uint32_t groups_wrap_bit(uint64_t e0, uint32_t quads) {
+  return (uint32_t)((((e0 >> 2) & 0xFFFFFFFFull) + (quads - 1u)) >> 32);
 }
 
 // Round 1's product of the per-lane counter word.  Streams of one group, and masks of one group
@@ -280,19 +317,19 @@ __device__ __forceinline__ Words philox_tile(uint64_t p0, uint32_t hi, uint32_t 
   return philox_tile_rk(p0, hi, c2, c3, rk0, rk1);
 }
 
+__device__ __forceinline__ Words philox_tile(uint64_t p0, uint32_t hi, uint32_t c2, uint32_t c3, const PhiloxKeys& K) {
+  return philox_tile_rk(p0, hi, c2, c3, K.k0, K.k1);
+}
+
 // The mask and noise words of one group: counter words 0-2 are equal in the two streams and c3
 // differs (ca, cb).  The streams share round 1's per-lane product p0; round 2's first product
 // operand is wave-uniform as in philox_tile_rk, and its result word 2 depends on counter words
 // 0-2 only, so round 3's second product is also common to both streams.  Rounds 3-10 of the two
 // streams run interleaved, which gives the wave two independent chains of products to issue.
 __device__ __forceinline__ void philox_tile_pair(uint64_t p0, uint32_t hi, uint32_t c2, uint32_t ca, uint32_t cb,
-                                                 uint32_t k0, uint32_t k1, Words& A, Words& B) {
-  uint32_t rk0[10], rk1[10];
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    rk0[r] = k0 + (uint32_t)r * kPhiloxW0;
-    rk1[r] = k1 + (uint32_t)r * kPhiloxW1;
-  }
+                                                 const PhiloxKeys& K, Words& A, Words& B) {
+  const uint32_t* rk0 = K.k0;
+  const uint32_t* rk1 = K.k1;
   // round 1: only p0 depends on the lane; the streams differ in word 2 (through c3)
   const uint64_t q1 = (uint64_t)c2 * kPhiloxM1;
   const uint32_t a0 = (uint32_t)(q1 >> 32) ^ hi ^ rk0[0], a1 = (uint32_t)q1;

@@ -27,8 +27,8 @@ namespace smat {
 // instantiation, so a block runs only the code of its tensor's case.  The calling kernel raises
 // the wave's priority at entry; the tile drops it as soon as its loads are issued.
 template <typename T0, typename TO, int KIND, bool MASK, bool NOISE>
-__device__ __forceinline__ void simulate_tile_case(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
-  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+__device__ __forceinline__ void simulate_tile_case(const Tile& T, const ParamRec& P, const PhiloxKeys& K,
+                                                   uint32_t step) {
   const uint32_t cmask = (step << 2) | kStreamMask;
   const uint32_t cnoise = (step << 2) | kStreamNoise;
   const uint32_t tensor_id = T.tensor_id;
@@ -43,9 +43,11 @@ __device__ __forceinline__ void simulate_tile_case(const Tile& T, const ParamRec
   void* out = T.out;
   const uint64_t e0 = T.e0;
 
-  // element by element: tensors whose pointers or offset break quad alignment, and the tile that
-  // holds a tensor's last 1-3 elements
-  if (!(T.sflags & kVecSim) || (len & 3u) || groups_wrap(e0, kBlock)) {
+  // element by element: tensors whose pointers or offset break quad alignment, the tile that holds
+  // a tensor's last 1-3 elements, and a tile whose groups cross a multiple of 2^32 (kSimWhole rules
+  // out all three for the whole tensor; otherwise they are tested as one word, in scalar registers)
+  if (!(T.sflags & kSimWhole) &&
+      (((T.sflags & kVecSim) ^ kVecSim) | (len & 3u) | groups_wrap_bit(e0, kBlock)) != 0u) {
     normal_priority();
     const uint32_t i0 = threadIdx.x * 4u;
     for (uint32_t i = i0; i < len && i < i0 + 4u; ++i) {
@@ -53,9 +55,9 @@ __device__ __forceinline__ void simulate_tile_case(const Tile& T, const ParamRec
       const uint64_t g = e >> 2;
       const uint32_t lane = (uint32_t)e & 3u;
       bool kept = all_kept;
-      if (MASK) kept = pick(group_words(g, tensor_id, cmask, k0, k1), lane) < thr;
+      if (MASK) kept = pick(group_words(g, tensor_id, cmask, K), lane) < thr;
       float y = sim_value(QuadIO<float>::load1(th, i), QuadIO<T0>::load1(t0, i), kept, t);
-      if (NOISE) y = __builtin_fmaf(sigma, lane_noise<KIND>(group_words(g, tensor_id, cnoise, k0, k1), lane), y);
+      if (NOISE) y = __builtin_fmaf(sigma, lane_noise<KIND>(group_words(g, tensor_id, cnoise, K), lane), y);
       QuadIO<TO>::store1(out, i, y);
     }
     return;
@@ -76,20 +78,20 @@ __device__ __forceinline__ void simulate_tile_case(const Tile& T, const ParamRec
   float z[4];
   if (MASK && NOISE) {
     Words wm, wn;
-    philox_tile_pair(p0, G.hi, tensor_id, cmask, cnoise, k0, k1, wm, wn);
+    philox_tile_pair(p0, G.hi, tensor_id, cmask, cnoise, K, wm, wn);
     kept[0] = wm.w0 < thr;
     kept[1] = wm.w1 < thr;
     kept[2] = wm.w2 < thr;
     kept[3] = wm.w3 < thr;
     quad_noise<KIND>(wn, z);
   } else if (MASK) {
-    const Words w = philox_tile(p0, G.hi, tensor_id, cmask, k0, k1);
+    const Words w = philox_tile(p0, G.hi, tensor_id, cmask, K);
     kept[0] = w.w0 < thr;
     kept[1] = w.w1 < thr;
     kept[2] = w.w2 < thr;
     kept[3] = w.w3 < thr;
   } else if (NOISE) {
-    quad_noise<KIND>(philox_tile(p0, G.hi, tensor_id, cnoise, k0, k1), z);
+    quad_noise<KIND>(philox_tile(p0, G.hi, tensor_id, cnoise, K), z);
   }
   __builtin_amdgcn_sched_barrier(0);
   float a[4], b[4], y[4];
@@ -108,29 +110,32 @@ __device__ __forceinline__ void simulate_tile_case(const Tile& T, const ParamRec
 // forms (eight instantiations), so that no block computes a draw it discards or selects between
 // noise forms per element.
 template <typename T0, typename TO>
-__device__ __forceinline__ void simulate_tile(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step) {
+__device__ __forceinline__ void simulate_tile(const Tile& T, const ParamRec& P, const PhiloxKeys& K, uint32_t step) {
   const uint32_t f = P.flags;
   const bool mask = (f & kFlagMask) != 0;
-  if (!(f & kFlagNoise)) {
+  // the hot path's case (masked tensors with Gaussian noise) is tested first
+  if ((f & (kFlagMask | kFlagNoise | kFlagUniform | kFlagLaplace)) == (kFlagMask | kFlagNoise)) {
+    simulate_tile_case<T0, TO, kGaussian, true, true>(T, P, K, step);
+  } else if (!(f & kFlagNoise)) {
     if (mask)
-      simulate_tile_case<T0, TO, kGaussian, true, false>(T, P, seed, step);
+      simulate_tile_case<T0, TO, kGaussian, true, false>(T, P, K, step);
     else
-      simulate_tile_case<T0, TO, kGaussian, false, false>(T, P, seed, step);
+      simulate_tile_case<T0, TO, kGaussian, false, false>(T, P, K, step);
   } else if (f & kFlagUniform) {
     if (mask)
-      simulate_tile_case<T0, TO, kUniform, true, true>(T, P, seed, step);
+      simulate_tile_case<T0, TO, kUniform, true, true>(T, P, K, step);
     else
-      simulate_tile_case<T0, TO, kUniform, false, true>(T, P, seed, step);
+      simulate_tile_case<T0, TO, kUniform, false, true>(T, P, K, step);
   } else if (f & kFlagLaplace) {
     if (mask)
-      simulate_tile_case<T0, TO, kLaplace, true, true>(T, P, seed, step);
+      simulate_tile_case<T0, TO, kLaplace, true, true>(T, P, K, step);
     else
-      simulate_tile_case<T0, TO, kLaplace, false, true>(T, P, seed, step);
+      simulate_tile_case<T0, TO, kLaplace, false, true>(T, P, K, step);
   } else {
     if (mask)
-      simulate_tile_case<T0, TO, kGaussian, true, true>(T, P, seed, step);
+      simulate_tile_case<T0, TO, kGaussian, true, true>(T, P, K, step);
     else
-      simulate_tile_case<T0, TO, kGaussian, false, true>(T, P, seed, step);
+      simulate_tile_case<T0, TO, kGaussian, false, true>(T, P, K, step);
   }
 }
 
@@ -140,11 +145,10 @@ __device__ __forceinline__ void simulate_tile(const Tile& T, const ParamRec& P, 
 // reading grad_theta (6 B per element): the same bits as accumulating into zeros, for a step whose
 // simulated-loss gradient is the only one.
 template <typename TG, int Q, bool ACC>
-__device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step,
+__device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, const PhiloxKeys& K, uint32_t step,
                                               float lambda) {
   const uint32_t flags = P.flags;
   if (ACC && (flags & kFlagDropAll)) return;  // every coordinate dropped: the gradient is left as it is
-  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
   const uint32_t tensor_id = T.tensor_id;
   const uint32_t len = T.len;
@@ -161,7 +165,7 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
   auto one = [&](uint32_t i) {
     const uint64_t e = e0 + i;
     bool kept = all_kept;
-    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
+    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, K), (uint32_t)e & 3u) < thr;
     if (ACC) {
       if (kept) QuadIO<float>::store1(gt, i, __builtin_fmaf(c, QuadIO<TG>::load1(gs, i), QuadIO<float>::load1(gt, i)));
     } else {
@@ -196,7 +200,7 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
 #pragma unroll
       for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
       if (use_mask) {
-        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, k0, k1);
+        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, K);
         kept[u][0] = w.w0 < thr;
         kept[u][1] = w.w1 < thr;
         kept[u][2] = w.w2 < thr;
@@ -223,48 +227,48 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
 
 // ---------------------------------------------------------------- kernels
 template <typename T0, typename TO>
-__global__ __launch_bounds__(kBlock) void k_simulate_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step) {
+__global__ __launch_bounds__(kBlock) void k_simulate_one(TensorRec R, ParamRec P, PhiloxKeys K, uint32_t step) {
   raise_priority();
   constexpr int64_t tile = tile_elems(kSimQuads);
-  simulate_tile<T0, TO>(tensor_tile<T0, TO>(R, (int64_t)blockIdx.x * tile, tile), P, seed, step);
+  simulate_tile<T0, TO>(tensor_tile<T0, TO>(R, (int64_t)blockIdx.x * tile, tile), P, K, step);
 }
 
 template <typename TG>
-__global__ __launch_bounds__(kBlock) void k_backward_one(TensorRec R, ParamRec P, uint64_t seed, uint32_t step,
+__global__ __launch_bounds__(kBlock) void k_backward_one(TensorRec R, ParamRec P, PhiloxKeys K, uint32_t step,
                                                          float lambda) {
   constexpr int64_t tile = tile_elems(kBwdQuads);
   const int64_t begin = (int64_t)blockIdx.x * tile;
   Tile T = tensor_tile<float, float>(R, begin, tile);
   T.grad_sim = advance<TG>(R.grad_sim, begin);
   T.grad_theta = R.grad_theta + begin;
-  backward_tile<TG, kBwdQuads, true>(T, P, seed, step, lambda);
+  backward_tile<TG, kBwdQuads, true>(T, P, K, step, lambda);
 }
 
 template <typename T0, typename TO>
 __global__ __launch_bounds__(kBlock) void k_simulate_multi(const TensorRec* __restrict__ recs,
                                                            const ParamRec* __restrict__ prms,
-                                                           const uint2* __restrict__ chunks, uint64_t seed,
+                                                           const uint2* __restrict__ chunks, PhiloxKeys K,
                                                            uint32_t step) {
   raise_priority();
   constexpr int64_t tile = tile_elems(kSimQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
-  const Tile T = list_tile<T0, TO, float>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  const Tile T = list_tile<T0, TO, float>(rec_at(recs, ch.x), ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;  // unused tile of a tensor's last chunk
-  simulate_tile<T0, TO>(T, prms[ch.x], seed, step);
+  simulate_tile<T0, TO>(T, rec_at(prms, ch.x), K, step);
 }
 
 template <typename TG, bool ACC>
 __global__ __launch_bounds__(kBlock) void k_backward_multi(const TensorRec* __restrict__ recs,
                                                            const ParamRec* __restrict__ prms,
-                                                           const uint2* __restrict__ chunks, uint64_t seed,
+                                                           const uint2* __restrict__ chunks, PhiloxKeys K,
                                                            uint32_t step, float lambda) {
   constexpr int64_t tile = tile_elems(kBwdQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
-  const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  const Tile T = list_tile<float, float, TG>(rec_at(recs, ch.x), ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;
-  backward_tile<TG, kBwdQuads, ACC>(T, prms[ch.x], seed, step, lambda);
+  backward_tile<TG, kBwdQuads, ACC>(T, rec_at(prms, ch.x), K, step, lambda);
 }
 
 // The same list kernels with the step's seed, step and scale read from device memory, so that a
@@ -280,12 +284,12 @@ __global__ __launch_bounds__(kBlock) void k_simulate_multi_dev(const TensorRec* 
   constexpr int64_t tile = tile_elems(kSimQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
-  const Tile T = list_tile<T0, TO, float>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  const Tile T = list_tile<T0, TO, float>(rec_at(recs, ch.x), ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;
   const StepState S = *state;
-  ParamRec P = prms[ch.x];
-  P.t = device_coefficient(S.scale, scales[ch.x]);
-  simulate_tile<T0, TO>(T, P, S.seed, S.step);
+  ParamRec P = rec_at(prms, ch.x);
+  P.t = device_coefficient(S.scale, rec_at(scales, ch.x));
+  simulate_tile<T0, TO>(T, P, philox_keys(S.seed), S.step);
 }
 
 template <typename TG, bool ACC>
@@ -297,12 +301,12 @@ __global__ __launch_bounds__(kBlock) void k_backward_multi_dev(const TensorRec* 
   constexpr int64_t tile = tile_elems(kBwdQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
-  const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  const Tile T = list_tile<float, float, TG>(rec_at(recs, ch.x), ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;
   const StepState S = *state;
-  ParamRec P = prms[ch.x];
-  P.t = device_coefficient(S.scale, scales[ch.x]);
-  backward_tile<TG, kBwdQuads, ACC>(T, P, S.seed, S.step, lambda);
+  ParamRec P = rec_at(prms, ch.x);
+  P.t = device_coefficient(S.scale, rec_at(scales, ch.x));
+  backward_tile<TG, kBwdQuads, ACC>(T, P, philox_keys(S.seed), S.step, lambda);
 }
 
 // One thread advances the step state: step += increment modulo 2^30 (the range of the counter's step
@@ -348,66 +352,70 @@ static inline uint32_t blocks_for(int64_t n, int64_t per_block) { return (uint32
 
 hipError_t launch_simulate_one(const TensorRec& rec, const ParamRec& prm, int theta0_dtype, int out_dtype,
                                uint64_t seed, uint32_t step, hipStream_t stream) {
+  const PhiloxKeys K = philox_keys(seed);
   constexpr int64_t tile = tile_elems(kSimQuads);
   return for_pieces((uint64_t)rec.n, (uint64_t)max_grid_blocks(kBlock) * tile, [&](uint64_t off, uint64_t len) {
     const TensorRec r = rec_piece(rec, off, len, theta0_dtype, out_dtype, 0);
     const dim3 grid(blocks_for((int64_t)len, tile)), block(kBlock);
     if (theta0_dtype == 1 && out_dtype == 1)
-      k_simulate_one<Bf16, Bf16><<<grid, block, 0, stream>>>(r, prm, seed, step);
+      k_simulate_one<Bf16, Bf16><<<grid, block, 0, stream>>>(r, prm, K, step);
     else if (theta0_dtype == 1 && out_dtype == 0)
-      k_simulate_one<Bf16, float><<<grid, block, 0, stream>>>(r, prm, seed, step);
+      k_simulate_one<Bf16, float><<<grid, block, 0, stream>>>(r, prm, K, step);
     else if (theta0_dtype == 0 && out_dtype == 1)
-      k_simulate_one<float, Bf16><<<grid, block, 0, stream>>>(r, prm, seed, step);
+      k_simulate_one<float, Bf16><<<grid, block, 0, stream>>>(r, prm, K, step);
     else
-      k_simulate_one<float, float><<<grid, block, 0, stream>>>(r, prm, seed, step);
+      k_simulate_one<float, float><<<grid, block, 0, stream>>>(r, prm, K, step);
   });
 }
 
 hipError_t launch_backward_one(const TensorRec& rec, const ParamRec& prm, int grad_dtype, float lambda,
                                uint64_t seed, uint32_t step, hipStream_t stream) {
+  const PhiloxKeys K = philox_keys(seed);
   constexpr int64_t tile = tile_elems(kBwdQuads);
   return for_pieces((uint64_t)rec.n, (uint64_t)max_grid_blocks(kBlock) * tile, [&](uint64_t off, uint64_t len) {
     const TensorRec r = rec_piece(rec, off, len, 0, 0, grad_dtype);
     const dim3 grid(blocks_for((int64_t)len, tile)), block(kBlock);
     if (grad_dtype == 1)
-      k_backward_one<Bf16><<<grid, block, 0, stream>>>(r, prm, seed, step, lambda);
+      k_backward_one<Bf16><<<grid, block, 0, stream>>>(r, prm, K, step, lambda);
     else
-      k_backward_one<float><<<grid, block, 0, stream>>>(r, prm, seed, step, lambda);
+      k_backward_one<float><<<grid, block, 0, stream>>>(r, prm, K, step, lambda);
   });
 }
 
 hipError_t launch_simulate_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                  int theta0_dtype, int out_dtype, uint64_t seed, uint32_t step, hipStream_t stream) {
+  const PhiloxKeys K = philox_keys(seed);
   constexpr uint32_t tpc = tiles_per_chunk(kSimQuads);
   return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
     const uint2* ch = chunks + first;
     const dim3 grid((uint32_t)count * tpc), block(kBlock);
     if (theta0_dtype == 1 && out_dtype == 1)
-      k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step);
+      k_simulate_multi<Bf16, Bf16><<<grid, block, 0, stream>>>(recs, prms, ch, K, step);
     else if (theta0_dtype == 1 && out_dtype == 0)
-      k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step);
+      k_simulate_multi<Bf16, float><<<grid, block, 0, stream>>>(recs, prms, ch, K, step);
     else if (theta0_dtype == 0 && out_dtype == 1)
-      k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step);
+      k_simulate_multi<float, Bf16><<<grid, block, 0, stream>>>(recs, prms, ch, K, step);
     else
-      k_simulate_multi<float, float><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step);
+      k_simulate_multi<float, float><<<grid, block, 0, stream>>>(recs, prms, ch, K, step);
   });
 }
 
 hipError_t launch_backward_multi(const TensorRec* recs, const ParamRec* prms, const uint2* chunks, uint32_t nchunks,
                                  int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
                                  hipStream_t stream) {
+  const PhiloxKeys K = philox_keys(seed);
   constexpr uint32_t tpc = tiles_per_chunk(kBwdQuads);
   return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
     const uint2* ch = chunks + first;
     const dim3 grid((uint32_t)count * tpc), block(kBlock);
     if (grad_dtype == 1 && accumulate)
-      k_backward_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step, lambda);
+      k_backward_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, ch, K, step, lambda);
     else if (grad_dtype == 1)
-      k_backward_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step, lambda);
+      k_backward_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, ch, K, step, lambda);
     else if (accumulate)
-      k_backward_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step, lambda);
+      k_backward_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, ch, K, step, lambda);
     else
-      k_backward_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, ch, seed, step, lambda);
+      k_backward_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, ch, K, step, lambda);
   });
 }
 

@@ -23,8 +23,7 @@ __device__ __forceinline__ void adam_element(float g, float& th, float& m1, floa
 
 template <typename TG, int Q, bool ACC>
 __device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p, const ParamRec& P,
-                                           const AdamConsts& A, uint64_t seed, uint32_t step, float lambda) {
-  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+                                           const AdamConsts& A, const PhiloxKeys& K, uint32_t step, float lambda) {
   const uint32_t cmask = (step << 2) | kStreamMask;
   const uint32_t flags = P.flags;
   const bool use_mask = (flags & kFlagMask) != 0;
@@ -45,7 +44,7 @@ __device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p
   auto one = [&](uint32_t i) {
     const uint64_t e = e0 + i;
     bool kept = all_kept;
-    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
+    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, K), (uint32_t)e & 3u) < thr;
     const float g = grad(kept, QuadIO<TG>::load1(gs, i), ACC ? QuadIO<float>::load1(ga, i) : 0.0f);
     float t = QuadIO<float>::load1(th, i), a = QuadIO<float>::load1(m1p, i), b = QuadIO<float>::load1(m2p, i);
     adam_element(g, t, a, b, A);
@@ -84,7 +83,7 @@ __device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p
 #pragma unroll
       for (int j = 0; j < 4; ++j) kept[u][j] = all_kept;
       if (use_mask) {
-        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, k0, k1);
+        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, K);
         kept[u][0] = w.w0 < thr;
         kept[u][1] = w.w1 < thr;
         kept[u][2] = w.w2 < thr;
@@ -115,7 +114,7 @@ __device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p
 }
 
 template <typename TG, bool ACC>
-__global__ __launch_bounds__(kBlock) void k_adamw_one(TensorRec R, AdamRec S, ParamRec P, AdamConsts A, uint64_t seed,
+__global__ __launch_bounds__(kBlock) void k_adamw_one(TensorRec R, AdamRec S, ParamRec P, AdamConsts A, PhiloxKeys K,
                                                       uint32_t step, float lambda, const float* dev_scale) {
   constexpr int64_t tile = tile_elems(kAdamQuads);
   if (dev_scale) A.grad_scale *= *dev_scale;
@@ -123,14 +122,14 @@ __global__ __launch_bounds__(kBlock) void k_adamw_one(TensorRec R, AdamRec S, Pa
   Tile T = tensor_tile<float, float>(R, begin, tile);
   T.grad_sim = advance<TG>(R.grad_sim, begin);
   T.grad_theta = R.grad_theta ? R.grad_theta + begin : nullptr;
-  adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, P, A, seed, step, lambda);
+  adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, P, A, K, step, lambda);
 }
 
 template <typename TG, bool ACC>
 __global__ __launch_bounds__(kBlock) void k_adamw_multi(const TensorRec* __restrict__ recs,
                                                         const AdamRec* __restrict__ states,
                                                         const ParamRec* __restrict__ prms,
-                                                        const uint2* __restrict__ chunks, AdamConsts A, uint64_t seed,
+                                                        const uint2* __restrict__ chunks, AdamConsts A, PhiloxKeys K,
                                                         uint32_t step, float lambda, const float* dev_scale) {
   constexpr int64_t tile = tile_elems(kAdamQuads);
   if (dev_scale) A.grad_scale *= *dev_scale;
@@ -141,7 +140,7 @@ __global__ __launch_bounds__(kBlock) void k_adamw_multi(const TensorRec* __restr
   const Tile T = list_tile<float, float, TG>(R, ch.y, blockIdx.x % tpc, tile);
   if (T.len == 0) return;
   const AdamRec S = states[ch.x];
-  adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, prms[ch.x], A, seed, step, lambda);
+  adamw_tile<TG, kAdamQuads, ACC>(T, S.exp_avg + begin, S.exp_avg_sq + begin, rec_at(prms, ch.x), A, K, step, lambda);
 }
 
 // The same list kernel with seed, step and scale read from device memory (each tensor's coefficient
@@ -169,7 +168,7 @@ __global__ __launch_bounds__(kBlock) void k_adamw_multi_dev(const TensorRec* __r
   ParamRec P = prms[ch.x];
   P.t = device_coefficient(S.scale, scales[ch.x]);
   const AdamRec M = states[ch.x];
-  adamw_tile<TG, kAdamQuads, ACC>(T, M.exp_avg + begin, M.exp_avg_sq + begin, P, A, S.seed, S.step, lambda);
+  adamw_tile<TG, kAdamQuads, ACC>(T, M.exp_avg + begin, M.exp_avg_sq + begin, P, A, philox_keys(S.seed), S.step, lambda);
 }
 
 // One thread forms the step's constants from the learning rate and step count in device memory.
@@ -195,12 +194,11 @@ constexpr int kSumBlock = 256;
 static_assert(kNormSums <= (uint32_t)kSumBlock, "the final block holds one block sum per thread");
 
 template <typename TG, bool ACC>
-__device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step,
+__device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, const PhiloxKeys& K, uint32_t step,
                                              float lambda) {
   const uint32_t flags = P.flags;
   if (!ACC && (flags & kFlagDropAll)) return 0.0f;
   const uint32_t len = T.len;
-  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
   const bool use_mask = (flags & kFlagMask) != 0;
   const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
@@ -217,7 +215,7 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, u
   auto one = [&](uint32_t i) {
     const uint64_t e = e0 + i;
     bool kept = all_kept;
-    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
+    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, K), (uint32_t)e & 3u) < thr;
     const float g = gval(kept, QuadIO<TG>::load1(gs, i), ACC ? QuadIO<float>::load1(ga, i) : 0.0f);
     s = __builtin_fmaf(g, g, s);
   };
@@ -248,7 +246,7 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, u
     if (use_mask) {
 #pragma unroll
       for (int u = 0; u < kNormQuads; ++u) {
-        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, k0, k1);
+        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, K);
         mw[u][0] = w.w0;
         mw[u][1] = w.w1;
         mw[u][2] = w.w2;
@@ -300,13 +298,13 @@ template <typename TG, bool ACC>
 __global__ __launch_bounds__(kBlock) void k_sqnorm_multi(const TensorRec* __restrict__ recs,
                                                          const ParamRec* __restrict__ prms,
                                                          const uint2* __restrict__ chunks, float* partials,
-                                                         uint64_t seed, uint32_t step, float lambda) {
+                                                         PhiloxKeys K, uint32_t step, float lambda) {
   constexpr int64_t tile = tile_elems(kNormQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kNormQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
-  const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  const Tile T = list_tile<float, float, TG>(rec_at(recs, ch.x), ch.y, blockIdx.x % tpc, tile);
   float s = 0.0f;
-  if (T.len > 0) s = tile_sqnorm<TG, ACC>(T, prms[ch.x], seed, step, lambda);
+  if (T.len > 0) s = tile_sqnorm<TG, ACC>(T, rec_at(prms, ch.x), K, step, lambda);
   s = block_sum<float, kBlock>(s);
   if (threadIdx.x == 0) partials[blockIdx.x] = s;
 }
@@ -320,13 +318,13 @@ __global__ __launch_bounds__(kBlock) void k_sqnorm_multi_dev(const TensorRec* __
   constexpr int64_t tile = tile_elems(kNormQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kNormQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
-  const Tile T = list_tile<float, float, TG>(recs[ch.x], ch.y, blockIdx.x % tpc, tile);
+  const Tile T = list_tile<float, float, TG>(rec_at(recs, ch.x), ch.y, blockIdx.x % tpc, tile);
   float s = 0.0f;
   if (T.len > 0) {
     const StepState S = *state;
     ParamRec P = prms[ch.x];
     P.t = device_coefficient(S.scale, scales[ch.x]);
-    s = tile_sqnorm<TG, ACC>(T, P, S.seed, S.step, lambda);
+    s = tile_sqnorm<TG, ACC>(T, P, philox_keys(S.seed), S.step, lambda);
   }
   s = block_sum<float, kBlock>(s);
   if (threadIdx.x == 0) partials[blockIdx.x] = s;
@@ -364,37 +362,39 @@ static inline uint32_t blocks_for(int64_t n, int64_t per_block) { return (uint32
 hipError_t launch_adamw_one(const TensorRec& rec, const AdamRec& st, const ParamRec& prm, const AdamConsts& A,
                             int grad_dtype, bool accumulate, float lambda, uint64_t seed, uint32_t step,
                             const float* dev_scale, hipStream_t stream) {
+  const PhiloxKeys K = philox_keys(seed);
   constexpr int64_t tile = tile_elems(kAdamQuads);
   return for_pieces((uint64_t)rec.n, (uint64_t)max_grid_blocks(kBlock) * tile, [&](uint64_t off, uint64_t len) {
     const TensorRec r = rec_piece(rec, off, len, 0, 0, grad_dtype);
     const AdamRec m{step_ptr(st.exp_avg, off, 4), step_ptr(st.exp_avg_sq, off, 4)};
     const dim3 grid(blocks_for((int64_t)len, tile)), block(kBlock);
     if (grad_dtype == 1 && accumulate)
-      k_adamw_one<Bf16, true><<<grid, block, 0, stream>>>(r, m, prm, A, seed, step, lambda, dev_scale);
+      k_adamw_one<Bf16, true><<<grid, block, 0, stream>>>(r, m, prm, A, K, step, lambda, dev_scale);
     else if (grad_dtype == 1)
-      k_adamw_one<Bf16, false><<<grid, block, 0, stream>>>(r, m, prm, A, seed, step, lambda, dev_scale);
+      k_adamw_one<Bf16, false><<<grid, block, 0, stream>>>(r, m, prm, A, K, step, lambda, dev_scale);
     else if (accumulate)
-      k_adamw_one<float, true><<<grid, block, 0, stream>>>(r, m, prm, A, seed, step, lambda, dev_scale);
+      k_adamw_one<float, true><<<grid, block, 0, stream>>>(r, m, prm, A, K, step, lambda, dev_scale);
     else
-      k_adamw_one<float, false><<<grid, block, 0, stream>>>(r, m, prm, A, seed, step, lambda, dev_scale);
+      k_adamw_one<float, false><<<grid, block, 0, stream>>>(r, m, prm, A, K, step, lambda, dev_scale);
   });
 }
 
 hipError_t launch_adamw_multi(const TensorRec* recs, const AdamRec* states, const ParamRec* prms, const uint2* chunks,
                               uint32_t nchunks, const AdamConsts& A, int grad_dtype, bool accumulate, float lambda,
                               uint64_t seed, uint32_t step, const float* dev_scale, hipStream_t stream) {
+  const PhiloxKeys K = philox_keys(seed);
   constexpr uint32_t tpc = tiles_per_chunk(kAdamQuads);
   return for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
     const uint2* ch = chunks + first;
     const dim3 grid((uint32_t)count * tpc), block(kBlock);
     if (grad_dtype == 1 && accumulate)
-      k_adamw_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, seed, step, lambda, dev_scale);
+      k_adamw_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, K, step, lambda, dev_scale);
     else if (grad_dtype == 1)
-      k_adamw_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, seed, step, lambda, dev_scale);
+      k_adamw_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, K, step, lambda, dev_scale);
     else if (accumulate)
-      k_adamw_multi<float, true><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, seed, step, lambda, dev_scale);
+      k_adamw_multi<float, true><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, K, step, lambda, dev_scale);
     else
-      k_adamw_multi<float, false><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, seed, step, lambda, dev_scale);
+      k_adamw_multi<float, false><<<grid, block, 0, stream>>>(recs, states, prms, ch, A, K, step, lambda, dev_scale);
   });
 }
 
@@ -414,19 +414,20 @@ hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, cons
                                float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
                                uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
                                hipStream_t stream) {
+  const PhiloxKeys K = philox_keys(seed);
   constexpr uint32_t tpc = kNormPartialsPerChunk;
   const hipError_t e = for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
     const uint2* ch = chunks + first;
     float* part = partials + first * tpc;
     const dim3 grid((uint32_t)count * tpc), block(kBlock);
     if (grad_dtype == 1 && accumulate)
-      k_sqnorm_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
+      k_sqnorm_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, K, step, lambda);
     else if (grad_dtype == 1)
-      k_sqnorm_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
+      k_sqnorm_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, K, step, lambda);
     else if (accumulate)
-      k_sqnorm_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
+      k_sqnorm_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, K, step, lambda);
     else
-      k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
+      k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, K, step, lambda);
   });
   if (e != hipSuccess) return e;
   return launch_sqnorm_reduce(partials, nchunks * tpc, sums, sumsq, clip_coef, max_norm, stream);
