@@ -193,12 +193,17 @@ __global__ __launch_bounds__(64) void k_adam_consts(const AdamStepState* __restr
 constexpr int kSumBlock = 256;
 static_assert(kNormSums <= (uint32_t)kSumBlock, "the final block holds one block sum per thread");
 
+// Unlike the one-quad kernels, the tile forms its Philox round keys from the seed itself: its eight
+// quads keep enough scalar registers live that twenty round keys held from the kernel arguments
+// spill to vector lanes, while keys formed by adds are recomputed where needed (measured on c4:
+// 3.39 ms against 3.48 ms with the keys as an argument).
 template <typename TG, bool ACC>
-__device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, const PhiloxKeys& K, uint32_t step,
+__device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, uint64_t seed, uint32_t step,
                                              float lambda) {
   const uint32_t flags = P.flags;
   if (!ACC && (flags & kFlagDropAll)) return 0.0f;
   const uint32_t len = T.len;
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   const uint32_t cmask = (step << 2) | kStreamMask;
   const bool use_mask = (flags & kFlagMask) != 0;
   const bool all_kept = (flags & (kFlagMask | kFlagDropAll)) == 0;
@@ -215,7 +220,7 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, c
   auto one = [&](uint32_t i) {
     const uint64_t e = e0 + i;
     bool kept = all_kept;
-    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, K), (uint32_t)e & 3u) < thr;
+    if (use_mask) kept = pick(group_words(e >> 2, tensor_id, cmask, k0, k1), (uint32_t)e & 3u) < thr;
     const float g = gval(kept, QuadIO<TG>::load1(gs, i), ACC ? QuadIO<float>::load1(ga, i) : 0.0f);
     s = __builtin_fmaf(g, g, s);
   };
@@ -246,7 +251,7 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, c
     if (use_mask) {
 #pragma unroll
       for (int u = 0; u < kNormQuads; ++u) {
-        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, K);
+        const Words w = philox_tile(philox_p0(G.lo + u * kBlock + threadIdx.x), G.hi, tensor_id, cmask, k0, k1);
         mw[u][0] = w.w0;
         mw[u][1] = w.w1;
         mw[u][2] = w.w2;
@@ -298,13 +303,13 @@ template <typename TG, bool ACC>
 __global__ __launch_bounds__(kBlock) void k_sqnorm_multi(const TensorRec* __restrict__ recs,
                                                          const ParamRec* __restrict__ prms,
                                                          const uint2* __restrict__ chunks, float* partials,
-                                                         PhiloxKeys K, uint32_t step, float lambda) {
+                                                         uint64_t seed, uint32_t step, float lambda) {
   constexpr int64_t tile = tile_elems(kNormQuads);
   constexpr uint32_t tpc = tiles_per_chunk(kNormQuads);
   const uint2 ch = chunks[blockIdx.x / tpc];
   const Tile T = list_tile<float, float, TG>(rec_at(recs, ch.x), ch.y, blockIdx.x % tpc, tile);
   float s = 0.0f;
-  if (T.len > 0) s = tile_sqnorm<TG, ACC>(T, rec_at(prms, ch.x), K, step, lambda);
+  if (T.len > 0) s = tile_sqnorm<TG, ACC>(T, rec_at(prms, ch.x), seed, step, lambda);
   s = block_sum<float, kBlock>(s);
   if (threadIdx.x == 0) partials[blockIdx.x] = s;
 }
@@ -324,7 +329,7 @@ __global__ __launch_bounds__(kBlock) void k_sqnorm_multi_dev(const TensorRec* __
     const StepState S = *state;
     ParamRec P = prms[ch.x];
     P.t = device_coefficient(S.scale, scales[ch.x]);
-    s = tile_sqnorm<TG, ACC>(T, P, philox_keys(S.seed), S.step, lambda);
+    s = tile_sqnorm<TG, ACC>(T, P, S.seed, S.step, lambda);
   }
   s = block_sum<float, kBlock>(s);
   if (threadIdx.x == 0) partials[blockIdx.x] = s;
@@ -414,20 +419,19 @@ hipError_t launch_sqnorm_multi(const TensorRec* recs, const ParamRec* prms, cons
                                float* partials, double* sums, int grad_dtype, bool accumulate, float lambda,
                                uint64_t seed, uint32_t step, double* sumsq, float* clip_coef, float max_norm,
                                hipStream_t stream) {
-  const PhiloxKeys K = philox_keys(seed);
   constexpr uint32_t tpc = kNormPartialsPerChunk;
   const hipError_t e = for_pieces(nchunks, max_grid_blocks(kBlock) / tpc, [&](uint64_t first, uint64_t count) {
     const uint2* ch = chunks + first;
     float* part = partials + first * tpc;
     const dim3 grid((uint32_t)count * tpc), block(kBlock);
     if (grad_dtype == 1 && accumulate)
-      k_sqnorm_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, K, step, lambda);
+      k_sqnorm_multi<Bf16, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
     else if (grad_dtype == 1)
-      k_sqnorm_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, K, step, lambda);
+      k_sqnorm_multi<Bf16, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
     else if (accumulate)
-      k_sqnorm_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, K, step, lambda);
+      k_sqnorm_multi<float, true><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
     else
-      k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, K, step, lambda);
+      k_sqnorm_multi<float, false><<<grid, block, 0, stream>>>(recs, prms, ch, part, seed, step, lambda);
   });
   if (e != hipSuccess) return e;
   return launch_sqnorm_reduce(partials, nchunks * tpc, sums, sumsq, clip_coef, max_norm, stream);
