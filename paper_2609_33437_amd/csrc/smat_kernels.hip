@@ -68,7 +68,7 @@ __device__ __forceinline__ void simulate_tile_case(const Tile& T, const ParamRec
   // tile's last quad (loads, draws and all), so it stores the very bytes that quad's own lane
   // stores, to the same place, and no branch splits the phases.
   const uint32_t nq = len >> 2;
-  const uint32_t q = threadIdx.x < nq ? threadIdx.x : nq - 1;
+  const uint32_t q = min((uint32_t)threadIdx.x, nq - 1u);
   const typename QuadIO<float>::Raw ra = QuadIO<float>::load_raw(th, q);
   const typename QuadIO<T0>::Raw rb = QuadIO<T0>::load_raw(t0, q);
   normal_priority();
@@ -189,7 +189,7 @@ __device__ __forceinline__ void backward_tile(const Tile& T, const ParamRec& P, 
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
       const uint32_t q = u * kBlock + threadIdx.x;
-      const uint32_t qc = q < nq ? q : nq - 1;
+      const uint32_t qc = min(q, nq - 1u);
       ra[u] = QuadIO<TG>::load_raw(gs, qc);
       if (ACC) rb[u] = QuadIO<float>::load_raw(gt, qc);
     }

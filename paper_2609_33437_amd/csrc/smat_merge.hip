@@ -56,7 +56,7 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
 #pragma unroll
       for (int u = 0; u < kMergeQuads; ++u) {
         const uint32_t q = u * kBlock + threadIdx.x;
-        r0[u] = QuadIO<T0>::load_raw(t0p, q < nq ? q : nq - 1);
+        r0[u] = QuadIO<T0>::load_raw(t0p, min(q, nq - 1u));
       }
       normal_priority();
 #pragma unroll
@@ -78,7 +78,7 @@ __device__ __forceinline__ void merge_tile(const void* t0p, void* outp, uint64_t
 #pragma unroll
       for (int u = 0; u < kMergeQuads; ++u) {
         const uint32_t q = u * kBlock + threadIdx.x;
-        rx[u] = QuadIO<TE>::load_raw(xp, q < nq ? q : nq - 1);
+        rx[u] = QuadIO<TE>::load_raw(xp, min(q, nq - 1u));
       }
       normal_priority();
       bool kept[kMergeQuads][4];

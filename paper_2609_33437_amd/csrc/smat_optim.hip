@@ -69,7 +69,7 @@ __device__ __forceinline__ void adamw_tile(const Tile& T, float* m1p, float* m2p
 #pragma unroll
     for (int u = 0; u < Q; ++u) {
       const uint32_t q = u * kBlock + threadIdx.x;
-      const uint32_t qc = q < nq ? q : nq - 1;
+      const uint32_t qc = min(q, nq - 1u);
       rg[u] = QuadIO<TG>::load_raw(gs, qc);
       if (ACC) racc[u] = QuadIO<float>::load_raw(ga, qc);
       rt[u] = QuadIO<float>::load_raw(th, qc);
@@ -240,7 +240,7 @@ __device__ __forceinline__ float tile_sqnorm(const Tile& T, const ParamRec& P, u
 #pragma unroll
     for (int u = 0; u < kNormQuads; ++u) {
       const uint32_t q = u * kBlock + threadIdx.x;
-      const uint32_t qc = q < nq ? q : nq - 1;
+      const uint32_t qc = min(q, nq - 1u);
       rg[u] = QuadIO<TG>::load_raw(gs, qc);
       if (ACC) ra[u] = QuadIO<float>::load_raw(ga, qc);
     }
