@@ -147,6 +147,12 @@ def test_plan_create_validation_without_gpu():
     assert plan([_desc(1 * A, 2 * A, None, None, None, 10, 0, 0, 11 * A)], offload=1, dts=(0, 1, 1)) == _lib.SMAT_ERR_INVALID
     # a plan without gradient pointers is valid for simulate-only use
     assert plan([_desc(1 * A, 2 * A, 3 * A, None, None, 10, 0)]) == _lib.SMAT_OK
+    # more tensors than the kernels address with 32-bit record offsets: refused on the count alone,
+    # before any descriptor is read (the array holds one)
+    one = (_lib.smat_tensor_desc * 1)(good[0])
+    p = ctypes.c_void_p()
+    assert lib.smat_plan_create(one, (1 << 26) + 1, 1, 1, 1, 0, ctypes.byref(p)) == _lib.SMAT_ERR_INVALID
+    assert b"at most" in lib.smat_last_error()
     # calls on an unbound plan fail with a state error and never launch
     arr = (_lib.smat_tensor_desc * 2)(*good)
     p = ctypes.c_void_p()
