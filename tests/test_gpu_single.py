@@ -10,7 +10,7 @@ import oracle
 import paper_2609_33437_amd as smat
 import workloads
 from helpers import host
-from tolerances import NONSTRICT_MAX_FRACTION, Z_TOL, check_grad, check_theta_tilde, ordered, theta_tilde_report
+from tolerances import Z_TOL, check_grad, check_theta_tilde, nonstrict_within_cap, ordered, theta_tilde_report
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -36,8 +36,7 @@ def compare_simulate(theta, theta0, out, p, seed, step, tid, off=0):
         want = oracle.round_to_bf16_bits(y)
         n, loose, worst, worst_strict = theta_tilde_report(got, want, strict)
         print(f"theta~ {n} elements: {loose} under the absolute clause, max {worst} ulp (strict {worst_strict})")
-        if n >= 1000:
-            assert loose <= NONSTRICT_MAX_FRACTION * n, (loose, n)
+        assert nonstrict_within_cap(loose, n), (loose, n)
         return np.abs(ordered(got) - ordered(want))[strict]
     return None
 

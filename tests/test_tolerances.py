@@ -71,3 +71,18 @@ def test_two_fma_lerp_needs_the_theta0_term_for_large_t():
     no_theta0_term = 4 * U * (np.abs(t0) + 10.0 * np.abs(th.astype(np.float64) - t0))
     assert (err > no_theta0_term).any()
     assert (err <= theta_tilde_bound(th.astype(np.float64), t0.astype(np.float64), 10.0, 0.0, 0.0)).all()
+
+
+def test_nonstrict_cap_allowance_is_a_poisson_tail():
+    """The small-tensor allowance of the non-strict cap: at the cap's own rate (one element per
+    1,000) a 1,000-element tensor reaches the allowance + 1 with probability about 1e-6, and the cap
+    is the larger of the allowance and the 1e-3 fraction."""
+    from scipy.stats import poisson
+
+    from tolerances import NONSTRICT_MAX_FRACTION, NONSTRICT_SMALL_ALLOWANCE, nonstrict_within_cap
+
+    tail = poisson.sf(NONSTRICT_SMALL_ALLOWANCE, NONSTRICT_MAX_FRACTION * 1000)
+    assert 1e-7 < tail < 2e-6
+    assert nonstrict_within_cap(8, 1042) and not nonstrict_within_cap(9, 1042)
+    assert nonstrict_within_cap(1000, 10 ** 6) and not nonstrict_within_cap(1001, 10 ** 6)
+    assert nonstrict_within_cap(0, 0)
